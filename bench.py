@@ -1,0 +1,265 @@
+#!/usr/bin/env python3
+"""Decode-step benchmark of the COUNTDOWN sparse Gated-MLP FFN on one MI355X.
+
+A step is one decode token through one FFN layer on the HIP path: the
+coefficient kernel (dense W_up projection, threshold, compaction, gathered
+gate rows) and the gathered down projection. Default workload: the
+Llama-7B-shaped layer (d_model 4096, d_ff 11008, bf16 weights N(0, 0.02^2),
+1% outlier input channels x20, batch 1), M-CountDown at sparsity k = 0.9 with
+the layerwise threshold calibrated on the GPU from 256 seeded tokens.
+Weights are rotated over several independent copies (> 1 GB in total) so
+the 256 MB Infinity Cache cannot serve them; inputs are resident in HBM
+before the timed region starts.
+
+Prints ONE JSON line on stdout; progress goes to stderr.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0  # MI355X HBM3E peak, GB/s
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def dev_bf16(a):
+    import torch
+
+    return torch.from_numpy(np.ascontiguousarray(a).view(np.int16)).view(torch.bfloat16).to("cuda")
+
+
+def parse():
+    p = argparse.ArgumentParser(description=__doc__.split("\n\n")[0])
+    p.add_argument("--gpus", type=int, default=1)
+    p.add_argument("--steps", type=int, default=2000)
+    p.add_argument("--warmup", type=int, default=200)
+    p.add_argument("--workload", default="llama7b_4096x11008")
+    p.add_argument("--variant", default="mono", choices=["mono", "dual_ideal", "dense"])
+    p.add_argument("--k", type=float, default=0.9)
+    p.add_argument("--copies", type=int, default=4, help="independent weight copies rotated")
+    p.add_argument("--tokens", type=int, default=64, help="distinct eval tokens rotated")
+    p.add_argument("--calib-tokens", type=int, default=256)
+    p.add_argument("--cpu-seconds", type=float, default=12.0,
+                   help="time budget of the oracle CPU baseline (0 disables it)")
+    p.add_argument("--no-extra", action="store_true", help="skip the secondary variants")
+    return p.parse_args()
+
+
+def time_steps(fn, steps, warmup, stream):
+    """Warm up, then time exactly `steps` calls between two synchronisations."""
+    import torch
+
+    for i in range(warmup):
+        fn(i)
+    torch.cuda.synchronize()
+    t0 = torch.cuda.Event(enable_timing=True)
+    t1 = torch.cuda.Event(enable_timing=True)
+    t0.record(stream)
+    for i in range(steps):
+        fn(i)
+    t1.record(stream)
+    torch.cuda.synchronize()
+    return t0.elapsed_time(t1) / steps  # ms per step
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU only (got --gpus {args.gpus}); the sparse FFN is "
+              "built and timed on a single MI355X in this build.", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+
+    from paper_2505_17701_amd import binding as cd
+    from paper_2505_17701_amd import traffic
+    from workloads import WORKLOADS
+    from workloads.synth import T_CALIB
+
+    cd.load_library()
+    if not torch.cuda.is_available():
+        sys.exit("bench.py needs a GPU")
+    torch.cuda.set_device(0)
+    w = WORKLOADS[args.workload]
+    dm, dff = w.d_model, w.d_ff
+    stream = torch.cuda.current_stream()
+
+    t = time.time()
+    layers = []
+    host0 = None
+    for c in range(args.copies):
+        L = w.layer(copy=c)
+        if c == 0:
+            host0 = L
+        layers.append({k: dev_bf16(v) for k, v in L.items()})
+    X_eval_h = w.tokens(args.tokens)
+    X_eval = dev_bf16(X_eval_h)
+    X_cal = dev_bf16(w.tokens(args.calib_tokens, purpose=T_CALIB))
+    torch.cuda.synchronize()
+    log(f"[bench] {args.copies} weight copies of {w.name} on device "
+        f"({args.copies * 3 * dm * dff * 2 / 1e9:.2f} GB) in {time.time() - t:.1f}s")
+
+    # layerwise thresholds, calibrated on the GPU (mean of per-token quantiles)
+    cal_plan = cd.Plan(dm, dff, max_batch=8)
+    thld = {}
+    for variant, vid in (("mono", cd.CD_VARIANT_MONO), ("dual_ideal", cd.CD_VARIANT_DUAL_IDEAL)):
+        for k in sorted(set((args.k,) + tuple(w.ks))):
+            L0 = layers[0]
+            th, _ = cd.countdown_calibrate(cal_plan, vid, X_cal, k, W_gate=L0["W_gate"],
+                                           W_up=L0["W_up"])
+            thld[(variant, k)] = float(th.item())
+    cal_plan.close()
+    log(f"[bench] thresholds: " + ", ".join(f"{v}@{k}={t:.4f}" for (v, k), t in thld.items()))
+
+    def make_step(plan, variant, k):
+        th = thld.get((variant, k), 0.0)
+        ntok = X_eval.shape[0]
+
+        def step(i):
+            L = layers[i % args.copies]
+            x = X_eval[i % ntok: i % ntok + 1]
+            if variant == "mono":
+                cd.countdown_ffn_mono(plan, x, L["W_gate"], L["W_up"], L["W_down"], th, y=y)
+            elif variant == "dual_ideal":
+                cd.countdown_ffn_dual(plan, x, L["W_gate"], L["W_up"], L["W_down"], th, y=y)
+            else:
+                cd.countdown_ffn_dense(plan, x, L["W_gate"], L["W_up"], L["W_down"], y=y)
+        return step
+
+    y = torch.empty((1, dm), dtype=torch.float32, device="cuda")
+
+    def measure(variant, k, steps, warmup):
+        plan = cd.Plan(dm, dff, max_batch=1)
+        ms = time_steps(make_step(plan, variant, k), steps, warmup, stream)
+        plan.close()
+        # second pass: per-kernel durations (event pair around each launch) and n_active
+        tplan = cd.Plan(dm, dff, max_batch=1, timing=True)
+        nsteps = min(steps, 512)
+        n_arr = torch.zeros(nsteps, dtype=torch.int32, device="cuda")
+        step = make_step(tplan, variant, k)
+        for i in range(min(warmup, 20)):
+            step(i)
+        torch.cuda.synchronize()
+        cd.countdown_timing_collect(tplan)
+        lib = cd.load_library()
+        for i in range(nsteps):
+            step(i)
+            lib.countdown_copy_last_active(tplan.handle, None, n_arr[i:i + 1].data_ptr(), None,
+                                           None, stream.cuda_stream)
+        torch.cuda.synchronize()
+        kt = cd.countdown_timing_collect(tplan)
+        tplan.close()
+        n = n_arr.cpu().numpy().astype(np.float64)
+        per = [traffic.algorithmic_bytes(variant, dm, dff, int(v)) for v in n]
+        res = {"ms_per_step": ms, "us_per_layer": ms * 1e3, "tokens_per_s": 1e3 / ms,
+               "n_active_mean": float(n.mean()), "realised_sparsity": float(1 - n.mean() / dff)}
+        tot_bytes = float(np.mean([p["total"] for p in per]))
+        res["algorithmic_bytes"] = tot_bytes
+        res["achieved_GBs"] = tot_bytes / (ms * 1e-3) / 1e9
+        res["frac_hbm_peak"] = res["achieved_GBs"] / HBM_PEAK_GBS
+        for name in ("coef", "down"):
+            cnt, tms = kt[name]
+            if cnt:
+                avg_us = tms / cnt * 1e3
+                kb = float(np.mean([p[name] for p in per]))
+                res[f"{name}_kernel_us"] = avg_us
+                res[f"{name}_kernel_GBs"] = kb / (avg_us * 1e-6) / 1e9
+                res[f"{name}_kernel_bytes"] = kb
+        return res
+
+    main_res = measure(args.variant, args.k, args.steps, args.warmup)
+    log(f"[bench] {args.variant} k={args.k}: {json.dumps(main_res)}")
+
+    extra = {}
+    if not args.no_extra:
+        for variant, k in (("dense", None), ("dual_ideal", 0.9), ("mono", 0.7), ("mono", 0.5)):
+            if variant == args.variant and k == args.k:
+                continue
+            r = measure(variant, k, max(200, args.steps // 4), 50)
+            extra[f"{variant}" + ("" if k is None else f"@k={k}")] = {
+                kk: r[kk] for kk in ("us_per_layer", "tokens_per_s", "achieved_GBs",
+                                     "frac_hbm_peak", "n_active_mean", "coef_kernel_us",
+                                     "down_kernel_us") if kk in r}
+            log(f"[bench] {variant} k={k}: {json.dumps(extra[list(extra)[-1]])}")
+        if "dense" in extra:
+            extra["speedup_vs_dense"] = extra["dense"]["us_per_layer"] / main_res["us_per_layer"]
+            dense_b = traffic.algorithmic_bytes("dense", dm, dff, dff)["total"]
+            extra["ideal_byte_ratio"] = dense_b / main_res["algorithmic_bytes"]
+
+    # CPU baseline: the fp64 oracle on host cores, bounded sample of the same workload
+    cpu = None
+    if args.cpu_seconds > 0:
+        import oracle
+
+        th = np.float32(thld.get((args.variant, args.k), 0.0))
+        fn = {"mono": oracle.ffn_mono, "dual_ideal": oracle.ffn_dual_ideal}.get(args.variant)
+        n_done, t0 = 0, time.perf_counter()
+        while n_done < 3 or time.perf_counter() - t0 < args.cpu_seconds:
+            x = X_eval_h[n_done % len(X_eval_h)][None]
+            if fn is None:
+                oracle.dense(x, host0["W_gate"], host0["W_up"], host0["W_down"])
+            else:
+                fn(x, host0["W_gate"], host0["W_up"], host0["W_down"], th)
+            n_done += 1
+        el = time.perf_counter() - t0
+        cpu = {"value": n_done / el, "unit": "tokens/s", "cores": oracle.num_threads(),
+               "kind": "oracle",
+               "sample": f"{n_done} decode tokens of {w.name} {args.variant} k={args.k}, "
+                         f"batch 1, one weight copy, fp64 C oracle ({el:.1f} s)"}
+        log(f"[bench] cpu baseline: {json.dumps(cpu)}")
+
+    coef_us = main_res.get("coef_kernel_us")
+    roof = None
+    if coef_us:
+        roof = {"bound": "hbm", "kernel": "coef (dense coefficient GEMV + threshold + "
+                                          "compaction + gathered gate)",
+                "achieved": main_res["coef_kernel_GBs"], "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                "frac": main_res["coef_kernel_GBs"] / HBM_PEAK_GBS, "traffic": None,
+                "bytes_per_launch": main_res["coef_kernel_bytes"], "avg_launch_us": coef_us}
+
+    out = {
+        "metric": "sparse-FFN decode tokens/s (one FFN layer, batch 1, k=0.9)",
+        "value": main_res["tokens_per_s"],
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": main_res["ms_per_step"],
+        "us_per_layer": main_res["us_per_layer"],
+        "achieved_GBs": main_res["achieved_GBs"],
+        "frac_hbm_peak": main_res["frac_hbm_peak"],
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16 weights, fp32 accumulate",
+        "data": "synthetic (seeded N(0, 0.02^2) weights, N(0,1) tokens with 1% outlier "
+                "channels x20)",
+        "config": {"workload": w.name, "d_model": dm, "d_ff": dff, "batch": 1,
+                   "variant": args.variant, "k": args.k,
+                   "thld": thld.get((args.variant, args.k)), "weight_copies": args.copies,
+                   "n_active_mean": main_res["n_active_mean"],
+                   "realised_sparsity": main_res["realised_sparsity"],
+                   "algorithmic_bytes_per_step": main_res["algorithmic_bytes"],
+                   "parallelism": "single GPU"},
+        "kernels": {k: main_res.get(k) for k in ("coef_kernel_us", "coef_kernel_GBs",
+                                                  "down_kernel_us", "down_kernel_GBs")},
+        "variants": extra,
+        "roofline": roof,
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,190 @@
+/*
+ * countdown.h -- C ABI of the MI355X (gfx950) COUNTDOWN sparse Gated-MLP FFN.
+ *
+ * The FFN of arXiv 2505.17701 (Sec. 3, Eq. 1) is
+ *     y = ((x.W_up) (.) SiLU(x.W_gate)) . W_down^T = sum_i s[i] W_down^T[i]   (Eq. 5)
+ * and the library evaluates it only on an index set IDX chosen per call by a
+ * coefficient and a per-layer threshold (Eq. 2, 3, 6; Sec. 4):
+ *   M-CountDown  (countdown_ffn_mono):        IDX = {i : |u[i]| > thld}, u = x.W_up;
+ *   D-CountDown  (countdown_ffn_dual, ideal): IDX = {i : |s[i]| > thld}, s computed densely;
+ *   D-CountDown  (countdown_ffn_dual, pred):  IDX = {i : s_hat[i] > thld},
+ *                                             s_hat = (x.theta_A).theta_B (signed score).
+ * For a batch of B tokens IDX is the union of the per-token sets and every
+ * token uses all rows of IDX with its own coefficients.
+ *
+ * Data conventions (all calls):
+ *  - bf16 tensors are passed as `const uint16_t *` (bf16 bit patterns);
+ *    fp32 tensors as `float *`.
+ *  - Every tensor pointer is a DEVICE pointer owned by the caller, 16-byte
+ *    aligned; the library neither frees nor retains it beyond the call.
+ *  - Weight matrices are neuron-major, row-major [d_ff][d_model]: row i is
+ *    the weight vector of intermediate neuron i (W_gate[i][j] is the paper's
+ *    W_gate[j][i]; W_down[i][:] is the paper's W_down^T[i]).
+ *    The predictor is A_t [d_rank][d_model] (theta_A transposed) and
+ *    B_t [d_ff][d_rank] (theta_B transposed).
+ *  - x is [B][d_model] bf16, y is [B][d_model] fp32 and is fully
+ *    overwritten (no pre-zeroing needed).
+ *  - `stream` is a hipStream_t (NULL = the default stream). Every call only
+ *    enqueues work on `stream` and returns without synchronising; outputs
+ *    are valid once the stream reaches that point. No call but
+ *    countdown_plan_create / countdown_plan_destroy / countdown_calibrate
+ *    allocates device memory.
+ *  - thld is one fp32 constant per layer (Sec. 4: the calibrated layerwise
+ *    threshold). Selection is strict (coefficient > thld). thld = -INFINITY
+ *    selects every row (the dense result); thld = +INFINITY selects none
+ *    (y = 0). A NaN thld is rejected with CD_EINVAL.
+ *  - Arguments are validated on the host before anything is enqueued;
+ *    on error nothing is launched. A launch failure returns CD_EHIP.
+ *  - A plan is not thread-safe: calls on one plan must not overlap (use one
+ *    plan per stream).
+ */
+#ifndef COUNTDOWN_H
+#define COUNTDOWN_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef int cd_status;
+#define CD_OK 0
+#define CD_EINVAL (-1)        /* bad argument (null/misaligned pointer, size, NaN thld) */
+#define CD_EUNSUPPORTED (-2)  /* shape outside what the kernels implement */
+#define CD_EHIP (-3)          /* a HIP runtime call or kernel launch failed */
+#define CD_ENOMEM (-4)        /* device allocation failed */
+
+/* Variants, for countdown_check_args and countdown_calibrate. */
+#define CD_VARIANT_MONO 0        /* M-CountDown, coefficient |u| (Eq. 6b) */
+#define CD_VARIANT_DUAL_IDEAL 1  /* D-CountDown ideal, coefficient |s| (Eq. 6c) */
+#define CD_VARIANT_DUAL_PRED 2   /* D-CountDown, predictor score s_hat (Sec. 4) */
+#define CD_VARIANT_DENSE 3       /* dense Gated-MLP (Eq. 1) */
+
+/* Plan flags. */
+#define CD_PLAN_KEEP_COEF 1u  /* also store the dense coefficient vector of each call
+                                 (u for mono, s for dual ideal, s_hat for dual pred) */
+#define CD_PLAN_TIMING 2u     /* record a HIP event pair around every kernel launch */
+
+typedef struct cd_plan cd_plan;
+
+/*
+ * Create a plan for one FFN shape. Allocates the plan's device workspace
+ * (per-block active lists, compacted IDX, coefficients) on the current
+ * device. d_model and d_ff must be positive multiples of 8 with
+ * d_model <= 8192; 1 <= max_batch <= 8; d_rank is 0 (no predictor) or a
+ * power of two in [8, 1024]; max_batch * d_model <= 32768. Returns CD_EINVAL
+ * for malformed sizes and CD_EUNSUPPORTED for well-formed sizes beyond those
+ * limits (both checked before any HIP call), CD_ENOMEM / CD_EHIP when the
+ * device is missing or allocation fails. *out is set only on success.
+ */
+cd_status countdown_plan_create(int d_model, int d_ff, int max_batch, int d_rank,
+                                unsigned flags, cd_plan **out);
+
+/* Release a plan and its workspace (synchronises the device first). NULL is a no-op. */
+cd_status countdown_plan_destroy(cd_plan *plan);
+
+/*
+ * M-CountDown (Eq. 6b; Sec. 4 "Constructing SP^Prac"): u = x.W_up over all
+ * rows; IDX = {i : exists b, |u_b[i]| > thld}; s_b[i] = u_b[i] SiLU(x_b.W_gate[i])
+ * on IDX only (Eq. 2); y_b = sum_{i in IDX} s_b[i] W_down[i] (Eq. 5).
+ * B in [1, max_batch]. W_gate, W_up, W_down: [d_ff][d_model] bf16.
+ */
+cd_status countdown_ffn_mono(cd_plan *plan, const uint16_t *x, int B, const uint16_t *W_gate,
+                             const uint16_t *W_up, const uint16_t *W_down, float thld, float *y,
+                             void *stream);
+
+/*
+ * D-CountDown (Eq. 6c; Sec. 4). With A_t == B_t == NULL (ideal): s is
+ * computed over all rows and IDX = {i : exists b, |s_b[i]| > thld}. With a
+ * predictor (both non-NULL, plan created with this d_rank): s_hat_b =
+ * (x_b.theta_A).theta_B, IDX = {i : exists b, s_hat_b[i] > thld} (signed),
+ * then gate and up are evaluated on IDX only. y by Eq. (5) over IDX.
+ * Passing exactly one of A_t / B_t is CD_EINVAL.
+ */
+cd_status countdown_ffn_dual(cd_plan *plan, const uint16_t *x, int B, const uint16_t *W_gate,
+                             const uint16_t *W_up, const uint16_t *W_down, const uint16_t *A_t,
+                             const uint16_t *B_t, float thld, float *y, void *stream);
+
+/* Dense Gated-MLP (Eq. 1) through the same kernels with every row active:
+ * the reference the sparse variants are timed against. */
+cd_status countdown_ffn_dense(cd_plan *plan, const uint16_t *x, int B, const uint16_t *W_gate,
+                              const uint16_t *W_up, const uint16_t *W_down, float *y,
+                              void *stream);
+
+/*
+ * Layerwise threshold calibration (Sec. 4): thld = (1/T) sum_t Quantile(k, c^(t))
+ * over T calibration tokens X [T][d_model], with c^(t) the variant's
+ * coefficient vector (|u| mono, |s| dual ideal, signed s_hat dual pred) and
+ * Quantile the linear interpolation between order statistics:
+ * h = k (d_ff - 1), q = v[floor h] + (h - floor h)(v[floor h + 1] - v[floor h]).
+ * Quantiles and the mean are formed in fp64; *thld_out (a DEVICE float) gets
+ * the mean rounded to fp32. q_out (DEVICE double[T], may be NULL) gets the
+ * per-token quantiles. k in [0, 1]. Allocates and frees temporary device
+ * memory, and synchronises `stream` before returning.
+ */
+cd_status countdown_calibrate(cd_plan *plan, int variant, const uint16_t *X, int T,
+                              const uint16_t *W_gate, const uint16_t *W_up, const uint16_t *A_t,
+                              const uint16_t *B_t, double k, float *thld_out, double *q_out,
+                              void *stream);
+
+/*
+ * Device views of the last call's results on this plan (valid after that
+ * call's stream work completes, until the next call): idx [d_ff] int32 holds
+ * the ascending IDX in its first *n_active entries; n_active [1] int32;
+ * s_c [max_batch][d_ff] fp32 holds s_b[IDX[j]] at s_c[b * d_ff + j];
+ * coef [max_batch][d_ff] fp32 the dense coefficient vector (NULL unless the
+ * plan has CD_PLAN_KEEP_COEF). Any output pointer may be NULL.
+ */
+cd_status countdown_last_active(const cd_plan *plan, const int32_t **idx,
+                                const int32_t **n_active, const float **s_c, const float **coef);
+
+/*
+ * Enqueue device-to-device copies of the last call's results into
+ * caller-owned DEVICE buffers on `stream` (any destination may be NULL):
+ * idx_dst int32[d_ff], n_dst int32[1], s_dst fp32[B_last * d_ff] (the s_c
+ * layout above), coef_dst fp32[B_last * d_ff] (CD_PLAN_KEEP_COEF plans only,
+ * else CD_EINVAL). B_last is the batch of the last FFN call on the plan.
+ */
+cd_status countdown_copy_last_active(const cd_plan *plan, int32_t *idx_dst, int32_t *n_dst,
+                                     float *s_dst, float *coef_dst, void *stream);
+
+/*
+ * Kernel timing of a CD_PLAN_TIMING plan: waits for the recorded launches,
+ * then writes per kernel kind (see CD_KERNEL_*) the number of launches and
+ * the summed duration in milliseconds since the last reset, and resets.
+ * counts / ms have CD_KERNEL_KINDS entries.
+ */
+#define CD_KERNEL_COEF 0     /* coefficient / threshold / local compaction (+ gate or gate+up) */
+#define CD_KERNEL_DOWN 1     /* gathered down projection and IDX export */
+#define CD_KERNEL_LATENT 2   /* predictor latent x.theta_A */
+#define CD_KERNEL_SELECT 3   /* calibration order statistics */
+#define CD_KERNEL_KINDS 4
+cd_status countdown_timing_collect(cd_plan *plan, int *counts, double *ms);
+
+/*
+ * Host-only validation of an FFN call's arguments against a shape, exactly
+ * as the entry points perform it before launching: pointers non-NULL and
+ * 16-byte aligned, 1 <= B <= max_batch, thld not NaN, predictor pointers
+ * both NULL or both set (dual only, and d_rank > 0 when set). Touches no
+ * device. variant is a CD_VARIANT_*.
+ */
+cd_status countdown_check_args(int variant, int d_model, int d_ff, int max_batch, int d_rank,
+                               const void *x, int B, const void *W_gate, const void *W_up,
+                               const void *W_down, const void *A_t, const void *B_t, float thld,
+                               const void *y);
+
+/* Host-only validation of plan sizes (the checks countdown_plan_create makes first). */
+cd_status countdown_check_shape(int d_model, int d_ff, int max_batch, int d_rank);
+
+/* Static description of a status code. */
+const char *countdown_status_string(cd_status status);
+
+/* ABI version of this header (bumped on any signature change). */
+#define COUNTDOWN_ABI_VERSION 1
+int countdown_abi_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* COUNTDOWN_H */

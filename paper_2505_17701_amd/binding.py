@@ -1,0 +1,255 @@
+"""Thin ctypes binding of ``libcountdown.so`` (declared in ``include/countdown.h``).
+
+The functions carry the C names and only marshal arguments: torch tensors
+become device pointers, ``stream`` defaults to torch's current HIP stream,
+and a non-OK status raises :class:`CountdownError`. All compute runs in the
+library's HIP kernels; there is no fallback when the library or the GPU is
+missing.
+"""
+from __future__ import annotations
+
+import ctypes as C
+import os
+
+PKG = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(PKG, "libcountdown.so")
+
+CD_OK, CD_EINVAL, CD_EUNSUPPORTED, CD_EHIP, CD_ENOMEM = 0, -1, -2, -3, -4
+CD_VARIANT_MONO, CD_VARIANT_DUAL_IDEAL, CD_VARIANT_DUAL_PRED, CD_VARIANT_DENSE = 0, 1, 2, 3
+CD_PLAN_KEEP_COEF, CD_PLAN_TIMING = 1, 2
+CD_KERNEL_COEF, CD_KERNEL_DOWN, CD_KERNEL_LATENT, CD_KERNEL_SELECT, CD_KERNEL_KINDS = 0, 1, 2, 3, 4
+KERNEL_NAMES = ("coef", "down", "latent", "select")
+
+# every symbol include/countdown.h declares
+EXPORTS = (
+    "countdown_plan_create", "countdown_plan_destroy", "countdown_ffn_mono", "countdown_ffn_dual",
+    "countdown_ffn_dense", "countdown_calibrate", "countdown_last_active",
+    "countdown_copy_last_active", "countdown_timing_collect", "countdown_check_args",
+    "countdown_check_shape", "countdown_status_string", "countdown_abi_version",
+)
+
+_lib = None
+
+
+class CountdownError(RuntimeError):
+    def __init__(self, status: int, what: str):
+        super().__init__(f"{what}: {status_string(status)}")
+        self.status = status
+
+
+def load_library(path: str = LIB_PATH):
+    """Load the built library (raises if it has not been built)."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(path):
+        raise RuntimeError(f"{path} is missing: build it with __graft_entry__.build() "
+                           "(python -m paper_2505_17701_amd.build)")
+    lib = C.CDLL(path)
+    vp, i, u, f, d = C.c_void_p, C.c_int, C.c_uint, C.c_float, C.c_double
+    sig = {
+        "countdown_plan_create": (i, [i, i, i, i, u, C.POINTER(vp)]),
+        "countdown_plan_destroy": (i, [vp]),
+        "countdown_ffn_mono": (i, [vp, vp, i, vp, vp, vp, f, vp, vp]),
+        "countdown_ffn_dual": (i, [vp, vp, i, vp, vp, vp, vp, vp, f, vp, vp]),
+        "countdown_ffn_dense": (i, [vp, vp, i, vp, vp, vp, vp, vp]),
+        "countdown_calibrate": (i, [vp, i, vp, i, vp, vp, vp, vp, d, vp, vp, vp]),
+        "countdown_last_active": (i, [vp, vp, vp, vp, vp]),
+        "countdown_copy_last_active": (i, [vp, vp, vp, vp, vp, vp]),
+        "countdown_timing_collect": (i, [vp, C.POINTER(i), C.POINTER(d)]),
+        "countdown_check_args": (i, [i, i, i, i, i, vp, i, vp, vp, vp, vp, vp, f, vp]),
+        "countdown_check_shape": (i, [i, i, i, i]),
+        "countdown_status_string": (C.c_char_p, [i]),
+        "countdown_abi_version": (i, []),
+    }
+    for name, (res, args) in sig.items():
+        fn = getattr(lib, name)
+        fn.restype = res
+        fn.argtypes = args
+    _lib = lib
+    return lib
+
+
+def status_string(status: int) -> str:
+    return load_library().countdown_status_string(int(status)).decode()
+
+
+def _check(status: int, what: str) -> None:
+    if status != CD_OK:
+        raise CountdownError(status, what)
+
+
+def _ptr(t) -> int | None:
+    """Device pointer of a torch tensor (None -> NULL)."""
+    if t is None:
+        return None
+    if not t.is_cuda:
+        raise ValueError("countdown tensors must live on the GPU")
+    if not t.is_contiguous():
+        raise ValueError("countdown tensors must be contiguous")
+    return t.data_ptr()
+
+
+def _stream(stream) -> int | None:
+    if stream is None:
+        import torch
+
+        return torch.cuda.current_stream().cuda_stream
+    return int(stream) if not hasattr(stream, "cuda_stream") else stream.cuda_stream
+
+
+def _bf16(t):
+    import torch
+
+    if t is not None and t.dtype != torch.bfloat16:
+        raise TypeError(f"expected a bfloat16 tensor, got {t.dtype}")
+    return t
+
+
+def _f32(t):
+    import torch
+
+    if t.dtype != torch.float32:
+        raise TypeError(f"expected a float32 tensor, got {t.dtype}")
+    return t
+
+
+class Plan:
+    """Owns a ``cd_plan``: shape, workspace, and optional timing/coefficient capture."""
+
+    def __init__(self, d_model: int, d_ff: int, max_batch: int = 1, d_rank: int = 0,
+                 keep_coef: bool = False, timing: bool = False):
+        self.d_model, self.d_ff, self.max_batch, self.d_rank = d_model, d_ff, max_batch, d_rank
+        flags = (CD_PLAN_KEEP_COEF if keep_coef else 0) | (CD_PLAN_TIMING if timing else 0)
+        h = C.c_void_p()
+        _check(load_library().countdown_plan_create(d_model, d_ff, max_batch, d_rank, flags,
+                                                    C.byref(h)), "countdown_plan_create")
+        self.handle = h.value
+        self.keep_coef = keep_coef
+        self.last_batch = 0
+
+    def close(self):
+        if getattr(self, "handle", None):
+            _check(load_library().countdown_plan_destroy(self.handle), "countdown_plan_destroy")
+            self.handle = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+    def __enter__(self):
+        return self
+
+    def __exit__(self, *exc):
+        self.close()
+
+
+def countdown_plan_create(d_model, d_ff, max_batch=1, d_rank=0, keep_coef=False, timing=False):
+    return Plan(d_model, d_ff, max_batch, d_rank, keep_coef, timing)
+
+
+def countdown_plan_destroy(plan: Plan) -> None:
+    plan.close()
+
+
+def _out(plan: Plan, x, y):
+    import torch
+
+    B = x.shape[0]
+    if y is None:
+        y = torch.empty((B, plan.d_model), dtype=torch.float32, device=x.device)
+    return B, _f32(y)
+
+
+def countdown_ffn_mono(plan: Plan, x, W_gate, W_up, W_down, thld: float, y=None, stream=None):
+    """M-CountDown FFN; returns y ``[B, d_model]`` fp32 (enqueued on ``stream``)."""
+    B, y = _out(plan, x, y)
+    _check(load_library().countdown_ffn_mono(
+        plan.handle, _ptr(_bf16(x)), B, _ptr(_bf16(W_gate)), _ptr(_bf16(W_up)),
+        _ptr(_bf16(W_down)), float(thld), _ptr(y), _stream(stream)), "countdown_ffn_mono")
+    plan.last_batch = B
+    return y
+
+
+def countdown_ffn_dual(plan: Plan, x, W_gate, W_up, W_down, thld: float, A_t=None, B_t=None,
+                       y=None, stream=None):
+    """D-CountDown FFN (ideal without a predictor, practical with ``A_t``/``B_t``)."""
+    B, y = _out(plan, x, y)
+    _check(load_library().countdown_ffn_dual(
+        plan.handle, _ptr(_bf16(x)), B, _ptr(_bf16(W_gate)), _ptr(_bf16(W_up)),
+        _ptr(_bf16(W_down)), _ptr(_bf16(A_t)), _ptr(_bf16(B_t)), float(thld), _ptr(y),
+        _stream(stream)), "countdown_ffn_dual")
+    plan.last_batch = B
+    return y
+
+
+def countdown_ffn_dense(plan: Plan, x, W_gate, W_up, W_down, y=None, stream=None):
+    """Dense Gated-MLP through the same kernels."""
+    B, y = _out(plan, x, y)
+    _check(load_library().countdown_ffn_dense(
+        plan.handle, _ptr(_bf16(x)), B, _ptr(_bf16(W_gate)), _ptr(_bf16(W_up)),
+        _ptr(_bf16(W_down)), _ptr(y), _stream(stream)), "countdown_ffn_dense")
+    plan.last_batch = B
+    return y
+
+
+def countdown_calibrate(plan: Plan, variant: int, X, k: float, W_gate=None, W_up=None, A_t=None,
+                        B_t=None, stream=None):
+    """Layerwise threshold; returns ``(thld fp32 tensor [1], per-token quantiles fp64 [T])``."""
+    import torch
+
+    T = X.shape[0]
+    thld = torch.empty(1, dtype=torch.float32, device=X.device)
+    q = torch.empty(T, dtype=torch.float64, device=X.device)
+    _check(load_library().countdown_calibrate(
+        plan.handle, int(variant), _ptr(_bf16(X)), T, _ptr(_bf16(W_gate)), _ptr(_bf16(W_up)),
+        _ptr(_bf16(A_t)), _ptr(_bf16(B_t)), float(k), _ptr(thld), _ptr(q), _stream(stream)),
+        "countdown_calibrate")
+    return thld, q
+
+
+def countdown_copy_last_active(plan: Plan, stream=None):
+    """Copies of the last call's ``(IDX [n] int32, s_c [B, n] fp32, coef [B, d_ff] or None)``.
+
+    Synchronises the stream to read ``n``.
+    """
+    import torch
+
+    dev = torch.device("cuda", torch.cuda.current_device())
+    B = max(plan.last_batch, 1)
+    idx = torch.empty(plan.d_ff, dtype=torch.int32, device=dev)
+    n = torch.empty(1, dtype=torch.int32, device=dev)
+    s = torch.empty((B, plan.d_ff), dtype=torch.float32, device=dev)
+    coef = torch.empty((B, plan.d_ff), dtype=torch.float32, device=dev) if plan.keep_coef else None
+    st = _stream(stream)
+    _check(load_library().countdown_copy_last_active(plan.handle, _ptr(idx), _ptr(n), _ptr(s),
+                                                     _ptr(coef), st), "countdown_copy_last_active")
+    torch.cuda.current_stream().synchronize() if stream is None else torch.cuda.synchronize()
+    m = int(n.item())
+    return idx[:m], s[:, :m], coef
+
+
+def countdown_timing_collect(plan: Plan) -> dict:
+    """Per kernel kind: ``{name: (launches, total_ms)}`` since the last collect."""
+    counts = (C.c_int * CD_KERNEL_KINDS)()
+    ms = (C.c_double * CD_KERNEL_KINDS)()
+    _check(load_library().countdown_timing_collect(plan.handle, counts, ms),
+           "countdown_timing_collect")
+    return {KERNEL_NAMES[i]: (counts[i], ms[i]) for i in range(CD_KERNEL_KINDS)}
+
+
+def countdown_check_args(variant, d_model, d_ff, max_batch, d_rank, x, B, W_gate, W_up, W_down,
+                         A_t, B_t, thld, y) -> int:
+    """Host-only argument validation (integer pointers); returns the status code."""
+    return load_library().countdown_check_args(variant, d_model, d_ff, max_batch, d_rank, x, B,
+                                               W_gate, W_up, W_down, A_t, B_t, float(thld), y)
+
+
+def countdown_check_shape(d_model, d_ff, max_batch, d_rank) -> int:
+    return load_library().countdown_check_shape(d_model, d_ff, max_batch, d_rank)
+
+
+def countdown_abi_version() -> int:
+    return load_library().countdown_abi_version()

@@ -1,0 +1,471 @@
+// C ABI of the COUNTDOWN sparse Gated-MLP FFN: plans, argument validation
+// and launch sequencing. The arithmetic is in cd_kernels.hip.
+#include <hip/hip_runtime.h>
+
+#include <cmath>
+#include <cstdint>
+#include <cstdlib>
+#include <new>
+#include <vector>
+
+#include "../../include/countdown.h"
+#include "cd_internal.hpp"
+
+namespace {
+
+constexpr int kMaxDModel = 8192;
+constexpr int kMaxBatch = 8;
+constexpr int kMaxRank = 1024;
+constexpr int kMaxBatchCols = 32768;   // max_batch * d_model (x staged in LDS)
+constexpr int kDefaultRows = 16;       // neurons per coefficient workgroup
+constexpr int kMaxTimedLaunches = 1 << 16;
+
+bool aligned16(const void *p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+bool is_pow2(int v) { return v > 0 && (v & (v - 1)) == 0; }
+
+struct Timed {
+    int kind;
+    hipEvent_t ev[2];
+};
+
+}  // namespace
+
+struct cd_plan {
+    int d_model, d_ff, max_batch, d_rank;
+    unsigned flags;
+    int device;
+    int R, nblk, ls_stride;
+    int last_batch;
+    int gc, gr;
+    int *cnt, *lidx, *idx_out, *n_out;
+    float *ls, *s_out, *coef, *lat;
+    std::vector<Timed> timed;     // recorded launches since the last collect
+    std::vector<hipEvent_t> pool; // free events
+};
+
+namespace {
+
+cd_status hip_status(hipError_t e) { return e == hipSuccess ? CD_OK : CD_EHIP; }
+
+hipEvent_t take_event(cd_plan *p)
+{
+    if (!p->pool.empty()) {
+        hipEvent_t e = p->pool.back();
+        p->pool.pop_back();
+        return e;
+    }
+    hipEvent_t e = nullptr;
+    if (hipEventCreate(&e) != hipSuccess)
+        return nullptr;
+    return e;
+}
+
+// Run one launch, bracketed by an event pair when the plan records timings.
+template <class F>
+cd_status timed_launch(cd_plan *p, int kind, hipStream_t s, F &&launch)
+{
+    const bool rec = (p->flags & CD_PLAN_TIMING) && (int)p->timed.size() < kMaxTimedLaunches;
+    Timed t{kind, {nullptr, nullptr}};
+    if (rec) {
+        t.ev[0] = take_event(p);
+        t.ev[1] = take_event(p);
+        if (!t.ev[0] || !t.ev[1] || hipEventRecord(t.ev[0], s) != hipSuccess)
+            return CD_EHIP;
+    }
+    const hipError_t e = launch();
+    if (e != hipSuccess)
+        return CD_EHIP;
+    if (rec) {
+        if (hipEventRecord(t.ev[1], s) != hipSuccess)
+            return CD_EHIP;
+        p->timed.push_back(t);
+    }
+    return CD_OK;
+}
+
+cd_status check_shape(int d_model, int d_ff, int max_batch, int d_rank)
+{
+    if (d_model < 8 || d_model % 8 || d_model > kMaxDModel)
+        return d_model > kMaxDModel && d_model % 8 == 0 ? CD_EUNSUPPORTED : CD_EINVAL;
+    if (d_ff < 8 || d_ff % 8)
+        return CD_EINVAL;
+    if (max_batch < 1)
+        return CD_EINVAL;
+    if (max_batch > kMaxBatch)
+        return CD_EUNSUPPORTED;
+    if (d_rank < 0)
+        return CD_EINVAL;
+    if (d_rank > 0 && (!is_pow2(d_rank) || d_rank < 8 || d_rank > kMaxRank))
+        return CD_EUNSUPPORTED;
+    if ((long long)max_batch * d_model > kMaxBatchCols)
+        return CD_EUNSUPPORTED;
+    return CD_OK;
+}
+
+cd_status check_args(int variant, int d_model, int d_ff, int max_batch, int d_rank, const void *x,
+                     int B, const void *W_gate, const void *W_up, const void *W_down,
+                     const void *A_t, const void *B_t, float thld, const void *y)
+{
+    cd_status st = check_shape(d_model, d_ff, max_batch, d_rank);
+    if (st != CD_OK)
+        return st;
+    if (variant < CD_VARIANT_MONO || variant > CD_VARIANT_DENSE)
+        return CD_EINVAL;
+    if (B < 1 || B > max_batch)
+        return CD_EINVAL;
+    if (std::isnan(thld))
+        return CD_EINVAL;
+    const void *req[] = {x, W_gate, W_up, W_down, y};
+    for (const void *p : req)
+        if (!p || !aligned16(p))
+            return CD_EINVAL;
+    if (variant == CD_VARIANT_DUAL_PRED) {
+        if (!A_t || !B_t || !aligned16(A_t) || !aligned16(B_t) || d_rank == 0)
+            return CD_EINVAL;
+    } else if (A_t || B_t) {
+        return CD_EINVAL;
+    }
+    return CD_OK;
+}
+
+cdk::CoefArgs coef_args(cd_plan *p, const uint16_t *x, int B, const uint16_t *Wg,
+                        const uint16_t *Wu, const uint16_t *Bt, float thld, float *y)
+{
+    cdk::CoefArgs a;
+    a.x = x;
+    a.nb = B;
+    a.Wg = Wg;
+    a.Wu = Wu;
+    a.Bt = Bt;
+    a.lat = p->lat;
+    a.d_model = p->d_model;
+    a.d_ff = p->d_ff;
+    a.d_rank = p->d_rank;
+    a.R = p->R;
+    a.thld = thld;
+    a.cnt = p->cnt;
+    a.lidx = p->lidx;
+    a.ls = p->ls;
+    a.ls_stride = p->ls_stride;
+    a.coef = p->coef;
+    a.y = y;
+    return a;
+}
+
+cdk::DownArgs down_args(cd_plan *p, int B, const uint16_t *Wd, float *y)
+{
+    cdk::DownArgs a;
+    a.cnt = p->cnt;
+    a.nblk = p->nblk;
+    a.R = p->R;
+    a.lidx = p->lidx;
+    a.ls = p->ls;
+    a.ls_stride = p->ls_stride;
+    a.nb = B;
+    a.Wd = Wd;
+    a.d_model = p->d_model;
+    a.d_ff = p->d_ff;
+    a.gc = p->gc;
+    a.gr = p->gr;
+    a.y = y;
+    a.idx_out = p->idx_out;
+    a.s_out = p->s_out;
+    a.n_out = p->n_out;
+    return a;
+}
+
+cd_status run_ffn(cd_plan *p, int variant, const uint16_t *x, int B, const uint16_t *Wg,
+                  const uint16_t *Wu, const uint16_t *Wd, const uint16_t *At, const uint16_t *Bt,
+                  float thld, float *y, void *stream)
+{
+    if (!p)
+        return CD_EINVAL;
+    cd_status st = check_args(variant, p->d_model, p->d_ff, p->max_batch, p->d_rank, x, B, Wg, Wu,
+                              Wd, At, Bt, thld, y);
+    if (st != CD_OK)
+        return st;
+    hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+    p->last_batch = B;
+    if (variant == CD_VARIANT_DUAL_PRED) {
+        st = timed_launch(p, CD_KERNEL_LATENT, s, [&] {
+            return cdk::launch_latent(x, B, At, p->d_model, p->d_rank, p->lat, s);
+        });
+        if (st != CD_OK)
+            return st;
+    }
+    const cdk::CoefArgs ca = coef_args(p, x, B, Wg, Wu, Bt, thld, y);
+    st = timed_launch(p, CD_KERNEL_COEF, s, [&] { return cdk::launch_coef(variant, ca, p->nblk, s); });
+    if (st != CD_OK)
+        return st;
+    const cdk::DownArgs da = down_args(p, B, Wd, y);
+    return timed_launch(p, CD_KERNEL_DOWN, s, [&] { return cdk::launch_down(da, s); });
+}
+
+template <class T>
+cd_status dalloc(T **ptr, size_t count)
+{
+    *ptr = nullptr;
+    if (count == 0)
+        return CD_OK;
+    const hipError_t e = hipMalloc(reinterpret_cast<void **>(ptr), count * sizeof(T));
+    if (e == hipSuccess)
+        return CD_OK;
+    *ptr = nullptr;
+    return e == hipErrorOutOfMemory ? CD_ENOMEM : CD_EHIP;
+}
+
+void release(cd_plan *p)
+{
+    void *bufs[] = {p->cnt, p->lidx, p->idx_out, p->n_out, p->ls, p->s_out, p->coef, p->lat};
+    for (void *b : bufs)
+        if (b)
+            (void)hipFree(b);
+    for (const Timed &t : p->timed) {
+        (void)hipEventDestroy(t.ev[0]);
+        (void)hipEventDestroy(t.ev[1]);
+    }
+    for (hipEvent_t e : p->pool)
+        (void)hipEventDestroy(e);
+    delete p;
+}
+
+}  // namespace
+
+extern "C" {
+
+int countdown_abi_version(void) { return COUNTDOWN_ABI_VERSION; }
+
+const char *countdown_status_string(cd_status st)
+{
+    switch (st) {
+    case CD_OK: return "CD_OK: success";
+    case CD_EINVAL: return "CD_EINVAL: invalid argument";
+    case CD_EUNSUPPORTED: return "CD_EUNSUPPORTED: shape not supported by the kernels";
+    case CD_EHIP: return "CD_EHIP: HIP runtime or launch failure";
+    case CD_ENOMEM: return "CD_ENOMEM: device allocation failed";
+    default: return "unknown countdown status";
+    }
+}
+
+cd_status countdown_check_shape(int d_model, int d_ff, int max_batch, int d_rank)
+{
+    return check_shape(d_model, d_ff, max_batch, d_rank);
+}
+
+cd_status countdown_check_args(int variant, int d_model, int d_ff, int max_batch, int d_rank,
+                               const void *x, int B, const void *W_gate, const void *W_up,
+                               const void *W_down, const void *A_t, const void *B_t, float thld,
+                               const void *y)
+{
+    return check_args(variant, d_model, d_ff, max_batch, d_rank, x, B, W_gate, W_up, W_down, A_t,
+                      B_t, thld, y);
+}
+
+cd_status countdown_plan_create(int d_model, int d_ff, int max_batch, int d_rank, unsigned flags,
+                                cd_plan **out)
+{
+    if (!out)
+        return CD_EINVAL;
+    cd_status st = check_shape(d_model, d_ff, max_batch, d_rank);
+    if (st != CD_OK)
+        return st;
+    if (flags & ~(CD_PLAN_KEEP_COEF | CD_PLAN_TIMING))
+        return CD_EINVAL;
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess)
+        return CD_EHIP;
+    cd_plan *p = new (std::nothrow) cd_plan();
+    if (!p)
+        return CD_ENOMEM;
+    p->d_model = d_model;
+    p->d_ff = d_ff;
+    p->max_batch = max_batch;
+    p->d_rank = d_rank;
+    p->flags = flags;
+    p->device = dev;
+    p->R = kDefaultRows;
+    if (const char *env = std::getenv("COUNTDOWN_ROWS_PER_BLOCK")) {
+        const int r = std::atoi(env);
+        if (r >= 4 && r <= 64 && r % 4 == 0)
+            p->R = r;
+    }
+    p->nblk = (d_ff + p->R - 1) / p->R;
+    p->ls_stride = p->nblk * p->R;
+    p->gc = (d_model + 511) / 512;
+    int gr = 512 / p->gc;
+    if (gr > d_ff / 16)
+        gr = d_ff / 16;
+    p->gr = gr < 1 ? 1 : gr;
+    const size_t mb = (size_t)max_batch;
+    st = dalloc(&p->cnt, (size_t)p->nblk);
+    if (st == CD_OK) st = dalloc(&p->lidx, (size_t)p->ls_stride);
+    if (st == CD_OK) st = dalloc(&p->ls, mb * p->ls_stride);
+    if (st == CD_OK) st = dalloc(&p->idx_out, (size_t)d_ff);
+    if (st == CD_OK) st = dalloc(&p->n_out, (size_t)1);
+    if (st == CD_OK) st = dalloc(&p->s_out, mb * d_ff);
+    if (st == CD_OK && (flags & CD_PLAN_KEEP_COEF)) st = dalloc(&p->coef, mb * d_ff);
+    if (st == CD_OK && d_rank > 0) st = dalloc(&p->lat, mb * d_rank);
+    if (st == CD_OK && hipMemset(p->n_out, 0, sizeof(int)) != hipSuccess) st = CD_EHIP;
+    if (st == CD_OK && hipMemset(p->cnt, 0, sizeof(int) * p->nblk) != hipSuccess) st = CD_EHIP;
+    if (st != CD_OK) {
+        release(p);
+        return st;
+    }
+    *out = p;
+    return CD_OK;
+}
+
+cd_status countdown_plan_destroy(cd_plan *plan)
+{
+    if (!plan)
+        return CD_OK;
+    const hipError_t e = hipDeviceSynchronize();
+    release(plan);
+    return hip_status(e);
+}
+
+cd_status countdown_ffn_mono(cd_plan *plan, const uint16_t *x, int B, const uint16_t *W_gate,
+                             const uint16_t *W_up, const uint16_t *W_down, float thld, float *y,
+                             void *stream)
+{
+    return run_ffn(plan, CD_VARIANT_MONO, x, B, W_gate, W_up, W_down, nullptr, nullptr, thld, y,
+                   stream);
+}
+
+cd_status countdown_ffn_dual(cd_plan *plan, const uint16_t *x, int B, const uint16_t *W_gate,
+                             const uint16_t *W_up, const uint16_t *W_down, const uint16_t *A_t,
+                             const uint16_t *B_t, float thld, float *y, void *stream)
+{
+    if (!plan)
+        return CD_EINVAL;
+    if ((A_t == nullptr) != (B_t == nullptr))
+        return CD_EINVAL;
+    const int variant = A_t ? CD_VARIANT_DUAL_PRED : CD_VARIANT_DUAL_IDEAL;
+    return run_ffn(plan, variant, x, B, W_gate, W_up, W_down, A_t, B_t, thld, y, stream);
+}
+
+cd_status countdown_ffn_dense(cd_plan *plan, const uint16_t *x, int B, const uint16_t *W_gate,
+                              const uint16_t *W_up, const uint16_t *W_down, float *y, void *stream)
+{
+    return run_ffn(plan, CD_VARIANT_DENSE, x, B, W_gate, W_up, W_down, nullptr, nullptr,
+                   -INFINITY, y, stream);
+}
+
+cd_status countdown_calibrate(cd_plan *p, int variant, const uint16_t *X, int T,
+                              const uint16_t *W_gate, const uint16_t *W_up, const uint16_t *A_t,
+                              const uint16_t *B_t, double k, float *thld_out, double *q_out,
+                              void *stream)
+{
+    if (!p || !X || !aligned16(X) || T < 1 || !thld_out || !(k >= 0.0 && k <= 1.0))
+        return CD_EINVAL;
+    if (variant != CD_VARIANT_MONO && variant != CD_VARIANT_DUAL_IDEAL &&
+        variant != CD_VARIANT_DUAL_PRED)
+        return CD_EINVAL;
+    const bool pred = variant == CD_VARIANT_DUAL_PRED;
+    if (pred) {
+        if (!A_t || !B_t || !aligned16(A_t) || !aligned16(B_t) || p->d_rank == 0)
+            return CD_EINVAL;
+    } else if (!W_up || !aligned16(W_up) ||
+               (variant == CD_VARIANT_DUAL_IDEAL && (!W_gate || !aligned16(W_gate)))) {
+        return CD_EINVAL;
+    }
+    hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+    const int tb = p->max_batch;
+    float *coef = nullptr, *ybuf = nullptr;
+    double *q = nullptr;
+    cd_status st = dalloc(&coef, (size_t)tb * p->d_ff);
+    if (st == CD_OK) st = dalloc(&ybuf, (size_t)tb * p->d_model);
+    if (st == CD_OK) st = dalloc(&q, (size_t)T);
+    // The coefficient kernels run with thld = +inf (no row active) and write
+    // the dense coefficient vector of up to max_batch tokens at a time.
+    const uint16_t *wg = W_gate ? W_gate : W_up;
+    for (int t0 = 0; st == CD_OK && t0 < T; t0 += tb) {
+        const int nb = T - t0 < tb ? T - t0 : tb;
+        const uint16_t *xb = X + (size_t)t0 * p->d_model;
+        if (pred) {
+            st = timed_launch(p, CD_KERNEL_LATENT, s, [&] {
+                return cdk::launch_latent(xb, nb, A_t, p->d_model, p->d_rank, p->lat, s);
+            });
+            if (st != CD_OK)
+                break;
+        }
+        cdk::CoefArgs a = coef_args(p, xb, nb, wg, W_up, B_t, INFINITY, ybuf);
+        a.coef = coef;
+        st = timed_launch(p, CD_KERNEL_COEF, s, [&] { return cdk::launch_coef(variant, a, p->nblk, s); });
+        if (st != CD_OK)
+            break;
+        st = timed_launch(p, CD_KERNEL_SELECT, s, [&] {
+            return cdk::launch_select(coef, p->d_ff, p->d_ff, nb, pred ? 0 : 1, k, q + t0, s);
+        });
+    }
+    if (st == CD_OK)
+        st = hip_status(cdk::launch_mean(q, T, thld_out, s));
+    if (st == CD_OK && q_out)
+        st = hip_status(hipMemcpyAsync(q_out, q, sizeof(double) * T, hipMemcpyDeviceToDevice, s));
+    const hipError_t se = hipStreamSynchronize(s);
+    if (st == CD_OK && se != hipSuccess)
+        st = CD_EHIP;
+    if (coef) (void)hipFree(coef);
+    if (ybuf) (void)hipFree(ybuf);
+    if (q) (void)hipFree(q);
+    return st;
+}
+
+cd_status countdown_last_active(const cd_plan *plan, const int32_t **idx, const int32_t **n_active,
+                                const float **s_c, const float **coef)
+{
+    if (!plan)
+        return CD_EINVAL;
+    if (idx) *idx = plan->idx_out;
+    if (n_active) *n_active = plan->n_out;
+    if (s_c) *s_c = plan->s_out;
+    if (coef) *coef = plan->coef;
+    return CD_OK;
+}
+
+cd_status countdown_copy_last_active(const cd_plan *p, int32_t *idx_dst, int32_t *n_dst,
+                                     float *s_dst, float *coef_dst, void *stream)
+{
+    if (!p || (coef_dst && !p->coef))
+        return CD_EINVAL;
+    hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+    const size_t nf = (size_t)p->last_batch * p->d_ff;
+    hipError_t e = hipSuccess;
+    if (idx_dst && e == hipSuccess)
+        e = hipMemcpyAsync(idx_dst, p->idx_out, sizeof(int32_t) * p->d_ff, hipMemcpyDeviceToDevice, s);
+    if (n_dst && e == hipSuccess)
+        e = hipMemcpyAsync(n_dst, p->n_out, sizeof(int32_t), hipMemcpyDeviceToDevice, s);
+    if (s_dst && nf && e == hipSuccess)
+        e = hipMemcpyAsync(s_dst, p->s_out, sizeof(float) * nf, hipMemcpyDeviceToDevice, s);
+    if (coef_dst && nf && e == hipSuccess)
+        e = hipMemcpyAsync(coef_dst, p->coef, sizeof(float) * nf, hipMemcpyDeviceToDevice, s);
+    return hip_status(e);
+}
+
+cd_status countdown_timing_collect(cd_plan *p, int *counts, double *ms)
+{
+    if (!p || !counts || !ms)
+        return CD_EINVAL;
+    for (int i = 0; i < CD_KERNEL_KINDS; ++i) {
+        counts[i] = 0;
+        ms[i] = 0.0;
+    }
+    cd_status st = CD_OK;
+    if (!p->timed.empty() && hipEventSynchronize(p->timed.back().ev[1]) != hipSuccess)
+        st = CD_EHIP;
+    for (const Timed &t : p->timed) {
+        float v = 0.0f;
+        if (st == CD_OK && hipEventElapsedTime(&v, t.ev[0], t.ev[1]) == hipSuccess &&
+            t.kind >= 0 && t.kind < CD_KERNEL_KINDS) {
+            counts[t.kind] += 1;
+            ms[t.kind] += v;
+        }
+        p->pool.push_back(t.ev[0]);
+        p->pool.push_back(t.ev[1]);
+    }
+    p->timed.clear();
+    return st;
+}
+
+}  // extern "C"

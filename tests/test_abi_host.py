@@ -1,0 +1,129 @@
+"""Host-side checks of the C ABI: the library loads, exports every symbol the
+header declares, and rejects bad arguments before touching a device."""
+import math
+import os
+import re
+import subprocess
+
+import pytest
+
+from paper_2505_17701_amd import binding as cd
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "countdown.h")
+
+
+@pytest.fixture(scope="module")
+def lib():
+    if not os.path.exists(cd.LIB_PATH):
+        from paper_2505_17701_amd import build
+
+        build.build()
+    return cd.load_library()
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(countdown_\w+)\s*\(", text)))
+
+
+def test_header_declarations_match_binding_list():
+    assert declared_functions() == sorted(cd.EXPORTS)
+
+
+def test_every_declared_symbol_is_exported(lib):
+    out = subprocess.run(["nm", "-D", "--defined-only", cd.LIB_PATH], capture_output=True,
+                         text=True, check=True).stdout
+    exported = set(re.findall(r"\bT (countdown_\w+)", out))
+    for name in declared_functions():
+        assert name in exported, name
+        assert getattr(lib, name) is not None
+
+
+def test_header_compiles_as_c():
+    src = f'#include "{HEADER}"\nint main(void) {{ return countdown_abi_version() == 0; }}\n'
+    res = subprocess.run(["gcc", "-x", "c", "-std=c99", "-Wall", "-Werror", "-fsyntax-only", "-"],
+                         input=src, text=True, capture_output=True)
+    assert res.returncode == 0, res.stderr
+
+
+def test_abi_version_and_status_strings(lib):
+    assert cd.countdown_abi_version() == 1
+    for st in (cd.CD_OK, cd.CD_EINVAL, cd.CD_EUNSUPPORTED, cd.CD_EHIP, cd.CD_ENOMEM):
+        assert cd.status_string(st).startswith(("CD_OK", "CD_E"))
+    assert "unknown" in cd.status_string(12345)
+
+
+@pytest.mark.parametrize("shape,expect", [
+    ((4096, 11008, 1, 0), cd.CD_OK),
+    ((8192, 28672, 4, 0), cd.CD_OK),
+    ((256, 688, 1, 0), cd.CD_OK),
+    ((4096, 14336, 8, 256), cd.CD_OK),
+    ((4100, 11008, 1, 0), cd.CD_EINVAL),        # d_model % 8
+    ((4096, 11004, 1, 0), cd.CD_EINVAL),        # d_ff % 8
+    ((0, 11008, 1, 0), cd.CD_EINVAL),
+    ((16384, 11008, 1, 0), cd.CD_EUNSUPPORTED),  # d_model > 8192
+    ((4096, 11008, 0, 0), cd.CD_EINVAL),
+    ((4096, 11008, 9, 0), cd.CD_EUNSUPPORTED),
+    ((8192, 28672, 8, 0), cd.CD_EUNSUPPORTED),   # batch x d_model > 32768
+    ((4096, 14336, 1, 200), cd.CD_EUNSUPPORTED), # rank not a power of two
+    ((4096, 14336, 1, -8), cd.CD_EINVAL),
+])
+def test_check_shape(lib, shape, expect):
+    assert cd.countdown_check_shape(*shape) == expect
+
+
+GOOD = dict(x=0x1000, W_gate=0x2000, W_up=0x3000, W_down=0x4000, y=0x5000)
+
+
+def check(variant=cd.CD_VARIANT_MONO, B=1, thld=1.0, A_t=None, B_t=None, d_rank=0, **kw):
+    p = dict(GOOD)
+    p.update(kw)
+    return cd.countdown_check_args(variant, 4096, 11008, 4, d_rank, p["x"], B, p["W_gate"],
+                                   p["W_up"], p["W_down"], A_t, B_t, thld, p["y"])
+
+
+def test_check_args_accepts_good_calls(lib):
+    assert check() == cd.CD_OK
+    assert check(B=4, thld=-math.inf) == cd.CD_OK
+    assert check(thld=math.inf) == cd.CD_OK
+    assert check(cd.CD_VARIANT_DUAL_IDEAL) == cd.CD_OK
+    assert check(cd.CD_VARIANT_DENSE) == cd.CD_OK
+    assert check(cd.CD_VARIANT_DUAL_PRED, A_t=0x6000, B_t=0x7000, d_rank=256) == cd.CD_OK
+
+
+@pytest.mark.parametrize("bad", [
+    dict(x=None), dict(W_gate=None), dict(W_up=None), dict(W_down=None), dict(y=None),
+    dict(x=0x1002), dict(W_up=0x3008), dict(y=0x5004),            # not 16-byte aligned
+    dict(B=0), dict(B=5), dict(thld=math.nan),
+])
+def test_check_args_rejects(lib, bad):
+    assert check(**bad) == cd.CD_EINVAL
+
+
+def test_predictor_pointer_rules(lib):
+    pred = cd.CD_VARIANT_DUAL_PRED
+    assert check(pred, A_t=0x6000, B_t=None, d_rank=256) == cd.CD_EINVAL
+    assert check(pred, A_t=None, B_t=0x7000, d_rank=256) == cd.CD_EINVAL
+    assert check(pred, A_t=0x6000, B_t=0x7000, d_rank=0) == cd.CD_EINVAL
+    assert check(pred, A_t=0x6004, B_t=0x7000, d_rank=256) == cd.CD_EINVAL
+    assert check(cd.CD_VARIANT_MONO, A_t=0x6000, B_t=0x7000, d_rank=256) == cd.CD_EINVAL
+
+
+def test_null_plan_is_rejected_without_device(lib):
+    assert lib.countdown_ffn_mono(None, 0x1000, 1, 0x2000, 0x3000, 0x4000, 1.0, 0x5000,
+                                  None) == cd.CD_EINVAL
+    assert lib.countdown_ffn_dual(None, 0x1000, 1, 0x2000, 0x3000, 0x4000, None, None, 1.0,
+                                  0x5000, None) == cd.CD_EINVAL
+    assert lib.countdown_plan_destroy(None) == cd.CD_OK
+    assert lib.countdown_timing_collect(None, None, None) == cd.CD_EINVAL
+
+
+def test_plan_create_rejects_bad_sizes_before_any_hip_call(lib):
+    import ctypes as C
+
+    h = C.c_void_p()
+    assert lib.countdown_plan_create(4100, 11008, 1, 0, 0, C.byref(h)) == cd.CD_EINVAL
+    assert lib.countdown_plan_create(4096, 11008, 1, 0, 0x80, C.byref(h)) == cd.CD_EINVAL
+    assert h.value is None

@@ -1,0 +1,68 @@
+"""GPU parity at the full workload shapes, in the launch configuration the
+bench times (one plan per shape, max_batch = the workload's largest batch)."""
+import numpy as np
+import pytest
+
+from workloads import WORKLOADS
+
+from test_gpu_parity import Layer, calibrated, compare, plan_for
+
+torch = pytest.importorskip("torch")
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+
+
+@pytest.fixture(scope="module")
+def llama7b():
+    w = WORKLOADS["llama7b_4096x11008"]
+    return w, Layer(w.layer())
+
+
+@pytest.mark.parametrize("variant", ["mono", "dual_ideal"])
+@pytest.mark.parametrize("k", [0.9, 0.5])
+def test_llama7b_layer(llama7b, variant, k):
+    w, layer = llama7b
+    thld = calibrated(variant, layer, w.wid, k, T=32, outlier_frac=w.outlier_frac)
+    plan = plan_for(layer)
+    X = w.tokens(3)
+    for t in range(3):
+        n, flips, rel = compare(plan, variant, layer, X[t:t + 1], thld,
+                                f"7b {variant} k={k} tok{t}")
+        assert abs(n / w.d_ff - (1 - k)) < 0.15, n
+        print(f"7b {variant} k={k} tok{t}: n={n} flips={flips} rel_err={rel:.2e}", flush=True)
+
+
+@pytest.fixture(scope="module")
+def llama3_pred():
+    w = WORKLOADS["llama3_8b_4096x14336_pred"]
+    return w, Layer(w.layer(), w.predictor())
+
+
+@pytest.mark.parametrize("B", [1, 4, 8])
+def test_llama3_predictor_batch_union(llama3_pred, B):
+    w, layer = llama3_pred
+    thld = calibrated("dual_pred", layer, w.wid, 0.9, T=32)
+    plan = plan_for(layer, max_batch=8)
+    X = w.tokens(B)
+    n, flips, rel = compare(plan, "dual_pred", layer, X, thld, f"8b pred B={B}")
+    expect = 1 - 0.9 ** B
+    assert abs(n / w.d_ff - expect) < 0.1, (n, expect)
+    print(f"8b pred B={B}: n={n} flips={flips} rel_err={rel:.2e}", flush=True)
+
+
+@pytest.mark.parametrize("k", [0.9])
+def test_llama70b_layer(k):
+    w = WORKLOADS["llama70b_8192x28672"]
+    layer = Layer(w.layer())
+    thld = calibrated("mono", layer, w.wid, k, T=8)
+    plan = plan_for(layer)
+    n, flips, rel = compare(plan, "mono", layer, w.tokens(1), thld, f"70b mono k={k}")
+    print(f"70b mono k={k}: n={n} flips={flips} rel_err={rel:.2e}", flush=True)
+    compare(plan, "dense", layer, w.tokens(1), 0.0, "70b dense", check_coef=False)
+    del layer
+    torch.cuda.empty_cache()

@@ -1,0 +1,323 @@
+"""GPU parity: the HIP path (through the C ABI) against the fp64 oracle.
+
+Same seeded inputs on both sides; IDX compared exactly except for neurons
+within the relative band of thld, y compared against the oracle evaluated
+on the GPU's IDX (a flipped boundary neuron moves y by more than the y
+tolerance, so the y check is made on the set the GPU actually used), the
+compact coefficients against the oracle's, and the dense coefficient
+vector against the oracle within an fp32 dot-product bound.
+"""
+import math
+
+import numpy as np
+import pytest
+
+from workloads import WORKLOADS, bf16_to_f32, make_layer, make_predictor, make_tokens
+from workloads.synth import T_CALIB
+
+from gpu_support import (COEF_TOL, check_idx, check_s, check_y, coef_max, dev_bf16, dot_bound)
+
+torch = pytest.importorskip("torch")
+pytestmark = pytest.mark.gpu
+
+import oracle  # noqa: E402
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    from paper_2505_17701_amd import binding
+
+    binding.load_library()
+    torch.cuda.set_device(0)
+
+
+def f64(a):
+    return bf16_to_f32(a).astype(np.float64)
+
+
+class Layer:
+    """A layer's weights on host (bf16 bits) and device."""
+
+    def __init__(self, L, P=None):
+        self.h = dict(L)
+        if P:
+            self.h.update(P)
+        self.d = {k: dev_bf16(v) for k, v in self.h.items()}
+        self.d_ff, self.d_model = self.h["W_up"].shape
+        self.d_rank = self.h["A_t"].shape[0] if P else 0
+
+
+def run_gpu(plan, variant, layer, x, thld):
+    from paper_2505_17701_amd import binding as cd
+
+    xd = dev_bf16(x)
+    D = layer.d
+    if variant == "mono":
+        y = cd.countdown_ffn_mono(plan, xd, D["W_gate"], D["W_up"], D["W_down"], thld)
+    elif variant == "dual_ideal":
+        y = cd.countdown_ffn_dual(plan, xd, D["W_gate"], D["W_up"], D["W_down"], thld)
+    elif variant == "dual_pred":
+        y = cd.countdown_ffn_dual(plan, xd, D["W_gate"], D["W_up"], D["W_down"], thld,
+                                  A_t=D["A_t"], B_t=D["B_t"])
+    elif variant == "dense":
+        y = cd.countdown_ffn_dense(plan, xd, D["W_gate"], D["W_up"], D["W_down"])
+    else:
+        raise ValueError(variant)
+    idx, s_c, coef = cd.countdown_copy_last_active(plan)
+    return (y.cpu().numpy().astype(np.float64), idx.cpu().numpy(), s_c.cpu().numpy(),
+            None if coef is None else coef.cpu().numpy())
+
+
+def run_oracle(variant, layer, x, thld):
+    H = layer.h
+    if variant == "mono":
+        return oracle.ffn_mono(x, H["W_gate"], H["W_up"], H["W_down"], thld, want_coef=True)
+    if variant == "dual_ideal":
+        return oracle.ffn_dual_ideal(x, H["W_gate"], H["W_up"], H["W_down"], thld, want_coef=True)
+    if variant == "dual_pred":
+        return oracle.ffn_dual_pred(x, H["W_gate"], H["W_up"], H["W_down"], H["A_t"], H["B_t"],
+                                    thld, want_coef=True)
+    if variant == "dense":
+        idx = np.arange(layer.d_ff, dtype=np.int32)
+        return idx, oracle.dense(x, H["W_gate"], H["W_up"], H["W_down"]), None
+    raise ValueError(variant)
+
+
+def compare(plan, variant, layer, x, thld, label, check_coef=True):
+    """Full parity check of one call; returns (n_active_gpu, n_flips, y_rel_err)."""
+    x = np.atleast_2d(x)
+    y_g, idx_g, s_g, coef_g = run_gpu(plan, variant, layer, x, thld)
+    idx_o, y_o, coef_o = run_oracle(variant, layer, x, thld)
+    H = layer.h
+    if variant == "dense":
+        np.testing.assert_array_equal(idx_g, np.arange(layer.d_ff))
+        flips = 0
+    else:
+        flips = check_idx(idx_g, idx_o, coef_max(variant, coef_o), thld, label)
+    # y and s on the GPU's own index set
+    y_on, s_on = oracle.ffn_on_idx(x, H["W_gate"], H["W_up"], H["W_down"], idx_g)
+    rel = check_y(y_g, y_on, label)
+    if flips == 0 and variant != "dense":
+        check_y(y_g, y_o, label + " (oracle IDX)")
+    check_s(s_g, s_on, label)
+    if check_coef and coef_g is not None and coef_o is not None:
+        xf = f64(x)
+        if variant == "mono":
+            bound = COEF_TOL * dot_bound(xf, f64(H["W_up"]))
+        elif variant == "dual_ideal":
+            u, g, _ = oracle.coefficients(x, H["W_gate"], H["W_up"])
+            su = np.array([[oracle.silu(v) for v in row] for row in g]) if g.size < 5000 else \
+                g / (1.0 + np.exp(-g))
+            bound = COEF_TOL * (dot_bound(xf, f64(H["W_up"])) * np.abs(su)
+                                + np.abs(u) * dot_bound(xf, f64(H["W_gate"])))
+        else:
+            lat = oracle.predictor(x, H["A_t"], H["B_t"])[0]
+            bound = COEF_TOL * (np.abs(lat) @ np.abs(f64(H["B_t"])).T
+                                + dot_bound(xf, f64(H["A_t"])) @ np.abs(f64(H["B_t"])).T)
+        err = np.abs(coef_g[: x.shape[0]] - coef_o)
+        assert np.all(err <= bound + 1e-30), f"{label}: coefficient error {err.max():.3e}"
+    return len(idx_g), flips, rel
+
+
+def plan_for(layer, max_batch=1, keep_coef=True, timing=False):
+    from paper_2505_17701_amd import binding as cd
+
+    return cd.Plan(layer.d_model, layer.d_ff, max_batch, layer.d_rank, keep_coef=keep_coef,
+                   timing=timing)
+
+
+def calibrated(variant, layer, wid, k, T=32, outlier_frac=0.0):
+    X = make_tokens(wid, T, layer.d_model, purpose=T_CALIB, outlier_frac=outlier_frac)
+    H = layer.h
+    t, _ = oracle.calibrate(variant, X, k, W_gate=H["W_gate"], W_up=H["W_up"],
+                            A_t=H.get("A_t"), B_t=H.get("B_t"))
+    return float(np.float32(t))
+
+
+# --------------------------------------------------------------- small shapes
+
+@pytest.fixture(scope="module")
+def tiny():
+    w = WORKLOADS["tiny_256x688"]
+    return w, Layer(w.layer())
+
+
+@pytest.mark.parametrize("variant", ["mono", "dual_ideal"])
+def test_tiny_parity_calibrated(tiny, variant):
+    w, layer = tiny
+    thld = calibrated(variant, layer, w.wid, 0.9, T=64)
+    plan = plan_for(layer)
+    X = w.tokens(16)
+    for t in range(16):
+        n, flips, _ = compare(plan, variant, layer, X[t:t + 1], thld, f"tiny {variant} tok{t}")
+        assert 20 < n < 140
+
+
+@pytest.mark.parametrize("variant", ["mono", "dual_ideal"])
+@pytest.mark.parametrize("B", [2, 3, 5, 8])
+def test_tiny_batch_union(tiny, variant, B):
+    w, layer = tiny
+    thld = calibrated(variant, layer, w.wid, 0.9, T=64)
+    plan = plan_for(layer, max_batch=8)
+    X = w.tokens(B)
+    n, _, _ = compare(plan, variant, layer, X, thld, f"tiny {variant} B={B}")
+    assert n > 69
+
+
+@pytest.mark.parametrize("variant", ["mono", "dual_ideal"])
+def test_all_rows_equals_dense_and_none_gives_zero(tiny, variant):
+    w, layer = tiny
+    plan = plan_for(layer, max_batch=2)
+    X = w.tokens(2)
+    n, _, _ = compare(plan, variant, layer, X, -math.inf, f"{variant} -inf")
+    assert n == layer.d_ff
+    y_all = run_gpu(plan, variant, layer, X, -math.inf)[0]
+    y_dense = run_gpu(plan, "dense", layer, X, 0.0)[0]
+    np.testing.assert_allclose(y_all, y_dense, rtol=0, atol=1e-5 * np.abs(y_dense).max())
+    y0, idx0, _, _ = run_gpu(plan, variant, layer, X, math.inf)
+    assert len(idx0) == 0 and np.all(y0 == 0.0)
+
+
+def test_dense_parity(tiny):
+    w, layer = tiny
+    plan = plan_for(layer, max_batch=4)
+    compare(plan, "dense", layer, w.tokens(4), 0.0, "dense")
+
+
+def test_single_active_row(tiny):
+    w, layer = tiny
+    x = w.tokens(1)
+    u = oracle.coefficients(x, layer.h["W_gate"], layer.h["W_up"])[0][0]
+    top = np.sort(np.abs(u))
+    thld = float(np.float32((top[-1] + top[-2]) / 2))
+    plan = plan_for(layer)
+    n, flips, _ = compare(plan, "mono", layer, x, thld, "single row")
+    assert n == 1 and flips == 0
+
+
+@pytest.mark.parametrize("d_model,d_ff,B", [(264, 1000, 3), (1032, 520, 2), (8, 8, 1),
+                                            (2056, 4104, 7), (512, 16, 4)])
+@pytest.mark.parametrize("variant", ["mono", "dual_ideal", "dual_pred"])
+def test_ragged_shapes(d_model, d_ff, B, variant):
+    L = make_layer(700 + d_model, d_model, d_ff, 0.05)
+    P = make_predictor(700 + d_model, d_model, 16, d_ff, 0.05) if variant == "dual_pred" else None
+    layer = Layer(L, P)
+    x = make_tokens(700 + d_model, B, d_model)
+    if variant == "dual_pred":
+        c = oracle.predictor(x, P["A_t"], P["B_t"])[1]
+    else:
+        u, g, s = oracle.coefficients(x, L["W_gate"], L["W_up"])
+        c = np.abs(u if variant == "mono" else s)
+    thld = float(np.float32(np.quantile(c, 0.7)))
+    plan = plan_for(layer, max_batch=8)
+    compare(plan, variant, layer, x, thld, f"ragged {d_model}x{d_ff} B={B} {variant}")
+
+
+def test_plan_reuse_with_shrinking_batch(tiny):
+    w, layer = tiny
+    thld = calibrated("mono", layer, w.wid, 0.9, T=64)
+    plan = plan_for(layer, max_batch=8)
+    for B in (8, 3, 1, 5):
+        compare(plan, "mono", layer, w.tokens(B), thld, f"reuse B={B}")
+
+
+def test_nondefault_stream_and_repeatability(tiny):
+    from paper_2505_17701_amd import binding as cd
+
+    w, layer = tiny
+    thld = calibrated("dual_ideal", layer, w.wid, 0.9, T=64)
+    plan = plan_for(layer, max_batch=2, keep_coef=False)
+    X = dev_bf16(w.tokens(2))
+    D = layer.d
+    s = torch.cuda.Stream()
+    with torch.cuda.stream(s):
+        y1 = cd.countdown_ffn_dual(plan, X, D["W_gate"], D["W_up"], D["W_down"], thld)
+        i1 = cd.countdown_copy_last_active(plan)[0].clone()
+        y2 = cd.countdown_ffn_dual(plan, X, D["W_gate"], D["W_up"], D["W_down"], thld)
+        i2 = cd.countdown_copy_last_active(plan)[0].clone()
+    s.synchronize()
+    assert torch.equal(i1, i2)
+    torch.testing.assert_close(y1, y2, rtol=0, atol=1e-6 * float(y1.abs().max()))
+
+
+def test_timing_records_every_launch(tiny):
+    from paper_2505_17701_amd import binding as cd
+
+    w, layer = tiny
+    plan = plan_for(layer, timing=True, keep_coef=False)
+    X = dev_bf16(w.tokens(1))
+    D = layer.d
+    for _ in range(5):
+        cd.countdown_ffn_mono(plan, X, D["W_gate"], D["W_up"], D["W_down"], 0.5)
+    t = cd.countdown_timing_collect(plan)
+    assert t["coef"][0] == 5 and t["down"][0] == 5 and t["latent"][0] == 0
+    assert t["coef"][1] > 0 and t["down"][1] > 0
+    assert cd.countdown_timing_collect(plan)["coef"][0] == 0
+
+
+def test_bad_calls_raise(tiny):
+    from paper_2505_17701_amd import binding as cd
+
+    w, layer = tiny
+    plan = plan_for(layer, max_batch=2)
+    D = layer.d
+    X = dev_bf16(w.tokens(3))
+    with pytest.raises(cd.CountdownError):
+        cd.countdown_ffn_mono(plan, X, D["W_gate"], D["W_up"], D["W_down"], 0.5)  # B > max_batch
+    with pytest.raises(cd.CountdownError):
+        cd.countdown_ffn_mono(plan, X[:1], D["W_gate"], D["W_up"], D["W_down"], float("nan"))
+    with pytest.raises(cd.CountdownError):
+        cd.countdown_ffn_dual(plan, X[:1], D["W_gate"], D["W_up"], D["W_down"], 0.5,
+                              A_t=D["W_up"], B_t=None)
+
+
+# ------------------------------------------------------------- calibration
+
+@pytest.mark.parametrize("variant", ["mono", "dual_ideal", "dual_pred"])
+def test_calibration_matches_oracle(variant):
+    from paper_2505_17701_amd import binding as cd
+
+    dm, dff = 512, 1376
+    L = make_layer(811, dm, dff, 0.02)
+    P = make_predictor(811, dm, 64, dff, 0.02) if variant == "dual_pred" else None
+    layer = Layer(L, P)
+    X = make_tokens(811, 20, dm, purpose=T_CALIB)
+    t_o, q_o = oracle.calibrate(variant, X, 0.9, W_gate=L["W_gate"], W_up=L["W_up"],
+                                A_t=P and P["A_t"], B_t=P and P["B_t"])
+    plan = cd.Plan(dm, dff, 8, layer.d_rank, keep_coef=True)
+    v = {"mono": cd.CD_VARIANT_MONO, "dual_ideal": cd.CD_VARIANT_DUAL_IDEAL,
+         "dual_pred": cd.CD_VARIANT_DUAL_PRED}[variant]
+    D = layer.d
+    thld, q = cd.countdown_calibrate(plan, v, dev_bf16(X), 0.9, W_gate=D["W_gate"], W_up=D["W_up"],
+                                     A_t=D.get("A_t"), B_t=D.get("B_t"))
+    q = q.cpu().numpy()
+    np.testing.assert_allclose(q, q_o, rtol=2e-5)
+    assert abs(float(thld.item()) - t_o) <= 2e-5 * abs(t_o)
+    assert float(thld.item()) == float(np.float32(q.mean()))  # fp64 mean, fp32 rounding
+
+
+def test_calibration_selects_exact_order_statistics():
+    """On the GPU's own fp32 coefficients the per-token quantile is exactly the
+    linear interpolation between the order statistics (numpy sort)."""
+    from paper_2505_17701_amd import binding as cd
+
+    dm, dff = 256, 688
+    L = make_layer(812, dm, dff, 0.02)
+    layer = Layer(L)
+    X = make_tokens(812, 6, dm, purpose=T_CALIB)
+    plan = cd.Plan(dm, dff, 8, 0, keep_coef=True)
+    D = layer.d
+    for k in (0.0, 0.5, 0.9, 0.999, 1.0):
+        _, q = cd.countdown_calibrate(plan, cd.CD_VARIANT_MONO, dev_bf16(X), k, W_up=D["W_up"])
+        y = cd.countdown_ffn_mono(plan, dev_bf16(X), D["W_gate"], D["W_up"], D["W_down"],
+                                  math.inf)
+        coef = cd.countdown_copy_last_active(plan)[2].cpu().numpy().astype(np.float64)
+        for t in range(6):
+            v = np.sort(np.abs(coef[t]))
+            h = k * (dff - 1)
+            lo = min(int(math.floor(h)), dff - 1)
+            hi = min(lo + 1, dff - 1)
+            assert q[t].item() == v[lo] + (h - lo) * (v[hi] - v[lo])
+        del y

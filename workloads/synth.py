@@ -43,14 +43,23 @@ def bf16_round(a) -> np.ndarray:
     """fp32 -> bf16 bit patterns (uint16), round to nearest, ties to even.
 
     NaN stays NaN (quietened); +-inf and overflow to inf follow IEEE rounding.
+    Works in uint32 (no finite pattern overflows: the largest, -inf, is
+    0xFF800000) over row chunks so that large matrices need little scratch.
     """
-    b = np.ascontiguousarray(a, dtype=np.float32).view(np.uint32).astype(np.uint64)
-    lsb = (b >> np.uint64(16)) & np.uint64(1)
-    r = ((b + np.uint64(0x7FFF) + lsb) >> np.uint64(16)).astype(np.uint16)
-    nan = (b & np.uint64(0x7FFFFFFF)) > np.uint64(0x7F800000)
-    if nan.any():
-        r[nan] = ((b[nan] >> np.uint64(16)) | np.uint64(0x40)).astype(np.uint16)
-    return r
+    a = np.ascontiguousarray(a, dtype=np.float32)
+    flat = a.reshape(-1).view(np.uint32)
+    out = np.empty(flat.shape, dtype=np.uint16)
+    step = 1 << 24
+    for lo in range(0, flat.size, step):
+        b = flat[lo:lo + step]
+        nan = (b & np.uint32(0x7FFFFFFF)) > np.uint32(0x7F800000)
+        r = b + (np.uint32(0x7FFF) + ((b >> np.uint32(16)) & np.uint32(1)))
+        r >>= np.uint32(16)
+        o = r.astype(np.uint16)
+        if nan.any():
+            o[nan] = ((b[nan] >> np.uint32(16)) | np.uint32(0x40)).astype(np.uint16)
+        out[lo:lo + step] = o
+    return out.reshape(a.shape)
 
 
 def bf16_to_f32(u16) -> np.ndarray:
