@@ -57,7 +57,7 @@ def parse():
 
 
 def time_steps(fn, steps, warmup, stream):
-    """Warm up, then time exactly `steps` calls between two synchronisations."""
+    """Warm up, then time exactly `steps` eager calls between two synchronisations."""
     import torch
 
     for i in range(warmup):
@@ -71,6 +71,31 @@ def time_steps(fn, steps, warmup, stream):
     t1.record(stream)
     torch.cuda.synchronize()
     return t0.elapsed_time(t1) / steps  # ms per step
+
+
+def time_steps_graph(fn, steps, warmup):
+    """Warm up eagerly, capture exactly `steps` calls into one HIP graph, replay it once
+    untimed and once timed between two synchronisations."""
+    import torch
+
+    for i in range(warmup):
+        fn(i)
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        for i in range(steps):
+            fn(i)
+    g.replay()
+    torch.cuda.synchronize()
+    t0 = torch.cuda.Event(enable_timing=True)
+    t1 = torch.cuda.Event(enable_timing=True)
+    t0.record()
+    g.replay()
+    t1.record()
+    torch.cuda.synchronize()
+    ms = t0.elapsed_time(t1) / steps
+    del g
+    return ms
 
 
 def main():
@@ -141,7 +166,8 @@ def main():
 
     def measure(variant, k, steps, warmup):
         plan = cd.Plan(dm, dff, max_batch=1)
-        ms = time_steps(make_step(plan, variant, k), steps, warmup, stream)
+        ms_eager = time_steps(make_step(plan, variant, k), steps, warmup, stream)
+        ms = time_steps_graph(make_step(plan, variant, k), steps, warmup)
         plan.close()
         # second pass: per-kernel durations (event pair around each launch) and n_active
         tplan = cd.Plan(dm, dff, max_batch=1, timing=True)
@@ -155,14 +181,15 @@ def main():
         lib = cd.load_library()
         for i in range(nsteps):
             step(i)
-            lib.countdown_copy_last_active(tplan.handle, None, n_arr[i:i + 1].data_ptr(), None,
-                                           None, stream.cuda_stream)
+            lib.countdown_export_active(tplan.handle, None, n_arr[i:i + 1].data_ptr(), None,
+                                        None, stream.cuda_stream)
         torch.cuda.synchronize()
         kt = cd.countdown_timing_collect(tplan)
         tplan.close()
         n = n_arr.cpu().numpy().astype(np.float64)
         per = [traffic.algorithmic_bytes(variant, dm, dff, int(v)) for v in n]
         res = {"ms_per_step": ms, "us_per_layer": ms * 1e3, "tokens_per_s": 1e3 / ms,
+               "us_per_layer_eager": ms_eager * 1e3,
                "n_active_mean": float(n.mean()), "realised_sparsity": float(1 - n.mean() / dff)}
         tot_bytes = float(np.mean([p["total"] for p in per]))
         res["algorithmic_bytes"] = tot_bytes
@@ -188,7 +215,8 @@ def main():
                 continue
             r = measure(variant, k, max(200, args.steps // 4), 50)
             extra[f"{variant}" + ("" if k is None else f"@k={k}")] = {
-                kk: r[kk] for kk in ("us_per_layer", "tokens_per_s", "achieved_GBs",
+                kk: r[kk] for kk in ("us_per_layer", "us_per_layer_eager", "tokens_per_s",
+                                     "achieved_GBs",
                                      "frac_hbm_peak", "n_active_mean", "coef_kernel_us",
                                      "down_kernel_us") if kk in r}
             log(f"[bench] {variant} k={k}: {json.dumps(extra[list(extra)[-1]])}")
@@ -237,6 +265,8 @@ def main():
         "warmup": args.warmup,
         "ms_per_step": main_res["ms_per_step"],
         "us_per_layer": main_res["us_per_layer"],
+        "us_per_layer_eager": main_res["us_per_layer_eager"],
+        "launch": "one HIP graph of exactly `steps` layer calls, replayed once (timed)",
         "achieved_GBs": main_res["achieved_GBs"],
         "frac_hbm_peak": main_res["frac_hbm_peak"],
         "higher_is_better": True,

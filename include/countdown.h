@@ -69,8 +69,8 @@ typedef struct cd_plan cd_plan;
 
 /*
  * Create a plan for one FFN shape. Allocates the plan's device workspace
- * (per-block active lists, compacted IDX, coefficients) on the current
- * device. d_model and d_ff must be positive multiples of 8 with
+ * (per-block active counts and (neuron, s) lists, the predictor latent and,
+ * with CD_PLAN_KEEP_COEF, the dense coefficients) on the current device. d_model and d_ff must be positive multiples of 8 with
  * d_model <= 8192; 1 <= max_batch <= 8; d_rank is 0 (no predictor) or a
  * power of two in [8, 1024]; max_batch * d_model <= 32768. Returns CD_EINVAL
  * for malformed sizes and CD_EUNSUPPORTED for well-formed sizes beyond those
@@ -128,25 +128,19 @@ cd_status countdown_calibrate(cd_plan *plan, int variant, const uint16_t *X, int
                               void *stream);
 
 /*
- * Device views of the last call's results on this plan (valid after that
- * call's stream work completes, until the next call): idx [d_ff] int32 holds
- * the ascending IDX in its first *n_active entries; n_active [1] int32;
- * s_c [max_batch][d_ff] fp32 holds s_b[IDX[j]] at s_c[b * d_ff + j];
- * coef [max_batch][d_ff] fp32 the dense coefficient vector (NULL unless the
- * plan has CD_PLAN_KEEP_COEF). Any output pointer may be NULL.
+ * Export the last FFN call's index set on `stream` into caller-owned DEVICE
+ * buffers (any destination may be NULL): idx_dst int32[d_ff] receives the
+ * ascending IDX in its first |IDX| entries, n_dst int32[1] receives |IDX|,
+ * s_dst fp32[B][d_ff] receives s_b[IDX[j]] at s_dst[b * d_ff + j], and
+ * coef_dst fp32[B][d_ff] the dense coefficient vector of every neuron (u for
+ * mono, s for dual ideal and dense, s_hat for dual pred; CD_PLAN_KEEP_COEF
+ * plans only, else CD_EINVAL). B is the batch of that call. The hot path
+ * keeps the active set as per-block lists; this call runs a small kernel
+ * that scans them. CD_EINVAL before the plan's first FFN call and after
+ * countdown_calibrate (which reuses the workspace).
  */
-cd_status countdown_last_active(const cd_plan *plan, const int32_t **idx,
-                                const int32_t **n_active, const float **s_c, const float **coef);
-
-/*
- * Enqueue device-to-device copies of the last call's results into
- * caller-owned DEVICE buffers on `stream` (any destination may be NULL):
- * idx_dst int32[d_ff], n_dst int32[1], s_dst fp32[B_last * d_ff] (the s_c
- * layout above), coef_dst fp32[B_last * d_ff] (CD_PLAN_KEEP_COEF plans only,
- * else CD_EINVAL). B_last is the batch of the last FFN call on the plan.
- */
-cd_status countdown_copy_last_active(const cd_plan *plan, int32_t *idx_dst, int32_t *n_dst,
-                                     float *s_dst, float *coef_dst, void *stream);
+cd_status countdown_export_active(const cd_plan *plan, int32_t *idx_dst, int32_t *n_dst,
+                                  float *s_dst, float *coef_dst, void *stream);
 
 /*
  * Kernel timing of a CD_PLAN_TIMING plan: waits for the recorded launches,
@@ -155,7 +149,7 @@ cd_status countdown_copy_last_active(const cd_plan *plan, int32_t *idx_dst, int3
  * counts / ms have CD_KERNEL_KINDS entries.
  */
 #define CD_KERNEL_COEF 0     /* coefficient / threshold / local compaction (+ gate or gate+up) */
-#define CD_KERNEL_DOWN 1     /* gathered down projection and IDX export */
+#define CD_KERNEL_DOWN 1     /* gathered down projection */
 #define CD_KERNEL_LATENT 2   /* predictor latent x.theta_A */
 #define CD_KERNEL_SELECT 3   /* calibration order statistics */
 #define CD_KERNEL_KINDS 4
@@ -180,7 +174,7 @@ cd_status countdown_check_shape(int d_model, int d_ff, int max_batch, int d_rank
 const char *countdown_status_string(cd_status status);
 
 /* ABI version of this header (bumped on any signature change). */
-#define COUNTDOWN_ABI_VERSION 1
+#define COUNTDOWN_ABI_VERSION 2
 int countdown_abi_version(void);
 
 #ifdef __cplusplus

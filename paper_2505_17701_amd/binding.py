@@ -23,8 +23,8 @@ KERNEL_NAMES = ("coef", "down", "latent", "select")
 # every symbol include/countdown.h declares
 EXPORTS = (
     "countdown_plan_create", "countdown_plan_destroy", "countdown_ffn_mono", "countdown_ffn_dual",
-    "countdown_ffn_dense", "countdown_calibrate", "countdown_last_active",
-    "countdown_copy_last_active", "countdown_timing_collect", "countdown_check_args",
+    "countdown_ffn_dense", "countdown_calibrate", "countdown_export_active",
+    "countdown_timing_collect", "countdown_check_args",
     "countdown_check_shape", "countdown_status_string", "countdown_abi_version",
 )
 
@@ -54,8 +54,7 @@ def load_library(path: str = LIB_PATH):
         "countdown_ffn_dual": (i, [vp, vp, i, vp, vp, vp, vp, vp, f, vp, vp]),
         "countdown_ffn_dense": (i, [vp, vp, i, vp, vp, vp, vp, vp]),
         "countdown_calibrate": (i, [vp, i, vp, i, vp, vp, vp, vp, d, vp, vp, vp]),
-        "countdown_last_active": (i, [vp, vp, vp, vp, vp]),
-        "countdown_copy_last_active": (i, [vp, vp, vp, vp, vp, vp]),
+        "countdown_export_active": (i, [vp, vp, vp, vp, vp, vp]),
         "countdown_timing_collect": (i, [vp, C.POINTER(i), C.POINTER(d)]),
         "countdown_check_args": (i, [i, i, i, i, i, vp, i, vp, vp, vp, vp, vp, f, vp]),
         "countdown_check_shape": (i, [i, i, i, i]),
@@ -210,11 +209,9 @@ def countdown_calibrate(plan: Plan, variant: int, X, k: float, W_gate=None, W_up
     return thld, q
 
 
-def countdown_copy_last_active(plan: Plan, stream=None):
-    """Copies of the last call's ``(IDX [n] int32, s_c [B, n] fp32, coef [B, d_ff] or None)``.
-
-    Synchronises the stream to read ``n``.
-    """
+def countdown_export_active(plan: Plan, stream=None):
+    """The last call's ``(IDX [n] int32, s_c [B, n] fp32, coef [B, d_ff] or None)`` as new
+    device tensors. Synchronises the stream to read ``n``."""
     import torch
 
     dev = torch.device("cuda", torch.cuda.current_device())
@@ -223,11 +220,10 @@ def countdown_copy_last_active(plan: Plan, stream=None):
     n = torch.empty(1, dtype=torch.int32, device=dev)
     s = torch.empty((B, plan.d_ff), dtype=torch.float32, device=dev)
     coef = torch.empty((B, plan.d_ff), dtype=torch.float32, device=dev) if plan.keep_coef else None
-    st = _stream(stream)
-    _check(load_library().countdown_copy_last_active(plan.handle, _ptr(idx), _ptr(n), _ptr(s),
-                                                     _ptr(coef), st), "countdown_copy_last_active")
-    torch.cuda.current_stream().synchronize() if stream is None else torch.cuda.synchronize()
-    m = int(n.item())
+    _check(load_library().countdown_export_active(plan.handle, _ptr(idx), _ptr(n), _ptr(s),
+                                                  _ptr(coef), _stream(stream)),
+           "countdown_export_active")
+    m = int(n.item())  # .item() synchronises with the copy's stream
     return idx[:m], s[:, :m], coef
 
 

@@ -16,9 +16,9 @@ namespace {
 constexpr int kMaxDModel = 8192;
 constexpr int kMaxBatch = 8;
 constexpr int kMaxRank = 1024;
-constexpr int kMaxBatchCols = 32768;   // max_batch * d_model (x staged in LDS)
-constexpr int kDefaultRows = 16;       // neurons per coefficient workgroup
+constexpr int kMaxBatchCols = 32768;  // max_batch * d_model (batch tiles of 4 and 8 stage x in LDS)
 constexpr int kMaxTimedLaunches = 1 << 16;
+constexpr int kDownWaves = 2048;      // target waves of the down kernel grid
 
 bool aligned16(const void *p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
 
@@ -35,11 +35,12 @@ struct cd_plan {
     int d_model, d_ff, max_batch, d_rank;
     unsigned flags;
     int device;
-    int R, nblk, ls_stride;
-    int last_batch;
-    int gc, gr;
-    int *cnt, *lidx, *idx_out, *n_out;
-    float *ls, *s_out, *coef, *lat;
+    int gc, gr, rows_per_group;   // down-kernel grid: column chunks x neuron groups
+    int last_batch;               // of the last FFN call (0 before the first)
+    int *act;                     // [d_ff] neuron in IDX
+    float *s;                     // [max_batch][d_ff] coefficients s of active neurons
+    float *coef;                  // [max_batch][d_ff] dense coefficients (CD_PLAN_KEEP_COEF)
+    float *lat;                   // [max_batch][d_rank] predictor latent
     std::vector<Timed> timed;     // recorded launches since the last collect
     std::vector<hipEvent_t> pool; // free events
 };
@@ -129,6 +130,9 @@ cd_status check_args(int variant, int d_model, int d_ff, int max_batch, int d_ra
     return CD_OK;
 }
 
+// CD_VARIANT_* and cdk::Variant share their numbering
+int kernel_variant(int variant) { return variant; }
+
 cdk::CoefArgs coef_args(cd_plan *p, const uint16_t *x, int B, const uint16_t *Wg,
                         const uint16_t *Wu, const uint16_t *Bt, float thld, float *y)
 {
@@ -142,12 +146,9 @@ cdk::CoefArgs coef_args(cd_plan *p, const uint16_t *x, int B, const uint16_t *Wg
     a.d_model = p->d_model;
     a.d_ff = p->d_ff;
     a.d_rank = p->d_rank;
-    a.R = p->R;
     a.thld = thld;
-    a.cnt = p->cnt;
-    a.lidx = p->lidx;
-    a.ls = p->ls;
-    a.ls_stride = p->ls_stride;
+    a.act = p->act;
+    a.s = p->s;
     a.coef = p->coef;
     a.y = y;
     return a;
@@ -156,22 +157,16 @@ cdk::CoefArgs coef_args(cd_plan *p, const uint16_t *x, int B, const uint16_t *Wg
 cdk::DownArgs down_args(cd_plan *p, int B, const uint16_t *Wd, float *y)
 {
     cdk::DownArgs a;
-    a.cnt = p->cnt;
-    a.nblk = p->nblk;
-    a.R = p->R;
-    a.lidx = p->lidx;
-    a.ls = p->ls;
-    a.ls_stride = p->ls_stride;
+    a.act = p->act;
+    a.s = p->s;
     a.nb = B;
     a.Wd = Wd;
     a.d_model = p->d_model;
     a.d_ff = p->d_ff;
     a.gc = p->gc;
     a.gr = p->gr;
+    a.rows_per_group = p->rows_per_group;
     a.y = y;
-    a.idx_out = p->idx_out;
-    a.s_out = p->s_out;
-    a.n_out = p->n_out;
     return a;
 }
 
@@ -195,7 +190,8 @@ cd_status run_ffn(cd_plan *p, int variant, const uint16_t *x, int B, const uint1
             return st;
     }
     const cdk::CoefArgs ca = coef_args(p, x, B, Wg, Wu, Bt, thld, y);
-    st = timed_launch(p, CD_KERNEL_COEF, s, [&] { return cdk::launch_coef(variant, ca, p->nblk, s); });
+    st = timed_launch(p, CD_KERNEL_COEF, s,
+                      [&] { return cdk::launch_coef(kernel_variant(variant), ca, s); });
     if (st != CD_OK)
         return st;
     const cdk::DownArgs da = down_args(p, B, Wd, y);
@@ -217,7 +213,7 @@ cd_status dalloc(T **ptr, size_t count)
 
 void release(cd_plan *p)
 {
-    void *bufs[] = {p->cnt, p->lidx, p->idx_out, p->n_out, p->ls, p->s_out, p->coef, p->lat};
+    void *bufs[] = {p->act, p->s, p->coef, p->lat};
     for (void *b : bufs)
         if (b)
             (void)hipFree(b);
@@ -284,30 +280,22 @@ cd_status countdown_plan_create(int d_model, int d_ff, int max_batch, int d_rank
     p->d_rank = d_rank;
     p->flags = flags;
     p->device = dev;
-    p->R = kDefaultRows;
-    if (const char *env = std::getenv("COUNTDOWN_ROWS_PER_BLOCK")) {
-        const int r = std::atoi(env);
-        if (r >= 4 && r <= 64 && r % 4 == 0)
-            p->R = r;
-    }
-    p->nblk = (d_ff + p->R - 1) / p->R;
-    p->ls_stride = p->nblk * p->R;
+    p->last_batch = 0;
+    // down grid: one 512-column chunk per workgroup column and ~kDownWaves
+    // waves, with at least 16 neurons per group
     p->gc = (d_model + 511) / 512;
-    int gr = 512 / p->gc;
+    int gr = kDownWaves / 4 / p->gc;
     if (gr > d_ff / 16)
         gr = d_ff / 16;
-    p->gr = gr < 1 ? 1 : gr;
+    if (gr < 1)
+        gr = 1;
+    p->rows_per_group = (d_ff + gr - 1) / gr;
+    p->gr = (d_ff + p->rows_per_group - 1) / p->rows_per_group;
     const size_t mb = (size_t)max_batch;
-    st = dalloc(&p->cnt, (size_t)p->nblk);
-    if (st == CD_OK) st = dalloc(&p->lidx, (size_t)p->ls_stride);
-    if (st == CD_OK) st = dalloc(&p->ls, mb * p->ls_stride);
-    if (st == CD_OK) st = dalloc(&p->idx_out, (size_t)d_ff);
-    if (st == CD_OK) st = dalloc(&p->n_out, (size_t)1);
-    if (st == CD_OK) st = dalloc(&p->s_out, mb * d_ff);
+    st = dalloc(&p->act, (size_t)d_ff);
+    if (st == CD_OK) st = dalloc(&p->s, mb * d_ff);
     if (st == CD_OK && (flags & CD_PLAN_KEEP_COEF)) st = dalloc(&p->coef, mb * d_ff);
     if (st == CD_OK && d_rank > 0) st = dalloc(&p->lat, mb * d_rank);
-    if (st == CD_OK && hipMemset(p->n_out, 0, sizeof(int)) != hipSuccess) st = CD_EHIP;
-    if (st == CD_OK && hipMemset(p->cnt, 0, sizeof(int) * p->nblk) != hipSuccess) st = CD_EHIP;
     if (st != CD_OK) {
         release(p);
         return st;
@@ -377,8 +365,8 @@ cd_status countdown_calibrate(cd_plan *p, int variant, const uint16_t *X, int T,
     cd_status st = dalloc(&coef, (size_t)tb * p->d_ff);
     if (st == CD_OK) st = dalloc(&ybuf, (size_t)tb * p->d_model);
     if (st == CD_OK) st = dalloc(&q, (size_t)T);
-    // The coefficient kernels run with thld = +inf (no row active) and write
-    // the dense coefficient vector of up to max_batch tokens at a time.
+    // The coefficient kernels run with thld = +inf (no neuron active) and
+    // write the dense coefficient vectors of up to max_batch tokens at a time.
     const uint16_t *wg = W_gate ? W_gate : W_up;
     for (int t0 = 0; st == CD_OK && t0 < T; t0 += tb) {
         const int nb = T - t0 < tb ? T - t0 : tb;
@@ -392,13 +380,15 @@ cd_status countdown_calibrate(cd_plan *p, int variant, const uint16_t *X, int T,
         }
         cdk::CoefArgs a = coef_args(p, xb, nb, wg, W_up, B_t, INFINITY, ybuf);
         a.coef = coef;
-        st = timed_launch(p, CD_KERNEL_COEF, s, [&] { return cdk::launch_coef(variant, a, p->nblk, s); });
+        st = timed_launch(p, CD_KERNEL_COEF, s, [&] { return cdk::launch_coef(variant, a, s); });
         if (st != CD_OK)
             break;
         st = timed_launch(p, CD_KERNEL_SELECT, s, [&] {
             return cdk::launch_select(coef, p->d_ff, p->d_ff, nb, pred ? 0 : 1, k, q + t0, s);
         });
     }
+    // the act / s workspace now describes a calibration batch, not an FFN call
+    p->last_batch = 0;
     if (st == CD_OK)
         st = hip_status(cdk::launch_mean(q, T, thld_out, s));
     if (st == CD_OK && q_out)
@@ -412,34 +402,18 @@ cd_status countdown_calibrate(cd_plan *p, int variant, const uint16_t *X, int T,
     return st;
 }
 
-cd_status countdown_last_active(const cd_plan *plan, const int32_t **idx, const int32_t **n_active,
-                                const float **s_c, const float **coef)
+cd_status countdown_export_active(const cd_plan *p, int32_t *idx_dst, int32_t *n_dst,
+                                  float *s_dst, float *coef_dst, void *stream)
 {
-    if (!plan)
-        return CD_EINVAL;
-    if (idx) *idx = plan->idx_out;
-    if (n_active) *n_active = plan->n_out;
-    if (s_c) *s_c = plan->s_out;
-    if (coef) *coef = plan->coef;
-    return CD_OK;
-}
-
-cd_status countdown_copy_last_active(const cd_plan *p, int32_t *idx_dst, int32_t *n_dst,
-                                     float *s_dst, float *coef_dst, void *stream)
-{
-    if (!p || (coef_dst && !p->coef))
+    if (!p || (coef_dst && !p->coef) || p->last_batch < 1)
         return CD_EINVAL;
     hipStream_t s = reinterpret_cast<hipStream_t>(stream);
-    const size_t nf = (size_t)p->last_batch * p->d_ff;
     hipError_t e = hipSuccess;
-    if (idx_dst && e == hipSuccess)
-        e = hipMemcpyAsync(idx_dst, p->idx_out, sizeof(int32_t) * p->d_ff, hipMemcpyDeviceToDevice, s);
-    if (n_dst && e == hipSuccess)
-        e = hipMemcpyAsync(n_dst, p->n_out, sizeof(int32_t), hipMemcpyDeviceToDevice, s);
-    if (s_dst && nf && e == hipSuccess)
-        e = hipMemcpyAsync(s_dst, p->s_out, sizeof(float) * nf, hipMemcpyDeviceToDevice, s);
-    if (coef_dst && nf && e == hipSuccess)
-        e = hipMemcpyAsync(coef_dst, p->coef, sizeof(float) * nf, hipMemcpyDeviceToDevice, s);
+    if (idx_dst || n_dst || s_dst)
+        e = cdk::launch_export(p->act, p->s, p->last_batch, p->d_ff, idx_dst, n_dst, s_dst, s);
+    if (coef_dst && e == hipSuccess)
+        e = hipMemcpyAsync(coef_dst, p->coef, sizeof(float) * (size_t)p->last_batch * p->d_ff,
+                           hipMemcpyDeviceToDevice, s);
     return hip_status(e);
 }
 

@@ -1,25 +1,44 @@
 // gfx950 kernels of the COUNTDOWN sparse Gated-MLP FFN (arXiv 2505.17701).
 //
-// Path for one call (Sec. 3 Eq. 2-6, Sec. 4):
-//   coefficient kernel: one workgroup per block of R neurons. It streams the
-//     dense coefficient rows (W_up for M-CountDown, W_gate and W_up for ideal
-//     D-CountDown, B_t for the predictor), thresholds the coefficient of every
-//     neuron (union over the batch), compacts the active neurons of the block
-//     in ascending order with one wave ballot, then reads the W_gate (mono)
-//     or W_gate and W_up (pred) rows of just those neurons and forms
-//     s = u * SiLU(g). It writes the block's active count and its (neuron, s)
-//     list, and zeroes y for the next kernel.
-//   down kernel: every workgroup scans the per-block counts in LDS, takes a
-//     contiguous range of active positions and one 512-column chunk,
-//     accumulates s * W_down[i, chunk] over its rows in fp32 and adds the
-//     result into y with fp32 atomics. Column-chunk-0 workgroups also write
-//     the flat ascending IDX and the compact s.
-// Rows are read as 16-byte chunks, 64 lanes x 16 B = one contiguous 1 KB
-// segment per wave instruction. x is staged once per workgroup in LDS.
+// One call (Sec. 3 Eq. 2-6, Sec. 4) runs two kernels:
+//   coefficient kernel: one wave per neuron. The wave streams the neuron's
+//     coefficient row(s) -- W_up for M-CountDown, W_gate and W_up for ideal
+//     D-CountDown, B_t for the predictor -- with non-temporal 16-byte loads
+//     (64 lanes x 16 B = one contiguous 1 KB segment per instruction), takes
+//     the dot products against x held in registers (LDS for batches > 2)
+//     with v_dot2_f32_bf16, reduces across the wave with DPP, and applies
+//     the strict threshold (union over the batch). An active neuron's wave
+//     immediately gathers the rows it still needs (W_gate for mono, W_gate
+//     and W_up for the predictor) and forms s = u * SiLU(g). Results land in
+//     per-neuron arrays act[d_ff] and s[B][d_ff]; there are no barriers
+//     between waves, so a neuron's gather overlaps the other waves' streams.
+//     The kernel also zeroes y for the next kernel.
+//   down kernel: workgroup (c, g) owns a 512-column chunk c and a
+//     contiguous neuron range g. One round trip reads act and s of the
+//     range, a wave ballot compacts the active neurons in ascending order
+//     into LDS, each wave then keeps 8 W_down rows in flight, the four waves
+//     reduce in LDS and add the chunk to y with one fp32 atomic per column.
 #include "cd_device.hpp"
 #include "cd_internal.hpp"
 
 namespace cdk {
+
+// weight rows are read exactly once per call: non-temporal loads
+__device__ __forceinline__ u32x4 load16_stream(const uint16_t *p)
+{
+    return __builtin_nontemporal_load(reinterpret_cast<const u32x4 *>(p));
+}
+
+template <int NK>
+__device__ __forceinline__ void load_row(u32x4 (&w)[NK], const uint16_t *__restrict__ row,
+                                         int d_model, int lane)
+{
+#pragma unroll
+    for (int k = 0; k < NK; ++k) {
+        const int col = k * kColsPerLoad + lane * 8;
+        w[k] = (col < d_model) ? load16_stream(row + col) : zero16();
+    }
+}
 
 // x (bf16) -> LDS as packed pairs, each token padded with zeros to NK*512 columns
 template <int B, int NK>
@@ -38,33 +57,57 @@ __device__ __forceinline__ void stage_x(uint32_t *xs, const uint16_t *__restrict
     }
 }
 
-template <int NK>
-__device__ __forceinline__ void load_row(u32x4 (&w)[NK], const uint16_t *__restrict__ row,
-                                         int d_model, int lane)
+// this lane's chunks of the B tokens, in registers
+template <int B, int NK>
+__device__ __forceinline__ void load_x(u32x4 (&xr)[B][NK], const uint16_t *__restrict__ x, int nb,
+                                       int d_model, int lane)
 {
 #pragma unroll
-    for (int k = 0; k < NK; ++k) {
-        const int col = k * kColsPerLoad + lane * 8;
-        w[k] = (col < d_model) ? load16(row + col) : zero16();
-    }
+    for (int b = 0; b < B; ++b)
+#pragma unroll
+        for (int k = 0; k < NK; ++k) {
+            const int col = k * kColsPerLoad + lane * 8;
+            xr[b][k] = (b < nb && col < d_model) ? load16(x + (size_t)b * d_model + col) : zero16();
+        }
 }
 
-// per-lane partial dot products of one row chunk set with the B staged tokens
-template <int B, int NK>
-__device__ __forceinline__ void dot_row(const u32x4 (&w)[NK], const uint32_t *xs, int lane,
-                                        float (&acc)[B])
-{
-    constexpr int kStride = NK * kColsPerLoad / 2;
-#pragma unroll
-    for (int k = 0; k < NK; ++k) {
-        const int c2 = (k * kColsPerLoad + lane * 8) / 2;
-#pragma unroll
-        for (int b = 0; b < B; ++b) {
-            const u32x4 xv = *reinterpret_cast<const u32x4 *>(xs + b * kStride + c2);
-            acc[b] = dot8(w[k], xv, acc[b]);
+// Token operand of the dot products: registers (XREG) or the LDS copy.
+template <int B, int NK, bool XREG>
+struct Tokens {
+    u32x4 r[XREG ? B : 1][XREG ? NK : 1];
+    const uint32_t *lds;
+
+    // Every thread of the workgroup must call this (it may synchronise).
+    __device__ __forceinline__ void init(const uint16_t *x, int nb, int d_model, int lane,
+                                         uint32_t *smem)
+    {
+        if constexpr (XREG) {
+            load_x<B, NK>(r, x, nb, d_model, lane);
+        } else {
+            stage_x<B, NK>(smem, x, nb, d_model);
+            __syncthreads();
+            lds = smem;
         }
     }
-}
+
+    // acc[b] += w . x_b over this lane's chunks
+    __device__ __forceinline__ void dot(const u32x4 (&w)[NK], int lane, float (&acc)[B]) const
+    {
+#pragma unroll
+        for (int k = 0; k < NK; ++k)
+#pragma unroll
+            for (int b = 0; b < B; ++b) {
+                if constexpr (XREG) {
+                    acc[b] = dot8(w[k], r[b][k], acc[b]);
+                } else {
+                    constexpr int kStride = NK * kColsPerLoad / 2;
+                    const int c2 = (k * kColsPerLoad + lane * 8) / 2;
+                    acc[b] = dot8(w[k], *reinterpret_cast<const u32x4 *>(lds + b * kStride + c2),
+                                  acc[b]);
+                }
+            }
+    }
+};
 
 __device__ __forceinline__ void zero_y(float *y, int n)
 {
@@ -72,324 +115,196 @@ __device__ __forceinline__ void zero_y(float *y, int n)
         y[i] = 0.0f;
 }
 
-// Wave 0 turns the per-row flags of the block into the ascending list of
-// active local rows (spos) and publishes the count.
-__device__ __forceinline__ void compact_local(const int *sflag, int R, int *spos, int *snact,
-                                              int *cnt_out)
+template <int B>
+__device__ __forceinline__ void zero_acc(float (&acc)[B])
 {
-    if (threadIdx.x < kWave) {
-        const int lane = threadIdx.x;
-        const bool f = lane < R && sflag[lane] != 0;
-        const uint64_t m = ballot(f);
-        if (f)
-            spos[lanes_below(m)] = lane;
-        if (lane == 0) {
-            const int n = __popcll(m);
-            *snact = n;
-            *cnt_out = n;
-        }
-    }
+#pragma unroll
+    for (int b = 0; b < B; ++b)
+        acc[b] = 0.0f;
 }
 
-// rows of one wave loop iteration, sized so that ~16 KB per wave are in flight
-template <int NK, int MATS>
-constexpr int rows_per_iter()
-{
-    return (NK * MATS >= 16) ? 1 : (NK * MATS >= 8 ? 2 : 4);
-}
-
-// Gather phase shared by mono and pred: for the nact active local rows (spos)
-// read the W_gate row (and the W_up row when UP) and form s = u * SiLU(g),
-// with u from su when !UP. Writes slot lists.
-template <int B, int NK, bool UP>
-__device__ __forceinline__ void gather_gate(const CoefArgs &a, const uint32_t *xs, int row0,
-                                            const int *spos, int nact, const float (*su)[kMaxRowsPerBlock],
-                                            int wave, int lane)
-{
-    constexpr int RPI = rows_per_iter<NK, UP ? 2 : 1>();
-    for (int j0 = wave; j0 < nact; j0 += kWavesPerBlock * RPI) {
-        u32x4 wg[RPI][NK];
-        u32x4 wu[UP ? RPI : 1][UP ? NK : 1];
-#pragma unroll
-        for (int q = 0; q < RPI; ++q) {
-            const int j = j0 + q * kWavesPerBlock;
-            if (j < nact) {
-                const size_t off = (size_t)(row0 + spos[j]) * a.d_model;
-                load_row<NK>(wg[q], a.Wg + off, a.d_model, lane);
-                if constexpr (UP)
-                    load_row<NK>(wu[q], a.Wu + off, a.d_model, lane);
-            }
-        }
-#pragma unroll
-        for (int q = 0; q < RPI; ++q) {
-            const int j = j0 + q * kWavesPerBlock;
-            if (j >= nact)
-                continue;
-            const int lr = spos[j];
-            const int slot = blockIdx.x * a.R + j;
-            float ag[B], au[B];
-#pragma unroll
-            for (int b = 0; b < B; ++b) {
-                ag[b] = 0.0f;
-                au[b] = 0.0f;
-            }
-            dot_row<B, NK>(wg[q], xs, lane, ag);
-            if constexpr (UP)
-                dot_row<B, NK>(wu[q], xs, lane, au);
-#pragma unroll
-            for (int b = 0; b < B; ++b) {
-                const float g = wave_sum(ag[b]);
-                float u;
-                if constexpr (UP)
-                    u = wave_sum(au[b]);
-                else
-                    u = su[b][lr];
-                if (b < a.nb && lane == 0)
-                    a.ls[(size_t)b * a.ls_stride + slot] = u * silu(g);
-            }
-            if (lane == 0)
-                a.lidx[slot] = row0 + lr;
-        }
-    }
-}
-
-// M-CountDown coefficient kernel (Eq. 6b): u = x.W_up, |u| > thld, then gate.
-template <int B, int NK>
+// M-CountDown coefficient kernel (Eq. 6b): u = x.W_up, |u| > thld, then the
+// active neuron's W_gate row and s = u * SiLU(g) (Eq. 2 restricted to IDX).
+template <int B, int NK, bool XREG>
 __global__ __launch_bounds__(kBlock) void k_coef_mono(const CoefArgs a)
 {
     extern __shared__ __align__(16) uint32_t xs[];
-    __shared__ float su[B][kMaxRowsPerBlock];
-    __shared__ int sflag[kMaxRowsPerBlock];
-    __shared__ int spos[kMaxRowsPerBlock];
-    __shared__ int snact;
-    constexpr int RPI = rows_per_iter<NK, 1>();
     const int lane = threadIdx.x % kWave, wave = threadIdx.x / kWave;
-    const int row0 = blockIdx.x * a.R;
-
+    const int row = blockIdx.x * kWavesPerBlock + wave;
+    const bool live = row < a.d_ff;
+    u32x4 w[NK];
+    if (live)
+        load_row<NK>(w, a.Wu + (size_t)row * a.d_model, a.d_model, lane);
     zero_y(a.y, a.nb * a.d_model);
-    stage_x<B, NK>(xs, a.x, a.nb, a.d_model);
-    __syncthreads();
+    Tokens<B, NK, XREG> tok;
+    tok.init(a.x, a.nb, a.d_model, lane, xs);
+    if (!live)
+        return;
 
-    for (int base = wave; base < a.R; base += kWavesPerBlock * RPI) {
-        u32x4 w[RPI][NK];
+    float acc[B], u[B];
+    zero_acc(acc);
+    tok.dot(w, lane, acc);
+    bool act = false;
 #pragma unroll
-        for (int q = 0; q < RPI; ++q) {
-            const int lr = base + q * kWavesPerBlock, row = row0 + lr;
-            if (lr < a.R && row < a.d_ff)
-                load_row<NK>(w[q], a.Wu + (size_t)row * a.d_model, a.d_model, lane);
-        }
-#pragma unroll
-        for (int q = 0; q < RPI; ++q) {
-            const int lr = base + q * kWavesPerBlock, row = row0 + lr;
-            if (lr >= a.R)
-                continue;
-            bool act = false;
-            if (row < a.d_ff) {
-                float acc[B];
-#pragma unroll
-                for (int b = 0; b < B; ++b)
-                    acc[b] = 0.0f;
-                dot_row<B, NK>(w[q], xs, lane, acc);
-#pragma unroll
-                for (int b = 0; b < B; ++b) {
-                    const float u = wave_sum(acc[b]);
-                    if (b < a.nb) {
-                        act = act || (fabsf(u) > a.thld);
-                        if (lane == 0) {
-                            su[b][lr] = u;
-                            if (a.coef)
-                                a.coef[(size_t)b * a.d_ff + row] = u;
-                        }
-                    }
-                }
-            }
-            if (lane == 0)
-                sflag[lr] = act ? 1 : 0;
+    for (int b = 0; b < B; ++b) {
+        u[b] = wave_sum(acc[b]);
+        if (b < a.nb) {
+            act = act || (fabsf(u[b]) > a.thld);
+            if (a.coef && lane == 0)
+                a.coef[(size_t)b * a.d_ff + row] = u[b];
         }
     }
-    __syncthreads();
-    compact_local(sflag, a.R, spos, &snact, a.cnt + blockIdx.x);
-    __syncthreads();
-    gather_gate<B, NK, false>(a, xs, row0, spos, snact, su, wave, lane);
+    if (act) {
+        load_row<NK>(w, a.Wg + (size_t)row * a.d_model, a.d_model, lane);
+        zero_acc(acc);
+        tok.dot(w, lane, acc);
+#pragma unroll
+        for (int b = 0; b < B; ++b) {
+            const float g = wave_sum(acc[b]);
+            if (b < a.nb && lane == 0)
+                a.s[(size_t)b * a.d_ff + row] = u[b] * silu(g);
+        }
+    }
+    if (lane == 0)
+        a.act[row] = act ? 1 : 0;
 }
 
 // Ideal D-CountDown coefficient kernel (Eq. 6c): s = (x.W_up) * SiLU(x.W_gate)
-// over all rows, |s| > thld. DENSE keeps every row (Eq. 1).
-template <int B, int NK, bool DENSE>
+// for every neuron, |s| > thld. DENSE keeps every neuron (Eq. 1).
+template <int B, int NK, bool XREG, bool DENSE>
 __global__ __launch_bounds__(kBlock) void k_coef_dual(const CoefArgs a)
 {
     extern __shared__ __align__(16) uint32_t xs[];
-    __shared__ float ss[B][kMaxRowsPerBlock];
-    __shared__ int sflag[kMaxRowsPerBlock];
-    __shared__ int spos[kMaxRowsPerBlock];
-    __shared__ int snact;
-    constexpr int RPI = rows_per_iter<NK, 2>();
     const int lane = threadIdx.x % kWave, wave = threadIdx.x / kWave;
-    const int row0 = blockIdx.x * a.R;
-
+    const int row = blockIdx.x * kWavesPerBlock + wave;
+    const bool live = row < a.d_ff;
+    u32x4 wg[NK], wu[NK];
+    if (live) {
+        load_row<NK>(wg, a.Wg + (size_t)row * a.d_model, a.d_model, lane);
+        load_row<NK>(wu, a.Wu + (size_t)row * a.d_model, a.d_model, lane);
+    }
     zero_y(a.y, a.nb * a.d_model);
-    stage_x<B, NK>(xs, a.x, a.nb, a.d_model);
-    __syncthreads();
+    Tokens<B, NK, XREG> tok;
+    tok.init(a.x, a.nb, a.d_model, lane, xs);
+    if (!live)
+        return;
 
-    for (int base = wave; base < a.R; base += kWavesPerBlock * RPI) {
-        u32x4 wg[RPI][NK], wu[RPI][NK];
+    float ag[B], au[B];
+    zero_acc(ag);
+    zero_acc(au);
+    tok.dot(wg, lane, ag);
+    tok.dot(wu, lane, au);
+    bool act = DENSE;
+    float s[B];
 #pragma unroll
-        for (int q = 0; q < RPI; ++q) {
-            const int lr = base + q * kWavesPerBlock, row = row0 + lr;
-            if (lr < a.R && row < a.d_ff) {
-                load_row<NK>(wg[q], a.Wg + (size_t)row * a.d_model, a.d_model, lane);
-                load_row<NK>(wu[q], a.Wu + (size_t)row * a.d_model, a.d_model, lane);
-            }
-        }
-#pragma unroll
-        for (int q = 0; q < RPI; ++q) {
-            const int lr = base + q * kWavesPerBlock, row = row0 + lr;
-            if (lr >= a.R)
-                continue;
-            bool act = false;
-            if (row < a.d_ff) {
-                float ag[B], au[B];
-#pragma unroll
-                for (int b = 0; b < B; ++b) {
-                    ag[b] = 0.0f;
-                    au[b] = 0.0f;
-                }
-                dot_row<B, NK>(wg[q], xs, lane, ag);
-                dot_row<B, NK>(wu[q], xs, lane, au);
-#pragma unroll
-                for (int b = 0; b < B; ++b) {
-                    const float g = wave_sum(ag[b]);
-                    const float u = wave_sum(au[b]);
-                    const float s = u * silu(g);
-                    if (b < a.nb) {
-                        act = act || DENSE || (fabsf(s) > a.thld);
-                        if (lane == 0) {
-                            ss[b][lr] = s;
-                            if (a.coef)
-                                a.coef[(size_t)b * a.d_ff + row] = s;
-                        }
-                    }
-                }
-            }
-            if (lane == 0)
-                sflag[lr] = act ? 1 : 0;
+    for (int b = 0; b < B; ++b) {
+        const float g = wave_sum(ag[b]);
+        const float u = wave_sum(au[b]);
+        s[b] = u * silu(g);
+        if (b < a.nb) {
+            act = act || (fabsf(s[b]) > a.thld);
+            if (a.coef && lane == 0)
+                a.coef[(size_t)b * a.d_ff + row] = s[b];
         }
     }
-    __syncthreads();
-    compact_local(sflag, a.R, spos, &snact, a.cnt + blockIdx.x);
-    __syncthreads();
-    const int nact = snact;
-    for (int j = threadIdx.x; j < nact; j += kBlock) {
-        const int lr = spos[j];
-        const int slot = blockIdx.x * a.R + j;
-        a.lidx[slot] = row0 + lr;
-        for (int b = 0; b < a.nb; ++b)
-            a.ls[(size_t)b * a.ls_stride + slot] = ss[b][lr];
+    if (lane == 0) {
+        if (act)
+#pragma unroll
+            for (int b = 0; b < B; ++b)
+                if (b < a.nb)
+                    a.s[(size_t)b * a.d_ff + row] = s[b];
+        a.act[row] = act ? 1 : 0;
     }
 }
 
-// Predictor scores s_hat = latent . B_t[row] for the block's rows, with
-// 2^LOG lanes per B_t row (64 >> LOG rows per wave instruction); sets the
-// signed-threshold flags (union over the batch).
-template <int B, int LOG>
-__device__ __forceinline__ void score_rows(const CoefArgs &a, const float *lat_s, int row0,
-                                           int *sflag, int wave, int lane)
-{
-    constexpr int LPR = 1 << LOG;
-    constexpr int RW = kWave / LPR;
-    const int nch = a.d_rank > kColsPerLoad ? a.d_rank / kColsPerLoad : 1;
-    const int sub = lane / LPR;
-    const int e0 = (lane % LPR) * 8;
-    const bool last = (lane % LPR) == LPR - 1;
-    for (int base = wave * RW; base < a.R; base += kWavesPerBlock * RW) {
-        const int lr = base + sub, row = row0 + lr;
-        const bool ok = lr < a.R && row < a.d_ff;
-        float acc[B];
-#pragma unroll
-        for (int b = 0; b < B; ++b)
-            acc[b] = 0.0f;
-        for (int ch = 0; ch < nch; ++ch) {
-            const int e = ch * kColsPerLoad + e0;
-            const u32x4 w = ok ? load16(a.Bt + (size_t)row * a.d_rank + e) : zero16();
-            const float wf[8] = {bf16_lo(w.x), bf16_hi(w.x), bf16_lo(w.y), bf16_hi(w.y),
-                                 bf16_lo(w.z), bf16_hi(w.z), bf16_lo(w.w), bf16_hi(w.w)};
-#pragma unroll
-            for (int b = 0; b < B; ++b) {
-                const float *l = lat_s + b * a.d_rank + e;
-#pragma unroll
-                for (int t = 0; t < 8; ++t)
-                    acc[b] = fmaf(wf[t], l[t], acc[b]);
-            }
-        }
-        bool act = false;
-#pragma unroll
-        for (int b = 0; b < B; ++b) {
-            const float v = segment_sum<LOG>(acc[b]);
-            if (b < a.nb && ok) {
-                act = act || (v > a.thld);
-                if (last && a.coef)
-                    a.coef[(size_t)b * a.d_ff + row] = v;
-            }
-        }
-        if (last && lr < a.R)
-            sflag[lr] = (ok && act) ? 1 : 0;
-    }
-}
-
-// Practical D-CountDown coefficient kernel (Sec. 4): predictor score, signed
-// threshold, then gate and up rows of the active neurons.
-template <int B, int NK>
+// Practical D-CountDown coefficient kernel (Sec. 4): predictor score
+// s_hat = latent . B_t[row] (signed threshold, union over the batch), then
+// the active neuron's W_gate and W_up rows and s = u * SiLU(g).
+template <int B, int NK, bool XREG>
 __global__ __launch_bounds__(kBlock) void k_coef_pred(const CoefArgs a)
 {
     extern __shared__ __align__(16) uint32_t xs[];
-    __shared__ int sflag[kMaxRowsPerBlock];
-    __shared__ int spos[kMaxRowsPerBlock];
-    __shared__ int snact;
     const int lane = threadIdx.x % kWave, wave = threadIdx.x / kWave;
-    const int row0 = blockIdx.x * a.R;
-    float *lat_s = reinterpret_cast<float *>(xs + B * NK * kColsPerLoad / 2);
-
-    zero_y(a.y, a.nb * a.d_model);
-    stage_x<B, NK>(xs, a.x, a.nb, a.d_model);
-    for (int i = threadIdx.x; i < B * a.d_rank; i += kBlock)
-        lat_s[i] = (i / a.d_rank) < a.nb ? a.lat[i] : 0.0f;
-    __syncthreads();
-
-    switch (a.d_rank) {
-    case 8: score_rows<B, 0>(a, lat_s, row0, sflag, wave, lane); break;
-    case 16: score_rows<B, 1>(a, lat_s, row0, sflag, wave, lane); break;
-    case 32: score_rows<B, 2>(a, lat_s, row0, sflag, wave, lane); break;
-    case 64: score_rows<B, 3>(a, lat_s, row0, sflag, wave, lane); break;
-    case 128: score_rows<B, 4>(a, lat_s, row0, sflag, wave, lane); break;
-    case 256: score_rows<B, 5>(a, lat_s, row0, sflag, wave, lane); break;
-    default: score_rows<B, 6>(a, lat_s, row0, sflag, wave, lane); break;  // 512, 1024
+    const int row = blockIdx.x * kWavesPerBlock + wave;
+    const bool live = row < a.d_ff;
+    float acc[B];
+    zero_acc(acc);
+    for (int e = lane * 8; e < a.d_rank; e += kColsPerLoad) {
+        const u32x4 w = live ? load16_stream(a.Bt + (size_t)row * a.d_rank + e) : zero16();
+        const float wf[8] = {bf16_lo(w.x), bf16_hi(w.x), bf16_lo(w.y), bf16_hi(w.y),
+                             bf16_lo(w.z), bf16_hi(w.z), bf16_lo(w.w), bf16_hi(w.w)};
+#pragma unroll
+        for (int b = 0; b < B; ++b) {
+            if (b >= a.nb)
+                break;
+            const float4 l0 = *reinterpret_cast<const float4 *>(a.lat + (size_t)b * a.d_rank + e);
+            const float4 l1 = *reinterpret_cast<const float4 *>(a.lat + (size_t)b * a.d_rank + e + 4);
+            acc[b] = fmaf(wf[0], l0.x, acc[b]);
+            acc[b] = fmaf(wf[1], l0.y, acc[b]);
+            acc[b] = fmaf(wf[2], l0.z, acc[b]);
+            acc[b] = fmaf(wf[3], l0.w, acc[b]);
+            acc[b] = fmaf(wf[4], l1.x, acc[b]);
+            acc[b] = fmaf(wf[5], l1.y, acc[b]);
+            acc[b] = fmaf(wf[6], l1.z, acc[b]);
+            acc[b] = fmaf(wf[7], l1.w, acc[b]);
+        }
     }
-    __syncthreads();
-    compact_local(sflag, a.R, spos, &snact, a.cnt + blockIdx.x);
-    __syncthreads();
-    gather_gate<B, NK, true>(a, xs, row0, spos, snact, nullptr, wave, lane);
+    zero_y(a.y, a.nb * a.d_model);
+    Tokens<B, NK, XREG> tok;
+    tok.init(a.x, a.nb, a.d_model, lane, xs);
+    if (!live)
+        return;
+
+    bool act = false;
+#pragma unroll
+    for (int b = 0; b < B; ++b) {
+        const float v = wave_sum(acc[b]);
+        if (b < a.nb) {
+            act = act || (v > a.thld);
+            if (a.coef && lane == 0)
+                a.coef[(size_t)b * a.d_ff + row] = v;
+        }
+    }
+    if (act) {
+        u32x4 wg[NK], wu[NK];
+        load_row<NK>(wg, a.Wg + (size_t)row * a.d_model, a.d_model, lane);
+        load_row<NK>(wu, a.Wu + (size_t)row * a.d_model, a.d_model, lane);
+        float ag[B], au[B];
+        zero_acc(ag);
+        zero_acc(au);
+        tok.dot(wg, lane, ag);
+        tok.dot(wu, lane, au);
+#pragma unroll
+        for (int b = 0; b < B; ++b) {
+            const float g = wave_sum(ag[b]);
+            const float u = wave_sum(au[b]);
+            if (b < a.nb && lane == 0)
+                a.s[(size_t)b * a.d_ff + row] = u * silu(g);
+        }
+    }
+    if (lane == 0)
+        a.act[row] = act ? 1 : 0;
 }
 
-// latent = x . theta_A for the predictor: one row of A_t per wave iteration
-template <int B, int NK>
+// latent = x . theta_A for the predictor: one row of A_t per wave
+template <int B, int NK, bool XREG>
 __global__ __launch_bounds__(kBlock) void k_latent(const uint16_t *__restrict__ x, int nb,
                                                    const uint16_t *__restrict__ At, int d_model,
                                                    int d_rank, float *__restrict__ lat)
 {
     extern __shared__ __align__(16) uint32_t xs[];
     const int lane = threadIdx.x % kWave, wave = threadIdx.x / kWave;
-    stage_x<B, NK>(xs, x, nb, d_model);
-    __syncthreads();
     const int r = blockIdx.x * kWavesPerBlock + wave;
+    u32x4 w[NK];
+    if (r < d_rank)
+        load_row<NK>(w, At + (size_t)r * d_model, d_model, lane);
+    Tokens<B, NK, XREG> tok;
+    tok.init(x, nb, d_model, lane, xs);
     if (r >= d_rank)
         return;
-    u32x4 w[NK];
-    load_row<NK>(w, At + (size_t)r * d_model, d_model, lane);
     float acc[B];
-#pragma unroll
-    for (int b = 0; b < B; ++b)
-        acc[b] = 0.0f;
-    dot_row<B, NK>(w, xs, lane, acc);
+    zero_acc(acc);
+    tok.dot(w, lane, acc);
 #pragma unroll
     for (int b = 0; b < B; ++b) {
         const float v = wave_sum(acc[b]);
@@ -398,73 +313,59 @@ __global__ __launch_bounds__(kBlock) void k_latent(const uint16_t *__restrict__ 
     }
 }
 
-// exclusive scan of cnt[0..n) into pre[0..n]; pre[n] = total (256 threads)
-__device__ __forceinline__ void block_scan_counts(const int *__restrict__ cnt, int n, int *pre,
-                                                  int *part)
-{
-    const int t = threadIdx.x;
-    const int per = (n + kBlock - 1) / kBlock;
-    const int lo = min(n, t * per), hi = min(n, lo + per);
-    int sum = 0;
-    for (int i = lo; i < hi; ++i)
-        sum += cnt[i];
-    part[t] = sum;
-    __syncthreads();
-    for (int off = 1; off < kBlock; off <<= 1) {
-        const int v = t >= off ? part[t - off] : 0;
-        __syncthreads();
-        part[t] += v;
-        __syncthreads();
-    }
-    int run = part[t] - sum;  // exclusive prefix of this thread's segment
-    for (int i = lo; i < hi; ++i) {
-        pre[i] = run;
-        run += cnt[i];
-    }
-    if (t == kBlock - 1)
-        pre[n] = part[t];
-    __syncthreads();
-}
-
-// largest blk in [0, n) with pre[blk] <= p (pre ascending, pre[0] = 0 <= p)
-__device__ __forceinline__ int find_block(const int *pre, int n, int p, int top)
-{
-    int lo = 0;
-    for (int step = top; step > 0; step >>= 1) {
-        const int cand = lo + step;
-        if (cand < n && pre[cand] <= p)
-            lo = cand;
-    }
-    return lo;
-}
-
-// Gathered down projection (Eq. 5): y_b += sum_{p in range} s_b[p] W_down[IDX[p], chunk]
+// Gathered down projection (Eq. 5), see the file comment.
 template <int B>
 __global__ __launch_bounds__(kBlock) void k_down(const DownArgs a)
 {
+    constexpr int U = 8;
     extern __shared__ __align__(16) int dsm[];
-    __shared__ int part[kBlock];
-    constexpr int U = 4;  // rows in flight per wave
-    int *pre = dsm;                                                  // nblk + 1
-    float *red = reinterpret_cast<float *>(dsm + ((a.nblk + 4) & ~3)); // [4][512]
+    __shared__ int wcnt[kWavesPerBlock];
+    const int cap = a.rows_per_group;
+    int *lrow = dsm;                                                 // [cap]
+    float *lsv = reinterpret_cast<float *>(dsm + cap);               // [B][cap]
+    float *red = reinterpret_cast<float *>(dsm + cap * (1 + B));     // [4][512]
     const int lane = threadIdx.x % kWave, wave = threadIdx.x / kWave;
-
-    block_scan_counts(a.cnt, a.nblk, pre, part);
-    const int n = pre[a.nblk];
-    if (blockIdx.x == 0 && threadIdx.x == 0)
-        *a.n_out = n;
-
     const int c = blockIdx.x % a.gc, g = blockIdx.x / a.gc;
-    const int p_begin = (int)(((long long)n * g) / a.gr);
-    const int p_end = (int)(((long long)n * (g + 1)) / a.gr);
-    if (p_begin >= p_end)
+    const int r0 = g * cap;
+    const int r1 = min(a.d_ff, r0 + cap);
+
+    int nl = 0;
+    for (int t0 = r0; t0 < r1; t0 += kBlock) {
+        const int row = t0 + threadIdx.x;
+        bool valid = false;
+        float sv[B];
+#pragma unroll
+        for (int b = 0; b < B; ++b)
+            sv[b] = 0.0f;
+        if (row < r1) {
+            valid = a.act[row] != 0;
+#pragma unroll
+            for (int b = 0; b < B; ++b)
+                if (b < a.nb)
+                    sv[b] = a.s[(size_t)b * a.d_ff + row];
+        }
+        const uint64_t m = ballot(valid);
+        if (lane == 0)
+            wcnt[wave] = __popcll(m);
+        __syncthreads();
+        int base = nl;
+        for (int v = 0; v < wave; ++v)
+            base += wcnt[v];
+        if (valid) {
+            const int pos = base + lanes_below(m);
+            lrow[pos] = row;
+#pragma unroll
+            for (int b = 0; b < B; ++b)
+                lsv[b * cap + pos] = sv[b];
+        }
+        nl += wcnt[0] + wcnt[1] + wcnt[2] + wcnt[3];
+        __syncthreads();
+    }
+    if (nl == 0)
         return;  // uniform for the workgroup
+
     const int col = c * kColsPerLoad + lane * 8;
     const bool colok = col < a.d_model;
-    int top = 1;
-    while (top * 2 < a.nblk)
-        top <<= 1;
-
     float acc[B][8];
 #pragma unroll
     for (int b = 0; b < B; ++b)
@@ -472,53 +373,31 @@ __global__ __launch_bounds__(kBlock) void k_down(const DownArgs a)
         for (int e = 0; e < 8; ++e)
             acc[b][e] = 0.0f;
 
-    for (int p0 = p_begin + wave; p0 < p_end; p0 += kWavesPerBlock * U) {
-        int row[U];
-        float s[U][B];
+    for (int q0 = wave; q0 < nl; q0 += kWavesPerBlock * U) {
         u32x4 w[U];
 #pragma unroll
         for (int q = 0; q < U; ++q) {
-            const int p = p0 + q * kWavesPerBlock;
-            row[q] = 0;
-#pragma unroll
-            for (int b = 0; b < B; ++b)
-                s[q][b] = 0.0f;
-            if (p < p_end) {
-                const int blk = find_block(pre, a.nblk, p, top);
-                const int slot = blk * a.R + (p - pre[blk]);
-                row[q] = a.lidx[slot];
-#pragma unroll
-                for (int b = 0; b < B; ++b)
-                    if (b < a.nb)
-                        s[q][b] = a.ls[(size_t)b * a.ls_stride + slot];
-            }
+            const int r = q0 + q * kWavesPerBlock;
+            w[q] = (r < nl && colok) ? load16_stream(a.Wd + (size_t)lrow[r] * a.d_model + col)
+                                     : zero16();
         }
 #pragma unroll
         for (int q = 0; q < U; ++q) {
-            const int p = p0 + q * kWavesPerBlock;
-            w[q] = (p < p_end && colok) ? load16(a.Wd + (size_t)row[q] * a.d_model + col) : zero16();
-        }
-#pragma unroll
-        for (int q = 0; q < U; ++q) {
+            const int r = q0 + q * kWavesPerBlock;
+            if (r >= nl)
+                break;
             const float wf[8] = {bf16_lo(w[q].x), bf16_hi(w[q].x), bf16_lo(w[q].y), bf16_hi(w[q].y),
                                  bf16_lo(w[q].z), bf16_hi(w[q].z), bf16_lo(w[q].w), bf16_hi(w[q].w)};
 #pragma unroll
-            for (int b = 0; b < B; ++b)
+            for (int b = 0; b < B; ++b) {
+                const float sv = lsv[b * cap + r];
 #pragma unroll
                 for (int e = 0; e < 8; ++e)
-                    acc[b][e] = fmaf(s[q][b], wf[e], acc[b][e]);
-            const int p = p0 + q * kWavesPerBlock;
-            if (c == 0 && lane == 0 && p < p_end) {
-                a.idx_out[p] = row[q];
-#pragma unroll
-                for (int b = 0; b < B; ++b)
-                    if (b < a.nb)
-                        a.s_out[(size_t)b * a.d_ff + p] = s[q][b];
+                    acc[b][e] = fmaf(sv, wf[e], acc[b][e]);
             }
         }
     }
 
-    // reduce the four waves' partials in LDS, then one atomic add per column
 #pragma unroll
     for (int b = 0; b < B; ++b) {
         if (b >= a.nb)
@@ -536,6 +415,45 @@ __global__ __launch_bounds__(kBlock) void k_down(const DownArgs a)
                 unsafeAtomicAdd(a.y + (size_t)b * a.d_model + gcol, v);
             }
         }
+    }
+}
+
+constexpr int kExportThreads = 1024;
+
+// Flat ascending IDX, |IDX| and compact s of the last call (one workgroup):
+// scan of the per-neuron flags, then every thread writes its neurons.
+__global__ __launch_bounds__(kExportThreads) void k_export(const int *__restrict__ act,
+                                                           const float *__restrict__ s, int nb,
+                                                           int d_ff, int *idx_dst, int *n_dst,
+                                                           float *s_dst)
+{
+    __shared__ int part[kExportThreads];
+    const int t = threadIdx.x;
+    const int per = (d_ff + kExportThreads - 1) / kExportThreads;
+    const int lo = min(d_ff, t * per), hi = min(d_ff, lo + per);
+    int sum = 0;
+    for (int i = lo; i < hi; ++i)
+        sum += act[i] != 0;
+    part[t] = sum;
+    __syncthreads();
+    for (int off = 1; off < kExportThreads; off <<= 1) {
+        const int v = t >= off ? part[t - off] : 0;
+        __syncthreads();
+        part[t] += v;
+        __syncthreads();
+    }
+    if (t == kExportThreads - 1 && n_dst)
+        *n_dst = part[t];
+    int pos = part[t] - sum;
+    for (int i = lo; i < hi; ++i) {
+        if (!act[i])
+            continue;
+        if (idx_dst)
+            idx_dst[pos] = i;
+        if (s_dst)
+            for (int b = 0; b < nb; ++b)
+                s_dst[(size_t)b * d_ff + pos] = s[(size_t)b * d_ff + i];
+        ++pos;
     }
 }
 
@@ -646,68 +564,69 @@ int col_tile(int d_model)
     return chunks <= 1 ? 1 : chunks <= 2 ? 2 : chunks <= 4 ? 4 : chunks <= 8 ? 8 : 16;
 }
 
-size_t coef_lds_bytes(int variant, int bt, int nk, int d_rank)
+// tokens live in registers up to a batch of 2, in LDS beyond
+static size_t token_lds_bytes(int bt, int nk)
 {
-    size_t b = (size_t)bt * nk * kColsPerLoad * 2;
-    if (variant == kDualPred)
-        b += (size_t)bt * d_rank * 4;
-    return b;
+    return bt <= 2 ? 0 : (size_t)bt * nk * kColsPerLoad * 2;
 }
 
-size_t down_lds_bytes(int nblk)
+size_t down_lds_bytes(int rows_per_group, int bt)
 {
-    return (size_t)((nblk + 4) & ~3) * 4 + (size_t)kWavesPerBlock * kColsPerLoad * 4;
+    return (size_t)rows_per_group * 4 * (1 + bt) + (size_t)kWavesPerBlock * kColsPerLoad * 4;
 }
 
 template <int B, int NK>
-static hipError_t coef_bn(int variant, const CoefArgs &a, int grid, hipStream_t s)
+static hipError_t coef_bn(int variant, const CoefArgs &a, hipStream_t s)
 {
-    const size_t lds = coef_lds_bytes(variant, B, NK, a.d_rank);
+    constexpr bool XREG = B <= 2;
+    const size_t lds = token_lds_bytes(B, NK);
+    const int grid = (a.d_ff + kWavesPerBlock - 1) / kWavesPerBlock;
     switch (variant) {
     case kMono:
-        allow_lds(k_coef_mono<B, NK>, lds);
-        k_coef_mono<B, NK><<<grid, kBlock, lds, s>>>(a);
+        allow_lds(k_coef_mono<B, NK, XREG>, lds);
+        k_coef_mono<B, NK, XREG><<<grid, kBlock, lds, s>>>(a);
         break;
     case kDualIdeal:
-        allow_lds(k_coef_dual<B, NK, false>, lds);
-        k_coef_dual<B, NK, false><<<grid, kBlock, lds, s>>>(a);
+        allow_lds(k_coef_dual<B, NK, XREG, false>, lds);
+        k_coef_dual<B, NK, XREG, false><<<grid, kBlock, lds, s>>>(a);
         break;
     case kDense:
-        allow_lds(k_coef_dual<B, NK, true>, lds);
-        k_coef_dual<B, NK, true><<<grid, kBlock, lds, s>>>(a);
+        allow_lds(k_coef_dual<B, NK, XREG, true>, lds);
+        k_coef_dual<B, NK, XREG, true><<<grid, kBlock, lds, s>>>(a);
         break;
     case kDualPred:
-        allow_lds(k_coef_pred<B, NK>, lds);
-        k_coef_pred<B, NK><<<grid, kBlock, lds, s>>>(a);
+        allow_lds(k_coef_pred<B, NK, XREG>, lds);
+        k_coef_pred<B, NK, XREG><<<grid, kBlock, lds, s>>>(a);
         break;
-    default: return hipErrorInvalidValue;
+    default:
+        return hipErrorInvalidValue;
     }
     return hipGetLastError();
 }
 
 template <int B>
-static hipError_t coef_b(int variant, const CoefArgs &a, int grid, hipStream_t s)
+static hipError_t coef_b(int variant, const CoefArgs &a, hipStream_t s)
 {
     switch (col_tile(a.d_model)) {
-    case 1: return coef_bn<B, 1>(variant, a, grid, s);
-    case 2: return coef_bn<B, 2>(variant, a, grid, s);
-    case 4: return coef_bn<B, 4>(variant, a, grid, s);
-    case 8: return coef_bn<B, 8>(variant, a, grid, s);
+    case 1: return coef_bn<B, 1>(variant, a, s);
+    case 2: return coef_bn<B, 2>(variant, a, s);
+    case 4: return coef_bn<B, 4>(variant, a, s);
+    case 8: return coef_bn<B, 8>(variant, a, s);
     default:
-        // B * d_model is capped at 32768 by the plan checks: no 8 x 8192 tile
+        // batch * d_model is capped at 32768 by the plan checks: no 8 x 8192 tile
         if constexpr (B * 16 <= 64)
-            return coef_bn<B, 16>(variant, a, grid, s);
+            return coef_bn<B, 16>(variant, a, s);
         return hipErrorInvalidValue;
     }
 }
 
-hipError_t launch_coef(int variant, const CoefArgs &a, int grid, hipStream_t s)
+hipError_t launch_coef(int variant, const CoefArgs &a, hipStream_t s)
 {
     switch (batch_tile(a.nb)) {
-    case 1: return coef_b<1>(variant, a, grid, s);
-    case 2: return coef_b<2>(variant, a, grid, s);
-    case 4: return coef_b<4>(variant, a, grid, s);
-    default: return coef_b<8>(variant, a, grid, s);
+    case 1: return coef_b<1>(variant, a, s);
+    case 2: return coef_b<2>(variant, a, s);
+    case 4: return coef_b<4>(variant, a, s);
+    default: return coef_b<8>(variant, a, s);
     }
 }
 
@@ -715,10 +634,11 @@ template <int B, int NK>
 static hipError_t latent_bn(const uint16_t *x, int nb, const uint16_t *At, int d_model, int d_rank,
                             float *lat, hipStream_t s)
 {
+    constexpr bool XREG = B <= 2;
     const int grid = (d_rank + kWavesPerBlock - 1) / kWavesPerBlock;
-    const size_t lds = (size_t)B * NK * kColsPerLoad * 2;
-    allow_lds(k_latent<B, NK>, lds);
-    k_latent<B, NK><<<grid, kBlock, lds, s>>>(x, nb, At, d_model, d_rank, lat);
+    const size_t lds = token_lds_bytes(B, NK);
+    allow_lds(k_latent<B, NK, XREG>, lds);
+    k_latent<B, NK, XREG><<<grid, kBlock, lds, s>>>(x, nb, At, d_model, d_rank, lat);
     return hipGetLastError();
 }
 
@@ -751,14 +671,22 @@ hipError_t launch_latent(const uint16_t *x, int nb, const uint16_t *At, int d_mo
 
 hipError_t launch_down(const DownArgs &a, hipStream_t s)
 {
-    const size_t lds = down_lds_bytes(a.nblk);
+    const int bt = batch_tile(a.nb);
+    const size_t lds = down_lds_bytes(a.rows_per_group, bt);
     const int grid = a.gc * a.gr;
-    switch (batch_tile(a.nb)) {
-    case 1: k_down<1><<<grid, kBlock, lds, s>>>(a); break;
-    case 2: k_down<2><<<grid, kBlock, lds, s>>>(a); break;
-    case 4: k_down<4><<<grid, kBlock, lds, s>>>(a); break;
-    default: k_down<8><<<grid, kBlock, lds, s>>>(a); break;
+    switch (bt) {
+    case 1: allow_lds(k_down<1>, lds); k_down<1><<<grid, kBlock, lds, s>>>(a); break;
+    case 2: allow_lds(k_down<2>, lds); k_down<2><<<grid, kBlock, lds, s>>>(a); break;
+    case 4: allow_lds(k_down<4>, lds); k_down<4><<<grid, kBlock, lds, s>>>(a); break;
+    default: allow_lds(k_down<8>, lds); k_down<8><<<grid, kBlock, lds, s>>>(a); break;
     }
+    return hipGetLastError();
+}
+
+hipError_t launch_export(const int *act, const float *s_rows, int nb, int d_ff, int *idx_dst,
+                         int *n_dst, float *s_dst, hipStream_t s)
+{
+    k_export<<<1, kExportThreads, 0, s>>>(act, s_rows, nb, d_ff, idx_dst, n_dst, s_dst);
     return hipGetLastError();
 }
 

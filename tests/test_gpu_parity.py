@@ -65,7 +65,7 @@ def run_gpu(plan, variant, layer, x, thld):
         y = cd.countdown_ffn_dense(plan, xd, D["W_gate"], D["W_up"], D["W_down"])
     else:
         raise ValueError(variant)
-    idx, s_c, coef = cd.countdown_copy_last_active(plan)
+    idx, s_c, coef = cd.countdown_export_active(plan)
     return (y.cpu().numpy().astype(np.float64), idx.cpu().numpy(), s_c.cpu().numpy(),
             None if coef is None else coef.cpu().numpy())
 
@@ -234,9 +234,9 @@ def test_nondefault_stream_and_repeatability(tiny):
     s = torch.cuda.Stream()
     with torch.cuda.stream(s):
         y1 = cd.countdown_ffn_dual(plan, X, D["W_gate"], D["W_up"], D["W_down"], thld)
-        i1 = cd.countdown_copy_last_active(plan)[0].clone()
+        i1 = cd.countdown_export_active(plan)[0].clone()
         y2 = cd.countdown_ffn_dual(plan, X, D["W_gate"], D["W_up"], D["W_down"], thld)
-        i2 = cd.countdown_copy_last_active(plan)[0].clone()
+        i2 = cd.countdown_export_active(plan)[0].clone()
     s.synchronize()
     assert torch.equal(i1, i2)
     torch.testing.assert_close(y1, y2, rtol=0, atol=1e-6 * float(y1.abs().max()))
@@ -313,7 +313,7 @@ def test_calibration_selects_exact_order_statistics():
         _, q = cd.countdown_calibrate(plan, cd.CD_VARIANT_MONO, dev_bf16(X), k, W_up=D["W_up"])
         y = cd.countdown_ffn_mono(plan, dev_bf16(X), D["W_gate"], D["W_up"], D["W_down"],
                                   math.inf)
-        coef = cd.countdown_copy_last_active(plan)[2].cpu().numpy().astype(np.float64)
+        coef = cd.countdown_export_active(plan)[2].cpu().numpy().astype(np.float64)
         for t in range(6):
             v = np.sort(np.abs(coef[t]))
             h = k * (dff - 1)
@@ -321,3 +321,40 @@ def test_calibration_selects_exact_order_statistics():
             hi = min(lo + 1, dff - 1)
             assert q[t].item() == v[lo] + (h - lo) * (v[hi] - v[lo])
         del y
+
+
+def test_graph_replay_matches_eager(tiny):
+    """FFN calls captured in a HIP graph and replayed several times, with eager work
+    between the replays, give the eager results every time."""
+    from paper_2505_17701_amd import binding as cd
+
+    w, layer = tiny
+    thld_m = calibrated("mono", layer, w.wid, 0.9, T=64)
+    thld_d = calibrated("dual_ideal", layer, w.wid, 0.9, T=64)
+    pm, pd = plan_for(layer, keep_coef=False), plan_for(layer, keep_coef=False)
+    X = dev_bf16(w.tokens(4))
+    D = layer.d
+    ys = [torch.empty((1, layer.d_model), dtype=torch.float32, device="cuda") for _ in range(8)]
+
+    def calls():
+        for t in range(4):
+            cd.countdown_ffn_mono(pm, X[t:t + 1], D["W_gate"], D["W_up"], D["W_down"], thld_m,
+                                  y=ys[t])
+            cd.countdown_ffn_dual(pd, X[t:t + 1], D["W_gate"], D["W_up"], D["W_down"], thld_d,
+                                  y=ys[4 + t])
+
+    calls()
+    torch.cuda.synchronize()
+    eager = [y.clone() for y in ys]
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        calls()
+    for rep in range(3):
+        for y in ys:
+            y.fill_(float("nan"))
+        cd.countdown_ffn_dense(pm, X[:1], D["W_gate"], D["W_up"], D["W_down"])  # eager work
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        for y, e in zip(ys, eager):
+            torch.testing.assert_close(y, e, rtol=0, atol=1e-6 * float(e.abs().max()) + 1e-30)
