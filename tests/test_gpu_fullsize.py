@@ -43,7 +43,7 @@ def llama3_pred():
     return w, Layer(w.layer(), w.predictor())
 
 
-@pytest.mark.parametrize("B", [1, 4, 8])
+@pytest.mark.parametrize("B", [1, 2, 4, 8])
 def test_llama3_predictor_batch_union(llama3_pred, B):
     w, layer = llama3_pred
     thld = calibrated("dual_pred", layer, w.wid, 0.9, T=32)
@@ -55,14 +55,20 @@ def test_llama3_predictor_batch_union(llama3_pred, B):
     print(f"8b pred B={B}: n={n} flips={flips} rel_err={rel:.2e}", flush=True)
 
 
-@pytest.mark.parametrize("k", [0.9])
-def test_llama70b_layer(k):
+@pytest.fixture(scope="module")
+def llama70b():
     w = WORKLOADS["llama70b_8192x28672"]
     layer = Layer(w.layer())
+    yield w, layer
+    del layer
+    torch.cuda.empty_cache()
+
+
+@pytest.mark.parametrize("k", [0.9, 0.7])
+def test_llama70b_layer(llama70b, k):
+    w, layer = llama70b
     thld = calibrated("mono", layer, w.wid, k, T=8)
     plan = plan_for(layer)
     n, flips, rel = compare(plan, "mono", layer, w.tokens(1), thld, f"70b mono k={k}")
     print(f"70b mono k={k}: n={n} flips={flips} rel_err={rel:.2e}", flush=True)
     compare(plan, "dense", layer, w.tokens(1), 0.0, "70b dense", check_coef=False)
-    del layer
-    torch.cuda.empty_cache()

@@ -180,10 +180,11 @@ def test_all_rows_equals_dense_and_none_gives_zero(tiny, variant):
     assert len(idx0) == 0 and np.all(y0 == 0.0)
 
 
-def test_dense_parity(tiny):
+@pytest.mark.parametrize("B", [1, 2, 4])
+def test_dense_parity(tiny, B):
     w, layer = tiny
     plan = plan_for(layer, max_batch=4)
-    compare(plan, "dense", layer, w.tokens(4), 0.0, "dense")
+    compare(plan, "dense", layer, w.tokens(B), 0.0, f"dense B={B}")
 
 
 def test_single_active_row(tiny):
@@ -198,7 +199,8 @@ def test_single_active_row(tiny):
 
 
 @pytest.mark.parametrize("d_model,d_ff,B", [(264, 1000, 3), (1032, 520, 2), (8, 8, 1),
-                                            (2056, 4104, 7), (512, 16, 4)])
+                                            (2056, 4104, 7), (512, 16, 4), (8192, 1048, 1),
+                                            (1544, 2056, 2), (4096, 776, 1)])
 @pytest.mark.parametrize("variant", ["mono", "dual_ideal", "dual_pred"])
 def test_ragged_shapes(d_model, d_ff, B, variant):
     L = make_layer(700 + d_model, d_model, d_ff, 0.05)
@@ -211,7 +213,7 @@ def test_ragged_shapes(d_model, d_ff, B, variant):
         u, g, s = oracle.coefficients(x, L["W_gate"], L["W_up"])
         c = np.abs(u if variant == "mono" else s)
     thld = float(np.float32(np.quantile(c, 0.7)))
-    plan = plan_for(layer, max_batch=8)
+    plan = plan_for(layer, max_batch=min(8, 32768 // d_model))
     compare(plan, variant, layer, x, thld, f"ragged {d_model}x{d_ff} B={B} {variant}")
 
 
@@ -219,7 +221,7 @@ def test_plan_reuse_with_shrinking_batch(tiny):
     w, layer = tiny
     thld = calibrated("mono", layer, w.wid, 0.9, T=64)
     plan = plan_for(layer, max_batch=8)
-    for B in (8, 3, 1, 5):
+    for B in (8, 3, 1, 5, 2, 1):
         compare(plan, "mono", layer, w.tokens(B), thld, f"reuse B={B}")
 
 
@@ -246,9 +248,9 @@ def test_timing_records_every_launch(tiny):
     from paper_2505_17701_amd import binding as cd
 
     w, layer = tiny
-    plan = plan_for(layer, timing=True, keep_coef=False)
     X = dev_bf16(w.tokens(1))
     D = layer.d
+    plan = plan_for(layer, timing=True, keep_coef=False)
     for _ in range(5):
         cd.countdown_ffn_mono(plan, X, D["W_gate"], D["W_up"], D["W_down"], 0.5)
     t = cd.countdown_timing_collect(plan)
