@@ -27,7 +27,8 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBS = 8000.0  # MI355X HBM3E peak, GB/s
-SPIN_CYCLES = 40_000_000  # bounded spin (tens of ms) that puts the timing pass behind a backlog
+KERNEL_SRC = os.path.join(ROOT, "paper_2505_17701_amd", "csrc", "cd_kernels.hip")
+TRAFFIC_SUMMARY = os.path.join(ROOT, "profiles", "k_coef_mono_llama7b_4096x11008_k0.9_traffic.md")
 
 
 def log(*a):
@@ -54,7 +55,31 @@ def parse():
     p.add_argument("--cpu-seconds", type=float, default=12.0,
                    help="time budget of the oracle CPU baseline (0 disables it)")
     p.add_argument("--no-extra", action="store_true", help="skip the secondary variants")
+    p.add_argument("--traffic-probe", action="store_true",
+                   help="first copy a 256 MiB device buffer 3 times (the known-size reference "
+                        "for FETCH_SIZE / WRITE_SIZE counters)")
     return p.parse_args()
+
+
+def measured_traffic():
+    """HBM bytes per launch of the dominant kernel from the committed FETCH_SIZE /
+    WRITE_SIZE summary, or None when the kernel source changed since it was taken."""
+    import hashlib
+
+    if not os.path.exists(TRAFFIC_SUMMARY):
+        return None
+    fields = {}
+    for line in open(TRAFFIC_SUMMARY):
+        if ":" in line and line.startswith("- "):
+            k, v = line[2:].split(":", 1)
+            fields[k.strip()] = v.strip().strip("`")
+    digest = hashlib.sha256(open(KERNEL_SRC, "rb").read()).hexdigest()
+    if fields.get("kernel_source_sha256") != digest:
+        return None
+    try:
+        return float(fields["hbm_bytes_per_launch"])
+    except (KeyError, ValueError):
+        return None
 
 
 def time_steps(fn, steps, warmup, stream):
@@ -120,6 +145,13 @@ def main():
     w = WORKLOADS[args.workload]
     dm, dff = w.d_model, w.d_ff
     stream = torch.cuda.current_stream()
+    if args.traffic_probe:
+        src = torch.ones(64 << 20, dtype=torch.float32, device="cuda")  # 256 MiB
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
 
     t = time.time()
     layers = []
@@ -167,52 +199,44 @@ def main():
 
     def measure(variant, k, steps, warmup):
         plan = cd.Plan(dm, dff, max_batch=1)
-        ms_eager = time_steps(make_step(plan, variant, k), steps, warmup, stream)
-        ms = time_steps_graph(make_step(plan, variant, k), steps, warmup)
-        plan.close()
-        # second pass: per-kernel durations from a HIP event pair around every launch on
-        # the launch stream. A bounded spin kernel first gives the stream a backlog so the
-        # host enqueues ahead of the GPU and each pair brackets only its kernel.
-        nsteps = min(steps, 256)
-        tplan = cd.Plan(dm, dff, max_batch=1, timing=True)
-        step = make_step(tplan, variant, k)
-        for i in range(min(warmup, 20)):
-            step(i)
-        torch.cuda.synchronize()
-        cd.countdown_timing_collect(tplan)
-        torch.cuda._sleep(SPIN_CYCLES)
-        for i in range(nsteps):
-            step(i)
-        kt = cd.countdown_timing_collect(tplan)
-        tplan.close()
-        # third pass: |IDX| of every call, for the byte counts
-        nplan = cd.Plan(dm, dff, max_batch=1)
-        n_arr = torch.zeros(nsteps, dtype=torch.int32, device="cuda")
-        step = make_step(nplan, variant, k)
+        step = make_step(plan, variant, k)
+        ms_eager = time_steps(step, steps, warmup, stream)
+        ms = time_steps_graph(step, steps, warmup)
+        # per-kernel averages: graph-replayed loops of a single kernel (the plan's phase
+        # selection), each bracketed by one HIP event pair on the launch stream
+        nk = min(steps, 512)
+        cd.countdown_plan_set_phases(plan, cd.CD_PHASE_COEF)
+        ms_coef = time_steps_graph(step, nk, 20)
         lib = cd.load_library()
-        for i in range(nsteps):
+        n_down = torch.zeros(1, dtype=torch.int32, device="cuda")
+        lib.countdown_export_active(plan.handle, None, n_down.data_ptr(), None, None,
+                                    stream.cuda_stream)
+        cd.countdown_plan_set_phases(plan, cd.CD_PHASE_DOWN)  # rows of the last coef call
+        ms_down = time_steps_graph(step, nk, 20)
+        cd.countdown_plan_set_phases(plan, cd.CD_PHASE_ALL)
+        # |IDX| of every call of the loop, for the byte counts
+        n_arr = torch.zeros(nk, dtype=torch.int32, device="cuda")
+        for i in range(nk):
             step(i)
-            lib.countdown_export_active(nplan.handle, None, n_arr[i:i + 1].data_ptr(), None,
+            lib.countdown_export_active(plan.handle, None, n_arr[i:i + 1].data_ptr(), None,
                                         None, stream.cuda_stream)
         torch.cuda.synchronize()
-        nplan.close()
+        plan.close()
         n = n_arr.cpu().numpy().astype(np.float64)
         per = [traffic.algorithmic_bytes(variant, dm, dff, int(v)) for v in n]
         res = {"ms_per_step": ms, "us_per_layer": ms * 1e3, "tokens_per_s": 1e3 / ms,
                "us_per_layer_eager": ms_eager * 1e3,
                "n_active_mean": float(n.mean()), "realised_sparsity": float(1 - n.mean() / dff)}
+        kbytes = {"coef": float(np.mean([p["coef"] for p in per])),
+                  "down": traffic.algorithmic_bytes(variant, dm, dff, int(n_down.item()))["down"]}
+        for name, kms in (("coef", ms_coef), ("down", ms_down)):
+            res[f"{name}_kernel_us"] = kms * 1e3
+            res[f"{name}_kernel_bytes"] = kbytes[name]
+            res[f"{name}_kernel_GBs"] = kbytes[name] / (kms * 1e-3) / 1e9
         tot_bytes = float(np.mean([p["total"] for p in per]))
         res["algorithmic_bytes"] = tot_bytes
         res["achieved_GBs"] = tot_bytes / (ms * 1e-3) / 1e9
         res["frac_hbm_peak"] = res["achieved_GBs"] / HBM_PEAK_GBS
-        for name in ("coef", "down"):
-            cnt, tms = kt[name]
-            if cnt:
-                avg_us = tms / cnt * 1e3
-                kb = float(np.mean([p[name] for p in per]))
-                res[f"{name}_kernel_us"] = avg_us
-                res[f"{name}_kernel_GBs"] = kb / (avg_us * 1e-6) / 1e9
-                res[f"{name}_kernel_bytes"] = kb
         return res
 
     main_res = measure(args.variant, args.k, args.steps, args.warmup)
@@ -263,7 +287,9 @@ def main():
         desc = "k_coef_mono (dense W_up GEMV, threshold, wave-local W_gate gather, s)"
         roof = {"bound": "hbm", "kernel": desc,
                 "achieved": main_res[f"{dom}_kernel_GBs"], "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                "frac": main_res[f"{dom}_kernel_GBs"] / HBM_PEAK_GBS, "traffic": None,
+                "frac": main_res[f"{dom}_kernel_GBs"] / HBM_PEAK_GBS,
+                "traffic": measured_traffic() if (args.workload, args.variant, args.k) ==
+                ("llama7b_4096x11008", "mono", 0.9) else None,
                 "bytes_per_launch": main_res[f"{dom}_kernel_bytes"],
                 "avg_launch_us": main_res[f"{dom}_kernel_us"]}
 

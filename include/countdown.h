@@ -63,7 +63,6 @@ typedef int cd_status;
 /* Plan flags. */
 #define CD_PLAN_KEEP_COEF 1u  /* also store the dense coefficient vector of each call
                                  (u for mono, s for dual ideal, s_hat for dual pred) */
-#define CD_PLAN_TIMING 2u     /* record a HIP event pair around every kernel launch */
 
 typedef struct cd_plan cd_plan;
 
@@ -143,17 +142,20 @@ cd_status countdown_export_active(const cd_plan *plan, int32_t *idx_dst, int32_t
                                   float *s_dst, float *coef_dst, void *stream);
 
 /*
- * Kernel timing of a CD_PLAN_TIMING plan: waits for the recorded launches,
- * then writes per kernel kind (see CD_KERNEL_*) the number of launches and
- * the summed duration in milliseconds since the last reset, and resets.
- * counts / ms have CD_KERNEL_KINDS entries.
+ * Measurement aid: choose which kernels the plan's subsequent FFN calls
+ * launch. Every call runs its coefficient kernel (predictor latent, dense
+ * coefficient, threshold, gathered gate or gate+up; it writes the plan's
+ * per-neuron active flags and coefficients and zeroes y) and then its down
+ * kernel (gathered down projection into y). CD_PHASE_COEF or CD_PHASE_DOWN
+ * alone launch only that kernel, so a loop of calls times one kernel in
+ * isolation; y is then not the FFN output. A down-only call uses the flags
+ * and coefficients left by the plan's last coefficient kernel (CD_EINVAL if
+ * there is none). Plans start at CD_PHASE_ALL.
  */
-#define CD_KERNEL_COEF 0     /* coefficient / threshold / local compaction (+ gate or gate+up) */
-#define CD_KERNEL_DOWN 1     /* gathered down projection */
-#define CD_KERNEL_LATENT 2   /* predictor latent x.theta_A */
-#define CD_KERNEL_SELECT 3   /* calibration order statistics */
-#define CD_KERNEL_KINDS 4
-cd_status countdown_timing_collect(cd_plan *plan, int *counts, double *ms);
+#define CD_PHASE_COEF 1u
+#define CD_PHASE_DOWN 2u
+#define CD_PHASE_ALL 3u
+cd_status countdown_plan_set_phases(cd_plan *plan, unsigned phases);
 
 /*
  * Host-only validation of an FFN call's arguments against a shape, exactly
@@ -174,7 +176,7 @@ cd_status countdown_check_shape(int d_model, int d_ff, int max_batch, int d_rank
 const char *countdown_status_string(cd_status status);
 
 /* ABI version of this header (bumped on any signature change). */
-#define COUNTDOWN_ABI_VERSION 2
+#define COUNTDOWN_ABI_VERSION 3
 int countdown_abi_version(void);
 
 #ifdef __cplusplus

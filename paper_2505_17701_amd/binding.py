@@ -16,15 +16,14 @@ LIB_PATH = os.path.join(PKG, "libcountdown.so")
 
 CD_OK, CD_EINVAL, CD_EUNSUPPORTED, CD_EHIP, CD_ENOMEM = 0, -1, -2, -3, -4
 CD_VARIANT_MONO, CD_VARIANT_DUAL_IDEAL, CD_VARIANT_DUAL_PRED, CD_VARIANT_DENSE = 0, 1, 2, 3
-CD_PLAN_KEEP_COEF, CD_PLAN_TIMING = 1, 2
-CD_KERNEL_COEF, CD_KERNEL_DOWN, CD_KERNEL_LATENT, CD_KERNEL_SELECT, CD_KERNEL_KINDS = 0, 1, 2, 3, 4
-KERNEL_NAMES = ("coef", "down", "latent", "select")
+CD_PLAN_KEEP_COEF = 1
+CD_PHASE_COEF, CD_PHASE_DOWN, CD_PHASE_ALL = 1, 2, 3
 
 # every symbol include/countdown.h declares
 EXPORTS = (
     "countdown_plan_create", "countdown_plan_destroy", "countdown_ffn_mono", "countdown_ffn_dual",
     "countdown_ffn_dense", "countdown_calibrate", "countdown_export_active",
-    "countdown_timing_collect", "countdown_check_args",
+    "countdown_plan_set_phases", "countdown_check_args",
     "countdown_check_shape", "countdown_status_string", "countdown_abi_version",
 )
 
@@ -55,7 +54,7 @@ def load_library(path: str = LIB_PATH):
         "countdown_ffn_dense": (i, [vp, vp, i, vp, vp, vp, vp, vp]),
         "countdown_calibrate": (i, [vp, i, vp, i, vp, vp, vp, vp, d, vp, vp, vp]),
         "countdown_export_active": (i, [vp, vp, vp, vp, vp, vp]),
-        "countdown_timing_collect": (i, [vp, C.POINTER(i), C.POINTER(d)]),
+        "countdown_plan_set_phases": (i, [vp, u]),
         "countdown_check_args": (i, [i, i, i, i, i, vp, i, vp, vp, vp, vp, vp, f, vp]),
         "countdown_check_shape": (i, [i, i, i, i]),
         "countdown_status_string": (C.c_char_p, [i]),
@@ -117,9 +116,9 @@ class Plan:
     """Owns a ``cd_plan``: shape, workspace, and optional timing/coefficient capture."""
 
     def __init__(self, d_model: int, d_ff: int, max_batch: int = 1, d_rank: int = 0,
-                 keep_coef: bool = False, timing: bool = False):
+                 keep_coef: bool = False):
         self.d_model, self.d_ff, self.max_batch, self.d_rank = d_model, d_ff, max_batch, d_rank
-        flags = (CD_PLAN_KEEP_COEF if keep_coef else 0) | (CD_PLAN_TIMING if timing else 0)
+        flags = CD_PLAN_KEEP_COEF if keep_coef else 0
         h = C.c_void_p()
         _check(load_library().countdown_plan_create(d_model, d_ff, max_batch, d_rank, flags,
                                                     C.byref(h)), "countdown_plan_create")
@@ -145,8 +144,8 @@ class Plan:
         self.close()
 
 
-def countdown_plan_create(d_model, d_ff, max_batch=1, d_rank=0, keep_coef=False, timing=False):
-    return Plan(d_model, d_ff, max_batch, d_rank, keep_coef, timing)
+def countdown_plan_create(d_model, d_ff, max_batch=1, d_rank=0, keep_coef=False):
+    return Plan(d_model, d_ff, max_batch, d_rank, keep_coef)
 
 
 def countdown_plan_destroy(plan: Plan) -> None:
@@ -227,13 +226,10 @@ def countdown_export_active(plan: Plan, stream=None):
     return idx[:m], s[:, :m], coef
 
 
-def countdown_timing_collect(plan: Plan) -> dict:
-    """Per kernel kind: ``{name: (launches, total_ms)}`` since the last collect."""
-    counts = (C.c_int * CD_KERNEL_KINDS)()
-    ms = (C.c_double * CD_KERNEL_KINDS)()
-    _check(load_library().countdown_timing_collect(plan.handle, counts, ms),
-           "countdown_timing_collect")
-    return {KERNEL_NAMES[i]: (counts[i], ms[i]) for i in range(CD_KERNEL_KINDS)}
+def countdown_plan_set_phases(plan: Plan, phases: int) -> None:
+    """Launch only the kernels in ``phases`` (CD_PHASE_*) on later calls (measurement aid)."""
+    _check(load_library().countdown_plan_set_phases(plan.handle, int(phases)),
+           "countdown_plan_set_phases")
 
 
 def countdown_check_args(variant, d_model, d_ff, max_batch, d_rank, x, B, W_gate, W_up, W_down,

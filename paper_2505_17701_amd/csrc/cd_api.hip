@@ -17,17 +17,11 @@ constexpr int kMaxDModel = 8192;
 constexpr int kMaxBatch = 8;
 constexpr int kMaxRank = 1024;
 constexpr int kMaxBatchCols = 32768;  // max_batch * d_model (batch tiles of 4 and 8 stage x in LDS)
-constexpr int kMaxTimedLaunches = 1 << 16;
 constexpr int kDownWaves = 2048;      // target waves of the down kernel grid
 
 bool aligned16(const void *p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
 
 bool is_pow2(int v) { return v > 0 && (v & (v - 1)) == 0; }
-
-struct Timed {
-    int kind;
-    hipEvent_t ev[2];
-};
 
 }  // namespace
 
@@ -41,49 +35,15 @@ struct cd_plan {
     float *s;                     // [max_batch][d_ff] coefficients s of active neurons
     float *coef;                  // [max_batch][d_ff] dense coefficients (CD_PLAN_KEEP_COEF)
     float *lat;                   // [max_batch][d_rank] predictor latent
-    std::vector<Timed> timed;     // recorded launches since the last collect
-    std::vector<hipEvent_t> pool; // free events
+    unsigned phases;              // kernels launched per call (CD_PHASE_*)
+    bool has_state;               // act / s hold a coefficient kernel's output
 };
 
 namespace {
 
 cd_status hip_status(hipError_t e) { return e == hipSuccess ? CD_OK : CD_EHIP; }
 
-hipEvent_t take_event(cd_plan *p)
-{
-    if (!p->pool.empty()) {
-        hipEvent_t e = p->pool.back();
-        p->pool.pop_back();
-        return e;
-    }
-    hipEvent_t e = nullptr;
-    if (hipEventCreate(&e) != hipSuccess)
-        return nullptr;
-    return e;
-}
-
-// Run one launch, bracketed by an event pair when the plan records timings.
-template <class F>
-cd_status timed_launch(cd_plan *p, int kind, hipStream_t s, F &&launch)
-{
-    const bool rec = (p->flags & CD_PLAN_TIMING) && (int)p->timed.size() < kMaxTimedLaunches;
-    Timed t{kind, {nullptr, nullptr}};
-    if (rec) {
-        t.ev[0] = take_event(p);
-        t.ev[1] = take_event(p);
-        if (!t.ev[0] || !t.ev[1] || hipEventRecord(t.ev[0], s) != hipSuccess)
-            return CD_EHIP;
-    }
-    const hipError_t e = launch();
-    if (e != hipSuccess)
-        return CD_EHIP;
-    if (rec) {
-        if (hipEventRecord(t.ev[1], s) != hipSuccess)
-            return CD_EHIP;
-        p->timed.push_back(t);
-    }
-    return CD_OK;
-}
+cd_status launched(hipError_t e) { return e == hipSuccess ? CD_OK : CD_EHIP; }
 
 cd_status check_shape(int d_model, int d_ff, int max_batch, int d_rank)
 {
@@ -181,21 +141,26 @@ cd_status run_ffn(cd_plan *p, int variant, const uint16_t *x, int B, const uint1
     if (st != CD_OK)
         return st;
     hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+    if (!(p->phases & CD_PHASE_COEF) && !p->has_state)
+        return CD_EINVAL;  // a down-only call needs a previous coefficient kernel's output
     p->last_batch = B;
-    if (variant == CD_VARIANT_DUAL_PRED) {
-        st = timed_launch(p, CD_KERNEL_LATENT, s, [&] {
-            return cdk::launch_latent(x, B, At, p->d_model, p->d_rank, p->lat, s);
-        });
+    if (p->phases & CD_PHASE_COEF) {
+        if (variant == CD_VARIANT_DUAL_PRED) {
+            st = launched(cdk::launch_latent(x, B, At, p->d_model, p->d_rank, p->lat, s));
+            if (st != CD_OK)
+                return st;
+        }
+        const cdk::CoefArgs ca = coef_args(p, x, B, Wg, Wu, Bt, thld, y);
+        st = launched(cdk::launch_coef(kernel_variant(variant), ca, s));
         if (st != CD_OK)
             return st;
+        p->has_state = true;
     }
-    const cdk::CoefArgs ca = coef_args(p, x, B, Wg, Wu, Bt, thld, y);
-    st = timed_launch(p, CD_KERNEL_COEF, s,
-                      [&] { return cdk::launch_coef(kernel_variant(variant), ca, s); });
-    if (st != CD_OK)
-        return st;
-    const cdk::DownArgs da = down_args(p, B, Wd, y);
-    return timed_launch(p, CD_KERNEL_DOWN, s, [&] { return cdk::launch_down(da, s); });
+    if (p->phases & CD_PHASE_DOWN) {
+        const cdk::DownArgs da = down_args(p, B, Wd, y);
+        st = launched(cdk::launch_down(da, s));
+    }
+    return st;
 }
 
 template <class T>
@@ -217,12 +182,6 @@ void release(cd_plan *p)
     for (void *b : bufs)
         if (b)
             (void)hipFree(b);
-    for (const Timed &t : p->timed) {
-        (void)hipEventDestroy(t.ev[0]);
-        (void)hipEventDestroy(t.ev[1]);
-    }
-    for (hipEvent_t e : p->pool)
-        (void)hipEventDestroy(e);
     delete p;
 }
 
@@ -266,7 +225,7 @@ cd_status countdown_plan_create(int d_model, int d_ff, int max_batch, int d_rank
     cd_status st = check_shape(d_model, d_ff, max_batch, d_rank);
     if (st != CD_OK)
         return st;
-    if (flags & ~(CD_PLAN_KEEP_COEF | CD_PLAN_TIMING))
+    if (flags & ~CD_PLAN_KEEP_COEF)
         return CD_EINVAL;
     int dev = 0;
     if (hipGetDevice(&dev) != hipSuccess)
@@ -281,6 +240,8 @@ cd_status countdown_plan_create(int d_model, int d_ff, int max_batch, int d_rank
     p->flags = flags;
     p->device = dev;
     p->last_batch = 0;
+    p->phases = CD_PHASE_ALL;
+    p->has_state = false;
     // down grid: one 512-column chunk per workgroup column and ~kDownWaves
     // waves, with at least 16 neurons per group
     p->gc = (d_model + 511) / 512;
@@ -372,23 +333,20 @@ cd_status countdown_calibrate(cd_plan *p, int variant, const uint16_t *X, int T,
         const int nb = T - t0 < tb ? T - t0 : tb;
         const uint16_t *xb = X + (size_t)t0 * p->d_model;
         if (pred) {
-            st = timed_launch(p, CD_KERNEL_LATENT, s, [&] {
-                return cdk::launch_latent(xb, nb, A_t, p->d_model, p->d_rank, p->lat, s);
-            });
+            st = launched(cdk::launch_latent(xb, nb, A_t, p->d_model, p->d_rank, p->lat, s));
             if (st != CD_OK)
                 break;
         }
         cdk::CoefArgs a = coef_args(p, xb, nb, wg, W_up, B_t, INFINITY, ybuf);
         a.coef = coef;
-        st = timed_launch(p, CD_KERNEL_COEF, s, [&] { return cdk::launch_coef(variant, a, s); });
+        st = launched(cdk::launch_coef(variant, a, s));
         if (st != CD_OK)
             break;
-        st = timed_launch(p, CD_KERNEL_SELECT, s, [&] {
-            return cdk::launch_select(coef, p->d_ff, p->d_ff, nb, pred ? 0 : 1, k, q + t0, s);
-        });
+        st = launched(cdk::launch_select(coef, p->d_ff, p->d_ff, nb, pred ? 0 : 1, k, q + t0, s));
     }
     // the act / s workspace now describes a calibration batch, not an FFN call
     p->last_batch = 0;
+    p->has_state = false;
     if (st == CD_OK)
         st = hip_status(cdk::launch_mean(q, T, thld_out, s));
     if (st == CD_OK && q_out)
@@ -417,29 +375,12 @@ cd_status countdown_export_active(const cd_plan *p, int32_t *idx_dst, int32_t *n
     return hip_status(e);
 }
 
-cd_status countdown_timing_collect(cd_plan *p, int *counts, double *ms)
+cd_status countdown_plan_set_phases(cd_plan *p, unsigned phases)
 {
-    if (!p || !counts || !ms)
+    if (!p || phases == 0 || (phases & ~CD_PHASE_ALL))
         return CD_EINVAL;
-    for (int i = 0; i < CD_KERNEL_KINDS; ++i) {
-        counts[i] = 0;
-        ms[i] = 0.0;
-    }
-    cd_status st = CD_OK;
-    if (!p->timed.empty() && hipEventSynchronize(p->timed.back().ev[1]) != hipSuccess)
-        st = CD_EHIP;
-    for (const Timed &t : p->timed) {
-        float v = 0.0f;
-        if (st == CD_OK && hipEventElapsedTime(&v, t.ev[0], t.ev[1]) == hipSuccess &&
-            t.kind >= 0 && t.kind < CD_KERNEL_KINDS) {
-            counts[t.kind] += 1;
-            ms[t.kind] += v;
-        }
-        p->pool.push_back(t.ev[0]);
-        p->pool.push_back(t.ev[1]);
-    }
-    p->timed.clear();
-    return st;
+    p->phases = phases;
+    return CD_OK;
 }
 
 }  // extern "C"

@@ -49,7 +49,7 @@ def test_header_compiles_as_c():
 
 
 def test_abi_version_and_status_strings(lib):
-    assert cd.countdown_abi_version() == 2
+    assert cd.countdown_abi_version() == 3
     for st in (cd.CD_OK, cd.CD_EINVAL, cd.CD_EUNSUPPORTED, cd.CD_EHIP, cd.CD_ENOMEM):
         assert cd.status_string(st).startswith(("CD_OK", "CD_E"))
     assert "unknown" in cd.status_string(12345)
@@ -117,7 +117,8 @@ def test_null_plan_is_rejected_without_device(lib):
     assert lib.countdown_ffn_dual(None, 0x1000, 1, 0x2000, 0x3000, 0x4000, None, None, 1.0,
                                   0x5000, None) == cd.CD_EINVAL
     assert lib.countdown_plan_destroy(None) == cd.CD_OK
-    assert lib.countdown_timing_collect(None, None, None) == cd.CD_EINVAL
+    assert lib.countdown_plan_set_phases(None, cd.CD_PHASE_ALL) == cd.CD_EINVAL
+    assert lib.countdown_export_active(None, None, None, None, None, None) == cd.CD_EINVAL
 
 
 def test_plan_create_rejects_bad_sizes_before_any_hip_call(lib):
@@ -126,4 +127,5 @@ def test_plan_create_rejects_bad_sizes_before_any_hip_call(lib):
     h = C.c_void_p()
     assert lib.countdown_plan_create(4100, 11008, 1, 0, 0, C.byref(h)) == cd.CD_EINVAL
     assert lib.countdown_plan_create(4096, 11008, 1, 0, 0x80, C.byref(h)) == cd.CD_EINVAL
+    assert lib.countdown_plan_create(4096, 11008, 1, 0, 2, C.byref(h)) == cd.CD_EINVAL
     assert h.value is None

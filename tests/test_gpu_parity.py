@@ -121,11 +121,10 @@ def compare(plan, variant, layer, x, thld, label, check_coef=True):
     return len(idx_g), flips, rel
 
 
-def plan_for(layer, max_batch=1, keep_coef=True, timing=False):
+def plan_for(layer, max_batch=1, keep_coef=True):
     from paper_2505_17701_amd import binding as cd
 
-    return cd.Plan(layer.d_model, layer.d_ff, max_batch, layer.d_rank, keep_coef=keep_coef,
-                   timing=timing)
+    return cd.Plan(layer.d_model, layer.d_ff, max_batch, layer.d_rank, keep_coef=keep_coef)
 
 
 def calibrated(variant, layer, wid, k, T=32, outlier_frac=0.0):
@@ -244,19 +243,38 @@ def test_nondefault_stream_and_repeatability(tiny):
     torch.testing.assert_close(y1, y2, rtol=0, atol=1e-6 * float(y1.abs().max()))
 
 
-def test_timing_records_every_launch(tiny):
+def test_phase_selection(tiny):
+    """Coefficient-only then down-only calls reproduce the full call; a down-only call
+    needs a previous coefficient kernel on the plan."""
     from paper_2505_17701_amd import binding as cd
 
     w, layer = tiny
-    X = dev_bf16(w.tokens(1))
+    thld = calibrated("mono", layer, w.wid, 0.9, T=64)
     D = layer.d
-    plan = plan_for(layer, timing=True, keep_coef=False)
-    for _ in range(5):
-        cd.countdown_ffn_mono(plan, X, D["W_gate"], D["W_up"], D["W_down"], 0.5)
-    t = cd.countdown_timing_collect(plan)
-    assert t["coef"][0] == 5 and t["down"][0] == 5 and t["latent"][0] == 0
-    assert t["coef"][1] > 0 and t["down"][1] > 0
-    assert cd.countdown_timing_collect(plan)["coef"][0] == 0
+    X = dev_bf16(w.tokens(2))
+    plan = plan_for(layer, max_batch=2, keep_coef=False)
+    y_full = cd.countdown_ffn_mono(plan, X, D["W_gate"], D["W_up"], D["W_down"], thld)
+    cd.countdown_plan_set_phases(plan, cd.CD_PHASE_COEF)
+    y_c = torch.full_like(y_full, float("nan"))
+    cd.countdown_ffn_mono(plan, X, D["W_gate"], D["W_up"], D["W_down"], thld, y=y_c)
+    torch.cuda.synchronize()
+    assert torch.all(y_c == 0)  # the coefficient kernel zeroes y for the down kernel
+    cd.countdown_plan_set_phases(plan, cd.CD_PHASE_DOWN)
+    for _ in range(2):
+        y_d = torch.zeros_like(y_full)
+        cd.countdown_ffn_mono(plan, X, D["W_gate"], D["W_up"], D["W_down"], thld, y=y_d)
+        torch.testing.assert_close(y_d, y_full, rtol=0, atol=1e-6 * float(y_full.abs().max()))
+    cd.countdown_plan_set_phases(plan, cd.CD_PHASE_ALL)
+    torch.testing.assert_close(
+        cd.countdown_ffn_mono(plan, X, D["W_gate"], D["W_up"], D["W_down"], thld), y_full,
+        rtol=0, atol=1e-6 * float(y_full.abs().max()))
+    fresh = plan_for(layer, keep_coef=False)
+    cd.countdown_plan_set_phases(fresh, cd.CD_PHASE_DOWN)
+    with pytest.raises(cd.CountdownError):
+        cd.countdown_ffn_mono(fresh, X[:1], D["W_gate"], D["W_up"], D["W_down"], thld)
+    for bad in (0, 4, 7):
+        with pytest.raises(cd.CountdownError):
+            cd.countdown_plan_set_phases(fresh, bad)
 
 
 def test_bad_calls_raise(tiny):
