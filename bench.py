@@ -54,7 +54,10 @@ def parse():
     p.add_argument("--calib-tokens", type=int, default=256)
     p.add_argument("--cpu-seconds", type=float, default=12.0,
                    help="time budget of the oracle CPU baseline (0 disables it)")
-    p.add_argument("--no-extra", action="store_true", help="skip the secondary variants")
+    p.add_argument("--no-extra", action="store_true",
+                   help="skip the secondary variants and the other workloads")
+    p.add_argument("--no-other", action="store_true",
+                   help="skip the 8B-predictor and 70B workloads")
     p.add_argument("--traffic-probe", action="store_true",
                    help="first copy a 256 MiB device buffer 3 times (the known-size reference "
                         "for FETCH_SIZE / WRITE_SIZE counters)")
@@ -124,82 +127,101 @@ def time_steps_graph(fn, steps, warmup):
     return ms
 
 
-def main():
-    args = parse()
-    if args.gpus != 1:
-        print(f"bench.py measures one GPU only (got --gpus {args.gpus}); the sparse FFN is "
-              "built and timed on a single MI355X in this build.", file=sys.stderr)
-        sys.exit(2)
+def brief(r):
+    return {kk: r[kk] for kk in ("us_per_layer", "us_per_layer_eager", "tokens_per_s",
+                                 "achieved_GBs", "frac_hbm_peak", "n_active_mean",
+                                 "realised_sparsity", "coef_kernel_us", "coef_kernel_GBs",
+                                 "down_kernel_us", "latent_kernel_us")
+            if kk in r}
 
-    import torch
 
-    from paper_2505_17701_amd import binding as cd
-    from paper_2505_17701_amd import traffic
-    from workloads import WORKLOADS
-    from workloads.synth import T_CALIB
+class Context:
+    """One workload on the device: rotated weight copies, eval tokens, thresholds
+    calibrated on the GPU (mean of per-token quantiles over seeded tokens)."""
 
-    cd.load_library()
-    if not torch.cuda.is_available():
-        sys.exit("bench.py needs a GPU")
-    torch.cuda.set_device(0)
-    w = WORKLOADS[args.workload]
-    dm, dff = w.d_model, w.d_ff
-    stream = torch.cuda.current_stream()
-    if args.traffic_probe:
-        src = torch.ones(64 << 20, dtype=torch.float32, device="cuda")  # 256 MiB
-        dst = torch.empty_like(src)
-        for _ in range(3):
-            dst.copy_(src)
+    def __init__(self, w, copies, ntok, ncal, ks, max_batch, variants=None):
+        import torch
+
+        from paper_2505_17701_amd import binding as cd
+        from workloads.synth import T_CALIB
+
+        self.w, self.copies, self.max_batch = w, copies, max_batch
+        self.dm, self.dff, self.dr = w.d_model, w.d_ff, w.d_rank
+        t = time.time()
+        self.layers = []
+        self.host0 = None
+        for c in range(copies):
+            L = w.layer(copy=c)
+            if w.d_rank:
+                L.update(w.predictor(copy=c))
+            if c == 0:
+                self.host0 = L
+            self.layers.append({k: dev_bf16(v) for k, v in L.items()})
+        self.X_eval_h = w.tokens(ntok)
+        self.X_eval = dev_bf16(self.X_eval_h)
+        X_cal = dev_bf16(w.tokens(ncal, purpose=T_CALIB))
         torch.cuda.synchronize()
-        del src, dst
+        gb = sum(v.numel() * 2 for v in self.layers[0].values()) * copies / 1e9
+        log(f"[bench] {copies} weight copies of {w.name} on device ({gb:.2f} GB) in "
+            f"{time.time() - t:.1f}s")
+        variants = variants or [v for v in w.variants if v != "dense"]
+        vids = {"mono": cd.CD_VARIANT_MONO, "dual_ideal": cd.CD_VARIANT_DUAL_IDEAL,
+                "dual_pred": cd.CD_VARIANT_DUAL_PRED}
+        # tokens per calibration launch: the widest batch tile the shape allows
+        cal_plan = cd.Plan(self.dm, self.dff, max_batch=min(8, 32768 // self.dm), d_rank=self.dr)
+        self.thld = {}
+        L0 = self.layers[0]
+        for variant in variants:
+            for k in ks:
+                th, _ = cd.countdown_calibrate(cal_plan, vids[variant], X_cal, k,
+                                               W_gate=L0["W_gate"], W_up=L0["W_up"],
+                                               A_t=L0.get("A_t"), B_t=L0.get("B_t"))
+                self.thld[(variant, k)] = float(th.item())
+        cal_plan.close()
+        del X_cal
+        log(f"[bench] thresholds: " + ", ".join(f"{v}@{k}={t:.4f}"
+                                                 for (v, k), t in self.thld.items()))
 
-    t = time.time()
-    layers = []
-    host0 = None
-    for c in range(args.copies):
-        L = w.layer(copy=c)
-        if c == 0:
-            host0 = L
-        layers.append({k: dev_bf16(v) for k, v in L.items()})
-    X_eval_h = w.tokens(args.tokens)
-    X_eval = dev_bf16(X_eval_h)
-    X_cal = dev_bf16(w.tokens(args.calib_tokens, purpose=T_CALIB))
-    torch.cuda.synchronize()
-    log(f"[bench] {args.copies} weight copies of {w.name} on device "
-        f"({args.copies * 3 * dm * dff * 2 / 1e9:.2f} GB) in {time.time() - t:.1f}s")
+    def free(self):
+        import torch
 
-    # layerwise thresholds, calibrated on the GPU (mean of per-token quantiles)
-    cal_plan = cd.Plan(dm, dff, max_batch=8)
-    thld = {}
-    for variant, vid in (("mono", cd.CD_VARIANT_MONO), ("dual_ideal", cd.CD_VARIANT_DUAL_IDEAL)):
-        for k in sorted(set((args.k,) + tuple(w.ks))):
-            L0 = layers[0]
-            th, _ = cd.countdown_calibrate(cal_plan, vid, X_cal, k, W_gate=L0["W_gate"],
-                                           W_up=L0["W_up"])
-            thld[(variant, k)] = float(th.item())
-    cal_plan.close()
-    log(f"[bench] thresholds: " + ", ".join(f"{v}@{k}={t:.4f}" for (v, k), t in thld.items()))
+        self.layers = None
+        self.X_eval = None
+        torch.cuda.empty_cache()
 
-    def make_step(plan, variant, k):
-        th = thld.get((variant, k), 0.0)
-        ntok = X_eval.shape[0]
+    def make_step(self, plan, variant, k, B, y):
+        from paper_2505_17701_amd import binding as cd
+
+        th = self.thld.get((variant, k), 0.0)
+        ntok = self.X_eval.shape[0] - B + 1
+        X, layers, copies = self.X_eval, self.layers, self.copies
 
         def step(i):
-            L = layers[i % args.copies]
-            x = X_eval[i % ntok: i % ntok + 1]
+            L = layers[i % copies]
+            x = X[i % ntok: i % ntok + B]
             if variant == "mono":
                 cd.countdown_ffn_mono(plan, x, L["W_gate"], L["W_up"], L["W_down"], th, y=y)
             elif variant == "dual_ideal":
                 cd.countdown_ffn_dual(plan, x, L["W_gate"], L["W_up"], L["W_down"], th, y=y)
+            elif variant == "dual_pred":
+                cd.countdown_ffn_dual(plan, x, L["W_gate"], L["W_up"], L["W_down"], th,
+                                      A_t=L["A_t"], B_t=L["B_t"], y=y)
             else:
                 cd.countdown_ffn_dense(plan, x, L["W_gate"], L["W_up"], L["W_down"], y=y)
         return step
 
-    y = torch.empty((1, dm), dtype=torch.float32, device="cuda")
+    def measure(self, variant, k, B, steps, warmup):
+        import torch
 
-    def measure(variant, k, steps, warmup):
-        plan = cd.Plan(dm, dff, max_batch=1)
-        step = make_step(plan, variant, k)
+        from paper_2505_17701_amd import binding as cd
+        from paper_2505_17701_amd import traffic
+
+        dm, dff, dr = self.dm, self.dff, self.dr
+        stream = torch.cuda.current_stream()
+        y = torch.empty((B, dm), dtype=torch.float32, device="cuda")
+        plan = cd.Plan(dm, dff, max_batch=max(B, self.max_batch),
+                       d_rank=dr if variant == "dual_pred" else 0)
+        step = self.make_step(plan, variant, k, B, y)
         ms_eager = time_steps(step, steps, warmup, stream)
         ms = time_steps_graph(step, steps, warmup)
         # per-kernel averages: graph-replayed loops of a single kernel (the plan's phase
@@ -223,41 +245,116 @@ def main():
         torch.cuda.synchronize()
         plan.close()
         n = n_arr.cpu().numpy().astype(np.float64)
-        per = [traffic.algorithmic_bytes(variant, dm, dff, int(v)) for v in n]
-        res = {"ms_per_step": ms, "us_per_layer": ms * 1e3, "tokens_per_s": 1e3 / ms,
-               "us_per_layer_eager": ms_eager * 1e3,
+        dr_v = dr if variant == "dual_pred" else 0
+        per = [traffic.algorithmic_bytes(variant, dm, dff, int(v), B=B, d_rank=dr_v) for v in n]
+        res = {"batch": B, "ms_per_step": ms, "us_per_layer": ms * 1e3,
+               "tokens_per_s": B * 1e3 / ms, "us_per_layer_eager": ms_eager * 1e3,
                "n_active_mean": float(n.mean()), "realised_sparsity": float(1 - n.mean() / dff)}
-        kbytes = {"coef": float(np.mean([p["coef"] for p in per])),
-                  "down": traffic.algorithmic_bytes(variant, dm, dff, int(n_down.item()))["down"]}
-        for name, kms in (("coef", ms_coef), ("down", ms_down)):
+        # the coefficient loop includes the predictor's latent kernel (one launch each)
+        coef_b = float(np.mean([p["coef"] + p.get("latent", 0) for p in per]))
+        down_b = traffic.algorithmic_bytes(variant, dm, dff, int(n_down.item()), B=B,
+                                           d_rank=dr_v)["down"]
+        for name, kms, kb in (("coef", ms_coef, coef_b), ("down", ms_down, down_b)):
             res[f"{name}_kernel_us"] = kms * 1e3
-            res[f"{name}_kernel_bytes"] = kbytes[name]
-            res[f"{name}_kernel_GBs"] = kbytes[name] / (kms * 1e-3) / 1e9
+            res[f"{name}_kernel_bytes"] = kb
+            res[f"{name}_kernel_GBs"] = kb / (kms * 1e-3) / 1e9
         tot_bytes = float(np.mean([p["total"] for p in per]))
         res["algorithmic_bytes"] = tot_bytes
         res["achieved_GBs"] = tot_bytes / (ms * 1e-3) / 1e9
         res["frac_hbm_peak"] = res["achieved_GBs"] / HBM_PEAK_GBS
         return res
 
-    main_res = measure(args.variant, args.k, args.steps, args.warmup)
-    log(f"[bench] {args.variant} k={args.k}: {json.dumps(main_res)}")
+
+def other_workloads(args):
+    """The remaining single-layer shapes: Llama-3-8B-shaped layer with the low-rank
+    predictor at batch 1/4/8, and the 70B-shaped layer (M-CountDown k 0.9 / 0.7
+    beside the dense FFN)."""
+    from paper_2505_17701_amd import traffic
+    from workloads import WORKLOADS
+
+    out = {}
+    w = WORKLOADS["llama3_8b_4096x14336_pred"]
+    ctx = Context(w, 4, 64, args.calib_tokens, [0.9], max_batch=8)
+    r8 = {}
+    for B in w.batches:
+        r = ctx.measure("dual_pred", 0.9, B, max(200, args.steps // 4), 50)
+        r8[f"B={B}"] = brief(r)
+        log(f"[bench] {w.name} dual_pred B={B}: {json.dumps(r8[f'B={B}'])}")
+    r = ctx.measure("dense", None, 1, max(200, args.steps // 4), 50)
+    r8["dense B=1"] = brief(r)
+    dense_b = traffic.algorithmic_bytes("dense", w.d_model, w.d_ff, w.d_ff)["total"]
+    for B in w.batches:
+        r8[f"B={B}"]["speedup_vs_dense_B1"] = r["us_per_layer"] / r8[f"B={B}"]["us_per_layer"]
+    ctx.free()
+    out[w.name] = r8
+
+    w = WORKLOADS["llama70b_8192x28672"]
+    ctx = Context(w, 1, 16, args.calib_tokens, list(w.ks), max_batch=1)
+    r70 = {}
+    for variant, k in (("mono", 0.9), ("mono", 0.7), ("dense", None)):
+        r = ctx.measure(variant, k, 1, max(100, args.steps // 8), 20)
+        r70[variant + ("" if k is None else f"@k={k}")] = brief(r)
+        log(f"[bench] {w.name} {variant} k={k}: {json.dumps(brief(r))}")
+    for key in ("mono@k=0.9", "mono@k=0.7"):
+        r70[key]["speedup_vs_dense"] = r70["dense"]["us_per_layer"] / r70[key]["us_per_layer"]
+    ctx.free()
+    out[w.name] = r70
+    del dense_b
+    return out
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU only (got --gpus {args.gpus}); the sparse FFN is "
+              "built and timed on a single MI355X in this build.", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+
+    from paper_2505_17701_amd import binding as cd
+    from paper_2505_17701_amd import traffic
+    from workloads import WORKLOADS
+
+    cd.load_library()
+    if not torch.cuda.is_available():
+        sys.exit("bench.py needs a GPU")
+    torch.cuda.set_device(0)
+    w = WORKLOADS[args.workload]
+    dm, dff = w.d_model, w.d_ff
+    if args.traffic_probe:
+        src = torch.ones(64 << 20, dtype=torch.float32, device="cuda")  # 256 MiB
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
+
+    main_ctx = Context(w, args.copies, args.tokens, args.calib_tokens,
+                       sorted(set((args.k,) + tuple(w.ks))), max_batch=1)
+    main_res = main_ctx.measure(args.variant, args.k, 1, args.steps, args.warmup)
+    log(f"[bench] {w.name} {args.variant} k={args.k}: {json.dumps(main_res)}")
 
     extra = {}
     if not args.no_extra:
         for variant, k in (("dense", None), ("dual_ideal", 0.9), ("mono", 0.7), ("mono", 0.5)):
             if variant == args.variant and k == args.k:
                 continue
-            r = measure(variant, k, max(200, args.steps // 4), 50)
-            extra[f"{variant}" + ("" if k is None else f"@k={k}")] = {
-                kk: r[kk] for kk in ("us_per_layer", "us_per_layer_eager", "tokens_per_s",
-                                     "achieved_GBs", "frac_hbm_peak", "n_active_mean",
-                                     "coef_kernel_us", "down_kernel_us")
-                if kk in r}
+            r = main_ctx.measure(variant, k, 1, max(200, args.steps // 4), 50)
+            extra[f"{variant}" + ("" if k is None else f"@k={k}")] = brief(r)
             log(f"[bench] {variant} k={k}: {json.dumps(extra[list(extra)[-1]])}")
         if "dense" in extra:
             extra["speedup_vs_dense"] = extra["dense"]["us_per_layer"] / main_res["us_per_layer"]
             dense_b = traffic.algorithmic_bytes("dense", dm, dff, dff)["total"]
             extra["ideal_byte_ratio"] = dense_b / main_res["algorithmic_bytes"]
+    host0 = main_ctx.host0
+    X_eval_h = main_ctx.X_eval_h
+    thld = main_ctx.thld
+    main_ctx.free()
+
+    others = {}
+    if not args.no_extra and not args.no_other:
+        others = other_workloads(args)
 
     # CPU baseline: the fp64 oracle on host cores, bounded sample of the same workload
     cpu = None
@@ -323,6 +420,7 @@ def main():
                                                   "down_kernel_us", "down_kernel_GBs")
                     if main_res.get(k) is not None},
         "variants": extra,
+        "other_workloads": others,
         "roofline": roof,
         "cpu_baseline": cpu,
     }

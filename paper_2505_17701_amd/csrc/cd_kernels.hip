@@ -90,22 +90,79 @@ struct Tokens {
         }
     }
 
+    // Address of this lane's 16 bytes of token b, chunk k, in the LDS copy. The
+    // offset goes through an empty asm so that a second pass over the tokens
+    // reads LDS again instead of keeping B x NK chunks alive in registers.
+    __device__ __forceinline__ const u32x4 *lds_chunk(int b, int k, int lane, int off) const
+    {
+        constexpr int kStride = NK * kColsPerLoad / 2;
+        return reinterpret_cast<const u32x4 *>(lds + off + b * kStride +
+                                               (k * kColsPerLoad + lane * 8) / 2);
+    }
+
+    static __device__ __forceinline__ int opaque_zero()
+    {
+        int z = 0;
+        asm volatile("" : "+s"(z));
+        return z;
+    }
+
+    // Materialise the accumulators here: keeps the dot products of one chunk
+    // from being deferred (with their token operands held live) past the next.
+    static __device__ __forceinline__ void settle(float (&acc)[B])
+    {
+#pragma unroll
+        for (int b = 0; b < B; ++b)
+            asm volatile("" : "+v"(acc[b]));
+    }
+
     // acc[b] += w . x_b over this lane's chunks
     __device__ __forceinline__ void dot(const u32x4 (&w)[NK], int lane, float (&acc)[B]) const
     {
+        if constexpr (XREG) {
 #pragma unroll
-        for (int k = 0; k < NK; ++k)
+            for (int k = 0; k < NK; ++k)
 #pragma unroll
-            for (int b = 0; b < B; ++b) {
-                if constexpr (XREG) {
+                for (int b = 0; b < B; ++b)
                     acc[b] = dot8(w[k], r[b][k], acc[b]);
-                } else {
-                    constexpr int kStride = NK * kColsPerLoad / 2;
-                    const int c2 = (k * kColsPerLoad + lane * 8) / 2;
-                    acc[b] = dot8(w[k], *reinterpret_cast<const u32x4 *>(lds + b * kStride + c2),
-                                  acc[b]);
-                }
+        } else {
+            const int off = opaque_zero();
+#pragma unroll
+            for (int k = 0; k < NK; ++k) {
+#pragma unroll
+                for (int b = 0; b < B; ++b)
+                    acc[b] = dot8(w[k], *lds_chunk(b, k, lane, off), acc[b]);
+                settle(acc);
             }
+        }
+    }
+
+    // ag[b] += wg . x_b and au[b] += wu . x_b, one read of each x chunk for both rows
+    __device__ __forceinline__ void dot2(const u32x4 (&wg)[NK], const u32x4 (&wu)[NK], int lane,
+                                         float (&ag)[B], float (&au)[B]) const
+    {
+        if constexpr (XREG) {
+#pragma unroll
+            for (int k = 0; k < NK; ++k)
+#pragma unroll
+                for (int b = 0; b < B; ++b) {
+                    ag[b] = dot8(wg[k], r[b][k], ag[b]);
+                    au[b] = dot8(wu[k], r[b][k], au[b]);
+                }
+        } else {
+            const int off = opaque_zero();
+#pragma unroll
+            for (int k = 0; k < NK; ++k) {
+#pragma unroll
+                for (int b = 0; b < B; ++b) {
+                    const u32x4 xv = *lds_chunk(b, k, lane, off);
+                    ag[b] = dot8(wg[k], xv, ag[b]);
+                    au[b] = dot8(wu[k], xv, au[b]);
+                }
+                settle(ag);
+                settle(au);
+            }
+        }
     }
 };
 
@@ -192,8 +249,7 @@ __global__ __launch_bounds__(kBlock) void k_coef_dual(const CoefArgs a)
     float ag[B], au[B];
     zero_acc(ag);
     zero_acc(au);
-    tok.dot(wg, lane, ag);
-    tok.dot(wu, lane, au);
+    tok.dot2(wg, wu, lane, ag, au);
     bool act = DENSE;
     float s[B];
 #pragma unroll
@@ -272,8 +328,7 @@ __global__ __launch_bounds__(kBlock) void k_coef_pred(const CoefArgs a)
         float ag[B], au[B];
         zero_acc(ag);
         zero_acc(au);
-        tok.dot(wg, lane, ag);
-        tok.dot(wu, lane, au);
+        tok.dot2(wg, wu, lane, ag, au);
 #pragma unroll
         for (int b = 0; b < B; ++b) {
             const float g = wave_sum(ag[b]);
