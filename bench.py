@@ -47,7 +47,9 @@ def parse():
     p.add_argument("--steps", type=int, default=2000)
     p.add_argument("--warmup", type=int, default=200)
     p.add_argument("--workload", default="llama7b_4096x11008")
-    p.add_argument("--variant", default="mono", choices=["mono", "dual_ideal", "dense"])
+    p.add_argument("--variant", default="mono",
+                   choices=["mono", "dual_ideal", "dual_pred", "dense"])
+    p.add_argument("--batch", type=int, default=1, help="decode tokens per call (union IDX)")
     p.add_argument("--k", type=float, default=0.9)
     p.add_argument("--copies", type=int, default=4, help="independent weight copies rotated")
     p.add_argument("--tokens", type=int, default=64, help="distinct eval tokens rotated")
@@ -331,12 +333,12 @@ def main():
         del src, dst
 
     main_ctx = Context(w, args.copies, args.tokens, args.calib_tokens,
-                       sorted(set((args.k,) + tuple(w.ks))), max_batch=1)
-    main_res = main_ctx.measure(args.variant, args.k, 1, args.steps, args.warmup)
+                       sorted(set((args.k,) + tuple(w.ks))), max_batch=args.batch)
+    main_res = main_ctx.measure(args.variant, args.k, args.batch, args.steps, args.warmup)
     log(f"[bench] {w.name} {args.variant} k={args.k}: {json.dumps(main_res)}")
 
     extra = {}
-    if not args.no_extra:
+    if not args.no_extra and "mono" in w.variants:
         for variant, k in (("dense", None), ("dual_ideal", 0.9), ("mono", 0.7), ("mono", 0.5)):
             if variant == args.variant and k == args.k:
                 continue
@@ -362,26 +364,35 @@ def main():
         import oracle
 
         th = np.float32(thld.get((args.variant, args.k), 0.0))
-        fn = {"mono": oracle.ffn_mono, "dual_ideal": oracle.ffn_dual_ideal}.get(args.variant)
+        H = host0
+        fns = {"mono": lambda x: oracle.ffn_mono(x, H["W_gate"], H["W_up"], H["W_down"], th),
+               "dual_ideal": lambda x: oracle.ffn_dual_ideal(x, H["W_gate"], H["W_up"],
+                                                             H["W_down"], th),
+               "dual_pred": lambda x: oracle.ffn_dual_pred(x, H["W_gate"], H["W_up"], H["W_down"],
+                                                           H.get("A_t"), H.get("B_t"), th),
+               "dense": lambda x: oracle.dense(x, H["W_gate"], H["W_up"], H["W_down"])}
+        fn = fns[args.variant]
         n_done, t0 = 0, time.perf_counter()
+        nt = len(X_eval_h) - args.batch + 1
         while n_done < 3 or time.perf_counter() - t0 < args.cpu_seconds:
-            x = X_eval_h[n_done % len(X_eval_h)][None]
-            if fn is None:
-                oracle.dense(x, host0["W_gate"], host0["W_up"], host0["W_down"])
-            else:
-                fn(x, host0["W_gate"], host0["W_up"], host0["W_down"], th)
+            i = n_done % nt
+            fn(X_eval_h[i:i + args.batch])
             n_done += 1
         el = time.perf_counter() - t0
-        cpu = {"value": n_done / el, "unit": "tokens/s", "cores": oracle.num_threads(),
-               "kind": "oracle",
-               "sample": f"{n_done} decode tokens of {w.name} {args.variant} k={args.k}, "
-                         f"batch 1, one weight copy, fp64 C oracle ({el:.1f} s)"}
+        cpu = {"value": n_done * args.batch / el, "unit": "tokens/s",
+               "cores": oracle.num_threads(), "kind": "oracle",
+               "sample": f"{n_done} calls of {w.name} {args.variant} k={args.k}, "
+                         f"batch {args.batch}, one weight copy, fp64 C oracle ({el:.1f} s)"}
         log(f"[bench] cpu baseline: {json.dumps(cpu)}")
 
     roof = None
     dom = "coef"
     if main_res.get(f"{dom}_kernel_us"):
-        desc = "k_coef_mono (dense W_up GEMV, threshold, wave-local W_gate gather, s)"
+        desc = {"mono": "k_coef_mono (dense W_up GEMV, threshold, wave-local W_gate gather, s)",
+                "dual_ideal": "k_coef_dual (dense W_gate + W_up GEMV, s, threshold)",
+                "dual_pred": "k_latent + k_coef_pred (predictor scores, threshold, block-local "
+                             "W_gate / W_up gather, s)",
+                "dense": "k_coef_dual (dense W_gate + W_up GEMV, s)"}[args.variant]
         roof = {"bound": "hbm", "kernel": desc,
                 "achieved": main_res[f"{dom}_kernel_GBs"], "peak": HBM_PEAK_GBS, "unit": "GB/s",
                 "frac": main_res[f"{dom}_kernel_GBs"] / HBM_PEAK_GBS,
@@ -391,7 +402,7 @@ def main():
                 "avg_launch_us": main_res[f"{dom}_kernel_us"]}
 
     out = {
-        "metric": "sparse-FFN decode tokens/s (one FFN layer, batch 1, k=0.9)",
+        "metric": f"sparse-FFN decode tokens/s (one FFN layer, batch {args.batch}, k={args.k})",
         "value": main_res["tokens_per_s"],
         "unit": "tokens/s",
         "n_gpus": 1,
@@ -407,9 +418,9 @@ def main():
         "scaling": "weak",
         "vs_baseline": None,
         "dtype": "bf16 weights, fp32 accumulate",
-        "data": "synthetic (seeded N(0, 0.02^2) weights, N(0,1) tokens with 1% outlier "
-                "channels x20)",
-        "config": {"workload": w.name, "d_model": dm, "d_ff": dff, "batch": 1,
+        "data": f"synthetic (seeded N(0, {w.sigma}^2) bf16 weights, N(0,1) tokens"
+                + (f" with {w.outlier_frac:.0%} outlier channels x20)" if w.outlier_frac else ")"),
+        "config": {"workload": w.name, "d_model": dm, "d_ff": dff, "batch": args.batch,
                    "variant": args.variant, "k": args.k,
                    "thld": thld.get((args.variant, args.k)), "weight_copies": args.copies,
                    "n_active_mean": main_res["n_active_mean"],

@@ -29,6 +29,18 @@ __device__ __forceinline__ u32x4 load16_stream(const uint16_t *p)
     return __builtin_nontemporal_load(reinterpret_cast<const u32x4 *>(p));
 }
 
+// Lanes whose chunk lies past the end of a row (ragged d_model) or of the
+// token batch load these 16 zero bytes instead: an address select before the
+// load rather than a select of the loaded data, which would make the compiler
+// wait for each load on its own.
+__device__ __align__(16) uint32_t kZeroChunk[4] = {0u, 0u, 0u, 0u};  // never written
+
+template <class T>
+__device__ __forceinline__ const T *or_zero(bool ok, const T *p)
+{
+    return ok ? p : reinterpret_cast<const T *>(kZeroChunk);
+}
+
 template <int NK>
 __device__ __forceinline__ void load_row(u32x4 (&w)[NK], const uint16_t *__restrict__ row,
                                          int d_model, int lane)
@@ -36,57 +48,70 @@ __device__ __forceinline__ void load_row(u32x4 (&w)[NK], const uint16_t *__restr
 #pragma unroll
     for (int k = 0; k < NK; ++k) {
         const int col = k * kColsPerLoad + lane * 8;
-        w[k] = (col < d_model) ? load16_stream(row + col) : zero16();
+        w[k] = load16_stream(or_zero(col < d_model, row + col));
     }
-}
-
-// x (bf16) -> LDS as packed pairs, each token padded with zeros to NK*512 columns
-template <int B, int NK>
-__device__ __forceinline__ void stage_x(uint32_t *xs, const uint16_t *__restrict__ x, int nb,
-                                        int d_model)
-{
-    constexpr int kCols = NK * kColsPerLoad;
-    constexpr int kChunksPerTok = kCols / 8;
-    for (int c = threadIdx.x; c < B * kChunksPerTok; c += kBlock) {
-        const int b = c / kChunksPerTok;
-        const int col = (c % kChunksPerTok) * 8;
-        u32x4 v = zero16();
-        if (b < nb && col < d_model)
-            v = load16(x + (size_t)b * d_model + col);
-        *reinterpret_cast<u32x4 *>(xs + (size_t)b * (kCols / 2) + col / 2) = v;
-    }
-}
-
-// this lane's chunks of the B tokens, in registers
-template <int B, int NK>
-__device__ __forceinline__ void load_x(u32x4 (&xr)[B][NK], const uint16_t *__restrict__ x, int nb,
-                                       int d_model, int lane)
-{
-#pragma unroll
-    for (int b = 0; b < B; ++b)
-#pragma unroll
-        for (int k = 0; k < NK; ++k) {
-            const int col = k * kColsPerLoad + lane * 8;
-            xr[b][k] = (b < nb && col < d_model) ? load16(x + (size_t)b * d_model + col) : zero16();
-        }
 }
 
 // Token operand of the dot products: registers (XREG) or the LDS copy.
 template <int B, int NK, bool XREG>
 struct Tokens {
+    static constexpr int kCols = NK * kColsPerLoad;
+    static constexpr int kChunksPerTok = kCols / 8;
+    static constexpr int kTotal = B * kChunksPerTok;  // 16-byte chunks of the LDS copy
+    static constexpr int kIter = XREG ? 1 : (kTotal + kBlock - 1) / kBlock;
     u32x4 r[XREG ? B : 1][XREG ? NK : 1];
+    u32x4 stage[kIter];  // LDS path: this thread's share of the copy, in flight
     const uint32_t *lds;
 
-    // Every thread of the workgroup must call this (it may synchronise).
-    __device__ __forceinline__ void init(const uint16_t *x, int nb, int d_model, int lane,
-                                         uint32_t *smem)
+    // Issue every global load of the tokens (this lane's chunks, or this
+    // thread's share of the LDS copy, padded with zeros to NK * 512 columns).
+    // A scheduling barrier keeps the loads ahead of whatever follows.
+    __device__ __forceinline__ void issue(const uint16_t *__restrict__ x, int nb, int d_model,
+                                          int lane)
     {
         if constexpr (XREG) {
-            load_x<B, NK>(r, x, nb, d_model, lane);
+#pragma unroll
+            for (int b = 0; b < B; ++b)
+#pragma unroll
+                for (int k = 0; k < NK; ++k) {
+                    const int col = k * kColsPerLoad + lane * 8;
+                    r[b][k] = load16(or_zero(b < nb && col < d_model, x + (size_t)b * d_model + col));
+                }
         } else {
-            stage_x<B, NK>(smem, x, nb, d_model);
-            __syncthreads();
+#pragma unroll
+            for (int i = 0; i < kIter; ++i) {
+                const int c = threadIdx.x + i * kBlock;
+                const int b = c / kChunksPerTok;
+                const int col = (c % kChunksPerTok) * 8;
+                stage[i] = load16(or_zero(c < kTotal && b < nb && col < d_model,
+                                          x + (size_t)b * d_model + col));
+            }
+        }
+        __builtin_amdgcn_sched_barrier(0);
+    }
+
+    // LDS path: write this thread's share of the copy to smem (the caller
+    // synchronises the workgroup before reading it). Register path: nothing.
+    __device__ __forceinline__ void write(uint32_t *smem)
+    {
+        if constexpr (!XREG) {
+#pragma unroll
+            for (int i = 0; i < kIter; ++i) {
+                const int c = threadIdx.x + i * kBlock;
+                if (c < kTotal)
+                    *reinterpret_cast<u32x4 *>(smem + (size_t)(c / kChunksPerTok) * (kCols / 2) +
+                                               (c % kChunksPerTok) * 4) = stage[i];
+            }
             lds = smem;
+        }
+    }
+
+    // write() and a workgroup barrier on the LDS path (every thread must call this)
+    __device__ __forceinline__ void commit(uint32_t *smem)
+    {
+        if constexpr (!XREG) {
+            write(smem);
+            __syncthreads();
         }
     }
 
@@ -190,11 +215,11 @@ __global__ __launch_bounds__(kBlock) void k_coef_mono(const CoefArgs a)
     const int row = blockIdx.x * kWavesPerBlock + wave;
     const bool live = row < a.d_ff;
     u32x4 w[NK];
-    if (live)
-        load_row<NK>(w, a.Wu + (size_t)row * a.d_model, a.d_model, lane);
-    zero_y(a.y, a.nb * a.d_model);
+    load_row<NK>(w, a.Wu + (size_t)(live ? row : 0) * a.d_model, a.d_model, lane);
     Tokens<B, NK, XREG> tok;
-    tok.init(a.x, a.nb, a.d_model, lane, xs);
+    tok.issue(a.x, a.nb, a.d_model, lane);
+    zero_y(a.y, a.nb * a.d_model);
+    tok.commit(xs);
     if (!live)
         return;
 
@@ -214,7 +239,7 @@ __global__ __launch_bounds__(kBlock) void k_coef_mono(const CoefArgs a)
     if (act) {
         load_row<NK>(w, a.Wg + (size_t)row * a.d_model, a.d_model, lane);
         zero_acc(acc);
-        tok.dot(w, lane, acc);
+            tok.dot(w, lane, acc);
 #pragma unroll
         for (int b = 0; b < B; ++b) {
             const float g = wave_sum(acc[b]);
@@ -236,13 +261,13 @@ __global__ __launch_bounds__(kBlock) void k_coef_dual(const CoefArgs a)
     const int row = blockIdx.x * kWavesPerBlock + wave;
     const bool live = row < a.d_ff;
     u32x4 wg[NK], wu[NK];
-    if (live) {
-        load_row<NK>(wg, a.Wg + (size_t)row * a.d_model, a.d_model, lane);
-        load_row<NK>(wu, a.Wu + (size_t)row * a.d_model, a.d_model, lane);
-    }
-    zero_y(a.y, a.nb * a.d_model);
+    const size_t roff = (size_t)(live ? row : 0) * a.d_model;
+    load_row<NK>(wg, a.Wg + roff, a.d_model, lane);
+    load_row<NK>(wu, a.Wu + roff, a.d_model, lane);
     Tokens<B, NK, XREG> tok;
-    tok.init(a.x, a.nb, a.d_model, lane, xs);
+    tok.issue(a.x, a.nb, a.d_model, lane);
+    zero_y(a.y, a.nb * a.d_model);
+    tok.commit(xs);
     if (!live)
         return;
 
@@ -273,98 +298,300 @@ __global__ __launch_bounds__(kBlock) void k_coef_dual(const CoefArgs a)
     }
 }
 
-// Practical D-CountDown coefficient kernel (Sec. 4): predictor score
-// s_hat = latent . B_t[row] (signed threshold, union over the batch), then
-// the active neuron's W_gate and W_up rows and s = u * SiLU(g).
-template <int B, int NK, bool XREG>
-__global__ __launch_bounds__(kBlock) void k_coef_pred(const CoefArgs a)
+constexpr int kPredRowsPerWave = 8;
+constexpr int kPredRows = kPredRowsPerWave * kWavesPerBlock;  // neurons per workgroup
+constexpr int kPredLoads = 8;  // 16-byte B_t loads per lane and pass (one pass up to rank 512)
+
+// Sum over aligned segments of 2^lg lanes with lg (0..6) known at run time
+// (wave-uniform); the last lane of every segment holds the segment sum.
+__device__ __forceinline__ float segment_sum_rt(float v, int lg)
 {
-    extern __shared__ __align__(16) uint32_t xs[];
-    const int lane = threadIdx.x % kWave, wave = threadIdx.x / kWave;
-    const int row = blockIdx.x * kWavesPerBlock + wave;
-    const bool live = row < a.d_ff;
-    float acc[B];
-    zero_acc(acc);
-    for (int e = lane * 8; e < a.d_rank; e += kColsPerLoad) {
-        const u32x4 w = live ? load16_stream(a.Bt + (size_t)row * a.d_rank + e) : zero16();
-        const float wf[8] = {bf16_lo(w.x), bf16_hi(w.x), bf16_lo(w.y), bf16_hi(w.y),
-                             bf16_lo(w.z), bf16_hi(w.z), bf16_lo(w.w), bf16_hi(w.w)};
+    if (lg >= 1) v += dpp0<kDppQuadSwap1>(v);
+    if (lg >= 2) v += dpp0<kDppQuadSwap2>(v);
+    if (lg >= 3) v += dpp0<kDppHalfMirror>(v);
+    if (lg >= 4) v += dpp0<kDppMirror>(v);
+    if (lg >= 5) v += dpp0<kDppBcast15, 0xA>(v);
+    if (lg >= 6) v += dpp0<kDppBcast31, 0xC>(v);
+    return v;
+}
+
+// The predictor latent [B][d_rank] fp32 on its way to LDS: the part a rank of up
+// to 256 needs is loaded with the kernel's other loads (issue), written after
+// (write); larger ranks take a second, plain pass. The caller synchronises.
+template <int B>
+struct LatentStage {
+    static constexpr int kFast = (B * 256 / 4 + kBlock - 1) / kBlock;
+    u32x4 v[kFast];  // 4 fp32 each, as raw bits
+
+    __device__ __forceinline__ void issue(const float *lat, int nb, int d_rank)
+    {
+        const int q4 = d_rank / 4;
+        const u32x4 *g = reinterpret_cast<const u32x4 *>(lat);
 #pragma unroll
-        for (int b = 0; b < B; ++b) {
-            if (b >= a.nb)
-                break;
-            const float4 l0 = *reinterpret_cast<const float4 *>(a.lat + (size_t)b * a.d_rank + e);
-            const float4 l1 = *reinterpret_cast<const float4 *>(a.lat + (size_t)b * a.d_rank + e + 4);
-            acc[b] = fmaf(wf[0], l0.x, acc[b]);
-            acc[b] = fmaf(wf[1], l0.y, acc[b]);
-            acc[b] = fmaf(wf[2], l0.z, acc[b]);
-            acc[b] = fmaf(wf[3], l0.w, acc[b]);
-            acc[b] = fmaf(wf[4], l1.x, acc[b]);
-            acc[b] = fmaf(wf[5], l1.y, acc[b]);
-            acc[b] = fmaf(wf[6], l1.z, acc[b]);
-            acc[b] = fmaf(wf[7], l1.w, acc[b]);
+        for (int t = 0; t < kFast; ++t) {
+            const int i = threadIdx.x + t * kBlock;
+            v[t] = *or_zero(i < B * q4 && i / q4 < nb, g + i);
         }
     }
-    zero_y(a.y, a.nb * a.d_model);
-    Tokens<B, NK, XREG> tok;
-    tok.init(a.x, a.nb, a.d_model, lane, xs);
-    if (!live)
-        return;
 
+    __device__ __forceinline__ void write(u32x4 *dst, const float *lat, int nb, int d_rank) const
+    {
+        const int q4 = d_rank / 4;
+        const u32x4 *g = reinterpret_cast<const u32x4 *>(lat);
+#pragma unroll
+        for (int t = 0; t < kFast; ++t) {
+            const int i = threadIdx.x + t * kBlock;
+            if (i < B * q4)
+                dst[i] = v[t];
+        }
+        for (int i = threadIdx.x + kFast * kBlock; i < B * q4; i += kBlock)
+            dst[i] = *or_zero(i / q4 < nb, g + i);
+    }
+};
+
+// One 16-byte B_t chunk per lane into the scores; every jpr-th chunk closes
+// the rows of its slot (segment sums, coefficient, union threshold, act
+// flag). Returns true on the lane that closed an active row of this wave.
+template <int B>
+__device__ __forceinline__ bool pred_slot(const u32x4 &w, int j, int lane, int lcpr, int jpr,
+                                          int seg_log, bool seg_end, int wr0, const float *lat,
+                                          const CoefArgs &a, float (&acc)[B])
+{
+    const int cpr = 1 << lcpr;
+    const int f = j * kWave + lane;
+    const int e = (f & (cpr - 1)) * 8;
+    const float wf[8] = {bf16_lo(w.x), bf16_hi(w.x), bf16_lo(w.y), bf16_hi(w.y),
+                         bf16_lo(w.z), bf16_hi(w.z), bf16_lo(w.w), bf16_hi(w.w)};
+#pragma unroll
+    for (int b = 0; b < B; ++b) {
+        if (b >= a.nb)
+            break;
+        const float4 l0 = *reinterpret_cast<const float4 *>(lat + b * a.d_rank + e);
+        const float4 l1 = *reinterpret_cast<const float4 *>(lat + b * a.d_rank + e + 4);
+        acc[b] = fmaf(wf[0], l0.x, acc[b]);
+        acc[b] = fmaf(wf[1], l0.y, acc[b]);
+        acc[b] = fmaf(wf[2], l0.z, acc[b]);
+        acc[b] = fmaf(wf[3], l0.w, acc[b]);
+        acc[b] = fmaf(wf[4], l1.x, acc[b]);
+        acc[b] = fmaf(wf[5], l1.y, acc[b]);
+        acc[b] = fmaf(wf[6], l1.z, acc[b]);
+        acc[b] = fmaf(wf[7], l1.w, acc[b]);
+    }
+    if ((j + 1) % jpr != 0)
+        return false;
+    const int rw = f >> lcpr;
+    const int row = wr0 + rw;
+    const bool live = seg_end && rw < kPredRowsPerWave && row < a.d_ff;
     bool act = false;
 #pragma unroll
     for (int b = 0; b < B; ++b) {
-        const float v = wave_sum(acc[b]);
+        const float v = segment_sum_rt(acc[b], seg_log);
+        acc[b] = 0.0f;
         if (b < a.nb) {
             act = act || (v > a.thld);
-            if (a.coef && lane == 0)
+            if (a.coef && live)
                 a.coef[(size_t)b * a.d_ff + row] = v;
         }
     }
-    if (act) {
-        u32x4 wg[NK], wu[NK];
-        load_row<NK>(wg, a.Wg + (size_t)row * a.d_model, a.d_model, lane);
-        load_row<NK>(wu, a.Wu + (size_t)row * a.d_model, a.d_model, lane);
-        float ag[B], au[B];
-        zero_acc(ag);
-        zero_acc(au);
-        tok.dot2(wg, wu, lane, ag, au);
-#pragma unroll
-        for (int b = 0; b < B; ++b) {
-            const float g = wave_sum(ag[b]);
-            const float u = wave_sum(au[b]);
-            if (b < a.nb && lane == 0)
-                a.s[(size_t)b * a.d_ff + row] = u * silu(g);
-        }
-    }
-    if (lane == 0)
+    if (live)
         a.act[row] = act ? 1 : 0;
+    return live && act;
 }
 
-// latent = x . theta_A for the predictor: one row of A_t per wave
+// The wave's kPredRowsPerWave B_t rows as one flat run of 16-byte chunks,
+// chunk f on lane f % 64; this pass issues chunks j0 * 64 ... (j0 + 8) * 64 - 1
+// (every load in flight at once).
+__device__ __forceinline__ void pred_load_bt(u32x4 (&wb)[kPredLoads], const CoefArgs &a, int wr0,
+                                             int lane, int lcpr, int J, int j0)
+{
+    const int cpr = 1 << lcpr;
+#pragma unroll
+    for (int t = 0; t < kPredLoads; ++t) {
+        const int j = j0 + t;
+        const int f = j * kWave + lane;
+        const int rw = f >> lcpr;
+        wb[t] = zero16();
+        if (j < J && rw < kPredRowsPerWave && wr0 + rw < a.d_ff)
+            wb[t] = load16_stream(a.Bt + (size_t)(wr0 + rw) * a.d_rank + (f & (cpr - 1)) * 8);
+    }
+}
+
+// Scores of one pass of B_t chunks (see pred_slot); returns the wave-uniform
+// mask of this wave's active neurons closed in the pass.
+template <int B>
+__device__ __forceinline__ uint32_t pred_scores(const u32x4 (&wb)[kPredLoads], int j0, int J,
+                                                int lane, int lcpr, int wr0, const float *lat,
+                                                const CoefArgs &a)
+{
+    const int cpr = 1 << lcpr;
+    const int jpr = cpr > kWave ? cpr / kWave : 1;
+    const int seg_log = min(lcpr, 6);
+    const bool seg_end = (lane & ((1 << seg_log) - 1)) == (1 << seg_log) - 1;
+    float acc[B];
+    zero_acc(acc);
+    uint32_t wmask = 0;
+#pragma unroll
+    for (int t = 0; t < kPredLoads; ++t) {
+        const int j = j0 + t;
+        if (j < J) {
+            const bool act = pred_slot<B>(wb[t], j, lane, lcpr, jpr, seg_log, seg_end, wr0, lat,
+                                          a, acc);
+            for (uint64_t m = ballot(act); m; m &= m - 1)
+                wmask |= 1u << ((j * kWave + __builtin_ctzll(m)) >> lcpr);
+        }
+    }
+    return wmask;
+}
+
+// s = u * SiLU(g) of one active neuron: its W_gate and W_up rows against the tokens
 template <int B, int NK, bool XREG>
+__device__ __forceinline__ void pred_gather(const CoefArgs &a, const Tokens<B, NK, XREG> &tok,
+                                            int row, int lane)
+{
+    u32x4 wg[NK], wu[NK];
+    load_row<NK>(wg, a.Wg + (size_t)row * a.d_model, a.d_model, lane);
+    load_row<NK>(wu, a.Wu + (size_t)row * a.d_model, a.d_model, lane);
+    float ag[B], au[B];
+    zero_acc(ag);
+    zero_acc(au);
+    tok.dot2(wg, wu, lane, ag, au);
+#pragma unroll
+    for (int b = 0; b < B; ++b) {
+        const float g = wave_sum(ag[b]);
+        const float u = wave_sum(au[b]);
+        if (b < a.nb && lane == 0)
+            a.s[(size_t)b * a.d_ff + row] = u * silu(g);
+    }
+}
+
+// Practical D-CountDown coefficient kernel for batches of 1-2 (Sec. 4). After
+// one barrier (the latent staged in LDS) the waves are independent: each
+// scores kPredRowsPerWave neurons (s_hat = latent . B_t[row], signed
+// threshold, union over the batch), then gathers the W_gate and W_up rows of
+// its own active neurons against the tokens in registers (loaded beside the
+// B_t rows) and writes s = u * SiLU(g).
+template <int B, int NK>
+__global__ __launch_bounds__(kBlock) void k_coef_pred_w(const CoefArgs a)
+{
+    extern __shared__ __align__(16) float lat_lds[];  // latent [B][d_rank]
+    const int lane = threadIdx.x % kWave, wave = threadIdx.x / kWave;
+    const int wr0 = (blockIdx.x * kWavesPerBlock + wave) * kPredRowsPerWave;
+    const int lcpr = 31 - __builtin_clz(a.d_rank / 8);
+    const int J = max(1, kPredRowsPerWave * (1 << lcpr) / kWave);  // B_t loads per lane
+    u32x4 wb[kPredLoads];
+    pred_load_bt(wb, a, wr0, lane, lcpr, J, 0);
+    Tokens<B, NK, true> tok;
+    tok.issue(a.x, a.nb, a.d_model, lane);
+    LatentStage<B> ls;
+    ls.issue(a.lat, a.nb, a.d_rank);
+    zero_y(a.y, a.nb * a.d_model);
+    ls.write(reinterpret_cast<u32x4 *>(lat_lds), a.lat, a.nb, a.d_rank);
+    __syncthreads();
+    if (wr0 >= a.d_ff)
+        return;
+
+    uint32_t wmask = pred_scores<B>(wb, 0, J, lane, lcpr, wr0, lat_lds, a);
+    for (int j0 = kPredLoads; j0 < J; j0 += kPredLoads) {
+        pred_load_bt(wb, a, wr0, lane, lcpr, J, j0);
+        wmask |= pred_scores<B>(wb, j0, J, lane, lcpr, wr0, lat_lds, a);
+    }
+    for (; wmask; wmask &= wmask - 1)
+        pred_gather<B, NK, true>(a, tok, wr0 + __builtin_ctz(wmask), lane);
+}
+
+// Practical D-CountDown coefficient kernel for batches of 4-8 (Sec. 4). A
+// workgroup owns a block of kPredRows neurons: it stages the tokens and the
+// latent in LDS once, scores its B_t rows (signed threshold, union over the
+// batch), and its four waves then share the block's active neurons: W_gate
+// and W_up rows against the LDS tokens, s = u * SiLU(g).
+template <int B, int NK>
+__global__ __launch_bounds__(kBlock) void k_coef_pred(const CoefArgs a)
+{
+    extern __shared__ __align__(16) uint32_t xs[];  // tokens [B][NK * 256], then latent [B][d_rank]
+    __shared__ uint32_t wflag[kWavesPerBlock];
+    const int lane = threadIdx.x % kWave, wave = threadIdx.x / kWave;
+    const int r0 = blockIdx.x * kPredRows;
+    const int wr0 = r0 + wave * kPredRowsPerWave;
+    const int lcpr = 31 - __builtin_clz(a.d_rank / 8);
+    const int J = max(1, kPredRowsPerWave * (1 << lcpr) / kWave);  // B_t loads per lane
+    u32x4 wb[kPredLoads];
+    pred_load_bt(wb, a, wr0, lane, lcpr, J, 0);
+    Tokens<B, NK, false> tok;
+    tok.issue(a.x, a.nb, a.d_model, lane);
+    LatentStage<B> ls;
+    ls.issue(a.lat, a.nb, a.d_rank);
+    zero_y(a.y, a.nb * a.d_model);
+    tok.write(xs);
+    u32x4 *lat4 = reinterpret_cast<u32x4 *>(xs + B * NK * kColsPerLoad / 2);
+    ls.write(lat4, a.lat, a.nb, a.d_rank);
+    const float *lat = reinterpret_cast<const float *>(lat4);
+    __syncthreads();
+
+    uint32_t wmask = pred_scores<B>(wb, 0, J, lane, lcpr, wr0, lat, a);
+    for (int j0 = kPredLoads; j0 < J; j0 += kPredLoads) {
+        pred_load_bt(wb, a, wr0, lane, lcpr, J, j0);
+        wmask |= pred_scores<B>(wb, j0, J, lane, lcpr, wr0, lat, a);
+    }
+    if (lane == 0)
+        wflag[wave] = wmask;
+    __syncthreads();
+
+    // the block's active neurons in ascending order, dealt round-robin to the waves
+    uint32_t M = 0;
+#pragma unroll
+    for (int v = 0; v < kWavesPerBlock; ++v)
+        M |= wflag[v] << (v * kPredRowsPerWave);
+    int e = 0;
+    for (; M; M &= M - 1, ++e)
+        if (e % kWavesPerBlock == wave)
+            pred_gather<B, NK, false>(a, tok, r0 + __builtin_ctz(M), lane);
+}
+
+// latent = x . theta_A for the predictor: one workgroup per row of A_t, the
+// four waves take every fourth 512-column chunk (tokens read straight from
+// global memory, each lane only its own chunks) and add up in LDS.
+template <int B, int NK>
 __global__ __launch_bounds__(kBlock) void k_latent(const uint16_t *__restrict__ x, int nb,
                                                    const uint16_t *__restrict__ At, int d_model,
                                                    int d_rank, float *__restrict__ lat)
 {
-    extern __shared__ __align__(16) uint32_t xs[];
+    constexpr int KW = (NK + kWavesPerBlock - 1) / kWavesPerBlock;  // chunks per wave
+    __shared__ float part[kWavesPerBlock][B];
     const int lane = threadIdx.x % kWave, wave = threadIdx.x / kWave;
-    const int r = blockIdx.x * kWavesPerBlock + wave;
-    u32x4 w[NK];
-    if (r < d_rank)
-        load_row<NK>(w, At + (size_t)r * d_model, d_model, lane);
-    Tokens<B, NK, XREG> tok;
-    tok.init(x, nb, d_model, lane, xs);
-    if (r >= d_rank)
-        return;
+    const int r = blockIdx.x;
+    const uint16_t *row = At + (size_t)r * d_model;
+    u32x4 w[KW];
+#pragma unroll
+    for (int t = 0; t < KW; ++t) {
+        const int col = (wave + t * kWavesPerBlock) * kColsPerLoad + lane * 8;
+        w[t] = col < d_model ? load16_stream(row + col) : zero16();
+    }
     float acc[B];
     zero_acc(acc);
-    tok.dot(w, lane, acc);
+#pragma unroll
+    for (int b = 0; b < B; ++b) {
+        if (b < nb) {
+#pragma unroll
+            for (int t = 0; t < KW; ++t) {
+                const int col = (wave + t * kWavesPerBlock) * kColsPerLoad + lane * 8;
+                acc[b] = dot8(w[t], load16(or_zero(col < d_model, x + (size_t)b * d_model + col)),
+                              acc[b]);
+            }
+        }
+    }
 #pragma unroll
     for (int b = 0; b < B; ++b) {
         const float v = wave_sum(acc[b]);
-        if (b < nb && lane == 0)
-            lat[(size_t)b * d_rank + r] = v;
+        if (lane == 0)
+            part[wave][b] = v;
+    }
+    __syncthreads();
+    if (threadIdx.x < nb) {
+        float v = 0.0f;
+#pragma unroll
+        for (int q = 0; q < kWavesPerBlock; ++q)
+            v += part[q][threadIdx.x];
+        lat[(size_t)threadIdx.x * d_rank + r] = v;
     }
 }
 
@@ -649,10 +876,18 @@ static hipError_t coef_bn(int variant, const CoefArgs &a, hipStream_t s)
         allow_lds(k_coef_dual<B, NK, XREG, true>, lds);
         k_coef_dual<B, NK, XREG, true><<<grid, kBlock, lds, s>>>(a);
         break;
-    case kDualPred:
-        allow_lds(k_coef_pred<B, NK, XREG>, lds);
-        k_coef_pred<B, NK, XREG><<<grid, kBlock, lds, s>>>(a);
+    case kDualPred: {
+        const int pgrid = (a.d_ff + kPredRows - 1) / kPredRows;
+        if constexpr (XREG) {
+            const size_t plds = (size_t)B * a.d_rank * 4;
+            k_coef_pred_w<B, NK><<<pgrid, kBlock, plds, s>>>(a);
+        } else {
+            const size_t plds = (size_t)B * NK * kColsPerLoad * 2 + (size_t)B * a.d_rank * 4;
+            allow_lds(k_coef_pred<B, NK>, plds);
+            k_coef_pred<B, NK><<<pgrid, kBlock, plds, s>>>(a);
+        }
         break;
+    }
     default:
         return hipErrorInvalidValue;
     }
@@ -685,32 +920,18 @@ hipError_t launch_coef(int variant, const CoefArgs &a, hipStream_t s)
     }
 }
 
-template <int B, int NK>
-static hipError_t latent_bn(const uint16_t *x, int nb, const uint16_t *At, int d_model, int d_rank,
-                            float *lat, hipStream_t s)
-{
-    constexpr bool XREG = B <= 2;
-    const int grid = (d_rank + kWavesPerBlock - 1) / kWavesPerBlock;
-    const size_t lds = token_lds_bytes(B, NK);
-    allow_lds(k_latent<B, NK, XREG>, lds);
-    k_latent<B, NK, XREG><<<grid, kBlock, lds, s>>>(x, nb, At, d_model, d_rank, lat);
-    return hipGetLastError();
-}
-
 template <int B>
 static hipError_t latent_b(const uint16_t *x, int nb, const uint16_t *At, int d_model, int d_rank,
                            float *lat, hipStream_t s)
 {
     switch (col_tile(d_model)) {
-    case 1: return latent_bn<B, 1>(x, nb, At, d_model, d_rank, lat, s);
-    case 2: return latent_bn<B, 2>(x, nb, At, d_model, d_rank, lat, s);
-    case 4: return latent_bn<B, 4>(x, nb, At, d_model, d_rank, lat, s);
-    case 8: return latent_bn<B, 8>(x, nb, At, d_model, d_rank, lat, s);
-    default:
-        if constexpr (B * 16 <= 64)
-            return latent_bn<B, 16>(x, nb, At, d_model, d_rank, lat, s);
-        return hipErrorInvalidValue;
+    case 1: k_latent<B, 1><<<d_rank, kBlock, 0, s>>>(x, nb, At, d_model, d_rank, lat); break;
+    case 2: k_latent<B, 2><<<d_rank, kBlock, 0, s>>>(x, nb, At, d_model, d_rank, lat); break;
+    case 4: k_latent<B, 4><<<d_rank, kBlock, 0, s>>>(x, nb, At, d_model, d_rank, lat); break;
+    case 8: k_latent<B, 8><<<d_rank, kBlock, 0, s>>>(x, nb, At, d_model, d_rank, lat); break;
+    default: k_latent<B, 16><<<d_rank, kBlock, 0, s>>>(x, nb, At, d_model, d_rank, lat); break;
     }
+    return hipGetLastError();
 }
 
 hipError_t launch_latent(const uint16_t *x, int nb, const uint16_t *At, int d_model, int d_rank,
