@@ -59,7 +59,8 @@ def parse():
     p.add_argument("--no-extra", action="store_true",
                    help="skip the secondary variants and the other workloads")
     p.add_argument("--no-other", action="store_true",
-                   help="skip the 8B-predictor and 70B workloads")
+                   help="skip the 8B-predictor, 70B and 32-layer stack workloads")
+    p.add_argument("--no-stack", action="store_true", help="skip the 32-layer stack")
     p.add_argument("--traffic-probe", action="store_true",
                    help="first copy a 256 MiB device buffer 3 times (the known-size reference "
                         "for FETCH_SIZE / WRITE_SIZE counters)")
@@ -305,6 +306,122 @@ def other_workloads(args):
     return out
 
 
+def stack_bench(args, steps_tokens=128, warmup_tokens=8):
+    """The 32-layer stack of 7B-shaped predictor layers joined by the residual stream
+    (h += y, x = bf16(RMSNorm(h))): per-layer thresholds calibrated at k on 256 seeded
+    tokens propagated through the dense stack, then 128 independent decode tokens at
+    batch 1, each through all layers. One HIP graph holds the whole timed run."""
+    import torch
+
+    from paper_2505_17701_amd import binding as cd
+    from workloads import WORKLOADS
+    from workloads.synth import T_CALIB, T_EVAL, stream
+
+    w = WORKLOADS["stack32_llama7b_pred"]
+    dm, dff, dr, nl = w.d_model, w.d_ff, w.d_rank, w.n_layers
+    k = 0.9
+    t = time.time()
+    layers = []
+    for l in range(nl):
+        L = dict(w.layer(layer=l))
+        L.update(w.predictor(layer=l))
+        layers.append({kk: dev_bf16(v) for kk, v in L.items()})
+    torch.cuda.synchronize()
+    gb = sum(v.numel() * 2 for v in layers[0].values()) * nl / 1e9
+    log(f"[bench] stack: {nl} layers of {dm}x{dff} (+ predictor rank {dr}) on device "
+        f"({gb:.2f} GB) in {time.time() - t:.1f}s")
+
+    def h0(n, purpose):
+        return torch.from_numpy(stream(w.wid, 0, purpose, 77).standard_normal(
+            (n, dm)).astype(np.float32)).cuda()
+
+    # calibration on inputs propagated through the dense stack
+    ncal, cb = args.calib_tokens, 8
+    hc = [h0(ncal, T_CALIB), torch.empty((ncal, dm), dtype=torch.float32, device="cuda")]
+    yc = torch.zeros((ncal, dm), dtype=torch.float32, device="cuda")
+    xc = torch.empty((ncal, dm), dtype=torch.bfloat16, device="cuda")
+    dplan = cd.Plan(dm, dff, max_batch=cb, d_rank=dr)
+    thld = []
+    for l, L in enumerate(layers):
+        src, dst = hc[l % 2], hc[(l + 1) % 2]
+        for i in range(0, ncal, cb):
+            cd.countdown_ffn_residual(dplan, cd.CD_VARIANT_DENSE, src[i:i + cb],
+                                      None if l == 0 else yc[i:i + cb], dst[i:i + cb],
+                                      xc[i:i + cb], L["W_gate"], L["W_up"], L["W_down"],
+                                      y=yc[i:i + cb])
+        th, _ = cd.countdown_calibrate(dplan, cd.CD_VARIANT_DUAL_PRED, xc, k, A_t=L["A_t"],
+                                       B_t=L["B_t"])
+        thld.append(float(th.item()))
+    dplan.close()
+    del hc, yc, xc
+    log(f"[bench] stack thresholds (k={k}): first {thld[:3]}, last {thld[-1]:.4f}")
+
+    H = h0(steps_tokens + warmup_tokens, T_EVAL)
+    hb = [torch.empty((1, dm), dtype=torch.float32, device="cuda") for _ in range(2)]
+    xb = torch.empty((1, dm), dtype=torch.bfloat16, device="cuda")
+    yb = torch.empty((1, dm), dtype=torch.float32, device="cuda")
+    plan = cd.Plan(dm, dff, max_batch=1, d_rank=dr)
+    n_arr = torch.zeros(nl, dtype=torch.int32, device="cuda")
+    lib = cd.load_library()
+
+    def token(i, variant, record=False):
+        for l, L in enumerate(layers):
+            src = H[i:i + 1] if l == 0 else hb[(l + 1) % 2]
+            cd.countdown_ffn_residual(plan, variant, src, None if l == 0 else yb, hb[l % 2], xb,
+                                      L["W_gate"], L["W_up"], L["W_down"], thld[l],
+                                      A_t=L["A_t"] if variant == cd.CD_VARIANT_DUAL_PRED else None,
+                                      B_t=L["B_t"] if variant == cd.CD_VARIANT_DUAL_PRED else None,
+                                      y=yb)
+            if record:
+                lib.countdown_export_active(plan.handle, None, n_arr[l:l + 1].data_ptr(), None,
+                                            None, torch.cuda.current_stream().cuda_stream)
+
+    res = {}
+    for name, variant in (("dual_pred", cd.CD_VARIANT_DUAL_PRED), ("dense", cd.CD_VARIANT_DENSE)):
+        ntok = steps_tokens if name == "dual_pred" else max(16, steps_tokens // 8)
+        for i in range(warmup_tokens):
+            token(steps_tokens + i, variant)
+        torch.cuda.synchronize()
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g):
+            for i in range(ntok):
+                token(i, variant)
+        g.replay()
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        g.replay()
+        e1.record()
+        torch.cuda.synchronize()
+        ms = e0.elapsed_time(e1)
+        del g
+        res[name] = {"tokens": ntok, "ms_total": ms, "tokens_per_s": ntok / (ms * 1e-3),
+                     "us_per_token": ms * 1e3 / ntok, "us_per_layer": ms * 1e3 / (ntok * nl)}
+    # |IDX| per layer for one token, and the algorithmic bytes of a token
+    token(0, cd.CD_VARIANT_DUAL_PRED, record=True)
+    torch.cuda.synchronize()
+    n = n_arr.cpu().numpy()
+    from paper_2505_17701_amd import traffic
+
+    tok_bytes = sum(traffic.algorithmic_bytes("dual_pred", dm, dff, int(v), d_rank=dr)["total"]
+                    for v in n)
+    dense_bytes = nl * traffic.algorithmic_bytes("dense", dm, dff, dff)["total"]
+    r = res["dual_pred"]
+    r["algorithmic_bytes_per_token"] = tok_bytes
+    r["achieved_GBs"] = tok_bytes / (r["us_per_token"] * 1e-6) / 1e9
+    r["frac_hbm_peak"] = r["achieved_GBs"] / HBM_PEAK_GBS
+    r["n_active_mean"] = float(n.mean())
+    r["realised_sparsity"] = float(1 - n.mean() / dff)
+    r["speedup_vs_dense"] = res["dense"]["us_per_token"] / r["us_per_token"]
+    r["ideal_byte_ratio"] = dense_bytes / tok_bytes
+    plan.close()
+    del layers
+    torch.cuda.empty_cache()
+    log(f"[bench] stack: {json.dumps(res)}")
+    return {"workload": w.name, "layers": nl, "k": k, "batch": 1,
+            "thld_first_last": [thld[0], thld[-1]], **res}
+
+
 def main():
     args = parse()
     if args.gpus != 1:
@@ -357,6 +474,8 @@ def main():
     others = {}
     if not args.no_extra and not args.no_other:
         others = other_workloads(args)
+        if not args.no_stack:
+            others["stack32_llama7b_pred"] = stack_bench(args)
 
     # CPU baseline: the fp64 oracle on host cores, bounded sample of the same workload
     cpu = None

@@ -111,6 +111,27 @@ cd_status countdown_ffn_dense(cd_plan *plan, const uint16_t *x, int B, const uin
                               void *stream);
 
 /*
+ * One layer of a stack of FFNs joined by a residual stream. The paper
+ * evaluates single Gated-MLP layers (Sec. 3); the stack workload adds, per
+ * token b, before the FFN of `variant` (CD_VARIANT_*, as in the calls above):
+ *   h_out_b = h_in_b + y_prev_b                    (fp32; y_prev NULL: h_out = h_in)
+ *   x_b = bf16(h_out_b / sqrt(mean_j(h_out_b[j]^2) + eps))   (RMSNorm, unit gain,
+ *                                                             round to nearest even)
+ * then y = FFN(x). x is written to x_out [B][d_model] bf16 (the FFN input).
+ * h_in, y_prev, h_out are [B][d_model] fp32. Only y_prev and y may share
+ * memory (y_prev is read before y is written); any other overlap among h_in,
+ * h_out, x_out, y and y_prev is CD_EINVAL. eps must be finite and >= 0.
+ * thld is ignored for CD_VARIANT_DENSE; A_t / B_t as for countdown_ffn_dual
+ * (both set exactly for CD_VARIANT_DUAL_PRED, else NULL). With the predictor
+ * the normalisation is computed inside the latent product's kernel.
+ */
+cd_status countdown_ffn_residual(cd_plan *plan, int variant, const float *h_in,
+                                 const float *y_prev, float *h_out, float eps, uint16_t *x_out,
+                                 int B, const uint16_t *W_gate, const uint16_t *W_up,
+                                 const uint16_t *W_down, const uint16_t *A_t, const uint16_t *B_t,
+                                 float thld, float *y, void *stream);
+
+/*
  * Layerwise threshold calibration (Sec. 4): thld = (1/T) sum_t Quantile(k, c^(t))
  * over T calibration tokens X [T][d_model], with c^(t) the variant's
  * coefficient vector (|u| mono, |s| dual ideal, signed s_hat dual pred) and
@@ -176,7 +197,7 @@ cd_status countdown_check_shape(int d_model, int d_ff, int max_batch, int d_rank
 const char *countdown_status_string(cd_status status);
 
 /* ABI version of this header (bumped on any signature change). */
-#define COUNTDOWN_ABI_VERSION 3
+#define COUNTDOWN_ABI_VERSION 4
 int countdown_abi_version(void);
 
 #ifdef __cplusplus

@@ -22,7 +22,8 @@ CD_PHASE_COEF, CD_PHASE_DOWN, CD_PHASE_ALL = 1, 2, 3
 # every symbol include/countdown.h declares
 EXPORTS = (
     "countdown_plan_create", "countdown_plan_destroy", "countdown_ffn_mono", "countdown_ffn_dual",
-    "countdown_ffn_dense", "countdown_calibrate", "countdown_export_active",
+    "countdown_ffn_dense", "countdown_ffn_residual", "countdown_calibrate",
+    "countdown_export_active",
     "countdown_plan_set_phases", "countdown_check_args",
     "countdown_check_shape", "countdown_status_string", "countdown_abi_version",
 )
@@ -52,6 +53,8 @@ def load_library(path: str = LIB_PATH):
         "countdown_ffn_mono": (i, [vp, vp, i, vp, vp, vp, f, vp, vp]),
         "countdown_ffn_dual": (i, [vp, vp, i, vp, vp, vp, vp, vp, f, vp, vp]),
         "countdown_ffn_dense": (i, [vp, vp, i, vp, vp, vp, vp, vp]),
+        "countdown_ffn_residual": (i, [vp, i, vp, vp, vp, f, vp, i, vp, vp, vp, vp, vp, f, vp,
+                                       vp]),
         "countdown_calibrate": (i, [vp, i, vp, i, vp, vp, vp, vp, d, vp, vp, vp]),
         "countdown_export_active": (i, [vp, vp, vp, vp, vp, vp]),
         "countdown_plan_set_phases": (i, [vp, u]),
@@ -179,6 +182,30 @@ def countdown_ffn_dual(plan: Plan, x, W_gate, W_up, W_down, thld: float, A_t=Non
         plan.handle, _ptr(_bf16(x)), B, _ptr(_bf16(W_gate)), _ptr(_bf16(W_up)),
         _ptr(_bf16(W_down)), _ptr(_bf16(A_t)), _ptr(_bf16(B_t)), float(thld), _ptr(y),
         _stream(stream)), "countdown_ffn_dual")
+    plan.last_batch = B
+    return y
+
+
+def countdown_ffn_residual(plan: Plan, variant: int, h_in, y_prev, h_out, x_out, W_gate, W_up,
+                           W_down, thld: float = 0.0, A_t=None, B_t=None, eps: float = 1e-5,
+                           y=None, stream=None):
+    """One layer of a residual stack: h_out = h_in + y_prev, x_out = bf16(RMSNorm(h_out)),
+    then the ``variant`` FFN of x_out into ``y`` (returned). ``y_prev`` may be None or ``y``."""
+    import torch
+
+    B = h_in.shape[0]
+    if y is None:
+        y = torch.empty((B, plan.d_model), dtype=torch.float32, device=h_in.device)
+    for t in (h_in, h_out, y) + (() if y_prev is None else (y_prev,)):
+        if t.dtype != torch.float32 or not t.is_contiguous() or tuple(t.shape) != (B, plan.d_model):
+            raise ValueError("h_in, y_prev, h_out and y must be contiguous fp32 [B, d_model]")
+    if tuple(x_out.shape) != (B, plan.d_model) or not x_out.is_contiguous():
+        raise ValueError("x_out must be a contiguous [B, d_model] bf16 tensor")
+    _check(load_library().countdown_ffn_residual(
+        plan.handle, int(variant), _ptr(h_in), _ptr(y_prev), _ptr(h_out), float(eps),
+        _ptr(_bf16(x_out)), B, _ptr(_bf16(W_gate)), _ptr(_bf16(W_up)), _ptr(_bf16(W_down)),
+        _ptr(_bf16(A_t)), _ptr(_bf16(B_t)), float(thld), _ptr(y), _stream(stream)),
+        "countdown_ffn_residual")
     plan.last_batch = B
     return y
 

@@ -163,6 +163,68 @@ cd_status run_ffn(cd_plan *p, int variant, const uint16_t *x, int B, const uint1
     return st;
 }
 
+// [a, a + na) and [b, b + nb) share a byte
+bool overlaps(const void *a, size_t na, const void *b, size_t nb)
+{
+    const uintptr_t x = reinterpret_cast<uintptr_t>(a), y = reinterpret_cast<uintptr_t>(b);
+    return x < y + nb && y < x + na;
+}
+
+cd_status run_ffn_residual(cd_plan *p, int variant, const float *h_in, const float *y_prev,
+                           float *h_out, float eps, uint16_t *x_out, int B, const uint16_t *Wg,
+                           const uint16_t *Wu, const uint16_t *Wd, const uint16_t *At,
+                           const uint16_t *Bt, float thld, float *y, void *stream)
+{
+    if (!p)
+        return CD_EINVAL;
+    cd_status st = check_args(variant, p->d_model, p->d_ff, p->max_batch, p->d_rank, x_out, B, Wg,
+                              Wu, Wd, At, Bt, thld, y);
+    if (st != CD_OK)
+        return st;
+    if (!h_in || !h_out || !aligned16(h_in) || !aligned16(h_out) ||
+        (y_prev && !aligned16(y_prev)) || !(eps >= 0.0f) || std::isinf(eps))
+        return CD_EINVAL;
+    const size_t fb = (size_t)B * p->d_model * sizeof(float);
+    const size_t xb = (size_t)B * p->d_model * sizeof(uint16_t);
+    // h_in and y_prev are read by every workgroup of the first kernel while h_out and
+    // x_out are written, and y is zeroed by the next: only y_prev and y may coincide
+    if (overlaps(h_in, fb, h_out, fb) || overlaps(h_in, fb, x_out, xb) ||
+        overlaps(h_out, fb, x_out, xb) || overlaps(h_out, fb, y, fb) ||
+        overlaps(x_out, xb, y, fb) || overlaps(h_in, fb, y, fb) ||
+        (y_prev && (overlaps(y_prev, fb, h_out, fb) || overlaps(y_prev, fb, x_out, xb))))
+        return CD_EINVAL;
+    hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+    if (!(p->phases & CD_PHASE_COEF) && !p->has_state)
+        return CD_EINVAL;
+    p->last_batch = B;
+    if (p->phases & CD_PHASE_COEF) {
+        cdk::NormArgs n;
+        n.h_in = h_in;
+        n.y_prev = y_prev;
+        n.h_out = h_out;
+        n.x_out = x_out;
+        n.nb = B;
+        n.d_model = p->d_model;
+        n.eps = eps;
+        if (variant == CD_VARIANT_DUAL_PRED)
+            st = launched(cdk::launch_latent_norm(n, At, p->d_rank, p->lat, s));
+        else
+            st = launched(cdk::launch_norm(n, s));
+        if (st != CD_OK)
+            return st;
+        const cdk::CoefArgs ca = coef_args(p, x_out, B, Wg, Wu, Bt, thld, y);
+        st = launched(cdk::launch_coef(kernel_variant(variant), ca, s));
+        if (st != CD_OK)
+            return st;
+        p->has_state = true;
+    }
+    if (p->phases & CD_PHASE_DOWN) {
+        const cdk::DownArgs da = down_args(p, B, Wd, y);
+        st = launched(cdk::launch_down(da, s));
+    }
+    return st;
+}
+
 template <class T>
 cd_status dalloc(T **ptr, size_t count)
 {
@@ -201,6 +263,18 @@ const char *countdown_status_string(cd_status st)
     case CD_ENOMEM: return "CD_ENOMEM: device allocation failed";
     default: return "unknown countdown status";
     }
+}
+
+cd_status countdown_ffn_residual(cd_plan *plan, int variant, const float *h_in, const float *y_prev,
+                                float *h_out, float eps, uint16_t *x_out, int B,
+                                const uint16_t *W_gate, const uint16_t *W_up,
+                                const uint16_t *W_down, const uint16_t *A_t, const uint16_t *B_t,
+                                float thld, float *y, void *stream)
+{
+    if (variant == CD_VARIANT_DENSE)
+        thld = -INFINITY;
+    return run_ffn_residual(plan, variant, h_in, y_prev, h_out, eps, x_out, B, W_gate, W_up,
+                            W_down, A_t, B_t, thld, y, stream);
 }
 
 cd_status countdown_check_shape(int d_model, int d_ff, int max_batch, int d_rank)

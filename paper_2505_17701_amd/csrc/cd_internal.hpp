@@ -37,6 +37,17 @@ struct DownArgs {
     float *y;            // [nb][d_model], accumulated
 };
 
+// Residual stream between stacked layers (not part of the paper's method):
+// h_out = h_in + y_prev, x_out = bf16(h_out / sqrt(mean(h_out^2) + eps)).
+struct NormArgs {
+    const float *h_in;    // [nb][d_model]
+    const float *y_prev;  // [nb][d_model] or NULL (no residual add)
+    float *h_out;         // [nb][d_model], distinct from h_in
+    uint16_t *x_out;      // [nb][d_model] bf16
+    int nb, d_model;
+    float eps;
+};
+
 // Smallest supported template widths for a call.
 int batch_tile(int B);        // 1, 2, 4 or 8
 int col_tile(int d_model);    // chunks of 512 columns: 1, 2, 4, 8 or 16
@@ -46,6 +57,11 @@ hipError_t launch_coef(int variant, const CoefArgs &a, hipStream_t s);
 hipError_t launch_latent(const uint16_t *x, int nb, const uint16_t *At, int d_model, int d_rank,
                          float *lat, hipStream_t s);
 hipError_t launch_down(const DownArgs &a, hipStream_t s);
+// x_out / h_out of the residual stream (one workgroup)
+hipError_t launch_norm(const NormArgs &n, hipStream_t s);
+// the same fused with the predictor latent: every workgroup normalises, the first writes
+hipError_t launch_latent_norm(const NormArgs &n, const uint16_t *At, int d_rank, float *lat,
+                              hipStream_t s);
 // Flat ascending IDX / |IDX| / compact s from the per-neuron arrays (any output may be NULL).
 hipError_t launch_export(const int *act, const float *s_rows, int nb, int d_ff, int *idx_dst,
                          int *n_dst, float *s_dst, hipStream_t s);

@@ -300,20 +300,6 @@ __global__ __launch_bounds__(kBlock) void k_coef_dual(const CoefArgs a)
 
 constexpr int kPredRowsPerWave = 8;
 constexpr int kPredRows = kPredRowsPerWave * kWavesPerBlock;  // neurons per workgroup
-constexpr int kPredLoads = 8;  // 16-byte B_t loads per lane and pass (one pass up to rank 512)
-
-// Sum over aligned segments of 2^lg lanes with lg (0..6) known at run time
-// (wave-uniform); the last lane of every segment holds the segment sum.
-__device__ __forceinline__ float segment_sum_rt(float v, int lg)
-{
-    if (lg >= 1) v += dpp0<kDppQuadSwap1>(v);
-    if (lg >= 2) v += dpp0<kDppQuadSwap2>(v);
-    if (lg >= 3) v += dpp0<kDppHalfMirror>(v);
-    if (lg >= 4) v += dpp0<kDppMirror>(v);
-    if (lg >= 5) v += dpp0<kDppBcast15, 0xA>(v);
-    if (lg >= 6) v += dpp0<kDppBcast31, 0xC>(v);
-    return v;
-}
 
 // The predictor latent [B][d_rank] fp32 on its way to LDS: the part a rank of up
 // to 256 needs is loaded with the kernel's other loads (issue), written after
@@ -349,108 +335,110 @@ struct LatentStage {
     }
 };
 
-// One 16-byte B_t chunk per lane into the scores; every jpr-th chunk closes
-// the rows of its slot (segment sums, coefficient, union threshold, act
-// flag). Returns true on the lane that closed an active row of this wave.
-template <int B>
-__device__ __forceinline__ bool pred_slot(const u32x4 &w, int j, int lane, int lcpr, int jpr,
-                                          int seg_log, bool seg_end, int wr0, const float *lat,
-                                          const CoefArgs &a, float (&acc)[B])
-{
-    const int cpr = 1 << lcpr;
-    const int f = j * kWave + lane;
-    const int e = (f & (cpr - 1)) * 8;
-    const float wf[8] = {bf16_lo(w.x), bf16_hi(w.x), bf16_lo(w.y), bf16_hi(w.y),
-                         bf16_lo(w.z), bf16_hi(w.z), bf16_lo(w.w), bf16_hi(w.w)};
-#pragma unroll
-    for (int b = 0; b < B; ++b) {
-        if (b >= a.nb)
-            break;
-        const float4 l0 = *reinterpret_cast<const float4 *>(lat + b * a.d_rank + e);
-        const float4 l1 = *reinterpret_cast<const float4 *>(lat + b * a.d_rank + e + 4);
-        acc[b] = fmaf(wf[0], l0.x, acc[b]);
-        acc[b] = fmaf(wf[1], l0.y, acc[b]);
-        acc[b] = fmaf(wf[2], l0.z, acc[b]);
-        acc[b] = fmaf(wf[3], l0.w, acc[b]);
-        acc[b] = fmaf(wf[4], l1.x, acc[b]);
-        acc[b] = fmaf(wf[5], l1.y, acc[b]);
-        acc[b] = fmaf(wf[6], l1.z, acc[b]);
-        acc[b] = fmaf(wf[7], l1.w, acc[b]);
-    }
-    if ((j + 1) % jpr != 0)
-        return false;
-    const int rw = f >> lcpr;
-    const int row = wr0 + rw;
-    const bool live = seg_end && rw < kPredRowsPerWave && row < a.d_ff;
-    bool act = false;
-#pragma unroll
-    for (int b = 0; b < B; ++b) {
-        const float v = segment_sum_rt(acc[b], seg_log);
-        acc[b] = 0.0f;
-        if (b < a.nb) {
-            act = act || (v > a.thld);
-            if (a.coef && live)
-                a.coef[(size_t)b * a.d_ff + row] = v;
-        }
-    }
-    if (live)
-        a.act[row] = act ? 1 : 0;
-    return live && act;
-}
+// Shape of one wave's B_t work at rank d_rank = 8 << LCPR: its kPredRowsPerWave
+// rows are one flat run of 16-byte chunks, chunk f on lane f % 64, kLoads per
+// lane. A row is a segment of min(cpr, 64) lanes (summed by DPP) spread over
+// kJpr consecutive loads when it is longer than 64 chunks.
+template <int LCPR>
+struct PredShape {
+    static constexpr int kCpr = 1 << LCPR;  // 16-byte chunks per B_t row
+    static constexpr int kLoads = kCpr * kPredRowsPerWave >= kWave ? kCpr * kPredRowsPerWave / kWave : 1;
+    static constexpr int kJpr = kCpr > kWave ? kCpr / kWave : 1;
+    static constexpr int kSegLog = LCPR < 6 ? LCPR : 6;
+    static constexpr int kSeg = 1 << kSegLog;
+};
 
-// The wave's kPredRowsPerWave B_t rows as one flat run of 16-byte chunks,
-// chunk f on lane f % 64; this pass issues chunks j0 * 64 ... (j0 + 8) * 64 - 1
-// (every load in flight at once).
-__device__ __forceinline__ void pred_load_bt(u32x4 (&wb)[kPredLoads], const CoefArgs &a, int wr0,
-                                             int lane, int lcpr, int J, int j0)
+template <int LCPR>
+__device__ __forceinline__ void pred_issue_bt(u32x4 (&wb)[PredShape<LCPR>::kLoads],
+                                              const CoefArgs &a, int wr0, int lane)
 {
-    const int cpr = 1 << lcpr;
+    using S = PredShape<LCPR>;
 #pragma unroll
-    for (int t = 0; t < kPredLoads; ++t) {
-        const int j = j0 + t;
+    for (int j = 0; j < S::kLoads; ++j) {
         const int f = j * kWave + lane;
-        const int rw = f >> lcpr;
-        wb[t] = zero16();
-        if (j < J && rw < kPredRowsPerWave && wr0 + rw < a.d_ff)
-            wb[t] = load16_stream(a.Bt + (size_t)(wr0 + rw) * a.d_rank + (f & (cpr - 1)) * 8);
+        const int rw = f >> LCPR;
+        wb[j] = zero16();
+        if (rw < kPredRowsPerWave && wr0 + rw < a.d_ff)
+            wb[j] = load16_stream(a.Bt + (size_t)(wr0 + rw) * a.d_rank + (f & (S::kCpr - 1)) * 8);
     }
 }
 
-// Scores of one pass of B_t chunks (see pred_slot); returns the wave-uniform
-// mask of this wave's active neurons closed in the pass.
-template <int B>
-__device__ __forceinline__ uint32_t pred_scores(const u32x4 (&wb)[kPredLoads], int j0, int J,
-                                                int lane, int lcpr, int wr0, const float *lat,
-                                                const CoefArgs &a)
+// s_hat_b = latent_b . B_t[row] for the wave's rows (latent from LDS), the
+// signed threshold with the union over the batch, act[] and (optionally) the
+// coefficients. Returns the wave-uniform mask of its active rows.
+template <int B, int LCPR>
+__device__ __forceinline__ uint32_t pred_score(const u32x4 (&wb)[PredShape<LCPR>::kLoads],
+                                               const float *lat, const CoefArgs &a, int wr0,
+                                               int lane)
 {
-    const int cpr = 1 << lcpr;
-    const int jpr = cpr > kWave ? cpr / kWave : 1;
-    const int seg_log = min(lcpr, 6);
-    const bool seg_end = (lane & ((1 << seg_log) - 1)) == (1 << seg_log) - 1;
+    using S = PredShape<LCPR>;
+    // up to rank 512 a lane meets the same 8 latent entries in every load: read once
+    constexpr bool kLatOnce = S::kCpr <= kWave;
+    const bool seg_end = (lane & (S::kSeg - 1)) == S::kSeg - 1;
     float acc[B];
     zero_acc(acc);
+    float lreg[kLatOnce ? B : 1][8];
+    if constexpr (kLatOnce) {
+        const int e = (lane & (S::kCpr - 1)) * 8;
+#pragma unroll
+        for (int b = 0; b < B; ++b)
+#pragma unroll
+            for (int q = 0; q < 8; ++q)
+                lreg[b][q] = b < a.nb ? lat[b * a.d_rank + e + q] : 0.0f;
+    }
     uint32_t wmask = 0;
 #pragma unroll
-    for (int t = 0; t < kPredLoads; ++t) {
-        const int j = j0 + t;
-        if (j < J) {
-            const bool act = pred_slot<B>(wb[t], j, lane, lcpr, jpr, seg_log, seg_end, wr0, lat,
-                                          a, acc);
-            for (uint64_t m = ballot(act); m; m &= m - 1)
-                wmask |= 1u << ((j * kWave + __builtin_ctzll(m)) >> lcpr);
+    for (int j = 0; j < S::kLoads; ++j) {
+        const int f = j * kWave + lane;
+        const int e = (f & (S::kCpr - 1)) * 8;
+        const u32x4 w = wb[j];
+        const float wf[8] = {bf16_lo(w.x), bf16_hi(w.x), bf16_lo(w.y), bf16_hi(w.y),
+                             bf16_lo(w.z), bf16_hi(w.z), bf16_lo(w.w), bf16_hi(w.w)};
+#pragma unroll
+        for (int b = 0; b < B; ++b) {
+            if (b < a.nb) {
+#pragma unroll
+                for (int q = 0; q < 8; ++q)
+                    acc[b] = fmaf(wf[q], kLatOnce ? lreg[b][q] : lat[b * a.d_rank + e + q], acc[b]);
+            }
+        }
+        if ((j + 1) % S::kJpr != 0)
+            continue;
+        // the segment ends of this load close its rows
+        const int rw = f >> LCPR;
+        const int row = wr0 + rw;
+        const bool live = seg_end && rw < kPredRowsPerWave && row < a.d_ff;
+        bool act = false;
+#pragma unroll
+        for (int b = 0; b < B; ++b) {
+            const float v = segment_sum<S::kSegLog>(acc[b]);
+            acc[b] = 0.0f;
+            if (b < a.nb) {
+                act = act || (v > a.thld);
+                if (a.coef && live)
+                    a.coef[(size_t)b * a.d_ff + row] = v;
+            }
+        }
+        if (live)
+            a.act[row] = act ? 1 : 0;
+        const uint64_t m = ballot(live && act);
+#pragma unroll
+        for (int i = 0; i < kWave / S::kSeg; ++i) {
+            const int end = (i + 1) * S::kSeg - 1;        // lane of segment i's sum
+            const int rwi = (j * kWave + end) >> LCPR;    // its row within the wave
+            if (rwi < kPredRowsPerWave)
+                wmask |= (uint32_t)((m >> end) & 1u) << rwi;
         }
     }
     return wmask;
 }
 
-// s = u * SiLU(g) of one active neuron: its W_gate and W_up rows against the tokens
+// s = u * SiLU(g) of one active neuron from its W_gate and W_up rows
 template <int B, int NK, bool XREG>
-__device__ __forceinline__ void pred_gather(const CoefArgs &a, const Tokens<B, NK, XREG> &tok,
-                                            int row, int lane)
+__device__ __forceinline__ void pred_finish(const CoefArgs &a, const Tokens<B, NK, XREG> &tok,
+                                            const u32x4 (&wg)[NK], const u32x4 (&wu)[NK], int row,
+                                            int lane)
 {
-    u32x4 wg[NK], wu[NK];
-    load_row<NK>(wg, a.Wg + (size_t)row * a.d_model, a.d_model, lane);
-    load_row<NK>(wu, a.Wu + (size_t)row * a.d_model, a.d_model, lane);
     float ag[B], au[B];
     zero_acc(ag);
     zero_acc(au);
@@ -464,87 +452,99 @@ __device__ __forceinline__ void pred_gather(const CoefArgs &a, const Tokens<B, N
     }
 }
 
-// Practical D-CountDown coefficient kernel for batches of 1-2 (Sec. 4). After
-// one barrier (the latent staged in LDS) the waves are independent: each
-// scores kPredRowsPerWave neurons (s_hat = latent . B_t[row], signed
-// threshold, union over the batch), then gathers the W_gate and W_up rows of
-// its own active neurons against the tokens in registers (loaded beside the
-// B_t rows) and writes s = u * SiLU(g).
-template <int B, int NK>
-__global__ __launch_bounds__(kBlock) void k_coef_pred_w(const CoefArgs a)
+// Next neuron of this wave's share of the block mask (every fourth active
+// neuron), or -1; advances the mask past it.
+__device__ __forceinline__ int pred_next(uint32_t &m)
 {
-    extern __shared__ __align__(16) float lat_lds[];  // latent [B][d_rank]
-    const int lane = threadIdx.x % kWave, wave = threadIdx.x / kWave;
-    const int wr0 = (blockIdx.x * kWavesPerBlock + wave) * kPredRowsPerWave;
-    const int lcpr = 31 - __builtin_clz(a.d_rank / 8);
-    const int J = max(1, kPredRowsPerWave * (1 << lcpr) / kWave);  // B_t loads per lane
-    u32x4 wb[kPredLoads];
-    pred_load_bt(wb, a, wr0, lane, lcpr, J, 0);
-    Tokens<B, NK, true> tok;
-    tok.issue(a.x, a.nb, a.d_model, lane);
-    LatentStage<B> ls;
-    ls.issue(a.lat, a.nb, a.d_rank);
-    zero_y(a.y, a.nb * a.d_model);
-    ls.write(reinterpret_cast<u32x4 *>(lat_lds), a.lat, a.nb, a.d_rank);
-    __syncthreads();
-    if (wr0 >= a.d_ff)
-        return;
-
-    uint32_t wmask = pred_scores<B>(wb, 0, J, lane, lcpr, wr0, lat_lds, a);
-    for (int j0 = kPredLoads; j0 < J; j0 += kPredLoads) {
-        pred_load_bt(wb, a, wr0, lane, lcpr, J, j0);
-        wmask |= pred_scores<B>(wb, j0, J, lane, lcpr, wr0, lat_lds, a);
-    }
-    for (; wmask; wmask &= wmask - 1)
-        pred_gather<B, NK, true>(a, tok, wr0 + __builtin_ctz(wmask), lane);
+    if (!m)
+        return -1;
+    const int r = __builtin_ctz(m);
+#pragma unroll
+    for (int k = 0; k < kWavesPerBlock; ++k)
+        m &= m - 1;
+    return r;
 }
 
-// Practical D-CountDown coefficient kernel for batches of 4-8 (Sec. 4). A
-// workgroup owns a block of kPredRows neurons: it stages the tokens and the
-// latent in LDS once, scores its B_t rows (signed threshold, union over the
-// batch), and its four waves then share the block's active neurons: W_gate
-// and W_up rows against the LDS tokens, s = u * SiLU(g).
-template <int B, int NK>
+// Practical D-CountDown coefficient kernel (Sec. 4). A workgroup owns a block
+// of kPredRows neurons (kPredRowsPerWave per wave). One round of loads brings
+// the wave's B_t rows, the tokens (registers for batches of 1-2, this
+// thread's share of an LDS copy for 4-8) and the latent (staged in LDS).
+// Each wave scores its rows (s_hat = latent . B_t[row], signed threshold,
+// union over the batch); the block's active neurons are then dealt
+// round-robin to the four waves, which gather their W_gate and W_up rows
+// (the next row's loads in flight while the current one is reduced) and
+// write s = u * SiLU(g).
+template <int B, int NK, bool XREG, int LCPR>
 __global__ __launch_bounds__(kBlock) void k_coef_pred(const CoefArgs a)
 {
-    extern __shared__ __align__(16) uint32_t xs[];  // tokens [B][NK * 256], then latent [B][d_rank]
+    extern __shared__ __align__(16) uint32_t xs[];  // [tokens [B][NK * 256]], latent [B][d_rank]
     __shared__ uint32_t wflag[kWavesPerBlock];
+    using S = PredShape<LCPR>;
+    constexpr bool kPrefetch = NK <= 8;  // two rows of W_gate + W_up in registers
     const int lane = threadIdx.x % kWave, wave = threadIdx.x / kWave;
     const int r0 = blockIdx.x * kPredRows;
     const int wr0 = r0 + wave * kPredRowsPerWave;
-    const int lcpr = 31 - __builtin_clz(a.d_rank / 8);
-    const int J = max(1, kPredRowsPerWave * (1 << lcpr) / kWave);  // B_t loads per lane
-    u32x4 wb[kPredLoads];
-    pred_load_bt(wb, a, wr0, lane, lcpr, J, 0);
-    Tokens<B, NK, false> tok;
+
+    u32x4 wb[S::kLoads];
+    pred_issue_bt<LCPR>(wb, a, wr0, lane);
+    Tokens<B, NK, XREG> tok;
     tok.issue(a.x, a.nb, a.d_model, lane);
     LatentStage<B> ls;
     ls.issue(a.lat, a.nb, a.d_rank);
     zero_y(a.y, a.nb * a.d_model);
     tok.write(xs);
-    u32x4 *lat4 = reinterpret_cast<u32x4 *>(xs + B * NK * kColsPerLoad / 2);
-    ls.write(lat4, a.lat, a.nb, a.d_rank);
-    const float *lat = reinterpret_cast<const float *>(lat4);
+    uint32_t *latw = xs + (XREG ? 0 : B * NK * kColsPerLoad / 2);
+    ls.write(reinterpret_cast<u32x4 *>(latw), a.lat, a.nb, a.d_rank);
     __syncthreads();
 
-    uint32_t wmask = pred_scores<B>(wb, 0, J, lane, lcpr, wr0, lat, a);
-    for (int j0 = kPredLoads; j0 < J; j0 += kPredLoads) {
-        pred_load_bt(wb, a, wr0, lane, lcpr, J, j0);
-        wmask |= pred_scores<B>(wb, j0, J, lane, lcpr, wr0, lat, a);
-    }
+    const uint32_t wmask = pred_score<B, LCPR>(wb, reinterpret_cast<const float *>(latw), a, wr0,
+                                               lane);
     if (lane == 0)
         wflag[wave] = wmask;
     __syncthreads();
-
-    // the block's active neurons in ascending order, dealt round-robin to the waves
-    uint32_t M = 0;
+    uint32_t m = 0;
 #pragma unroll
     for (int v = 0; v < kWavesPerBlock; ++v)
-        M |= wflag[v] << (v * kPredRowsPerWave);
-    int e = 0;
-    for (; M; M &= M - 1, ++e)
-        if (e % kWavesPerBlock == wave)
-            pred_gather<B, NK, false>(a, tok, r0 + __builtin_ctz(M), lane);
+        m |= wflag[v] << (v * kPredRowsPerWave);
+    for (int v = 0; v < wave; ++v)  // this wave's share starts at active neuron number `wave`
+        m &= m - 1;
+
+    int ra = pred_next(m);
+    if (ra < 0)
+        return;
+    u32x4 ga[NK], ua[NK];
+    load_row<NK>(ga, a.Wg + (size_t)(r0 + ra) * a.d_model, a.d_model, lane);
+    load_row<NK>(ua, a.Wu + (size_t)(r0 + ra) * a.d_model, a.d_model, lane);
+    if constexpr (kPrefetch) {
+        u32x4 gb[NK], ub[NK];
+        for (;;) {
+            const int rb = pred_next(m);
+            if (rb >= 0) {
+                load_row<NK>(gb, a.Wg + (size_t)(r0 + rb) * a.d_model, a.d_model, lane);
+                load_row<NK>(ub, a.Wu + (size_t)(r0 + rb) * a.d_model, a.d_model, lane);
+            }
+            pred_finish<B, NK, XREG>(a, tok, ga, ua, r0 + ra, lane);
+            if (rb < 0)
+                break;
+            ra = pred_next(m);
+            if (ra >= 0) {
+                load_row<NK>(ga, a.Wg + (size_t)(r0 + ra) * a.d_model, a.d_model, lane);
+                load_row<NK>(ua, a.Wu + (size_t)(r0 + ra) * a.d_model, a.d_model, lane);
+            }
+            pred_finish<B, NK, XREG>(a, tok, gb, ub, r0 + rb, lane);
+            if (ra < 0)
+                break;
+        }
+    } else {
+        for (;;) {
+            pred_finish<B, NK, XREG>(a, tok, ga, ua, r0 + ra, lane);
+            ra = pred_next(m);
+            if (ra < 0)
+                break;
+            load_row<NK>(ga, a.Wg + (size_t)(r0 + ra) * a.d_model, a.d_model, lane);
+            load_row<NK>(ua, a.Wu + (size_t)(r0 + ra) * a.d_model, a.d_model, lane);
+        }
+    }
 }
 
 // latent = x . theta_A for the predictor: one workgroup per row of A_t, the
@@ -587,6 +587,154 @@ __global__ __launch_bounds__(kBlock) void k_latent(const uint16_t *__restrict__ 
     }
     __syncthreads();
     if (threadIdx.x < nb) {
+        float v = 0.0f;
+#pragma unroll
+        for (int q = 0; q < kWavesPerBlock; ++q)
+            v += part[q][threadIdx.x];
+        lat[(size_t)threadIdx.x * d_rank + r] = v;
+    }
+}
+
+// ----------------------------------------------------- residual + RMSNorm
+// Joins the layers of a stack of FFNs (the paper's method stops at one layer):
+// per token h = h_in + y_prev (fp32) and x = bf16(h / sqrt(mean(h^2) + eps)),
+// round to nearest even. A 256-thread workgroup holds a token's values in the
+// column layout of the latent product: wave w, lane l owns the 8 columns
+// (w + 4t) * 512 + 8l + [0, 8), t < KW.
+
+__device__ __forceinline__ uint32_t pack_bf16(float lo, float hi)
+{
+    const uint32_t l = __builtin_bit_cast(uint16_t, static_cast<__bf16>(lo));
+    const uint32_t h = __builtin_bit_cast(uint16_t, static_cast<__bf16>(hi));
+    return l | (h << 16);
+}
+
+__device__ __forceinline__ float f32_of(uint32_t v) { return __uint_as_float(v); }
+
+// Normalised tokens of this thread's columns, xq[b][t] (8 bf16 each). With
+// WRITE the thread also stores its columns of h_out and x_out. red: LDS
+// [kWavesPerBlock][B] floats. Every thread of the workgroup must call this.
+template <int B, int KW, bool WRITE>
+__device__ __forceinline__ void residual_norm(const NormArgs &n, int lane, int wave, float *red,
+                                              u32x4 (&xq)[B][KW])
+{
+    u32x4 hv[B][KW][2];  // 8 fp32 of h per (token, chunk), raw bits
+#pragma unroll
+    for (int b = 0; b < B; ++b)
+#pragma unroll
+        for (int t = 0; t < KW; ++t) {
+            const int col = (wave + t * kWavesPerBlock) * kColsPerLoad + lane * 8;
+            const bool ok = b < n.nb && col < n.d_model;
+            const size_t off = (size_t)b * n.d_model + col;
+            const u32x4 *hp = reinterpret_cast<const u32x4 *>(n.h_in + off);
+            hv[b][t][0] = *or_zero(ok, hp);
+            hv[b][t][1] = *or_zero(ok, hp + 1);
+            if (n.y_prev) {
+                const u32x4 *yp = reinterpret_cast<const u32x4 *>(n.y_prev + off);
+                const u32x4 y0 = *or_zero(ok, yp), y1 = *or_zero(ok, yp + 1);
+#pragma unroll
+                for (int q = 0; q < 4; ++q) {
+                    hv[b][t][0][q] = __float_as_uint(f32_of(hv[b][t][0][q]) + f32_of(y0[q]));
+                    hv[b][t][1][q] = __float_as_uint(f32_of(hv[b][t][1][q]) + f32_of(y1[q]));
+                }
+            }
+        }
+    float ss[B];
+#pragma unroll
+    for (int b = 0; b < B; ++b) {
+        float v = 0.0f;
+#pragma unroll
+        for (int t = 0; t < KW; ++t)
+#pragma unroll
+            for (int q = 0; q < 4; ++q)
+                v += f32_of(hv[b][t][0][q]) * f32_of(hv[b][t][0][q]) +
+                     f32_of(hv[b][t][1][q]) * f32_of(hv[b][t][1][q]);
+        ss[b] = wave_sum(v);
+    }
+    if (lane == 0)
+#pragma unroll
+        for (int b = 0; b < B; ++b)
+            red[wave * B + b] = ss[b];
+    __syncthreads();
+#pragma unroll
+    for (int b = 0; b < B; ++b) {
+        float tot = 0.0f;
+#pragma unroll
+        for (int v = 0; v < kWavesPerBlock; ++v)
+            tot += red[v * B + b];
+        const float inv = 1.0f / sqrtf(tot / (float)n.d_model + n.eps);
+#pragma unroll
+        for (int t = 0; t < KW; ++t) {
+            const u32x4 h0 = hv[b][t][0], h1 = hv[b][t][1];
+            xq[b][t] = u32x4{pack_bf16(f32_of(h0.x) * inv, f32_of(h0.y) * inv),
+                             pack_bf16(f32_of(h0.z) * inv, f32_of(h0.w) * inv),
+                             pack_bf16(f32_of(h1.x) * inv, f32_of(h1.y) * inv),
+                             pack_bf16(f32_of(h1.z) * inv, f32_of(h1.w) * inv)};
+            if constexpr (WRITE) {
+                const int col = (wave + t * kWavesPerBlock) * kColsPerLoad + lane * 8;
+                if (b < n.nb && col < n.d_model) {
+                    const size_t off = (size_t)b * n.d_model + col;
+                    u32x4 *ho = reinterpret_cast<u32x4 *>(n.h_out + off);
+                    ho[0] = h0;
+                    ho[1] = h1;
+                    *reinterpret_cast<u32x4 *>(n.x_out + off) = xq[b][t];
+                }
+            }
+        }
+    }
+}
+
+// Residual stream step alone (variants without a latent product): one workgroup.
+template <int B, int NK>
+__global__ __launch_bounds__(kBlock) void k_norm(const NormArgs n)
+{
+    constexpr int KW = (NK + kWavesPerBlock - 1) / kWavesPerBlock;
+    __shared__ float red[kWavesPerBlock * B];
+    const int lane = threadIdx.x % kWave, wave = threadIdx.x / kWave;
+    u32x4 xq[B][KW];
+    residual_norm<B, KW, true>(n, lane, wave, red, xq);
+}
+
+// Residual stream step fused with latent = x . theta_A: one workgroup per row
+// of A_t; each normalises the tokens itself (the first also writes h_out and
+// x_out for the kernels that follow) and takes the dot products with its row.
+template <int B, int NK>
+__global__ __launch_bounds__(kBlock) void k_latent_norm(const NormArgs n,
+                                                        const uint16_t *__restrict__ At,
+                                                        int d_rank, float *__restrict__ lat)
+{
+    constexpr int KW = (NK + kWavesPerBlock - 1) / kWavesPerBlock;
+    __shared__ float red[kWavesPerBlock * B];
+    __shared__ float part[kWavesPerBlock][B];
+    const int lane = threadIdx.x % kWave, wave = threadIdx.x / kWave;
+    const int r = blockIdx.x;
+    const uint16_t *row = At + (size_t)r * n.d_model;
+    u32x4 w[KW];
+#pragma unroll
+    for (int t = 0; t < KW; ++t) {
+        const int col = (wave + t * kWavesPerBlock) * kColsPerLoad + lane * 8;
+        w[t] = col < n.d_model ? load16_stream(row + col) : zero16();
+    }
+    u32x4 xq[B][KW];
+    if (blockIdx.x == 0)
+        residual_norm<B, KW, true>(n, lane, wave, red, xq);
+    else
+        residual_norm<B, KW, false>(n, lane, wave, red, xq);
+    float acc[B];
+    zero_acc(acc);
+#pragma unroll
+    for (int b = 0; b < B; ++b)
+#pragma unroll
+        for (int t = 0; t < KW; ++t)
+            acc[b] = dot8(w[t], xq[b][t], acc[b]);  // chunks past d_model hold zeros in w
+#pragma unroll
+    for (int b = 0; b < B; ++b) {
+        const float v = wave_sum(acc[b]);
+        if (lane == 0)
+            part[wave][b] = v;
+    }
+    __syncthreads();
+    if (threadIdx.x < n.nb) {
         float v = 0.0f;
 #pragma unroll
         for (int q = 0; q < kWavesPerBlock; ++q)
@@ -857,6 +1005,33 @@ size_t down_lds_bytes(int rows_per_group, int bt)
     return (size_t)rows_per_group * 4 * (1 + bt) + (size_t)kWavesPerBlock * kColsPerLoad * 4;
 }
 
+template <int B, int NK, bool XREG, int LCPR>
+static void coef_pred_lcpr(const CoefArgs &a, hipStream_t s)
+{
+    const size_t lds = (XREG ? 0 : (size_t)B * NK * kColsPerLoad * 2) + (size_t)B * a.d_rank * 4;
+    const int grid = (a.d_ff + kPredRows - 1) / kPredRows;
+    allow_lds(k_coef_pred<B, NK, XREG, LCPR>, lds);
+    k_coef_pred<B, NK, XREG, LCPR><<<grid, kBlock, lds, s>>>(a);
+}
+
+// the predictor kernel is specialised on log2 of the B_t row length in 16-byte chunks
+template <int B, int NK, bool XREG>
+static hipError_t coef_pred_launch(const CoefArgs &a, hipStream_t s)
+{
+    switch (a.d_rank) {
+    case 8: coef_pred_lcpr<B, NK, XREG, 0>(a, s); break;
+    case 16: coef_pred_lcpr<B, NK, XREG, 1>(a, s); break;
+    case 32: coef_pred_lcpr<B, NK, XREG, 2>(a, s); break;
+    case 64: coef_pred_lcpr<B, NK, XREG, 3>(a, s); break;
+    case 128: coef_pred_lcpr<B, NK, XREG, 4>(a, s); break;
+    case 256: coef_pred_lcpr<B, NK, XREG, 5>(a, s); break;
+    case 512: coef_pred_lcpr<B, NK, XREG, 6>(a, s); break;
+    case 1024: coef_pred_lcpr<B, NK, XREG, 7>(a, s); break;
+    default: return hipErrorInvalidValue;
+    }
+    return hipGetLastError();
+}
+
 template <int B, int NK>
 static hipError_t coef_bn(int variant, const CoefArgs &a, hipStream_t s)
 {
@@ -876,18 +1051,8 @@ static hipError_t coef_bn(int variant, const CoefArgs &a, hipStream_t s)
         allow_lds(k_coef_dual<B, NK, XREG, true>, lds);
         k_coef_dual<B, NK, XREG, true><<<grid, kBlock, lds, s>>>(a);
         break;
-    case kDualPred: {
-        const int pgrid = (a.d_ff + kPredRows - 1) / kPredRows;
-        if constexpr (XREG) {
-            const size_t plds = (size_t)B * a.d_rank * 4;
-            k_coef_pred_w<B, NK><<<pgrid, kBlock, plds, s>>>(a);
-        } else {
-            const size_t plds = (size_t)B * NK * kColsPerLoad * 2 + (size_t)B * a.d_rank * 4;
-            allow_lds(k_coef_pred<B, NK>, plds);
-            k_coef_pred<B, NK><<<pgrid, kBlock, plds, s>>>(a);
-        }
-        break;
-    }
+    case kDualPred:
+        return coef_pred_launch<B, NK, XREG>(a, s);
     default:
         return hipErrorInvalidValue;
     }
@@ -943,6 +1108,54 @@ hipError_t launch_latent(const uint16_t *x, int nb, const uint16_t *At, int d_mo
     case 4: return latent_b<4>(x, nb, At, d_model, d_rank, lat, s);
     default: return latent_b<8>(x, nb, At, d_model, d_rank, lat, s);
     }
+}
+
+template <int B>
+static hipError_t norm_b(const NormArgs &n, const uint16_t *At, int d_rank, float *lat,
+                         hipStream_t s)
+{
+    const bool fused = At != nullptr;
+#define CD_NORM_CASE(NK)                                                                  \
+    if (fused)                                                                            \
+        k_latent_norm<B, NK><<<d_rank, kBlock, 0, s>>>(n, At, d_rank, lat);               \
+    else                                                                                  \
+        k_norm<B, NK><<<1, kBlock, 0, s>>>(n);                                            \
+    break;
+    switch (col_tile(n.d_model)) {
+    case 1: CD_NORM_CASE(1)
+    case 2: CD_NORM_CASE(2)
+    case 4: CD_NORM_CASE(4)
+    case 8: CD_NORM_CASE(8)
+    default:
+        if constexpr (B * 16 <= 64) {  // batch * d_model <= 32768
+            CD_NORM_CASE(16)
+        }
+        return hipErrorInvalidValue;
+    }
+#undef CD_NORM_CASE
+    return hipGetLastError();
+}
+
+static hipError_t norm_dispatch(const NormArgs &n, const uint16_t *At, int d_rank, float *lat,
+                                hipStream_t s)
+{
+    switch (batch_tile(n.nb)) {
+    case 1: return norm_b<1>(n, At, d_rank, lat, s);
+    case 2: return norm_b<2>(n, At, d_rank, lat, s);
+    case 4: return norm_b<4>(n, At, d_rank, lat, s);
+    default: return norm_b<8>(n, At, d_rank, lat, s);
+    }
+}
+
+hipError_t launch_norm(const NormArgs &n, hipStream_t s)
+{
+    return norm_dispatch(n, nullptr, 0, nullptr, s);
+}
+
+hipError_t launch_latent_norm(const NormArgs &n, const uint16_t *At, int d_rank, float *lat,
+                              hipStream_t s)
+{
+    return norm_dispatch(n, At, d_rank, lat, s);
 }
 
 hipError_t launch_down(const DownArgs &a, hipStream_t s)

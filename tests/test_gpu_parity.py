@@ -88,7 +88,15 @@ def run_oracle(variant, layer, x, thld):
 def compare(plan, variant, layer, x, thld, label, check_coef=True):
     """Full parity check of one call; returns (n_active_gpu, n_flips, y_rel_err)."""
     x = np.atleast_2d(x)
-    y_g, idx_g, s_g, coef_g = run_gpu(plan, variant, layer, x, thld)
+    return check_call(variant, layer, x, thld, run_gpu(plan, variant, layer, x, thld), label,
+                      check_coef)
+
+
+def check_call(variant, layer, x, thld, gpu_out, label, check_coef=True):
+    """Parity of one GPU call's outputs (y, IDX, compact s, coefficients) against the
+    oracle on the same bf16 input x; returns (n_active_gpu, n_flips, y_rel_err)."""
+    x = np.atleast_2d(x)
+    y_g, idx_g, s_g, coef_g = gpu_out
     idx_o, y_o, coef_o = run_oracle(variant, layer, x, thld)
     H = layer.h
     if variant == "dense":
