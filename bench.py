@@ -27,7 +27,8 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBS = 8000.0  # MI355X HBM3E peak, GB/s
-KERNEL_SRC = os.path.join(ROOT, "paper_2505_17701_amd", "csrc", "cd_kernels.hip")
+KERNEL_SRCS = [os.path.join(ROOT, "paper_2505_17701_amd", "csrc", f)
+               for f in ("cd_kernels.hip", "cd_device.hpp", "cd_internal.hpp")]
 TRAFFIC_SUMMARY = os.path.join(ROOT, "profiles", "k_coef_mono_llama7b_4096x11008_k0.9_traffic.md")
 
 
@@ -67,11 +68,24 @@ def parse():
     return p.parse_args()
 
 
+def kernel_source_digest():
+    """sha256 of the device sources with comments and whitespace removed: the
+    identity of the kernels a traffic measurement belongs to."""
+    import hashlib
+    import re
+
+    h = hashlib.sha256()
+    for path in KERNEL_SRCS:
+        src = open(path).read()
+        src = re.sub(r"/\*.*?\*/", " ", src, flags=re.S)
+        src = re.sub(r"//[^\n]*", " ", src)
+        h.update(" ".join(src.split()).encode())
+    return h.hexdigest()
+
+
 def measured_traffic():
     """HBM bytes per launch of the dominant kernel from the committed FETCH_SIZE /
     WRITE_SIZE summary, or None when the kernel source changed since it was taken."""
-    import hashlib
-
     if not os.path.exists(TRAFFIC_SUMMARY):
         return None
     fields = {}
@@ -79,8 +93,7 @@ def measured_traffic():
         if ":" in line and line.startswith("- "):
             k, v = line[2:].split(":", 1)
             fields[k.strip()] = v.strip().strip("`")
-    digest = hashlib.sha256(open(KERNEL_SRC, "rb").read()).hexdigest()
-    if fields.get("kernel_source_sha256") != digest:
+    if fields.get("kernel_source_digest") != kernel_source_digest():
         return None
     try:
         return float(fields["hbm_bytes_per_launch"])

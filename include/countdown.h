@@ -68,8 +68,9 @@ typedef struct cd_plan cd_plan;
 
 /*
  * Create a plan for one FFN shape. Allocates the plan's device workspace
- * (per-block active counts and (neuron, s) lists, the predictor latent and,
- * with CD_PLAN_KEEP_COEF, the dense coefficients) on the current device. d_model and d_ff must be positive multiples of 8 with
+ * (a per-neuron active flag, the coefficients s of the active neurons, the
+ * predictor latent and, with CD_PLAN_KEEP_COEF, the dense coefficients) on
+ * the current device. d_model and d_ff must be positive multiples of 8 with
  * d_model <= 8192; 1 <= max_batch <= 8; d_rank is 0 (no predictor) or a
  * power of two in [8, 1024]; max_batch * d_model <= 32768. Returns CD_EINVAL
  * for malformed sizes and CD_EUNSUPPORTED for well-formed sizes beyond those
@@ -83,7 +84,7 @@ cd_status countdown_plan_create(int d_model, int d_ff, int max_batch, int d_rank
 cd_status countdown_plan_destroy(cd_plan *plan);
 
 /*
- * M-CountDown (Eq. 6b; Sec. 4 "Constructing SP^Prac"): u = x.W_up over all
+ * M-CountDown (Eq. 6b; Sec. 4, layerwise threshold): u = x.W_up over all
  * rows; IDX = {i : exists b, |u_b[i]| > thld}; s_b[i] = u_b[i] SiLU(x_b.W_gate[i])
  * on IDX only (Eq. 2); y_b = sum_{i in IDX} s_b[i] W_down[i] (Eq. 5).
  * B in [1, max_batch]. W_gate, W_up, W_down: [d_ff][d_model] bf16.
@@ -155,8 +156,8 @@ cd_status countdown_calibrate(cd_plan *plan, int variant, const uint16_t *X, int
  * coef_dst fp32[B][d_ff] the dense coefficient vector of every neuron (u for
  * mono, s for dual ideal and dense, s_hat for dual pred; CD_PLAN_KEEP_COEF
  * plans only, else CD_EINVAL). B is the batch of that call. The hot path
- * keeps the active set as per-block lists; this call runs a small kernel
- * that scans them. CD_EINVAL before the plan's first FFN call and after
+ * keeps the active set as per-neuron flags; this call runs a small kernel
+ * that scans them in order. CD_EINVAL before the plan's first FFN call and after
  * countdown_calibrate (which reuses the workspace).
  */
 cd_status countdown_export_active(const cd_plan *plan, int32_t *idx_dst, int32_t *n_dst,

@@ -1,23 +1,27 @@
 // gfx950 kernels of the COUNTDOWN sparse Gated-MLP FFN (arXiv 2505.17701).
 //
-// One call (Sec. 3 Eq. 2-6, Sec. 4) runs two kernels:
-//   coefficient kernel: one wave per neuron. The wave streams the neuron's
-//     coefficient row(s) -- W_up for M-CountDown, W_gate and W_up for ideal
-//     D-CountDown, B_t for the predictor -- with non-temporal 16-byte loads
-//     (64 lanes x 16 B = one contiguous 1 KB segment per instruction), takes
-//     the dot products against x held in registers (LDS for batches > 2)
-//     with v_dot2_f32_bf16, reduces across the wave with DPP, and applies
-//     the strict threshold (union over the batch). An active neuron's wave
-//     immediately gathers the rows it still needs (W_gate for mono, W_gate
-//     and W_up for the predictor) and forms s = u * SiLU(g). Results land in
-//     per-neuron arrays act[d_ff] and s[B][d_ff]; there are no barriers
-//     between waves, so a neuron's gather overlaps the other waves' streams.
-//     The kernel also zeroes y for the next kernel.
+// One call (Sec. 3 Eq. 2-6, Sec. 4) runs two kernels (three with the predictor):
+//   coefficient kernel, M-CountDown and ideal D-CountDown: one wave per
+//     neuron. The wave streams the neuron's coefficient row(s) -- W_up, or
+//     W_gate and W_up -- with non-temporal 16-byte loads (64 lanes x 16 B =
+//     one contiguous 1 KB segment per instruction), takes the dot products
+//     against x (registers for batches of 1-2, an LDS copy for 4-8) with
+//     v_dot2_f32_bf16, reduces across the wave with DPP and applies the
+//     strict threshold (union over the batch). For M-CountDown an active
+//     neuron's wave immediately reads its W_gate row and forms s = u *
+//     SiLU(g). Results land in per-neuron arrays act[d_ff] and s[B][d_ff];
+//     there are no barriers between waves. The kernel also zeroes y.
+//   predictor (practical D-CountDown): the latent x . theta_A (one workgroup
+//     per A_t row), then a coefficient kernel over blocks of 32 neurons: B_t
+//     scores, signed threshold, and the block's active neurons dealt to its
+//     waves for the W_gate / W_up gather.
 //   down kernel: workgroup (c, g) owns a 512-column chunk c and a
 //     contiguous neuron range g. One round trip reads act and s of the
 //     range, a wave ballot compacts the active neurons in ascending order
 //     into LDS, each wave then keeps 8 W_down rows in flight, the four waves
 //     reduce in LDS and add the chunk to y with one fp32 atomic per column.
+// The residual stream of a layer stack (h += y, x = bf16(RMSNorm(h))) is a
+// small kernel of its own, or part of the latent kernel with the predictor.
 #include "cd_device.hpp"
 #include "cd_internal.hpp"
 
