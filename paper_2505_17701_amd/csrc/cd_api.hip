@@ -17,7 +17,6 @@ constexpr int kMaxDModel = 8192;
 constexpr int kMaxBatch = 8;
 constexpr int kMaxRank = 1024;
 constexpr int kMaxBatchCols = 32768;  // max_batch * d_model (batch tiles of 4 and 8 stage x in LDS)
-constexpr int kDownWaves = 2048;      // target waves of the down kernel grid
 
 bool aligned16(const void *p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
 
@@ -29,7 +28,6 @@ struct cd_plan {
     int d_model, d_ff, max_batch, d_rank;
     unsigned flags;
     int device;
-    int gc, gr, rows_per_group;   // down-kernel grid: column chunks x neuron groups
     int last_batch;               // of the last FFN call (0 before the first)
     int *act;                     // [d_ff] neuron in IDX
     float *s;                     // [max_batch][d_ff] coefficients s of active neurons
@@ -123,9 +121,7 @@ cdk::DownArgs down_args(cd_plan *p, int B, const uint16_t *Wd, float *y)
     a.Wd = Wd;
     a.d_model = p->d_model;
     a.d_ff = p->d_ff;
-    a.gc = p->gc;
-    a.gr = p->gr;
-    a.rows_per_group = p->rows_per_group;
+    a.gc = a.gr = a.rows_per_group = 0;  // chosen per batch tile by launch_down
     a.y = y;
     return a;
 }
@@ -316,16 +312,6 @@ cd_status countdown_plan_create(int d_model, int d_ff, int max_batch, int d_rank
     p->last_batch = 0;
     p->phases = CD_PHASE_ALL;
     p->has_state = false;
-    // down grid: one 512-column chunk per workgroup column and ~kDownWaves
-    // waves, with at least 16 neurons per group
-    p->gc = (d_model + 511) / 512;
-    int gr = kDownWaves / 4 / p->gc;
-    if (gr > d_ff / 16)
-        gr = d_ff / 16;
-    if (gr < 1)
-        gr = 1;
-    p->rows_per_group = (d_ff + gr - 1) / gr;
-    p->gr = (d_ff + p->rows_per_group - 1) / p->rows_per_group;
     const size_t mb = (size_t)max_batch;
     st = dalloc(&p->act, (size_t)d_ff);
     if (st == CD_OK) st = dalloc(&p->s, mb * d_ff);

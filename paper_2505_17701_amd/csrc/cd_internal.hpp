@@ -32,7 +32,7 @@ struct DownArgs {
     int nb;
     const uint16_t *Wd;  // [d_ff][d_model]
     int d_model, d_ff;
-    int gc, gr;          // column chunks x neuron groups (grid = gc * gr)
+    int gc, gr;          // column chunks x neuron ranges (set by launch_down)
     int rows_per_group;  // ceil(d_ff / gr)
     float *y;            // [nb][d_model], accumulated
 };

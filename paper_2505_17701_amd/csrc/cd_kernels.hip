@@ -367,29 +367,47 @@ __device__ __forceinline__ void pred_issue_bt(u32x4 (&wb)[PredShape<LCPR>::kLoad
     }
 }
 
-// s_hat_b = latent_b . B_t[row] for the wave's rows (latent from LDS), the
-// signed threshold with the union over the batch, act[] and (optionally) the
-// coefficients. Returns the wave-uniform mask of its active rows.
+// The latent entries a lane multiplies. Up to rank 512 a lane meets the same
+// 8 entries of each token in every one of its B_t loads, so they are loaded
+// once, from global memory, with the kernel's first loads; rank 1024 rows
+// read the LDS copy instead.
+template <int B, int LCPR>
+struct LatentRegs {
+    static constexpr bool kRegs = PredShape<LCPR>::kCpr <= kWave;
+    u32x4 v[kRegs ? B : 1][2];  // 8 fp32 per token as raw bits
+
+    __device__ __forceinline__ void issue(const float *lat, int nb, int d_rank, int lane)
+    {
+        if constexpr (kRegs) {
+            const int e = (lane & (PredShape<LCPR>::kCpr - 1)) * 8;
+#pragma unroll
+            for (int b = 0; b < B; ++b) {
+                const u32x4 *p = reinterpret_cast<const u32x4 *>(lat + (size_t)b * d_rank + e);
+                v[b][0] = *or_zero(b < nb, p);
+                v[b][1] = *or_zero(b < nb, p + 1);
+            }
+        }
+    }
+
+    __device__ __forceinline__ float get(int b, int q) const
+    {
+        return __uint_as_float(v[b][q / 4][q % 4]);
+    }
+};
+
+// s_hat_b = latent_b . B_t[row] for the wave's rows (latent from lr, or from
+// the LDS copy lat for rank 1024), the signed threshold with the union over
+// the batch, act[] and (optionally) the coefficients. Returns the
+// wave-uniform mask of its active rows.
 template <int B, int LCPR>
 __device__ __forceinline__ uint32_t pred_score(const u32x4 (&wb)[PredShape<LCPR>::kLoads],
-                                               const float *lat, const CoefArgs &a, int wr0,
-                                               int lane)
+                                               const LatentRegs<B, LCPR> &lr, const float *lat,
+                                               const CoefArgs &a, int wr0, int lane)
 {
     using S = PredShape<LCPR>;
-    // up to rank 512 a lane meets the same 8 latent entries in every load: read once
-    constexpr bool kLatOnce = S::kCpr <= kWave;
     const bool seg_end = (lane & (S::kSeg - 1)) == S::kSeg - 1;
     float acc[B];
     zero_acc(acc);
-    float lreg[kLatOnce ? B : 1][8];
-    if constexpr (kLatOnce) {
-        const int e = (lane & (S::kCpr - 1)) * 8;
-#pragma unroll
-        for (int b = 0; b < B; ++b)
-#pragma unroll
-            for (int q = 0; q < 8; ++q)
-                lreg[b][q] = b < a.nb ? lat[b * a.d_rank + e + q] : 0.0f;
-    }
     uint32_t wmask = 0;
 #pragma unroll
     for (int j = 0; j < S::kLoads; ++j) {
@@ -403,7 +421,9 @@ __device__ __forceinline__ uint32_t pred_score(const u32x4 (&wb)[PredShape<LCPR>
             if (b < a.nb) {
 #pragma unroll
                 for (int q = 0; q < 8; ++q)
-                    acc[b] = fmaf(wf[q], kLatOnce ? lreg[b][q] : lat[b * a.d_rank + e + q], acc[b]);
+                    acc[b] = fmaf(wf[q],
+                                  LatentRegs<B, LCPR>::kRegs ? lr.get(b, q) : lat[b * a.d_rank + e + q],
+                                  acc[b]);
             }
         }
         if ((j + 1) % S::kJpr != 0)
@@ -489,20 +509,26 @@ __global__ __launch_bounds__(kBlock) void k_coef_pred(const CoefArgs a)
     const int r0 = blockIdx.x * kPredRows;
     const int wr0 = r0 + wave * kPredRowsPerWave;
 
+    using LR = LatentRegs<B, LCPR>;
     u32x4 wb[S::kLoads];
     pred_issue_bt<LCPR>(wb, a, wr0, lane);
     Tokens<B, NK, XREG> tok;
     tok.issue(a.x, a.nb, a.d_model, lane);
-    LatentStage<B> ls;
-    ls.issue(a.lat, a.nb, a.d_rank);
+    LR lr;
+    lr.issue(a.lat, a.nb, a.d_rank, lane);
+    LatentStage<LR::kRegs ? 1 : B> ls;  // the LDS copy, rank 1024 only
+    if constexpr (!LR::kRegs)
+        ls.issue(a.lat, a.nb, a.d_rank);
     zero_y(a.y, a.nb * a.d_model);
     tok.write(xs);
     uint32_t *latw = xs + (XREG ? 0 : B * NK * kColsPerLoad / 2);
-    ls.write(reinterpret_cast<u32x4 *>(latw), a.lat, a.nb, a.d_rank);
-    __syncthreads();
+    if constexpr (!LR::kRegs)
+        ls.write(reinterpret_cast<u32x4 *>(latw), a.lat, a.nb, a.d_rank);
+    if constexpr (!XREG || !LR::kRegs)
+        __syncthreads();
 
-    const uint32_t wmask = pred_score<B, LCPR>(wb, reinterpret_cast<const float *>(latw), a, wr0,
-                                               lane);
+    const uint32_t wmask = pred_score<B, LCPR>(wb, lr, reinterpret_cast<const float *>(latw), a,
+                                               wr0, lane);
     if (lane == 0)
         wflag[wave] = wmask;
     __syncthreads();
@@ -548,6 +574,193 @@ __global__ __launch_bounds__(kBlock) void k_coef_pred(const CoefArgs a)
             load_row<NK>(ga, a.Wg + (size_t)(r0 + ra) * a.d_model, a.d_model, lane);
             load_row<NK>(ua, a.Wu + (size_t)(r0 + ra) * a.d_model, a.d_model, lane);
         }
+    }
+}
+
+// ------------------------------------------- MFMA gather for batches of 4-8
+// For 4-8 tokens the gathered products are small dense contractions: a tile
+// of 16 active neurons times the batch, on v_mfma_f32_16x16x32_bf16. Lane
+// l = i + 16 g (i = l % 16, g = l / 16) supplies row i of the tile (A operand)
+// and token i of the batch (B operand, zero for i >= B), each with the 8
+// columns 32 s + 8 g + [0, 8) of step s, so both operands use the same
+// column order. The four waves take a quarter of the steps each and add
+// their 16 x 16 partial sums in LDS; lane l holds D[4 (l / 16) + r][l % 16].
+
+typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
+typedef float f32x4_t __attribute__((ext_vector_type(4)));
+
+constexpr int kTile = 16;
+constexpr int kMfmaSteps = 8;  // 32-column steps per load batch (16 loads of 16 B per lane)
+
+__device__ __forceinline__ f32x4_t mfma16(const u32x4 &a, const u32x4 &b, f32x4_t c)
+{
+    return __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, a),
+                                                    __builtin_bit_cast(bf16x8_t, b), c, 0, 0, 0);
+}
+
+// LDS token rows for the MFMA kernel: a 16-byte pad per row keeps the 16
+// tokens of one step on distinct banks; one zero chunk serves tokens >= B.
+template <int NK>
+struct MfmaTokLayout {
+    static constexpr int kCols = NK * kColsPerLoad;
+    static constexpr int kStride = kCols / 2 + 4;  // u32 per token row
+};
+
+template <int B, int NK>
+__host__ __device__ constexpr size_t mfma_lds_tokens_u32()
+{
+    return (size_t)B * MfmaTokLayout<NK>::kStride + 4;
+}
+
+// one batch of kMfmaSteps steps of the tile's W_gate and W_up rows
+template <int NK>
+__device__ __forceinline__ void mfma_load(u32x4 (&ga)[kMfmaSteps], u32x4 (&ua)[kMfmaSteps],
+                                          const uint16_t *wg_row, const uint16_t *wu_row,
+                                          bool have, int s, int s1, int g, int d_model)
+{
+#pragma unroll
+    for (int q = 0; q < kMfmaSteps; ++q) {
+        const int col = (s + q) * 32 + g * 8;
+        ga[q] = zero16();
+        ua[q] = zero16();
+        if (have && s + q < s1 && col < d_model) {
+            ga[q] = load16_stream(wg_row + col);
+            ua[q] = load16_stream(wu_row + col);
+        }
+    }
+}
+
+__device__ __forceinline__ void mfma_consume(const u32x4 (&ga)[kMfmaSteps],
+                                             const u32x4 (&ua)[kMfmaSteps], const uint32_t *xrow,
+                                             bool xreal, int s, int s1, int g, f32x4_t &dg,
+                                             f32x4_t &du)
+{
+#pragma unroll
+    for (int q = 0; q < kMfmaSteps; ++q) {
+        if (s + q < s1) {  // uniform
+            const u32x4 xv =
+                *reinterpret_cast<const u32x4 *>(xrow + (xreal ? ((s + q) * 32 + g * 8) / 2 : 0));
+            dg = mfma16(ga[q], xv, dg);
+            du = mfma16(ua[q], xv, du);
+        }
+    }
+}
+
+// Practical D-CountDown coefficient kernel for batches of 4-8 (Sec. 4): the
+// scoring of k_coef_pred, then the block's active neurons in tiles of 16 on MFMA.
+template <int B, int NK, int LCPR>
+__global__ __launch_bounds__(kBlock) void k_coef_pred_mfma(const CoefArgs a)
+{
+    // LDS: tokens [B][kStride] (+ zero chunk), then the latent [B][d_rank] fp32,
+    // whose space later holds the partial sums [4 waves][2][16 x 16] fp32
+    extern __shared__ __align__(16) uint32_t xs[];
+    __shared__ uint32_t wflag[kWavesPerBlock];
+    __shared__ int lrow[kPredRows];
+    using S = PredShape<LCPR>;
+    using TL = MfmaTokLayout<NK>;
+    constexpr int kChunksPerTok = TL::kCols / 8;
+    constexpr int kTotal = B * kChunksPerTok;
+    constexpr int kIter = (kTotal + kBlock - 1) / kBlock;
+    const int lane = threadIdx.x % kWave, wave = threadIdx.x / kWave;
+    const int r0 = blockIdx.x * kPredRows;
+    const int wr0 = r0 + wave * kPredRowsPerWave;
+
+    using LR = LatentRegs<B, LCPR>;
+    u32x4 wb[S::kLoads];
+    pred_issue_bt<LCPR>(wb, a, wr0, lane);
+    u32x4 stage[kIter];
+#pragma unroll
+    for (int t = 0; t < kIter; ++t) {
+        const int c = threadIdx.x + t * kBlock;
+        const int b = c / kChunksPerTok, col = (c % kChunksPerTok) * 8;
+        stage[t] = load16(or_zero(c < kTotal && b < a.nb && col < a.d_model,
+                                  a.x + (size_t)b * a.d_model + col));
+    }
+    LR lr;
+    lr.issue(a.lat, a.nb, a.d_rank, lane);
+    LatentStage<LR::kRegs ? 1 : B> ls;  // the LDS copy, rank 1024 only
+    if constexpr (!LR::kRegs)
+        ls.issue(a.lat, a.nb, a.d_rank);
+    __builtin_amdgcn_sched_barrier(0);
+    zero_y(a.y, a.nb * a.d_model);
+#pragma unroll
+    for (int t = 0; t < kIter; ++t) {
+        const int c = threadIdx.x + t * kBlock;
+        if (c < kTotal)
+            *reinterpret_cast<u32x4 *>(xs + (size_t)(c / kChunksPerTok) * TL::kStride +
+                                       (c % kChunksPerTok) * 4) = stage[t];
+    }
+    uint32_t *zchunk = xs + (size_t)B * TL::kStride;
+    if (threadIdx.x == 0)
+        *reinterpret_cast<u32x4 *>(zchunk) = zero16();
+    uint32_t *latw = xs + mfma_lds_tokens_u32<B, NK>();
+    if constexpr (!LR::kRegs)
+        ls.write(reinterpret_cast<u32x4 *>(latw), a.lat, a.nb, a.d_rank);
+    __syncthreads();
+
+    const uint32_t wmask = pred_score<B, LCPR>(wb, lr, reinterpret_cast<const float *>(latw), a,
+                                               wr0, lane);
+    if (lane == 0)
+        wflag[wave] = wmask;
+    __syncthreads();
+    uint32_t M = 0;
+#pragma unroll
+    for (int v = 0; v < kWavesPerBlock; ++v)
+        M |= wflag[v] << (v * kPredRowsPerWave);
+    const int n = __builtin_popcount(M);
+    if (threadIdx.x < kPredRows && ((M >> threadIdx.x) & 1u))
+        lrow[__builtin_popcount(M & ((1u << threadIdx.x) - 1u))] = r0 + threadIdx.x;
+    __syncthreads();  // lrow visible; the latent is no longer read
+
+    // tiles of 16 active neurons: one tile takes the four waves, two tiles a pair each;
+    // the waves of a tile split its 32-column steps into contiguous ranges
+    const int ntiles = (n + kTile - 1) / kTile;  // 0, 1 or 2
+    if (ntiles == 0)
+        return;
+    float *part = reinterpret_cast<float *>(latw);  // [4 waves][2][16 x 16]
+    const int wpt = kWavesPerBlock / ntiles;
+    const int t0 = (wave / wpt) * kTile, kw = wave % wpt;
+    const int i = lane % kTile, g = lane / kTile;
+    const int steps = (a.d_model + 31) / 32;
+    const int sw = (steps + wpt - 1) / wpt;
+    const int s0 = min(steps, kw * sw), s1 = min(steps, s0 + sw);
+    const bool xreal = i < a.nb;
+    const uint32_t *xrow = xreal ? xs + (size_t)i * TL::kStride : zchunk;
+    const bool have = t0 + i < n;
+    const int row = have ? lrow[t0 + i] : r0;
+    const uint16_t *wg_row = a.Wg + (size_t)row * a.d_model;
+    const uint16_t *wu_row = a.Wu + (size_t)row * a.d_model;
+    f32x4_t dg = {0.0f, 0.0f, 0.0f, 0.0f}, du = {0.0f, 0.0f, 0.0f, 0.0f};
+    u32x4 ga[kMfmaSteps], ua[kMfmaSteps], gb[kMfmaSteps], ub[kMfmaSteps];
+    mfma_load<NK>(ga, ua, wg_row, wu_row, have, s0, s1, g, a.d_model);
+    for (int s = s0; s < s1; s += 2 * kMfmaSteps) {
+        const int sb = s + kMfmaSteps;
+        if (sb < s1)
+            mfma_load<NK>(gb, ub, wg_row, wu_row, have, sb, s1, g, a.d_model);
+        mfma_consume(ga, ua, xrow, xreal, s, s1, g, dg, du);
+        if (sb >= s1)
+            break;
+        if (sb + kMfmaSteps < s1)
+            mfma_load<NK>(ga, ua, wg_row, wu_row, have, sb + kMfmaSteps, s1, g, a.d_model);
+        mfma_consume(gb, ub, xrow, xreal, sb, s1, g, dg, du);
+    }
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+        const int e = (4 * g + r) * kTile + i;  // D[4g + r][i]
+        part[(wave * 2 + 0) * 256 + e] = dg[r];
+        part[(wave * 2 + 1) * 256 + e] = du[r];
+    }
+    __syncthreads();
+    const int ti = threadIdx.x / kTile, tj = threadIdx.x % kTile;  // D[ti][tj] of each tile
+    for (int tile = 0; tile < ntiles; ++tile) {
+        float gs = 0.0f, us = 0.0f;
+        for (int v = tile * wpt; v < (tile + 1) * wpt; ++v) {
+            gs += part[(v * 2 + 0) * 256 + threadIdx.x];
+            us += part[(v * 2 + 1) * 256 + threadIdx.x];
+        }
+        const int rank = tile * kTile + ti;
+        if (rank < n && tj < a.nb)
+            a.s[(size_t)tj * a.d_ff + lrow[rank]] = us * silu(gs);
     }
 }
 
@@ -747,7 +960,12 @@ __global__ __launch_bounds__(kBlock) void k_latent_norm(const NormArgs n,
     }
 }
 
-// Gathered down projection (Eq. 5), see the file comment.
+// Gathered down projection (Eq. 5). Workgroup (c, g) owns a 512-column chunk
+// c and a contiguous neuron range g: one round trip reads act and s of the
+// range, a wave ballot compacts the active neurons in ascending order into
+// LDS, each wave then keeps U rows in flight (1 KB of a row per load), the
+// four waves reduce in LDS and add the chunk to y with one fp32 atomic per
+// column and token.
 template <int B>
 __global__ __launch_bounds__(kBlock) void k_down(const DownArgs a)
 {
@@ -1009,13 +1227,43 @@ size_t down_lds_bytes(int rows_per_group, int bt)
     return (size_t)rows_per_group * 4 * (1 + bt) + (size_t)kWavesPerBlock * kColsPerLoad * 4;
 }
 
+// Down-kernel grid: 512-column chunks x 64 neuron ranges of at least 16
+// neurons (measured best at 4096 x 11008, 4096 x 14336 and 8192 x 28672 among
+// 16-128 ranges and 128-512-column chunks), more ranges when a range's lists
+// would not fit in 64 KB of LDS.
+void down_grid(int d_model, int d_ff, int bt, int *gc, int *gr, int *rows_per_group)
+{
+    *gc = (d_model + kColsPerLoad - 1) / kColsPerLoad;
+    int r = 64;
+    if (r > d_ff / 16)
+        r = d_ff / 16;
+    if (r < 1)
+        r = 1;
+    const int max_rows = (int)((65536 - down_lds_bytes(0, bt)) / (4 * (1 + bt)));
+    if ((d_ff + r - 1) / r > max_rows)
+        r = (d_ff + max_rows - 1) / max_rows;
+    *rows_per_group = (d_ff + r - 1) / r;
+    *gr = (d_ff + *rows_per_group - 1) / *rows_per_group;
+}
+
 template <int B, int NK, bool XREG, int LCPR>
 static void coef_pred_lcpr(const CoefArgs &a, hipStream_t s)
 {
-    const size_t lds = (XREG ? 0 : (size_t)B * NK * kColsPerLoad * 2) + (size_t)B * a.d_rank * 4;
     const int grid = (a.d_ff + kPredRows - 1) / kPredRows;
-    allow_lds(k_coef_pred<B, NK, XREG, LCPR>, lds);
-    k_coef_pred<B, NK, XREG, LCPR><<<grid, kBlock, lds, s>>>(a);
+    const size_t lat_lds = LatentRegs<B, LCPR>::kRegs ? 0 : (size_t)B * a.d_rank * 4;
+    // MFMA tiles pay off at 8 tokens; at 4, a block's ~11 active neurons leave a
+    // 16-row tile a third empty and the per-wave v_dot2 gather is faster (measured)
+    if constexpr (B >= 8) {
+        // tokens (padded rows + zero chunk), then max(latent, 4 x 2 x 16 x 16 partial sums)
+        const size_t lds = mfma_lds_tokens_u32<B, NK>() * 4 +
+                           max(lat_lds, (size_t)kWavesPerBlock * 2 * 256 * 4);
+        allow_lds(k_coef_pred_mfma<B, NK, LCPR>, lds);
+        k_coef_pred_mfma<B, NK, LCPR><<<grid, kBlock, lds, s>>>(a);
+    } else {
+        const size_t lds = (XREG ? 0 : (size_t)B * NK * kColsPerLoad * 2) + lat_lds;
+        allow_lds(k_coef_pred<B, NK, XREG, LCPR>, lds);
+        k_coef_pred<B, NK, XREG, LCPR><<<grid, kBlock, lds, s>>>(a);
+    }
 }
 
 // the predictor kernel is specialised on log2 of the B_t row length in 16-byte chunks
@@ -1162,9 +1410,11 @@ hipError_t launch_latent_norm(const NormArgs &n, const uint16_t *At, int d_rank,
     return norm_dispatch(n, At, d_rank, lat, s);
 }
 
-hipError_t launch_down(const DownArgs &a, hipStream_t s)
+hipError_t launch_down(const DownArgs &args, hipStream_t s)
 {
-    const int bt = batch_tile(a.nb);
+    const int bt = batch_tile(args.nb);
+    DownArgs a = args;
+    down_grid(a.d_model, a.d_ff, bt, &a.gc, &a.gr, &a.rows_per_group);
     const size_t lds = down_lds_bytes(a.rows_per_group, bt);
     const int grid = a.gc * a.gr;
     switch (bt) {
