@@ -17,7 +17,9 @@
  *   Sec. 4 "Constructing SP^Prac": layerwise constant threshold
  *     tau_hat = (1/T) sum_t Quantile(k, |u^(t)|) and the low-rank predictor
  *     s_hat = x.theta_A.theta_B with predicted set {i : s_hat[i] > tau};
- *   Limitations section: batch > 1 takes the union of the index sets.
+ *   Limitations section: batch > 1 takes the union of the index sets;
+ *   the per-token form of Eq. (6): each token's threshold is the quantile of
+ *   its own coefficients (cdo_ffn_topk).
  *
  * Inputs are the exact bf16 values the GPU consumes (uint16 bit patterns),
  * widened exactly to double; thresholds arrive as the fp32 value the GPU
@@ -449,6 +451,58 @@ double cdo_calibrate(int kind, const uint16_t *X, int T, const uint16_t *W_gate,
     }
     free(c);
     return sum / (double)T;
+}
+
+/* Per-token threshold: Eq. (6) with each token's threshold taken as the
+ * quantile of its own coefficient vector (the ideal, per-token form of the
+ * sparsity definition, Sec. 3; Sec. 4 replaces it by the calibrated mean):
+ *   thld_b = Quantile(k, c_b),  IDX = {i : exists b, c_b[i] > thld_b},
+ * c_b the variant's coefficient vector of token b (kind as in cdo_calibrate:
+ * |u|, |s|, signed s_hat or |h|), union over the batch; y by Eq. (5) over IDX
+ * with the dense-equivalent s. q_out (optional) receives the B thresholds.
+ * Returns |IDX| or a negative status. */
+int64_t cdo_ffn_topk(int kind, const uint16_t *x, int B, const uint16_t *W_gate,
+                     const uint16_t *W_up, const uint16_t *W_down, const uint16_t *A_t,
+                     const uint16_t *B_t, int d_model, int d_rank, int d_ff, double k,
+                     int32_t *idx, double *y, double *q_out)
+{
+    if (!x || !W_gate || !W_up || !W_down || !idx || !y || B < 1 || d_model < 1 || d_ff < 1 ||
+        !(k >= 0.0 && k <= 1.0))
+        return CDO_EINVAL;
+    double *c = (double *)malloc(sizeof(double) * (size_t)B * (size_t)d_ff);
+    double *q = (double *)malloc(sizeof(double) * (size_t)B);
+    if (!c || !q) {
+        free(c);
+        free(q);
+        return CDO_ENOMEM;
+    }
+    for (int b = 0; b < B; b++) {
+        double *cb = c + (int64_t)b * d_ff;
+        int rc = token_coef(kind, x + (int64_t)b * d_model, W_gate, W_up, A_t, B_t, d_model,
+                            d_rank, d_ff, cb);
+        if (rc < 0) {
+            free(c);
+            free(q);
+            return rc;
+        }
+        q[b] = cdo_quantile_linear(k, cb, d_ff);
+    }
+    int64_t n = 0;
+    for (int64_t i = 0; i < d_ff; i++) {
+        int keep = 0;
+        for (int b = 0; b < B; b++)
+            if (c[(int64_t)b * d_ff + i] > q[b])
+                keep = 1;
+        if (keep)
+            idx[n++] = (int32_t)i;
+    }
+    free(c);
+    int rc = cdo_ffn_on_idx(x, B, W_gate, W_up, W_down, d_model, d_ff, idx, n, y, NULL);
+    if (rc >= 0 && q_out)
+        for (int b = 0; b < B; b++)
+            q_out[b] = q[b];
+    free(q);
+    return rc < 0 ? rc : n;
 }
 
 /* Residual + RMSNorm between stacked layers (not part of the paper; used by the

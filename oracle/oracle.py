@@ -25,7 +25,7 @@ _lib = None
 __all__ = [
     "build", "load", "num_threads", "silu", "coefficients", "predictor", "select", "combine",
     "dense", "ffn_on_idx", "ffn_mono", "ffn_dual_ideal", "ffn_dual_pred", "quantile_linear",
-    "calibrate", "residual_rmsnorm", "KIND",
+    "calibrate", "ffn_topk", "residual_rmsnorm", "KIND",
 ]
 
 
@@ -80,6 +80,9 @@ def load():
         lib.cdo_calibrate.restype = C.c_double
         lib.cdo_calibrate.argtypes = [C.c_int, u16p, C.c_int, vp, vp, vp, vp, C.c_int, C.c_int,
                                       C.c_int, C.c_double, vp]
+        lib.cdo_ffn_topk.restype = C.c_int64
+        lib.cdo_ffn_topk.argtypes = [C.c_int, u16p, C.c_int, u16p, u16p, u16p, vp, vp, C.c_int,
+                                     C.c_int, C.c_int, C.c_double, i32p, f64p, f64p]
         lib.cdo_residual_rmsnorm.restype = C.c_int
         lib.cdo_residual_rmsnorm.argtypes = [f64p, vp, C.c_int, C.c_double, f64p]
         _lib = lib
@@ -240,6 +243,23 @@ def calibrate(variant: str, X, k: float, W_gate=None, W_up=None, A_t=None, B_t=N
     if np.isnan(t):
         raise ValueError("oracle calibrate failed")
     return t, q
+
+
+def ffn_topk(variant: str, x, W_gate, W_up, W_down, k: float, A_t=None, B_t=None):
+    """Per-token threshold (Eq. 6 with thld_b = Quantile(k, c_b) of each token's own
+    coefficients, union over the batch): returns ``(IDX, y, per-token thresholds)``."""
+    x = _tok(x)
+    B, dm = x.shape
+    dff = W_up.shape[0]
+    dr = 0 if A_t is None else A_t.shape[0]
+    idx = np.empty(dff, dtype=np.int32)
+    y = np.empty((B, dm))
+    q = np.empty(B)
+    n = _check(load().cdo_ffn_topk(KIND[variant], x, B, _u16(W_gate), _u16(W_up), _u16(W_down),
+                                   _ptr(None if A_t is None else _u16(A_t)),
+                                   _ptr(None if B_t is None else _u16(B_t)), dm, dr, dff,
+                                   float(k), idx, y, q), "ffn_topk")
+    return idx[:n].copy(), y, q
 
 
 def residual_rmsnorm(h, y, eps: float = 1e-5):

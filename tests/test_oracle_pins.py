@@ -398,3 +398,94 @@ def test_bad_arguments_are_rejected():
         oracle.combine(np.zeros((1, 40)), L["W_down"], np.array([40], dtype=np.int32))
     with pytest.raises(TypeError):
         oracle.dense(x.astype(np.int16), L["W_gate"], L["W_up"], L["W_down"])
+
+
+# ------------------------------------------- per-token threshold (Eq. 6, per token)
+
+def _brute_cs(x, L, mode, A_t=None, B_t=None):
+    """Coefficient vectors c_b and s_b by pure-Python loops (Sec. 3, Sec. 4)."""
+    X, G, U = (f64(a).tolist() for a in (x, L["W_gate"], L["W_up"]))
+
+    def dot(a, b):
+        t = 0.0
+        for p, q in zip(a, b):
+            t += p * q
+        return t
+
+    def silu(z):
+        return z / (1.0 + math.exp(-z)) if z >= 0 else z * math.exp(z) / (1.0 + math.exp(z))
+
+    B, dff = len(X), len(U)
+    u = [[dot(X[b], U[i]) for i in range(dff)] for b in range(B)]
+    s = [[u[b][i] * silu(dot(X[b], G[i])) for i in range(dff)] for b in range(B)]
+    if mode == "mono":
+        c = [[abs(v) for v in row] for row in u]
+    elif mode == "dual_ideal":
+        c = [[abs(v) for v in row] for row in s]
+    else:
+        A, Bm = f64(A_t).tolist(), f64(B_t).tolist()
+        lat = [[dot(X[b], A[r]) for r in range(len(A))] for b in range(B)]
+        c = [[dot(lat[b], Bm[i]) for i in range(dff)] for b in range(B)]
+    return c, s
+
+
+def _brute_quantile(v, k):
+    w = sorted(v)
+    h = k * (len(w) - 1)
+    lo = math.floor(h)
+    hi = min(lo + 1, len(w) - 1)
+    return w[lo] + (h - lo) * (w[hi] - w[lo])
+
+
+@pytest.mark.parametrize("mode", ["mono", "dual_ideal", "dual_pred"])
+@pytest.mark.parametrize("B,k", [(1, 0.75), (3, 0.5), (2, 0.9)])
+def test_topk_matches_brute_force(mode, B, k):
+    dm, dff, dr = 8, 16, 4
+    L = make_layer(960, dm, dff, 0.5)
+    P = make_predictor(960, dm, dr, dff, 0.5)
+    x = make_tokens(960, B, dm)
+    c, s = _brute_cs(x, L, mode, P["A_t"], P["B_t"])
+    q = [_brute_quantile(c[b], k) for b in range(B)]
+    idx_b = [i for i in range(dff) if any(c[b][i] > q[b] for b in range(B))]
+    D = f64(L["W_down"]).tolist()
+    y_b = [[sum(s[b][i] * D[i][j] for i in idx_b) for j in range(dm)] for b in range(B)]
+    pred = mode == "dual_pred"
+    idx, y, qo = oracle.ffn_topk(mode, x, L["W_gate"], L["W_up"], L["W_down"], k,
+                                 A_t=P["A_t"] if pred else None, B_t=P["B_t"] if pred else None)
+    np.testing.assert_array_equal(idx, idx_b)
+    np.testing.assert_allclose(qo, q, rtol=1e-13, atol=0)
+    np.testing.assert_allclose(y, np.array(y_b), rtol=1e-12, atol=1e-13)
+
+
+@pytest.mark.parametrize("mode", ["mono", "dual_ideal"])
+def test_topk_count_law_and_constant_threshold_equivalence(mode):
+    """Batch 1: |IDX| = n - 1 - floor(k (n - 1)) for distinct coefficients, and the
+    result equals the constant-threshold path run at that token's quantile."""
+    w = WORKLOADS["tiny_256x688"]
+    L = w.layer()
+    x = w.tokens(1)
+    k = 0.9
+    idx, y, q = oracle.ffn_topk(mode, x, L["W_gate"], L["W_up"], L["W_down"], k)
+    n = w.d_ff
+    assert len(idx) == n - 1 - math.floor(k * (n - 1))
+    fn = oracle.ffn_mono if mode == "mono" else oracle.ffn_dual_ideal
+    idx_c, y_c, _ = fn(x, L["W_gate"], L["W_up"], L["W_down"], q[0])
+    np.testing.assert_array_equal(idx, idx_c)
+    np.testing.assert_array_equal(y, y_c)
+
+
+def test_topk_identical_tokens_and_extremes():
+    w = WORKLOADS["tiny_256x688"]
+    L = w.layer()
+    x = w.tokens(1)
+    idx1, y1, q1 = oracle.ffn_topk("mono", x, L["W_gate"], L["W_up"], L["W_down"], 0.8)
+    idx3, y3, q3 = oracle.ffn_topk("mono", np.repeat(x, 3, axis=0), L["W_gate"], L["W_up"],
+                                   L["W_down"], 0.8)
+    np.testing.assert_array_equal(idx1, idx3)
+    np.testing.assert_array_equal(q3, np.repeat(q1, 3))
+    for b in range(3):
+        np.testing.assert_array_equal(y3[b], y1[0])
+    idx, y, _ = oracle.ffn_topk("mono", x, L["W_gate"], L["W_up"], L["W_down"], 1.0)
+    assert len(idx) == 0 and not y.any()          # nothing exceeds the maximum
+    idx, _, _ = oracle.ffn_topk("mono", x, L["W_gate"], L["W_up"], L["W_down"], 0.0)
+    assert len(idx) == w.d_ff - 1                 # everything but the minimum
