@@ -49,7 +49,8 @@ def parse():
     p.add_argument("--warmup", type=int, default=200)
     p.add_argument("--workload", default="llama7b_4096x11008")
     p.add_argument("--variant", default="mono",
-                   choices=["mono", "dual_ideal", "dual_pred", "dense"])
+                   choices=["mono", "dual_ideal", "dual_pred", "dense", "mono_topk",
+                            "dual_ideal_topk", "dual_pred_topk"])
     p.add_argument("--batch", type=int, default=1, help="decode tokens per call (union IDX)")
     p.add_argument("--k", type=float, default=0.9)
     p.add_argument("--copies", type=int, default=4, help="independent weight copies rotated")
@@ -212,10 +213,19 @@ class Context:
         ntok = self.X_eval.shape[0] - B + 1
         X, layers, copies = self.X_eval, self.layers, self.copies
 
+        topk = variant.endswith("_topk")
+        base = variant[:-5] if topk else variant
+        vid = {"mono": cd.CD_VARIANT_MONO, "dual_ideal": cd.CD_VARIANT_DUAL_IDEAL,
+               "dual_pred": cd.CD_VARIANT_DUAL_PRED}.get(base)
+
         def step(i):
             L = layers[i % copies]
             x = X[i % ntok: i % ntok + B]
-            if variant == "mono":
+            if topk:  # per-token threshold: the k-quantile of each token's own coefficients
+                cd.countdown_ffn_topk(plan, vid, x, L["W_gate"], L["W_up"], L["W_down"], k,
+                                      A_t=L.get("A_t") if base == "dual_pred" else None,
+                                      B_t=L.get("B_t") if base == "dual_pred" else None, y=y)
+            elif variant == "mono":
                 cd.countdown_ffn_mono(plan, x, L["W_gate"], L["W_up"], L["W_down"], th, y=y)
             elif variant == "dual_ideal":
                 cd.countdown_ffn_dual(plan, x, L["W_gate"], L["W_up"], L["W_down"], th, y=y)
@@ -235,8 +245,9 @@ class Context:
         dm, dff, dr = self.dm, self.dff, self.dr
         stream = torch.cuda.current_stream()
         y = torch.empty((B, dm), dtype=torch.float32, device="cuda")
+        base = variant[:-5] if variant.endswith("_topk") else variant
         plan = cd.Plan(dm, dff, max_batch=max(B, self.max_batch),
-                       d_rank=dr if variant == "dual_pred" else 0)
+                       d_rank=dr if base == "dual_pred" else 0)
         step = self.make_step(plan, variant, k, B, y)
         ms_eager = time_steps(step, steps, warmup, stream)
         ms = time_steps_graph(step, steps, warmup)
@@ -261,14 +272,14 @@ class Context:
         torch.cuda.synchronize()
         plan.close()
         n = n_arr.cpu().numpy().astype(np.float64)
-        dr_v = dr if variant == "dual_pred" else 0
-        per = [traffic.algorithmic_bytes(variant, dm, dff, int(v), B=B, d_rank=dr_v) for v in n]
+        dr_v = dr if base == "dual_pred" else 0
+        per = [traffic.algorithmic_bytes(base, dm, dff, int(v), B=B, d_rank=dr_v) for v in n]
         res = {"batch": B, "ms_per_step": ms, "us_per_layer": ms * 1e3,
                "tokens_per_s": B * 1e3 / ms, "us_per_layer_eager": ms_eager * 1e3,
                "n_active_mean": float(n.mean()), "realised_sparsity": float(1 - n.mean() / dff)}
         # the coefficient loop includes the predictor's latent kernel (one launch each)
         coef_b = float(np.mean([p["coef"] + p.get("latent", 0) for p in per]))
-        down_b = traffic.algorithmic_bytes(variant, dm, dff, int(n_down.item()), B=B,
+        down_b = traffic.algorithmic_bytes(base, dm, dff, int(n_down.item()), B=B,
                                            d_rank=dr_v)["down"]
         for name, kms, kb in (("coef", ms_coef, coef_b), ("down", ms_down, down_b)):
             res[f"{name}_kernel_us"] = kms * 1e3
@@ -296,6 +307,9 @@ def other_workloads(args):
         r = ctx.measure("dual_pred", 0.9, B, max(200, args.steps // 4), 50)
         r8[f"B={B}"] = brief(r)
         log(f"[bench] {w.name} dual_pred B={B}: {json.dumps(r8[f'B={B}'])}")
+    r = ctx.measure("dual_pred_topk", 0.9, 1, max(200, args.steps // 4), 50)
+    r8["per-token k=0.9 B=1"] = brief(r)
+    log(f"[bench] {w.name} dual_pred per-token B=1: {json.dumps(r8['per-token k=0.9 B=1'])}")
     r = ctx.measure("dense", None, 1, max(200, args.steps // 4), 50)
     r8["dense B=1"] = brief(r)
     dense_b = traffic.algorithmic_bytes("dense", w.d_model, w.d_ff, w.d_ff)["total"]
@@ -469,7 +483,8 @@ def main():
 
     extra = {}
     if not args.no_extra and "mono" in w.variants:
-        for variant, k in (("dense", None), ("dual_ideal", 0.9), ("mono", 0.7), ("mono", 0.5)):
+        for variant, k in (("dense", None), ("dual_ideal", 0.9), ("mono", 0.7), ("mono", 0.5),
+                           ("mono_topk", 0.9), ("dual_ideal_topk", 0.9)):
             if variant == args.variant and k == args.k:
                 continue
             r = main_ctx.measure(variant, k, 1, max(200, args.steps // 4), 50)
@@ -503,6 +518,10 @@ def main():
                "dual_pred": lambda x: oracle.ffn_dual_pred(x, H["W_gate"], H["W_up"], H["W_down"],
                                                            H.get("A_t"), H.get("B_t"), th),
                "dense": lambda x: oracle.dense(x, H["W_gate"], H["W_up"], H["W_down"])}
+        for base in ("mono", "dual_ideal", "dual_pred"):
+            fns[base + "_topk"] = (lambda b: lambda x: oracle.ffn_topk(
+                b, x, H["W_gate"], H["W_up"], H["W_down"], args.k, A_t=H.get("A_t"),
+                B_t=H.get("B_t")))(base)
         fn = fns[args.variant]
         n_done, t0 = 0, time.perf_counter()
         nt = len(X_eval_h) - args.batch + 1
@@ -524,7 +543,12 @@ def main():
                 "dual_ideal": "k_coef_dual (dense W_gate + W_up GEMV, s, threshold)",
                 "dual_pred": "k_latent + k_coef_pred (predictor scores, threshold, block-local "
                              "W_gate / W_up gather, s)",
-                "dense": "k_coef_dual (dense W_gate + W_up GEMV, s)"}[args.variant]
+                "dense": "k_coef_dual (dense W_gate + W_up GEMV, s)",
+                "mono_topk": "k_coef_mono + k_topk_select + k_gather_topk (per-token threshold)",
+                "dual_ideal_topk": "k_coef_dual + k_topk_select + k_gather_topk (per-token "
+                                   "threshold)",
+                "dual_pred_topk": "k_latent + k_coef_pred + k_topk_select + k_gather_topk "
+                                  "(per-token threshold)"}[args.variant]
         roof = {"bound": "hbm", "kernel": desc,
                 "achieved": main_res[f"{dom}_kernel_GBs"], "peak": HBM_PEAK_GBS, "unit": "GB/s",
                 "frac": main_res[f"{dom}_kernel_GBs"] / HBM_PEAK_GBS,

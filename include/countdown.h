@@ -112,6 +112,27 @@ cd_status countdown_ffn_dense(cd_plan *plan, const uint16_t *x, int B, const uin
                               void *stream);
 
 /*
+ * Per-token threshold (the per-token form of Eq. 6: the threshold of each
+ * token is the quantile of its own coefficient vector, as in the ideal
+ * sparsity of Sec. 3, instead of the calibrated layer constant of Sec. 4):
+ *   thld_b = Quantile(k, c_b), linear interpolation between order statistics,
+ *   IDX = {i : exists b, c_b[i] > thld_b}   (strict, union over the batch),
+ * c_b = |u_b| (CD_VARIANT_MONO), |s_b| (CD_VARIANT_DUAL_IDEAL) or the signed
+ * predictor score s_hat_b (CD_VARIANT_DUAL_PRED, A_t / B_t set); then s on
+ * IDX and y by Eq. (5) as in the constant-threshold calls. A batch-1 call
+ * keeps exactly d_ff - 1 - floor(k (d_ff - 1)) neurons when the coefficients
+ * are distinct. thld_out (DEVICE double[B], 8-byte aligned, may be NULL)
+ * receives the per-token thresholds, computed in fp64 from the fp32
+ * coefficients. k in [0, 1]; d_ff <= 32768 (CD_EUNSUPPORTED beyond). The
+ * call runs the coefficient kernel over all neurons, a per-token selection
+ * kernel, the gather of IDX and the down projection.
+ */
+cd_status countdown_ffn_topk(cd_plan *plan, int variant, const uint16_t *x, int B,
+                             const uint16_t *W_gate, const uint16_t *W_up, const uint16_t *W_down,
+                             const uint16_t *A_t, const uint16_t *B_t, double k, double *thld_out,
+                             float *y, void *stream);
+
+/*
  * One layer of a stack of FFNs joined by a residual stream. The paper
  * evaluates single Gated-MLP layers (Sec. 3); the stack workload adds, per
  * token b, before the FFN of `variant` (CD_VARIANT_*, as in the calls above):
@@ -198,7 +219,7 @@ cd_status countdown_check_shape(int d_model, int d_ff, int max_batch, int d_rank
 const char *countdown_status_string(cd_status status);
 
 /* ABI version of this header (bumped on any signature change). */
-#define COUNTDOWN_ABI_VERSION 4
+#define COUNTDOWN_ABI_VERSION 5
 int countdown_abi_version(void);
 
 #ifdef __cplusplus

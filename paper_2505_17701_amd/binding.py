@@ -22,7 +22,7 @@ CD_PHASE_COEF, CD_PHASE_DOWN, CD_PHASE_ALL = 1, 2, 3
 # every symbol include/countdown.h declares
 EXPORTS = (
     "countdown_plan_create", "countdown_plan_destroy", "countdown_ffn_mono", "countdown_ffn_dual",
-    "countdown_ffn_dense", "countdown_ffn_residual", "countdown_calibrate",
+    "countdown_ffn_dense", "countdown_ffn_topk", "countdown_ffn_residual", "countdown_calibrate",
     "countdown_export_active",
     "countdown_plan_set_phases", "countdown_check_args",
     "countdown_check_shape", "countdown_status_string", "countdown_abi_version",
@@ -55,6 +55,7 @@ def load_library(path: str = LIB_PATH):
         "countdown_ffn_dense": (i, [vp, vp, i, vp, vp, vp, vp, vp]),
         "countdown_ffn_residual": (i, [vp, i, vp, vp, vp, f, vp, i, vp, vp, vp, vp, vp, f, vp,
                                        vp]),
+        "countdown_ffn_topk": (i, [vp, i, vp, i, vp, vp, vp, vp, vp, d, vp, vp, vp]),
         "countdown_calibrate": (i, [vp, i, vp, i, vp, vp, vp, vp, d, vp, vp, vp]),
         "countdown_export_active": (i, [vp, vp, vp, vp, vp, vp]),
         "countdown_plan_set_phases": (i, [vp, u]),
@@ -182,6 +183,24 @@ def countdown_ffn_dual(plan: Plan, x, W_gate, W_up, W_down, thld: float, A_t=Non
         plan.handle, _ptr(_bf16(x)), B, _ptr(_bf16(W_gate)), _ptr(_bf16(W_up)),
         _ptr(_bf16(W_down)), _ptr(_bf16(A_t)), _ptr(_bf16(B_t)), float(thld), _ptr(y),
         _stream(stream)), "countdown_ffn_dual")
+    plan.last_batch = B
+    return y
+
+
+def countdown_ffn_topk(plan: Plan, variant: int, x, W_gate, W_up, W_down, k: float, A_t=None,
+                       B_t=None, y=None, thld_out=None, stream=None):
+    """Per-token threshold: each token keeps the neurons above the k-quantile of its
+    own coefficients (union over the batch). ``thld_out``: optional fp64 [B] device
+    tensor for the thresholds. Returns y."""
+    import torch
+
+    B, y = _out(plan, x, y)
+    if thld_out is not None and (thld_out.dtype != torch.float64 or thld_out.numel() < B):
+        raise ValueError("thld_out must be a float64 device tensor with at least B entries")
+    _check(load_library().countdown_ffn_topk(
+        plan.handle, int(variant), _ptr(_bf16(x)), B, _ptr(_bf16(W_gate)), _ptr(_bf16(W_up)),
+        _ptr(_bf16(W_down)), _ptr(_bf16(A_t)), _ptr(_bf16(B_t)), float(k), _ptr(thld_out),
+        _ptr(y), _stream(stream)), "countdown_ffn_topk")
     plan.last_batch = B
     return y
 

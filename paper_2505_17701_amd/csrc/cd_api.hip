@@ -31,7 +31,9 @@ struct cd_plan {
     int last_batch;               // of the last FFN call (0 before the first)
     int *act;                     // [d_ff] neuron in IDX
     float *s;                     // [max_batch][d_ff] coefficients s of active neurons
-    float *coef;                  // [max_batch][d_ff] dense coefficients (CD_PLAN_KEEP_COEF)
+    float *coef;                  // [max_batch][d_ff] dense coefficients (written by every
+                                  // call with CD_PLAN_KEEP_COEF, by the per-token path always)
+    double *q;                    // [max_batch] per-token thresholds of the last per-token call
     float *lat;                   // [max_batch][d_rank] predictor latent
     unsigned phases;              // kernels launched per call (CD_PHASE_*)
     bool has_state;               // act / s hold a coefficient kernel's output
@@ -107,7 +109,7 @@ cdk::CoefArgs coef_args(cd_plan *p, const uint16_t *x, int B, const uint16_t *Wg
     a.thld = thld;
     a.act = p->act;
     a.s = p->s;
-    a.coef = p->coef;
+    a.coef = (p->flags & CD_PLAN_KEEP_COEF) ? p->coef : nullptr;
     a.y = y;
     return a;
 }
@@ -221,6 +223,51 @@ cd_status run_ffn_residual(cd_plan *p, int variant, const float *h_in, const flo
     return st;
 }
 
+cd_status run_ffn_topk(cd_plan *p, int variant, const uint16_t *x, int B, const uint16_t *Wg,
+                       const uint16_t *Wu, const uint16_t *Wd, const uint16_t *At,
+                       const uint16_t *Bt, double k, double *thld_out, float *y, void *stream)
+{
+    if (!p)
+        return CD_EINVAL;
+    if (variant != CD_VARIANT_MONO && variant != CD_VARIANT_DUAL_IDEAL &&
+        variant != CD_VARIANT_DUAL_PRED)
+        return CD_EINVAL;
+    if (!(k >= 0.0 && k <= 1.0) || (thld_out && (reinterpret_cast<uintptr_t>(thld_out) & 7u)))
+        return CD_EINVAL;
+    cd_status st = check_args(variant, p->d_model, p->d_ff, p->max_batch, p->d_rank, x, B, Wg, Wu,
+                              Wd, At, Bt, 0.0f, y);
+    if (st != CD_OK)
+        return st;
+    if (p->d_ff > cdk::kTopkMaxDff)
+        return CD_EUNSUPPORTED;
+    hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+    if (!(p->phases & CD_PHASE_COEF) && !p->has_state)
+        return CD_EINVAL;
+    p->last_batch = B;
+    if (p->phases & CD_PHASE_COEF) {
+        if (variant == CD_VARIANT_DUAL_PRED) {
+            st = launched(cdk::launch_latent(x, B, At, p->d_model, p->d_rank, p->lat, s));
+            if (st != CD_OK)
+                return st;
+        }
+        // dense coefficients of every neuron (threshold +inf: nothing is gathered yet)
+        cdk::CoefArgs ca = coef_args(p, x, B, Wg, Wu, Bt, INFINITY, y);
+        ca.coef = p->coef;
+        st = launched(cdk::launch_coef(kernel_variant(variant), ca, s));
+        if (st != CD_OK)
+            return st;
+        st = launched(cdk::launch_topk(kernel_variant(variant), ca, k, thld_out ? thld_out : p->q, s));
+        if (st != CD_OK)
+            return st;
+        p->has_state = true;
+    }
+    if (p->phases & CD_PHASE_DOWN) {
+        const cdk::DownArgs da = down_args(p, B, Wd, y);
+        st = launched(cdk::launch_down(da, s));
+    }
+    return st;
+}
+
 template <class T>
 cd_status dalloc(T **ptr, size_t count)
 {
@@ -236,7 +283,7 @@ cd_status dalloc(T **ptr, size_t count)
 
 void release(cd_plan *p)
 {
-    void *bufs[] = {p->act, p->s, p->coef, p->lat};
+    void *bufs[] = {p->act, p->s, p->coef, p->lat, p->q};
     for (void *b : bufs)
         if (b)
             (void)hipFree(b);
@@ -271,6 +318,15 @@ cd_status countdown_ffn_residual(cd_plan *plan, int variant, const float *h_in, 
         thld = -INFINITY;
     return run_ffn_residual(plan, variant, h_in, y_prev, h_out, eps, x_out, B, W_gate, W_up,
                             W_down, A_t, B_t, thld, y, stream);
+}
+
+cd_status countdown_ffn_topk(cd_plan *plan, int variant, const uint16_t *x, int B,
+                             const uint16_t *W_gate, const uint16_t *W_up, const uint16_t *W_down,
+                             const uint16_t *A_t, const uint16_t *B_t, double k, double *thld_out,
+                             float *y, void *stream)
+{
+    return run_ffn_topk(plan, variant, x, B, W_gate, W_up, W_down, A_t, B_t, k, thld_out, y,
+                        stream);
 }
 
 cd_status countdown_check_shape(int d_model, int d_ff, int max_batch, int d_rank)
@@ -315,7 +371,8 @@ cd_status countdown_plan_create(int d_model, int d_ff, int max_batch, int d_rank
     const size_t mb = (size_t)max_batch;
     st = dalloc(&p->act, (size_t)d_ff);
     if (st == CD_OK) st = dalloc(&p->s, mb * d_ff);
-    if (st == CD_OK && (flags & CD_PLAN_KEEP_COEF)) st = dalloc(&p->coef, mb * d_ff);
+    if (st == CD_OK) st = dalloc(&p->coef, mb * d_ff);
+    if (st == CD_OK) st = dalloc(&p->q, mb);
     if (st == CD_OK && d_rank > 0) st = dalloc(&p->lat, mb * d_rank);
     if (st != CD_OK) {
         release(p);
@@ -423,7 +480,7 @@ cd_status countdown_calibrate(cd_plan *p, int variant, const uint16_t *X, int T,
 cd_status countdown_export_active(const cd_plan *p, int32_t *idx_dst, int32_t *n_dst,
                                   float *s_dst, float *coef_dst, void *stream)
 {
-    if (!p || (coef_dst && !p->coef) || p->last_batch < 1)
+    if (!p || (coef_dst && !(p->flags & CD_PLAN_KEEP_COEF)) || p->last_batch < 1)
         return CD_EINVAL;
     hipStream_t s = reinterpret_cast<hipStream_t>(stream);
     hipError_t e = hipSuccess;

@@ -1197,6 +1197,269 @@ __global__ void k_mean(const double *__restrict__ q, int T, float *__restrict__ 
     }
 }
 
+// ------------------------------------------------- per-token threshold path
+// The per-token form of Eq. 6: each token's threshold is the quantile of its
+// own coefficients. The coefficient kernel first writes the dense
+// coefficients (threshold +inf, nothing gathered); k_topk_select finds each
+// token's quantile; k_gather_topk thresholds against it and gathers.
+
+constexpr int kTopkThreads = 1024;
+constexpr int kTopkPerThread = 32;  // keys per thread: d_ff <= 32768
+
+// One workgroup per token: q = v[lo] + (h - lo)(v[lo + 1] - v[lo]), h = k (n - 1).
+// The order statistic of rank lo comes from 3 passes of radix select (11, 11
+// and 10 bits, most significant first) over order-preserving keys held in
+// registers: a shared LDS histogram of the keys that match the prefix so far,
+// a block-wide scan of its bins, and the bin that holds the rank. An 11-bit
+// top digit (sign, exponent, two mantissa bits) spreads typical coefficients
+// over tens of bins, so the atomics hardly contend. Rank lo + 1 is the same
+// key when it repeats, else the smallest key above it. fp64 interpolation.
+constexpr int kSelBins = 2048;
+
+__global__ __launch_bounds__(kTopkThreads) void k_topk_select(const float *__restrict__ coef, int ld,
+                                                              int n, int use_abs, double k,
+                                                              double *__restrict__ q)
+{
+    constexpr int kWaves = kTopkThreads / kWave;
+    __shared__ uint32_t hist[kSelBins];
+    __shared__ uint32_t wsum[kWaves];
+    __shared__ int sel[3];
+    __shared__ uint32_t umin[kWaves];
+    const int lane = threadIdx.x % kWave, wave = threadIdx.x / kWave;
+    const float *c = coef + (size_t)blockIdx.x * ld;
+    const int jn = (n + kTopkThreads - 1) / kTopkThreads;  // key slots in use (uniform)
+    float cv[kTopkPerThread];
+#pragma unroll
+    for (int j = 0; j < kTopkPerThread; ++j) {
+        const int i = threadIdx.x + j * kTopkThreads;
+        cv[j] = 0.0f;
+        if (j < jn)  // uniform
+            cv[j] = *or_zero(i < n, c + i);
+    }
+    uint32_t key[kTopkPerThread];
+    uint32_t valid = 0u;  // bit j: slot j holds a key
+#pragma unroll
+    for (int j = 0; j < kTopkPerThread; ++j) {
+        key[j] = order_key(cv[j], use_abs);
+        if (j < jn && threadIdx.x + j * kTopkThreads < n)
+            valid |= 1u << j;
+    }
+    const double h = k * (double)(n - 1);
+    int lo = (int)floor(h);
+    if (lo > n - 1)
+        lo = n - 1;
+
+    uint32_t prefix = 0u, mask = 0u;
+    int r = lo;
+    int last_count = 0;  // keys equal to the selected key (after the last pass)
+#pragma unroll
+    for (int pass = 0; pass < 3; ++pass) {
+        const int shift = pass == 0 ? 21 : pass == 1 ? 10 : 0;
+        const uint32_t dmask = pass == 2 ? 0x3ffu : 0x7ffu;
+        hist[2 * threadIdx.x] = 0u;
+        hist[2 * threadIdx.x + 1] = 0u;
+        __syncthreads();
+#pragma unroll
+        for (int j = 0; j < kTopkPerThread; ++j)
+            if (j < jn && ((valid >> j) & 1u) && (key[j] & mask) == prefix)
+                atomicAdd(&hist[(key[j] >> shift) & dmask], 1u);
+        __syncthreads();
+        // block scan: thread t owns bins 2t and 2t + 1
+        const uint32_t h0 = hist[2 * threadIdx.x], h1 = hist[2 * threadIdx.x + 1];
+        const uint32_t tot = h0 + h1;
+        uint32_t inc = tot;
+#pragma unroll
+        for (int off = 1; off < kWave; off <<= 1) {
+            const uint32_t v = (uint32_t)__shfl_up((int)inc, off);
+            if (lane >= off)
+                inc += v;
+        }
+        if (lane == kWave - 1)
+            wsum[wave] = inc;
+        __syncthreads();
+        uint32_t cum = inc - tot;
+        for (int w = 0; w < wave; ++w)
+            cum += wsum[w];
+        const uint32_t rr = (uint32_t)r;
+        if (rr >= cum && rr < cum + h0) {
+            sel[0] = 2 * threadIdx.x;
+            sel[1] = (int)(rr - cum);
+            sel[2] = (int)h0;
+        } else if (rr >= cum + h0 && rr < cum + tot) {
+            sel[0] = 2 * threadIdx.x + 1;
+            sel[1] = (int)(rr - cum - h0);
+            sel[2] = (int)h1;
+        }
+        __syncthreads();
+        prefix |= (uint32_t)sel[0] << shift;
+        mask |= dmask << shift;
+        r = sel[1];
+        last_count = sel[2];
+    }
+    const uint32_t k0 = prefix;
+    uint32_t k1 = k0;
+    if (lo + 1 < n && r + 1 >= last_count) {
+        // rank lo + 1 is the smallest key above k0
+        uint32_t m = 0xffffffffu;
+#pragma unroll
+        for (int j = 0; j < kTopkPerThread; ++j)
+            if (j < jn && ((valid >> j) & 1u) && key[j] > k0)
+                m = min(m, key[j]);
+#pragma unroll
+        for (int off = 32; off >= 1; off >>= 1)
+            m = min(m, (uint32_t)__shfl_xor((int)m, off));
+        if (lane == 0)
+            umin[wave] = m;
+        __syncthreads();
+        m = 0xffffffffu;
+#pragma unroll
+        for (int w = 0; w < kWaves; ++w)
+            m = min(m, umin[w]);
+        k1 = m;
+    }
+    if (threadIdx.x == 0) {
+        const double v0 = (double)key_value(k0, use_abs);
+        const double v1 = (double)key_value(k1, use_abs);
+        q[blockIdx.x] = v0 + (h - (double)lo) * (v1 - v0);
+    }
+}
+
+// s = u * SiLU(g) of one active M-CountDown neuron: its W_gate row, u from the
+// dense coefficients
+template <int B, int NK, bool XREG>
+__device__ __forceinline__ void mono_finish(const CoefArgs &a, const Tokens<B, NK, XREG> &tok,
+                                            const u32x4 (&wg)[NK], int row, int lane)
+{
+    float ag[B];
+    zero_acc(ag);
+    tok.dot(wg, lane, ag);
+#pragma unroll
+    for (int b = 0; b < B; ++b) {
+        const float g = wave_sum(ag[b]);
+        if (b < a.nb && lane == 0)
+            a.s[(size_t)b * a.d_ff + row] = a.coef[(size_t)b * a.d_ff + row] * silu(g);
+    }
+}
+
+// Per-token threshold and gather for batches of 4-8: a workgroup owns kPredRows neurons; its
+// first kPredRows threads test them against every token's own threshold
+// (|u|, |s| or signed s_hat > q_b, union over the batch) and set act; the
+// active neurons are dealt round-robin to the four waves, which gather W_gate
+// (mono) or W_gate and W_up (pred) and write s; ideal D-CountDown copies s.
+template <int B, int NK, bool XREG, int VARIANT>
+__global__ __launch_bounds__(kBlock) void k_gather_topk(const CoefArgs a, const double *__restrict__ q)
+{
+    extern __shared__ __align__(16) uint32_t xs[];
+    __shared__ uint32_t mask;
+    constexpr bool kGather = VARIANT != kDualIdeal;
+    const int lane = threadIdx.x % kWave, wave = threadIdx.x / kWave;
+    const int r0 = blockIdx.x * kPredRows;
+    Tokens<B, NK, XREG> tok;
+    if constexpr (kGather)
+        tok.issue(a.x, a.nb, a.d_model, lane);
+    bool act = false;
+    const int row = r0 + threadIdx.x;
+    if (threadIdx.x < kPredRows && row < a.d_ff) {
+#pragma unroll
+        for (int b = 0; b < B; ++b) {
+            if (b < a.nb) {
+                const float c = a.coef[(size_t)b * a.d_ff + row];
+                act = act || ((double)(VARIANT == kDualPred ? c : fabsf(c)) > q[b]);
+            }
+        }
+        a.act[row] = act ? 1 : 0;
+        if (VARIANT == kDualIdeal && act)
+#pragma unroll
+            for (int b = 0; b < B; ++b)
+                if (b < a.nb)
+                    a.s[(size_t)b * a.d_ff + row] = a.coef[(size_t)b * a.d_ff + row];
+    }
+    const uint64_t m = ballot(act);
+    if (threadIdx.x == 0)
+        mask = (uint32_t)m;  // the first kPredRows threads are lanes 0..31 of wave 0
+    zero_y(a.y, a.nb * a.d_model);
+    if constexpr (kGather) {
+        tok.write(xs);
+        __syncthreads();
+        uint32_t mm = mask;
+        for (int v = 0; v < wave; ++v)
+            mm &= mm - 1;
+        for (int r = pred_next(mm); r >= 0; r = pred_next(mm)) {
+            u32x4 wg[NK];
+            load_row<NK>(wg, a.Wg + (size_t)(r0 + r) * a.d_model, a.d_model, lane);
+            if constexpr (VARIANT == kMono) {
+                mono_finish<B, NK, XREG>(a, tok, wg, r0 + r, lane);
+            } else {
+                u32x4 wu[NK];
+                load_row<NK>(wu, a.Wu + (size_t)(r0 + r) * a.d_model, a.d_model, lane);
+                pred_finish<B, NK, XREG>(a, tok, wg, wu, r0 + r, lane);
+            }
+        }
+    }
+}
+
+// Per-token threshold and gather for batches of 1-2: one wave per neuron.
+// Lane b reads token b's coefficient and threshold; an inactive neuron's wave
+// only writes its flag, an active one issues its token loads with its weight
+// rows at once (W_gate for mono, W_gate and W_up for pred) and writes s, so
+// every active row of the call is in flight together.
+template <int B, int NK, int VARIANT>
+__global__ __launch_bounds__(kBlock) void k_gather_topk_w(const CoefArgs a, const double *__restrict__ q)
+{
+    const int lane = threadIdx.x % kWave, wave = threadIdx.x / kWave;
+    const int row = blockIdx.x * kWavesPerBlock + wave;
+    zero_y(a.y, a.nb * a.d_model);
+    if (row >= a.d_ff)
+        return;
+    float cb = 0.0f;
+    bool mine = false;
+    if (lane < a.nb) {
+        cb = a.coef[(size_t)lane * a.d_ff + row];
+        mine = (double)(VARIANT == kDualPred ? cb : fabsf(cb)) > q[lane];
+    }
+    const bool act = ballot(mine) != 0;
+    if (lane == 0)
+        a.act[row] = act ? 1 : 0;
+    if (!act)
+        return;
+    if constexpr (VARIANT == kDualIdeal) {
+        if (lane < a.nb)
+            a.s[(size_t)lane * a.d_ff + row] = cb;  // s itself is the coefficient
+    } else {
+        u32x4 wg[NK];
+        load_row<NK>(wg, a.Wg + (size_t)row * a.d_model, a.d_model, lane);
+        u32x4 wu[VARIANT == kDualPred ? NK : 1];
+        if constexpr (VARIANT == kDualPred)
+            load_row<NK>(wu, a.Wu + (size_t)row * a.d_model, a.d_model, lane);
+        Tokens<B, NK, true> tok;
+        tok.issue(a.x, a.nb, a.d_model, lane);
+        float ag[B];
+        zero_acc(ag);
+        if constexpr (VARIANT == kDualPred) {
+            float au[B];
+            zero_acc(au);
+            tok.dot2(wg, wu, lane, ag, au);
+#pragma unroll
+            for (int b = 0; b < B; ++b) {
+                const float g = wave_sum(ag[b]);
+                const float u = wave_sum(au[b]);
+                if (b < a.nb && lane == 0)
+                    a.s[(size_t)b * a.d_ff + row] = u * silu(g);
+            }
+        } else {
+            tok.dot(wg, lane, ag);
+#pragma unroll
+            for (int b = 0; b < B; ++b) {
+                const float g = wave_sum(ag[b]);
+                const float u = __builtin_bit_cast(
+                    float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, cb), b));
+                if (b < a.nb && lane == 0)
+                    a.s[(size_t)b * a.d_ff + row] = u * silu(g);
+            }
+        }
+    }
+}
+
 // ------------------------------------------------------------------ launchers
 
 // kernels staging more than 64 KB in LDS opt in to the larger gfx950 limit
@@ -1424,6 +1687,72 @@ hipError_t launch_down(const DownArgs &args, hipStream_t s)
     default: allow_lds(k_down<8>, lds); k_down<8><<<grid, kBlock, lds, s>>>(a); break;
     }
     return hipGetLastError();
+}
+
+template <int B, int NK>
+static hipError_t gather_topk_bn(int variant, const CoefArgs &a, const double *q, hipStream_t s)
+{
+    constexpr bool XREG = B <= 2;
+    if constexpr (XREG) {
+        const int wgrid = (a.d_ff + kWavesPerBlock - 1) / kWavesPerBlock;
+        switch (variant) {
+        case kMono: k_gather_topk_w<B, NK, kMono><<<wgrid, kBlock, 0, s>>>(a, q); break;
+        case kDualIdeal: k_gather_topk_w<B, NK, kDualIdeal><<<wgrid, kBlock, 0, s>>>(a, q); break;
+        case kDualPred: k_gather_topk_w<B, NK, kDualPred><<<wgrid, kBlock, 0, s>>>(a, q); break;
+        default: return hipErrorInvalidValue;
+        }
+    } else {
+        const size_t lds = token_lds_bytes(B, NK);
+        const int grid = (a.d_ff + kPredRows - 1) / kPredRows;
+        switch (variant) {
+        case kMono:
+            allow_lds(k_gather_topk<B, NK, XREG, kMono>, lds);
+            k_gather_topk<B, NK, XREG, kMono><<<grid, kBlock, lds, s>>>(a, q);
+            break;
+        case kDualIdeal:
+            k_gather_topk<B, NK, XREG, kDualIdeal><<<grid, kBlock, 0, s>>>(a, q);
+            break;
+        case kDualPred:
+            allow_lds(k_gather_topk<B, NK, XREG, kDualPred>, lds);
+            k_gather_topk<B, NK, XREG, kDualPred><<<grid, kBlock, lds, s>>>(a, q);
+            break;
+        default:
+            return hipErrorInvalidValue;
+        }
+    }
+    return hipGetLastError();
+}
+
+template <int B>
+static hipError_t gather_topk_b(int variant, const CoefArgs &a, const double *q, hipStream_t s)
+{
+    switch (col_tile(a.d_model)) {
+    case 1: return gather_topk_bn<B, 1>(variant, a, q, s);
+    case 2: return gather_topk_bn<B, 2>(variant, a, q, s);
+    case 4: return gather_topk_bn<B, 4>(variant, a, q, s);
+    case 8: return gather_topk_bn<B, 8>(variant, a, q, s);
+    default:
+        if constexpr (B * 16 <= 64)
+            return gather_topk_bn<B, 16>(variant, a, q, s);
+        return hipErrorInvalidValue;
+    }
+}
+
+hipError_t launch_topk(int variant, const CoefArgs &a, double k, double *q, hipStream_t s)
+{
+    if (a.d_ff > kTopkThreads * kTopkPerThread)
+        return hipErrorInvalidValue;
+    k_topk_select<<<a.nb, kTopkThreads, 0, s>>>(a.coef, a.d_ff, a.d_ff,
+                                                 variant == kDualPred ? 0 : 1, k, q);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess)
+        return e;
+    switch (batch_tile(a.nb)) {
+    case 1: return gather_topk_b<1>(variant, a, q, s);
+    case 2: return gather_topk_b<2>(variant, a, q, s);
+    case 4: return gather_topk_b<4>(variant, a, q, s);
+    default: return gather_topk_b<8>(variant, a, q, s);
+    }
 }
 
 hipError_t launch_export(const int *act, const float *s_rows, int nb, int d_ff, int *idx_dst,
