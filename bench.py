@@ -49,8 +49,8 @@ def parse():
     p.add_argument("--warmup", type=int, default=200)
     p.add_argument("--workload", default="llama7b_4096x11008")
     p.add_argument("--variant", default="mono",
-                   choices=["mono", "dual_ideal", "dual_pred", "dense", "mono_topk",
-                            "dual_ideal_topk", "dual_pred_topk"])
+                   choices=["mono", "dual_ideal", "dual_pred", "dense", "cats", "mono_topk",
+                            "dual_ideal_topk", "dual_pred_topk", "cats_topk"])
     p.add_argument("--batch", type=int, default=1, help="decode tokens per call (union IDX)")
     p.add_argument("--k", type=float, default=0.9)
     p.add_argument("--copies", type=int, default=4, help="independent weight copies rotated")
@@ -183,7 +183,7 @@ class Context:
             f"{time.time() - t:.1f}s")
         variants = variants or [v for v in w.variants if v != "dense"]
         vids = {"mono": cd.CD_VARIANT_MONO, "dual_ideal": cd.CD_VARIANT_DUAL_IDEAL,
-                "dual_pred": cd.CD_VARIANT_DUAL_PRED}
+                "dual_pred": cd.CD_VARIANT_DUAL_PRED, "cats": cd.CD_VARIANT_CATS}
         # tokens per calibration launch: the widest batch tile the shape allows
         cal_plan = cd.Plan(self.dm, self.dff, max_batch=min(8, 32768 // self.dm), d_rank=self.dr)
         self.thld = {}
@@ -216,7 +216,7 @@ class Context:
         topk = variant.endswith("_topk")
         base = variant[:-5] if topk else variant
         vid = {"mono": cd.CD_VARIANT_MONO, "dual_ideal": cd.CD_VARIANT_DUAL_IDEAL,
-               "dual_pred": cd.CD_VARIANT_DUAL_PRED}.get(base)
+               "dual_pred": cd.CD_VARIANT_DUAL_PRED, "cats": cd.CD_VARIANT_CATS}.get(base)
 
         def step(i):
             L = layers[i % copies]
@@ -229,6 +229,8 @@ class Context:
                 cd.countdown_ffn_mono(plan, x, L["W_gate"], L["W_up"], L["W_down"], th, y=y)
             elif variant == "dual_ideal":
                 cd.countdown_ffn_dual(plan, x, L["W_gate"], L["W_up"], L["W_down"], th, y=y)
+            elif variant == "cats":
+                cd.countdown_ffn_cats(plan, x, L["W_gate"], L["W_up"], L["W_down"], th, y=y)
             elif variant == "dual_pred":
                 cd.countdown_ffn_dual(plan, x, L["W_gate"], L["W_up"], L["W_down"], th,
                                       A_t=L["A_t"], B_t=L["B_t"], y=y)
@@ -477,19 +479,30 @@ def main():
         del src, dst
 
     main_ctx = Context(w, args.copies, args.tokens, args.calib_tokens,
-                       sorted(set((args.k,) + tuple(w.ks))), max_batch=args.batch)
+                       sorted(set((args.k,) + tuple(w.ks))), max_batch=args.batch,
+                       variants=(["mono", "dual_ideal", "cats"] if "mono" in w.variants
+                                 else None))
     main_res = main_ctx.measure(args.variant, args.k, args.batch, args.steps, args.warmup)
     log(f"[bench] {w.name} {args.variant} k={args.k}: {json.dumps(main_res)}")
 
     extra = {}
     if not args.no_extra and "mono" in w.variants:
         for variant, k in (("dense", None), ("dual_ideal", 0.9), ("mono", 0.7), ("mono", 0.5),
-                           ("mono_topk", 0.9), ("dual_ideal_topk", 0.9)):
+                           ("cats", 0.9), ("mono_topk", 0.9), ("dual_ideal_topk", 0.9),
+                           ("cats_topk", 0.9)):
             if variant == args.variant and k == args.k:
                 continue
             r = main_ctx.measure(variant, k, 1, max(200, args.steps // 4), 50)
             extra[f"{variant}" + ("" if k is None else f"@k={k}")] = brief(r)
             log(f"[bench] {variant} k={k}: {json.dumps(extra[list(extra)[-1]])}")
+        # mask agreement of u and h with s (CIF / CAF) on the layer's eval tokens
+        from paper_2505_17701_amd.metrics import cif_caf, masks_on_gpu
+
+        extra["cif_caf"] = {}
+        for k in (0.5, 0.7, 0.9):
+            m = cif_caf(*masks_on_gpu(main_ctx.layers[0], main_ctx.X_eval[:32], k))
+            extra["cif_caf"][f"k={k}"] = {kk: round(v, 4) for kk, v in m.items()}
+        log(f"[bench] CIF/CAF: {json.dumps(extra['cif_caf'])}")
         if "dense" in extra:
             extra["speedup_vs_dense"] = extra["dense"]["us_per_layer"] / main_res["us_per_layer"]
             dense_b = traffic.algorithmic_bytes("dense", dm, dff, dff)["total"]
@@ -517,8 +530,9 @@ def main():
                                                              H["W_down"], th),
                "dual_pred": lambda x: oracle.ffn_dual_pred(x, H["W_gate"], H["W_up"], H["W_down"],
                                                            H.get("A_t"), H.get("B_t"), th),
-               "dense": lambda x: oracle.dense(x, H["W_gate"], H["W_up"], H["W_down"])}
-        for base in ("mono", "dual_ideal", "dual_pred"):
+               "dense": lambda x: oracle.dense(x, H["W_gate"], H["W_up"], H["W_down"]),
+               "cats": lambda x: oracle.ffn_cats(x, H["W_gate"], H["W_up"], H["W_down"], th)}
+        for base in ("mono", "dual_ideal", "dual_pred", "cats"):
             fns[base + "_topk"] = (lambda b: lambda x: oracle.ffn_topk(
                 b, x, H["W_gate"], H["W_up"], H["W_down"], args.k, A_t=H.get("A_t"),
                 B_t=H.get("B_t")))(base)
@@ -548,7 +562,10 @@ def main():
                 "dual_ideal_topk": "k_coef_dual + k_topk_select + k_gather_topk (per-token "
                                    "threshold)",
                 "dual_pred_topk": "k_latent + k_coef_pred + k_topk_select + k_gather_topk "
-                                  "(per-token threshold)"}[args.variant]
+                                  "(per-token threshold)",
+                "cats": "k_coef_mono<CATS> (dense W_gate GEMV, SiLU, threshold, W_up gather)",
+                "cats_topk": "k_coef_mono<CATS> + k_topk_select + k_gather_topk "
+                             "(per-token threshold)"}[args.variant]
         roof = {"bound": "hbm", "kernel": desc,
                 "achieved": main_res[f"{dom}_kernel_GBs"], "peak": HBM_PEAK_GBS, "unit": "GB/s",
                 "frac": main_res[f"{dom}_kernel_GBs"] / HBM_PEAK_GBS,

@@ -59,6 +59,7 @@ typedef int cd_status;
 #define CD_VARIANT_DUAL_IDEAL 1  /* D-CountDown ideal, coefficient |s| (Eq. 6c) */
 #define CD_VARIANT_DUAL_PRED 2   /* D-CountDown, predictor score s_hat (Sec. 4) */
 #define CD_VARIANT_DENSE 3       /* dense Gated-MLP (Eq. 1) */
+#define CD_VARIANT_CATS 4        /* CATS, the comparison method: |SiLU(x.W_gate)| (Eq. 6a) */
 
 /* Plan flags. */
 #define CD_PLAN_KEEP_COEF 1u  /* also store the dense coefficient vector of each call
@@ -112,13 +113,24 @@ cd_status countdown_ffn_dense(cd_plan *plan, const uint16_t *x, int B, const uin
                               void *stream);
 
 /*
+ * CATS (Eq. 6a; the comparison method of Sec. 3), through the same kernels:
+ * h = SiLU(x.W_gate) over all rows; IDX = {i : exists b, |h_b[i]| > thld};
+ * u_b[i] = x_b.W_up[i] on IDX only; y_b = sum_{i in IDX} u_b[i] h_b[i] W_down[i].
+ * Conventions as countdown_ffn_mono (the roles of W_gate and W_up swapped).
+ */
+cd_status countdown_ffn_cats(cd_plan *plan, const uint16_t *x, int B, const uint16_t *W_gate,
+                             const uint16_t *W_up, const uint16_t *W_down, float thld, float *y,
+                             void *stream);
+
+/*
  * Per-token threshold (the per-token form of Eq. 6: the threshold of each
  * token is the quantile of its own coefficient vector, as in the ideal
  * sparsity of Sec. 3, instead of the calibrated layer constant of Sec. 4):
  *   thld_b = Quantile(k, c_b), linear interpolation between order statistics,
  *   IDX = {i : exists b, c_b[i] > thld_b}   (strict, union over the batch),
- * c_b = |u_b| (CD_VARIANT_MONO), |s_b| (CD_VARIANT_DUAL_IDEAL) or the signed
- * predictor score s_hat_b (CD_VARIANT_DUAL_PRED, A_t / B_t set); then s on
+ * c_b = |u_b| (CD_VARIANT_MONO), |s_b| (CD_VARIANT_DUAL_IDEAL), |h_b|
+ * (CD_VARIANT_CATS) or the signed predictor score s_hat_b
+ * (CD_VARIANT_DUAL_PRED, A_t / B_t set); then s on
  * IDX and y by Eq. (5) as in the constant-threshold calls. A batch-1 call
  * keeps exactly d_ff - 1 - floor(k (d_ff - 1)) neurons when the coefficients
  * are distinct. thld_out (DEVICE double[B], 8-byte aligned, may be NULL)
@@ -219,7 +231,7 @@ cd_status countdown_check_shape(int d_model, int d_ff, int max_batch, int d_rank
 const char *countdown_status_string(cd_status status);
 
 /* ABI version of this header (bumped on any signature change). */
-#define COUNTDOWN_ABI_VERSION 5
+#define COUNTDOWN_ABI_VERSION 6
 int countdown_abi_version(void);
 
 #ifdef __cplusplus

@@ -308,6 +308,35 @@ int64_t cdo_ffn_mono(const uint16_t *x, int B, const uint16_t *W_gate, const uin
     return rc < 0 ? rc : n;
 }
 
+/* CATS, the comparison method (Eq. 6a): h = SiLU(x.W_gate) densely;
+ * IDX = {i : exists b, |h_b[i]| > thld}; up only on IDX; y by Eq. (5).
+ * coef (optional) receives h [B][d_ff]. Returns |IDX| or a negative error. */
+int64_t cdo_ffn_cats(const uint16_t *x, int B, const uint16_t *W_gate, const uint16_t *W_up,
+                     const uint16_t *W_down, int d_model, int d_ff, double thld, int32_t *idx,
+                     double *y, double *coef)
+{
+    if (!x || !W_gate || !W_up || !W_down || !y || !idx || B < 1 || d_model < 1 || d_ff < 1 ||
+        isnan(thld))
+        return CDO_EINVAL;
+    double *h = (double *)malloc(sizeof(double) * (size_t)B * (size_t)d_ff);
+    if (!h)
+        return CDO_ENOMEM;
+    for (int b = 0; b < B; b++) {
+        double *hb = h + (int64_t)b * d_ff;
+        project_bf16(x + (int64_t)b * d_model, W_gate, d_ff, d_model, hb);
+        for (int64_t i = 0; i < d_ff; i++)
+            hb[i] = cdo_silu(hb[i]);
+    }
+    if (coef)
+        memcpy(coef, h, sizeof(double) * (size_t)B * (size_t)d_ff);
+    int64_t n = cdo_select(h, B, d_ff, 1, thld, idx);
+    free(h);
+    if (n < 0)
+        return n;
+    int rc = cdo_ffn_on_idx(x, B, W_gate, W_up, W_down, d_model, d_ff, idx, n, y, NULL);
+    return rc < 0 ? rc : n;
+}
+
 /* D-CountDown, ideal (Eq. 6c): s computed densely; IDX = {i : exists b, |s_b[i]| > thld};
  * y by Eq. (5) over IDX. coef (optional) receives s [B][d_ff]. */
 int64_t cdo_ffn_dual_ideal(const uint16_t *x, int B, const uint16_t *W_gate,

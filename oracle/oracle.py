@@ -25,7 +25,7 @@ _lib = None
 __all__ = [
     "build", "load", "num_threads", "silu", "coefficients", "predictor", "select", "combine",
     "dense", "ffn_on_idx", "ffn_mono", "ffn_dual_ideal", "ffn_dual_pred", "quantile_linear",
-    "calibrate", "ffn_topk", "residual_rmsnorm", "KIND",
+    "calibrate", "ffn_topk", "ffn_cats", "residual_rmsnorm", "KIND",
 ]
 
 
@@ -67,7 +67,7 @@ def load():
         lib.cdo_ffn_on_idx.restype = C.c_int
         lib.cdo_ffn_on_idx.argtypes = [u16p, C.c_int, u16p, u16p, u16p, C.c_int, C.c_int, vp,
                                        C.c_int64, f64p, vp]
-        for name in ("cdo_ffn_mono", "cdo_ffn_dual_ideal"):
+        for name in ("cdo_ffn_mono", "cdo_ffn_dual_ideal", "cdo_ffn_cats"):
             f = getattr(lib, name)
             f.restype = C.c_int64
             f.argtypes = [u16p, C.c_int, u16p, u16p, u16p, C.c_int, C.c_int, C.c_double, i32p,
@@ -198,6 +198,11 @@ def _variant(fn, x, W_gate, W_up, W_down, thld, want_coef):
 def ffn_mono(x, W_gate, W_up, W_down, thld, want_coef=False):
     """M-CountDown (Eq. 6b): returns ``(IDX, y, u or None)``."""
     return _variant(load().cdo_ffn_mono, x, W_gate, W_up, W_down, thld, want_coef)
+
+
+def ffn_cats(x, W_gate, W_up, W_down, thld, want_coef=False):
+    """CATS (Eq. 6a, the comparison method): returns ``(IDX, y, h or None)``."""
+    return _variant(load().cdo_ffn_cats, x, W_gate, W_up, W_down, thld, want_coef)
 
 
 def ffn_dual_ideal(x, W_gate, W_up, W_down, thld, want_coef=False):

@@ -16,13 +16,15 @@ LIB_PATH = os.path.join(PKG, "libcountdown.so")
 
 CD_OK, CD_EINVAL, CD_EUNSUPPORTED, CD_EHIP, CD_ENOMEM = 0, -1, -2, -3, -4
 CD_VARIANT_MONO, CD_VARIANT_DUAL_IDEAL, CD_VARIANT_DUAL_PRED, CD_VARIANT_DENSE = 0, 1, 2, 3
+CD_VARIANT_CATS = 4
 CD_PLAN_KEEP_COEF = 1
 CD_PHASE_COEF, CD_PHASE_DOWN, CD_PHASE_ALL = 1, 2, 3
 
 # every symbol include/countdown.h declares
 EXPORTS = (
     "countdown_plan_create", "countdown_plan_destroy", "countdown_ffn_mono", "countdown_ffn_dual",
-    "countdown_ffn_dense", "countdown_ffn_topk", "countdown_ffn_residual", "countdown_calibrate",
+    "countdown_ffn_dense", "countdown_ffn_cats", "countdown_ffn_topk", "countdown_ffn_residual",
+    "countdown_calibrate",
     "countdown_export_active",
     "countdown_plan_set_phases", "countdown_check_args",
     "countdown_check_shape", "countdown_status_string", "countdown_abi_version",
@@ -53,6 +55,7 @@ def load_library(path: str = LIB_PATH):
         "countdown_ffn_mono": (i, [vp, vp, i, vp, vp, vp, f, vp, vp]),
         "countdown_ffn_dual": (i, [vp, vp, i, vp, vp, vp, vp, vp, f, vp, vp]),
         "countdown_ffn_dense": (i, [vp, vp, i, vp, vp, vp, vp, vp]),
+        "countdown_ffn_cats": (i, [vp, vp, i, vp, vp, vp, f, vp, vp]),
         "countdown_ffn_residual": (i, [vp, i, vp, vp, vp, f, vp, i, vp, vp, vp, vp, vp, f, vp,
                                        vp]),
         "countdown_ffn_topk": (i, [vp, i, vp, i, vp, vp, vp, vp, vp, d, vp, vp, vp]),
@@ -183,6 +186,16 @@ def countdown_ffn_dual(plan: Plan, x, W_gate, W_up, W_down, thld: float, A_t=Non
         plan.handle, _ptr(_bf16(x)), B, _ptr(_bf16(W_gate)), _ptr(_bf16(W_up)),
         _ptr(_bf16(W_down)), _ptr(_bf16(A_t)), _ptr(_bf16(B_t)), float(thld), _ptr(y),
         _stream(stream)), "countdown_ffn_dual")
+    plan.last_batch = B
+    return y
+
+
+def countdown_ffn_cats(plan: Plan, x, W_gate, W_up, W_down, thld: float, y=None, stream=None):
+    """CATS (Eq. 6a): keep |SiLU(x.W_gate)| > thld, gather W_up on the kept neurons."""
+    B, y = _out(plan, x, y)
+    _check(load_library().countdown_ffn_cats(
+        plan.handle, _ptr(_bf16(x)), B, _ptr(_bf16(W_gate)), _ptr(_bf16(W_up)),
+        _ptr(_bf16(W_down)), float(thld), _ptr(y), _stream(stream)), "countdown_ffn_cats")
     plan.last_batch = B
     return y
 

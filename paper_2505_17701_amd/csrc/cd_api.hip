@@ -71,7 +71,7 @@ cd_status check_args(int variant, int d_model, int d_ff, int max_batch, int d_ra
     cd_status st = check_shape(d_model, d_ff, max_batch, d_rank);
     if (st != CD_OK)
         return st;
-    if (variant < CD_VARIANT_MONO || variant > CD_VARIANT_DENSE)
+    if (variant < CD_VARIANT_MONO || variant > CD_VARIANT_CATS)
         return CD_EINVAL;
     if (B < 1 || B > max_batch)
         return CD_EINVAL;
@@ -230,7 +230,7 @@ cd_status run_ffn_topk(cd_plan *p, int variant, const uint16_t *x, int B, const 
     if (!p)
         return CD_EINVAL;
     if (variant != CD_VARIANT_MONO && variant != CD_VARIANT_DUAL_IDEAL &&
-        variant != CD_VARIANT_DUAL_PRED)
+        variant != CD_VARIANT_DUAL_PRED && variant != CD_VARIANT_CATS)
         return CD_EINVAL;
     if (!(k >= 0.0 && k <= 1.0) || (thld_out && (reinterpret_cast<uintptr_t>(thld_out) & 7u)))
         return CD_EINVAL;
@@ -318,6 +318,14 @@ cd_status countdown_ffn_residual(cd_plan *plan, int variant, const float *h_in, 
         thld = -INFINITY;
     return run_ffn_residual(plan, variant, h_in, y_prev, h_out, eps, x_out, B, W_gate, W_up,
                             W_down, A_t, B_t, thld, y, stream);
+}
+
+cd_status countdown_ffn_cats(cd_plan *plan, const uint16_t *x, int B, const uint16_t *W_gate,
+                             const uint16_t *W_up, const uint16_t *W_down, float thld, float *y,
+                             void *stream)
+{
+    return run_ffn(plan, CD_VARIANT_CATS, x, B, W_gate, W_up, W_down, nullptr, nullptr, thld, y,
+                   stream);
 }
 
 cd_status countdown_ffn_topk(cd_plan *plan, int variant, const uint16_t *x, int B,
@@ -426,11 +434,14 @@ cd_status countdown_calibrate(cd_plan *p, int variant, const uint16_t *X, int T,
     if (!p || !X || !aligned16(X) || T < 1 || !thld_out || !(k >= 0.0 && k <= 1.0))
         return CD_EINVAL;
     if (variant != CD_VARIANT_MONO && variant != CD_VARIANT_DUAL_IDEAL &&
-        variant != CD_VARIANT_DUAL_PRED)
+        variant != CD_VARIANT_DUAL_PRED && variant != CD_VARIANT_CATS)
         return CD_EINVAL;
     const bool pred = variant == CD_VARIANT_DUAL_PRED;
     if (pred) {
         if (!A_t || !B_t || !aligned16(A_t) || !aligned16(B_t) || p->d_rank == 0)
+            return CD_EINVAL;
+    } else if (variant == CD_VARIANT_CATS) {
+        if (!W_gate || !aligned16(W_gate))  // h = SiLU(x.W_gate) needs W_gate only
             return CD_EINVAL;
     } else if (!W_up || !aligned16(W_up) ||
                (variant == CD_VARIANT_DUAL_IDEAL && (!W_gate || !aligned16(W_gate)))) {
@@ -446,6 +457,7 @@ cd_status countdown_calibrate(cd_plan *p, int variant, const uint16_t *X, int T,
     // The coefficient kernels run with thld = +inf (no neuron active) and
     // write the dense coefficient vectors of up to max_batch tokens at a time.
     const uint16_t *wg = W_gate ? W_gate : W_up;
+    const uint16_t *wu = W_up ? W_up : W_gate;  // CATS calibration reads W_gate only
     for (int t0 = 0; st == CD_OK && t0 < T; t0 += tb) {
         const int nb = T - t0 < tb ? T - t0 : tb;
         const uint16_t *xb = X + (size_t)t0 * p->d_model;
@@ -454,7 +466,7 @@ cd_status countdown_calibrate(cd_plan *p, int variant, const uint16_t *X, int T,
             if (st != CD_OK)
                 break;
         }
-        cdk::CoefArgs a = coef_args(p, xb, nb, wg, W_up, B_t, INFINITY, ybuf);
+        cdk::CoefArgs a = coef_args(p, xb, nb, wg, wu, B_t, INFINITY, ybuf);
         a.coef = coef;
         st = launched(cdk::launch_coef(variant, a, s));
         if (st != CD_OK)

@@ -6,7 +6,7 @@
 
 namespace cdk {
 
-enum Variant { kMono = 0, kDualIdeal = 1, kDualPred = 2, kDense = 3 };
+enum Variant { kMono = 0, kDualIdeal = 1, kDualPred = 2, kDense = 3, kCats = 4 };
 
 // Arguments of the coefficient kernels: dense coefficient projection,
 // threshold, and (mono / pred) the gathered gate (mono) or gate+up (pred)

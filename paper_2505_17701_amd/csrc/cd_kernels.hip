@@ -209,17 +209,22 @@ __device__ __forceinline__ void zero_acc(float (&acc)[B])
         acc[b] = 0.0f;
 }
 
-// M-CountDown coefficient kernel (Eq. 6b): u = x.W_up, |u| > thld, then the
-// active neuron's W_gate row and s = u * SiLU(g) (Eq. 2 restricted to IDX).
-template <int B, int NK, bool XREG>
+// Single-projection coefficient kernel. M-CountDown (Eq. 6b): u = x.W_up,
+// |u| > thld, then the active neuron's W_gate row and s = u * SiLU(g) (Eq. 2
+// restricted to IDX). CATS (Eq. 6a, the comparison method): h = SiLU(x.W_gate),
+// |h| > thld, then the active neuron's W_up row and s = u * h. The stored
+// coefficient is u (M) or h (CATS).
+template <int B, int NK, bool XREG, bool CATS>
 __global__ __launch_bounds__(kBlock) void k_coef_mono(const CoefArgs a)
 {
     extern __shared__ __align__(16) uint32_t xs[];
     const int lane = threadIdx.x % kWave, wave = threadIdx.x / kWave;
     const int row = blockIdx.x * kWavesPerBlock + wave;
     const bool live = row < a.d_ff;
+    const uint16_t *first = CATS ? a.Wg : a.Wu;   // the coefficient's projection
+    const uint16_t *second = CATS ? a.Wu : a.Wg;  // gathered for the active neurons
     u32x4 w[NK];
-    load_row<NK>(w, a.Wu + (size_t)(live ? row : 0) * a.d_model, a.d_model, lane);
+    load_row<NK>(w, first + (size_t)(live ? row : 0) * a.d_model, a.d_model, lane);
     Tokens<B, NK, XREG> tok;
     tok.issue(a.x, a.nb, a.d_model, lane);
     zero_y(a.y, a.nb * a.d_model);
@@ -227,28 +232,29 @@ __global__ __launch_bounds__(kBlock) void k_coef_mono(const CoefArgs a)
     if (!live)
         return;
 
-    float acc[B], u[B];
+    float acc[B], c[B];
     zero_acc(acc);
     tok.dot(w, lane, acc);
     bool act = false;
 #pragma unroll
     for (int b = 0; b < B; ++b) {
-        u[b] = wave_sum(acc[b]);
+        const float p = wave_sum(acc[b]);
+        c[b] = CATS ? silu(p) : p;
         if (b < a.nb) {
-            act = act || (fabsf(u[b]) > a.thld);
+            act = act || (fabsf(c[b]) > a.thld);
             if (a.coef && lane == 0)
-                a.coef[(size_t)b * a.d_ff + row] = u[b];
+                a.coef[(size_t)b * a.d_ff + row] = c[b];
         }
     }
     if (act) {
-        load_row<NK>(w, a.Wg + (size_t)row * a.d_model, a.d_model, lane);
+        load_row<NK>(w, second + (size_t)row * a.d_model, a.d_model, lane);
         zero_acc(acc);
-            tok.dot(w, lane, acc);
+        tok.dot(w, lane, acc);
 #pragma unroll
         for (int b = 0; b < B; ++b) {
-            const float g = wave_sum(acc[b]);
+            const float p = wave_sum(acc[b]);
             if (b < a.nb && lane == 0)
-                a.s[(size_t)b * a.d_ff + row] = u[b] * silu(g);
+                a.s[(size_t)b * a.d_ff + row] = CATS ? p * c[b] : c[b] * silu(p);
         }
     }
     if (lane == 0)
@@ -1324,20 +1330,22 @@ __global__ __launch_bounds__(kTopkThreads) void k_topk_select(const float *__res
     }
 }
 
-// s = u * SiLU(g) of one active M-CountDown neuron: its W_gate row, u from the
-// dense coefficients
-template <int B, int NK, bool XREG>
+// s of one active neuron of a single-projection variant from its second row
+// (W_gate for M-CountDown: s = u * SiLU(g); W_up for CATS: s = u * h), the
+// first factor from the dense coefficients
+template <int B, int NK, bool XREG, bool CATS>
 __device__ __forceinline__ void mono_finish(const CoefArgs &a, const Tokens<B, NK, XREG> &tok,
-                                            const u32x4 (&wg)[NK], int row, int lane)
+                                            const u32x4 (&w2)[NK], int row, int lane)
 {
     float ag[B];
     zero_acc(ag);
-    tok.dot(wg, lane, ag);
+    tok.dot(w2, lane, ag);
 #pragma unroll
     for (int b = 0; b < B; ++b) {
-        const float g = wave_sum(ag[b]);
+        const float p = wave_sum(ag[b]);
+        const float c = a.coef[(size_t)b * a.d_ff + row];
         if (b < a.nb && lane == 0)
-            a.s[(size_t)b * a.d_ff + row] = a.coef[(size_t)b * a.d_ff + row] * silu(g);
+            a.s[(size_t)b * a.d_ff + row] = CATS ? p * c : c * silu(p);
     }
 }
 
@@ -1386,9 +1394,10 @@ __global__ __launch_bounds__(kBlock) void k_gather_topk(const CoefArgs a, const 
             mm &= mm - 1;
         for (int r = pred_next(mm); r >= 0; r = pred_next(mm)) {
             u32x4 wg[NK];
-            load_row<NK>(wg, a.Wg + (size_t)(r0 + r) * a.d_model, a.d_model, lane);
-            if constexpr (VARIANT == kMono) {
-                mono_finish<B, NK, XREG>(a, tok, wg, r0 + r, lane);
+            const uint16_t *w2 = VARIANT == kCats ? a.Wu : a.Wg;
+            load_row<NK>(wg, w2 + (size_t)(r0 + r) * a.d_model, a.d_model, lane);
+            if constexpr (VARIANT == kMono || VARIANT == kCats) {
+                mono_finish<B, NK, XREG, VARIANT == kCats>(a, tok, wg, r0 + r, lane);
             } else {
                 u32x4 wu[NK];
                 load_row<NK>(wu, a.Wu + (size_t)(r0 + r) * a.d_model, a.d_model, lane);
@@ -1427,7 +1436,8 @@ __global__ __launch_bounds__(kBlock) void k_gather_topk_w(const CoefArgs a, cons
             a.s[(size_t)lane * a.d_ff + row] = cb;  // s itself is the coefficient
     } else {
         u32x4 wg[NK];
-        load_row<NK>(wg, a.Wg + (size_t)row * a.d_model, a.d_model, lane);
+        load_row<NK>(wg, (VARIANT == kCats ? a.Wu : a.Wg) + (size_t)row * a.d_model, a.d_model,
+                     lane);
         u32x4 wu[VARIANT == kDualPred ? NK : 1];
         if constexpr (VARIANT == kDualPred)
             load_row<NK>(wu, a.Wu + (size_t)row * a.d_model, a.d_model, lane);
@@ -1450,11 +1460,11 @@ __global__ __launch_bounds__(kBlock) void k_gather_topk_w(const CoefArgs a, cons
             tok.dot(wg, lane, ag);
 #pragma unroll
             for (int b = 0; b < B; ++b) {
-                const float g = wave_sum(ag[b]);
-                const float u = __builtin_bit_cast(
+                const float p = wave_sum(ag[b]);
+                const float cv = __builtin_bit_cast(
                     float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, cb), b));
-                if (b < a.nb && lane == 0)
-                    a.s[(size_t)b * a.d_ff + row] = u * silu(g);
+                if (b < a.nb && lane == 0)  // M: u * SiLU(g); CATS: u * h
+                    a.s[(size_t)b * a.d_ff + row] = VARIANT == kCats ? p * cv : cv * silu(p);
             }
         }
     }
@@ -1555,8 +1565,12 @@ static hipError_t coef_bn(int variant, const CoefArgs &a, hipStream_t s)
     const int grid = (a.d_ff + kWavesPerBlock - 1) / kWavesPerBlock;
     switch (variant) {
     case kMono:
-        allow_lds(k_coef_mono<B, NK, XREG>, lds);
-        k_coef_mono<B, NK, XREG><<<grid, kBlock, lds, s>>>(a);
+        allow_lds(k_coef_mono<B, NK, XREG, false>, lds);
+        k_coef_mono<B, NK, XREG, false><<<grid, kBlock, lds, s>>>(a);
+        break;
+    case kCats:
+        allow_lds(k_coef_mono<B, NK, XREG, true>, lds);
+        k_coef_mono<B, NK, XREG, true><<<grid, kBlock, lds, s>>>(a);
         break;
     case kDualIdeal:
         allow_lds(k_coef_dual<B, NK, XREG, false>, lds);
@@ -1697,6 +1711,7 @@ static hipError_t gather_topk_bn(int variant, const CoefArgs &a, const double *q
         const int wgrid = (a.d_ff + kWavesPerBlock - 1) / kWavesPerBlock;
         switch (variant) {
         case kMono: k_gather_topk_w<B, NK, kMono><<<wgrid, kBlock, 0, s>>>(a, q); break;
+        case kCats: k_gather_topk_w<B, NK, kCats><<<wgrid, kBlock, 0, s>>>(a, q); break;
         case kDualIdeal: k_gather_topk_w<B, NK, kDualIdeal><<<wgrid, kBlock, 0, s>>>(a, q); break;
         case kDualPred: k_gather_topk_w<B, NK, kDualPred><<<wgrid, kBlock, 0, s>>>(a, q); break;
         default: return hipErrorInvalidValue;
@@ -1708,6 +1723,10 @@ static hipError_t gather_topk_bn(int variant, const CoefArgs &a, const double *q
         case kMono:
             allow_lds(k_gather_topk<B, NK, XREG, kMono>, lds);
             k_gather_topk<B, NK, XREG, kMono><<<grid, kBlock, lds, s>>>(a, q);
+            break;
+        case kCats:
+            allow_lds(k_gather_topk<B, NK, XREG, kCats>, lds);
+            k_gather_topk<B, NK, XREG, kCats><<<grid, kBlock, lds, s>>>(a, q);
             break;
         case kDualIdeal:
             k_gather_topk<B, NK, XREG, kDualIdeal><<<grid, kBlock, 0, s>>>(a, q);
@@ -1765,8 +1784,12 @@ hipError_t launch_export(const int *act, const float *s_rows, int nb, int d_ff, 
 hipError_t launch_select(const float *coef, int ld, int n, int T, int use_abs, double k,
                          double *q_out, hipStream_t s)
 {
-    allow_lds(k_select_quantile, (size_t)n * 4);
-    k_select_quantile<<<T, kSelThreads, (size_t)n * 4, s>>>(coef, ld, n, use_abs, k, q_out);
+    if (n <= kTopkThreads * kTopkPerThread) {  // keys fit in registers: the faster select
+        k_topk_select<<<T, kTopkThreads, 0, s>>>(coef, ld, n, use_abs, k, q_out);
+    } else {
+        allow_lds(k_select_quantile, (size_t)n * 4);
+        k_select_quantile<<<T, kSelThreads, (size_t)n * 4, s>>>(coef, ld, n, use_abs, k, q_out);
+    }
     return hipGetLastError();
 }
 

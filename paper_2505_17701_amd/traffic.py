@@ -71,7 +71,7 @@ def algorithmic_bytes(variant: str, d_model: int, d_ff: int, n_active: int, B: i
     row = BF16 * d_model
     x = BF16 * B * d_model
     y = F32 * B * d_model
-    if variant == "mono":
+    if variant in ("mono", "cats"):  # one dense projection, the other gathered
         k = {"coef": d_ff * row + n_active * row + x, "down": n_active * row + y}
     elif variant == "dual_ideal":
         k = {"coef": 2 * d_ff * row + x, "down": n_active * row + y}
@@ -93,6 +93,7 @@ def algorithmic_flops(variant: str, d_model: int, d_ff: int, n_active: int, B: i
     """Multiply-adds x 2 of one call (activation and threshold work not counted)."""
     mac = {
         "mono": d_ff * d_model + 2 * n_active * d_model,
+        "cats": d_ff * d_model + 2 * n_active * d_model,
         "dual_ideal": 2 * d_ff * d_model + n_active * d_model,
         "dense": 3 * d_ff * d_model,
         "dual_pred": d_rank * d_model + d_ff * d_rank + 3 * n_active * d_model,

@@ -63,6 +63,8 @@ def run_gpu(plan, variant, layer, x, thld):
                                   A_t=D["A_t"], B_t=D["B_t"])
     elif variant == "dense":
         y = cd.countdown_ffn_dense(plan, xd, D["W_gate"], D["W_up"], D["W_down"])
+    elif variant == "cats":
+        y = cd.countdown_ffn_cats(plan, xd, D["W_gate"], D["W_up"], D["W_down"], thld)
     else:
         raise ValueError(variant)
     idx, s_c, coef = cd.countdown_export_active(plan)
@@ -82,6 +84,8 @@ def run_oracle(variant, layer, x, thld):
     if variant == "dense":
         idx = np.arange(layer.d_ff, dtype=np.int32)
         return idx, oracle.dense(x, H["W_gate"], H["W_up"], H["W_down"]), None
+    if variant == "cats":
+        return oracle.ffn_cats(x, H["W_gate"], H["W_up"], H["W_down"], thld, want_coef=True)
     raise ValueError(variant)
 
 
@@ -120,6 +124,9 @@ def check_call(variant, layer, x, thld, gpu_out, label, check_coef=True):
                 g / (1.0 + np.exp(-g))
             bound = COEF_TOL * (dot_bound(xf, f64(H["W_up"])) * np.abs(su)
                                 + np.abs(u) * dot_bound(xf, f64(H["W_gate"])))
+        elif variant == "cats":
+            # h = SiLU(g): |dh| <= max|SiLU'| |dg|, max|SiLU'| < 1.1
+            bound = COEF_TOL * 1.1 * dot_bound(xf, f64(H["W_gate"]))
         else:
             lat = oracle.predictor(x, H["A_t"], H["B_t"])[0]
             bound = COEF_TOL * (np.abs(lat) @ np.abs(f64(H["B_t"])).T
@@ -151,7 +158,7 @@ def tiny():
     return w, Layer(w.layer())
 
 
-@pytest.mark.parametrize("variant", ["mono", "dual_ideal"])
+@pytest.mark.parametrize("variant", ["mono", "dual_ideal", "cats"])
 def test_tiny_parity_calibrated(tiny, variant):
     w, layer = tiny
     thld = calibrated(variant, layer, w.wid, 0.9, T=64)
@@ -162,7 +169,7 @@ def test_tiny_parity_calibrated(tiny, variant):
         assert 20 < n < 140
 
 
-@pytest.mark.parametrize("variant", ["mono", "dual_ideal"])
+@pytest.mark.parametrize("variant", ["mono", "dual_ideal", "cats"])
 @pytest.mark.parametrize("B", [2, 3, 5, 8])
 def test_tiny_batch_union(tiny, variant, B):
     w, layer = tiny
@@ -173,7 +180,7 @@ def test_tiny_batch_union(tiny, variant, B):
     assert n > 69
 
 
-@pytest.mark.parametrize("variant", ["mono", "dual_ideal"])
+@pytest.mark.parametrize("variant", ["mono", "dual_ideal", "cats"])
 def test_all_rows_equals_dense_and_none_gives_zero(tiny, variant):
     w, layer = tiny
     plan = plan_for(layer, max_batch=2)
@@ -208,7 +215,7 @@ def test_single_active_row(tiny):
 @pytest.mark.parametrize("d_model,d_ff,B", [(264, 1000, 3), (1032, 520, 2), (8, 8, 1),
                                             (2056, 4104, 7), (512, 16, 4), (8192, 1048, 1),
                                             (1544, 2056, 2), (4096, 776, 1)])
-@pytest.mark.parametrize("variant", ["mono", "dual_ideal", "dual_pred"])
+@pytest.mark.parametrize("variant", ["mono", "dual_ideal", "dual_pred", "cats"])
 def test_ragged_shapes(d_model, d_ff, B, variant):
     L = make_layer(700 + d_model, d_model, d_ff, 0.05)
     P = make_predictor(700 + d_model, d_model, 16, d_ff, 0.05) if variant == "dual_pred" else None
@@ -218,7 +225,7 @@ def test_ragged_shapes(d_model, d_ff, B, variant):
         c = oracle.predictor(x, P["A_t"], P["B_t"])[1]
     else:
         u, g, s = oracle.coefficients(x, L["W_gate"], L["W_up"])
-        c = np.abs(u if variant == "mono" else s)
+        c = np.abs({"mono": u, "dual_ideal": s, "cats": g / (1.0 + np.exp(-g))}[variant])
     thld = float(np.float32(np.quantile(c, 0.7)))
     plan = plan_for(layer, max_batch=min(8, 32768 // d_model))
     compare(plan, variant, layer, x, thld, f"ragged {d_model}x{d_ff} B={B} {variant}")
@@ -303,7 +310,7 @@ def test_bad_calls_raise(tiny):
 
 # ------------------------------------------------------------- calibration
 
-@pytest.mark.parametrize("variant", ["mono", "dual_ideal", "dual_pred"])
+@pytest.mark.parametrize("variant", ["mono", "dual_ideal", "dual_pred", "cats"])
 def test_calibration_matches_oracle(variant):
     from paper_2505_17701_amd import binding as cd
 
@@ -316,7 +323,7 @@ def test_calibration_matches_oracle(variant):
                                 A_t=P and P["A_t"], B_t=P and P["B_t"])
     plan = cd.Plan(dm, dff, 8, layer.d_rank, keep_coef=True)
     v = {"mono": cd.CD_VARIANT_MONO, "dual_ideal": cd.CD_VARIANT_DUAL_IDEAL,
-         "dual_pred": cd.CD_VARIANT_DUAL_PRED}[variant]
+         "dual_pred": cd.CD_VARIANT_DUAL_PRED, "cats": cd.CD_VARIANT_CATS}[variant]
     D = layer.d
     thld, q = cd.countdown_calibrate(plan, v, dev_bf16(X), 0.9, W_gate=D["W_gate"], W_up=D["W_up"],
                                      A_t=D.get("A_t"), B_t=D.get("B_t"))

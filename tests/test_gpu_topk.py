@@ -17,7 +17,7 @@ from workloads import WORKLOADS, make_layer, make_predictor, make_tokens
 torch = pytest.importorskip("torch")
 pytestmark = pytest.mark.gpu
 
-VID = {"mono": 0, "dual_ideal": 1, "dual_pred": 2}
+VID = {"mono": 0, "dual_ideal": 1, "dual_pred": 2, "cats": 4}
 Q_TOL = 1e-5  # relative to max(|q|, rms(c)): fp32 coefficients against fp64
 
 
@@ -31,8 +31,8 @@ def oracle_coef(variant, layer, x):
     H = layer.h
     if variant == "dual_pred":
         return oracle.predictor(x, H["A_t"], H["B_t"])[1]
-    u, _, s = oracle.coefficients(x, H["W_gate"], H["W_up"])
-    return np.abs(u if variant == "mono" else s)
+    u, g, s = oracle.coefficients(x, H["W_gate"], H["W_up"])
+    return np.abs({"mono": u, "dual_ideal": s, "cats": g / (1.0 + np.exp(-g))}[variant])
 
 
 def run_topk(variant, layer, x, k):
@@ -83,7 +83,7 @@ def small(variant, dm, dff, seed):
     return Layer(L, P)
 
 
-@pytest.mark.parametrize("variant", ["mono", "dual_ideal", "dual_pred"])
+@pytest.mark.parametrize("variant", ["mono", "dual_ideal", "dual_pred", "cats"])
 @pytest.mark.parametrize("shape", [(256, 688, 1, 0.9), (1032, 1000, 3, 0.75), (4096, 1376, 2, 0.5),
                                    (2048, 776, 8, 0.9), (264, 16, 1, 0.5)])
 def test_topk_small(variant, shape):
@@ -144,3 +144,30 @@ def test_topk_rejects():
     Lb = Layer(make_layer(1501, 256, 32776, 0.03))
     with pytest.raises(cd.CountdownError):
         cd.countdown_ffn_topk(big, 0, x, Lb.d["W_gate"], Lb.d["W_up"], Lb.d["W_down"], 0.9)
+
+
+def test_cif_caf_masks_match_oracle():
+    """The masks behind CIF / CAF (per-token |s|, |u|, |h| quantile sets) from the GPU
+    equal the oracle's up to neurons at their token's threshold; the metrics agree."""
+    from paper_2505_17701_amd.metrics import cif_caf, masks_on_gpu
+
+    w = WORKLOADS["tiny_256x688"]
+    layer = Layer(w.layer())
+    X = w.tokens(8)
+    k = 0.7
+    S, U, H = masks_on_gpu(layer.d, dev_bf16(X), k)
+    ref = []
+    for variant in ("dual_ideal", "mono", "cats"):
+        m = np.zeros((8, w.d_ff), dtype=bool)
+        for t in range(8):
+            idx, _, _ = oracle.ffn_topk(variant, X[t:t + 1], layer.h["W_gate"], layer.h["W_up"],
+                                        layer.h["W_down"], k)
+            m[t, idx] = True
+        ref.append(m)
+    for got, want, name in zip((S, U, H), ref, "SUH"):
+        mism = np.count_nonzero(got != want)
+        assert mism <= 2, f"mask {name}: {mism} differences"
+    a, b = cif_caf(S, U, H), cif_caf(*ref)
+    for key in a:
+        assert abs(a[key] - b[key]) <= 2e-3, (key, a[key], b[key])
+    print({k2: round(v, 3) for k2, v in a.items()}, flush=True)

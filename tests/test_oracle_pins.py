@@ -489,3 +489,37 @@ def test_topk_identical_tokens_and_extremes():
     assert len(idx) == 0 and not y.any()          # nothing exceeds the maximum
     idx, _, _ = oracle.ffn_topk("mono", x, L["W_gate"], L["W_up"], L["W_down"], 0.0)
     assert len(idx) == w.d_ff - 1                 # everything but the minimum
+
+
+# ------------------------------------------------------ CATS coefficient (Eq. 6a)
+
+@pytest.mark.parametrize("B", [1, 3])
+def test_cats_matches_brute_force(B):
+    """CATS keeps {i : |SiLU(x.W_gate)[i]| > thld} (union over the batch)."""
+    dm, dff = 8, 16
+    L = make_layer(970, dm, dff, 0.5)
+    x = make_tokens(970, B, dm)
+    X, G, U, D = (f64(a).tolist() for a in (x, L["W_gate"], L["W_up"], L["W_down"]))
+
+    def dot(a, b):
+        t = 0.0
+        for p, q in zip(a, b):
+            t += p * q
+        return t
+
+    def silu(z):
+        return z / (1.0 + math.exp(-z)) if z >= 0 else z * math.exp(z) / (1.0 + math.exp(z))
+
+    h = [[silu(dot(X[b], G[i])) for i in range(dff)] for b in range(B)]
+    u = [[dot(X[b], U[i]) for i in range(dff)] for b in range(B)]
+    thld = float(np.float32(np.quantile(np.abs(h[0]), 0.6)))
+    idx_b = [i for i in range(dff) if any(abs(h[b][i]) > thld for b in range(B))]
+    y_b = [[sum(u[b][i] * h[b][i] * D[i][j] for i in idx_b) for j in range(dm)] for b in range(B)]
+    idx, y, hc = oracle.ffn_cats(x, L["W_gate"], L["W_up"], L["W_down"], thld, want_coef=True)
+    np.testing.assert_array_equal(idx, idx_b)
+    np.testing.assert_allclose(y, np.array(y_b), rtol=1e-12, atol=1e-13)
+    np.testing.assert_allclose(hc, np.array(h), rtol=1e-14, atol=0)
+    # CATS through the per-token path with the CATS coefficient
+    idx_t, _, q = oracle.ffn_topk("cats", x, L["W_gate"], L["W_up"], L["W_down"], 0.5)
+    for b in range(B):
+        assert q[b] == np.quantile(np.abs(h[b]), 0.5)

@@ -2,6 +2,7 @@
 import json
 import os
 
+import numpy as np
 import pytest
 
 from paper_2505_17701_amd import traffic
@@ -46,3 +47,34 @@ def test_algorithmic_bytes_hand_counts():
     p = traffic.algorithmic_bytes("dual_pred", 4096, 14336, 1434, B=1, d_rank=256)
     assert abs(p["total"] / 1e6 - 44.7) < 0.2
     assert traffic.algorithmic_flops("dense", dm, dff, dff) == 6 * dm * dff
+
+
+def test_cif_caf_closed_form():
+    """Masks small enough to count by hand (sparsity-analysis metrics of Sec. 6)."""
+    from paper_2505_17701_amd.metrics import cif_caf
+
+    S = [[1, 1, 1, 0, 0, 0]]
+    U = [[1, 0, 1, 1, 0, 0]]
+    H = [[0, 1, 0, 1, 1, 0]]
+    m = cif_caf(S, U, H)
+    # alive: S = {0,1,2}; ~H there = {0,2}; of those U keeps {0,2}
+    assert m["CIF(u,alive)"] == 2 / 3 and m["CAF(u,alive)"] == 2 / 3
+    # h: ~U on S = {1}; H keeps 1
+    assert m["CIF(h,alive)"] == 1 / 3 and m["CAF(h,alive)"] == 1 / 3
+    # dead: ~S = {3,4,5}; H there = {3,4}; ~U of those = {4}
+    assert m["CIF(u,dead)"] == 2 / 3 and m["CAF(u,dead)"] == 1 / 3
+    # h dead: U on ~S = {3}; ~H of those = {} -> 0
+    assert m["CIF(h,dead)"] == 1 / 3 and m["CAF(h,dead)"] == 0.0
+
+
+def test_cif_caf_pools_tokens():
+    from paper_2505_17701_amd.metrics import cif_caf
+
+    rng = np.random.default_rng(0)
+    S, U, H = (rng.random((5, 40)) < 0.3 for _ in range(3))
+    pooled = cif_caf(S, U, H)
+    assert pooled["CIF(u,alive)"] == (S & ~H).sum() / S.sum()
+    # u and h exchange roles exactly
+    swapped = cif_caf(S, H, U)
+    assert swapped["CIF(u,alive)"] == pooled["CIF(h,alive)"]
+    assert swapped["CAF(h,dead)"] == pooled["CAF(u,dead)"]
