@@ -63,6 +63,7 @@ def parse():
     p.add_argument("--no-other", action="store_true",
                    help="skip the 8B-predictor, 70B and 32-layer stack workloads")
     p.add_argument("--no-stack", action="store_true", help="skip the 32-layer stack")
+    p.add_argument("--no-train", action="store_true", help="skip the predictor-training run")
     p.add_argument("--traffic-probe", action="store_true",
                    help="first copy a 256 MiB device buffer 3 times (the known-size reference "
                         "for FETCH_SIZE / WRITE_SIZE counters)")
@@ -335,6 +336,54 @@ def other_workloads(args):
     return out
 
 
+def predictor_training_bench(args, n_train=8192, n_test=256, epochs=4):
+    """Alg. 1 on the Llama-3-8B-shaped layer (d_rank 256): targets S^k from the HIP
+    per-token ideal-D path, BCE + AdamW (lr 1e-3, batch 16) in PyTorch, then the
+    predictor through the HIP predictor path, before and after training, at its
+    Sec. 4 threshold calibrated at k and at thld 0. Weights and tokens are seeded
+    random: a random W_gate has a flat spectrum, so a rank-256 predictor can only
+    capture a small part of the targets, and F1 shows learning against the
+    untrained start, not the paper's F1 values."""
+    import torch
+
+    from paper_2505_17701_amd.predictor import (calibrated_threshold, f1_score, ideal_masks,
+                                                 predicted_masks, train_low_rank)
+    from workloads import WORKLOADS
+    from workloads.synth import T_CALIB
+
+    w = WORKLOADS["llama3_8b_4096x14336_pred"]
+    L = {kk: dev_bf16(v) for kk, v in w.layer().items()}
+    Xtr = dev_bf16(w.tokens(n_train, purpose=T_CALIB))
+    Xte = dev_bf16(w.tokens(n_test))
+    out = {"d_rank": w.d_rank, "train_tokens": n_train, "test_tokens": n_test,
+           "epochs": epochs}
+    for k in (0.7, 0.9):
+        t = time.time()
+        Ytr = ideal_masks(L, Xtr, k)
+        Yte = ideal_masks(L, Xte, k)
+        t_mask = time.time() - t
+        A0, B0, _ = train_low_rank(Xtr, Ytr, w.d_rank, epochs=0)
+        A, B, tl = train_low_rank(Xtr, Ytr, w.d_rank, epochs=epochs)
+        ytrue = Yte.cpu().numpy()
+        r = {"target_alive_frac": round(float(ytrue.mean()), 4)}
+        for name, (At, Bt) in (("untrained", (A0, B0)), ("trained", (A, B))):
+            th = calibrated_threshold(At, Bt, Xtr[:256], k)
+            P = predicted_masks(L, At, Bt, Xte, th).cpu().numpy()
+            P_0 = predicted_masks(L, At, Bt, Xte, 0.0).cpu().numpy()
+            r[name] = {"thld": round(th, 5), "f1": round(f1_score(P, ytrue), 4),
+                       "alive_frac": round(float(P.mean()), 4),
+                       "f1_thld0": round(f1_score(P_0, ytrue), 4),
+                       "alive_frac_thld0": round(float(P_0.mean()), 4)}
+        r.update({"epoch_loss": [round(v, 5) for v in tl["epoch_loss"]],
+                  "train_seconds": round(tl["seconds"], 2), "mask_seconds": round(t_mask, 2)})
+        out[f"k={k}"] = r
+        log(f"[bench] predictor training k={k}: {json.dumps(out[f'k={k}'])}")
+        del A0, B0, A, B, Ytr, Yte
+    del L, Xtr, Xte
+    torch.cuda.empty_cache()
+    return out
+
+
 def stack_bench(args, steps_tokens=128, warmup_tokens=8):
     """The 32-layer stack of 7B-shaped predictor layers joined by the residual stream
     (h += y, x = bf16(RMSNorm(h))): per-layer thresholds calibrated at k on 256 seeded
@@ -517,6 +566,8 @@ def main():
         others = other_workloads(args)
         if not args.no_stack:
             others["stack32_llama7b_pred"] = stack_bench(args)
+        if not args.no_train:
+            others["predictor_training_llama3_8b"] = predictor_training_bench(args)
 
     # CPU baseline: the fp64 oracle on host cores, bounded sample of the same workload
     cpu = None

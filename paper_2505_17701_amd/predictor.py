@@ -1,0 +1,118 @@
+"""Training the low-rank predictor of practical D-CountDown (Sec. 4, Alg. 1).
+
+The target of token x is the ideal mask S^k = {i : |s[i]| > Quantile(k, |s|)}
+(the per-token form of Eq. 6c), produced here by the HIP per-token threshold
+path (countdown_ffn_topk with the ideal D coefficient). The predictor scores
+s_hat = x . theta_A . theta_B (rank d_rank) and is trained with binary cross
+entropy on the logits and AdamW, as in the paper's training table; at
+inference a neuron is predicted alive when s_hat > thld (0 for the trained
+logit). Training is plain PyTorch: only inference runs on the HIP kernels.
+
+Layout: the returned predictor is in the kernels' layout, A_t [d_rank][d_model]
+and B_t [d_ff][d_rank], bf16.
+"""
+from __future__ import annotations
+
+import time
+
+import numpy as np
+
+
+def ideal_masks(layer: dict, X, k: float):
+    """S^k of every token of X [T, d_model] (bf16, on the GPU) as a bool tensor [T, d_ff]."""
+    import torch
+
+    from . import binding as cd
+
+    T, dm = X.shape
+    dff = layer["W_up"].shape[0]
+    plan = cd.Plan(dm, dff, max_batch=1)
+    masks = torch.zeros((T, dff), dtype=torch.bool, device=X.device)
+    for t in range(T):
+        cd.countdown_ffn_topk(plan, cd.CD_VARIANT_DUAL_IDEAL, X[t:t + 1], layer["W_gate"],
+                              layer["W_up"], layer["W_down"], k)
+        idx, _, _ = cd.countdown_export_active(plan)
+        masks[t, idx.long()] = True
+    plan.close()
+    return masks
+
+
+def f1_score(pred, true) -> float:
+    """F1 of predicted against true alive masks (bool arrays of one shape), pooled."""
+    pred = np.asarray(pred, dtype=bool)
+    true = np.asarray(true, dtype=bool)
+    tp = np.count_nonzero(pred & true)
+    fp = np.count_nonzero(pred & ~true)
+    fn = np.count_nonzero(~pred & true)
+    return 2.0 * tp / (2.0 * tp + fp + fn) if tp + fp + fn else 1.0
+
+
+def train_low_rank(X, masks, d_rank: int, epochs: int = 10, lr: float = 1e-3, batch: int = 16,
+                   seed: int = 42, weight_decay: float = 0.01):
+    """Fit s_hat = x . theta_A . theta_B to the masks with BCE-with-logits and AdamW.
+
+    X: [N, d_model] bf16 tokens on the GPU; masks: [N, d_ff] bool. Returns
+    (A_t [d_rank, d_model] bf16, B_t [d_ff, d_rank] bf16, log dict)."""
+    import torch
+
+    g = torch.Generator(device=X.device).manual_seed(seed)
+    N, dm = X.shape
+    dff = masks.shape[1]
+    xf = X.float()
+    yf = masks.float()
+    theta_a = (torch.randn(dm, d_rank, generator=g, device=X.device) / dm ** 0.5).requires_grad_()
+    theta_b = (torch.randn(d_rank, dff, generator=g, device=X.device) / d_rank ** 0.5)
+    theta_b.requires_grad_()
+    opt = torch.optim.AdamW([theta_a, theta_b], lr=lr, weight_decay=weight_decay)
+    loss_fn = torch.nn.BCEWithLogitsLoss()
+    losses = []
+    t0 = time.time()
+    for _ in range(epochs):
+        perm = torch.randperm(N, generator=g, device=X.device)
+        tot, nb = 0.0, 0
+        for i in range(0, N, batch):
+            j = perm[i:i + batch]
+            logits = (xf[j] @ theta_a) @ theta_b
+            loss = loss_fn(logits, yf[j])
+            opt.zero_grad(set_to_none=True)
+            loss.backward()
+            opt.step()
+            tot += float(loss.detach())
+            nb += 1
+        losses.append(tot / nb)
+    torch.cuda.synchronize()
+    A_t = theta_a.detach().t().contiguous().to(torch.bfloat16)
+    B_t = theta_b.detach().t().contiguous().to(torch.bfloat16)
+    return A_t, B_t, {"epoch_loss": losses, "seconds": time.time() - t0}
+
+
+def calibrated_threshold(A_t, B_t, X, k: float) -> float:
+    """The Sec. 4 layerwise threshold of the predictor score s_hat at k over the
+    calibration tokens X (mean of the per-token k-quantiles of s_hat)."""
+    from . import binding as cd
+
+    dm = X.shape[1]
+    plan = cd.Plan(dm, B_t.shape[0], max_batch=max(1, min(8, 32768 // dm)), d_rank=A_t.shape[0])
+    th, _ = cd.countdown_calibrate(plan, cd.CD_VARIANT_DUAL_PRED, X, k, A_t=A_t, B_t=B_t)
+    plan.close()
+    return float(th.item())
+
+
+def predicted_masks(layer: dict, A_t, B_t, X, thld: float = 0.0):
+    """The predictor's alive masks {s_hat > thld} of every token of X, from the HIP
+    predictor path (countdown_ffn_dual with A_t / B_t) at batch 1."""
+    import torch
+
+    from . import binding as cd
+
+    T, dm = X.shape
+    dff = layer["W_up"].shape[0]
+    plan = cd.Plan(dm, dff, max_batch=1, d_rank=A_t.shape[0])
+    masks = torch.zeros((T, dff), dtype=torch.bool, device=X.device)
+    for t in range(T):
+        cd.countdown_ffn_dual(plan, X[t:t + 1], layer["W_gate"], layer["W_up"], layer["W_down"],
+                              thld, A_t=A_t, B_t=B_t)
+        idx, _, _ = cd.countdown_export_active(plan)
+        masks[t, idx.long()] = True
+    plan.close()
+    return masks

@@ -78,3 +78,15 @@ def test_cif_caf_pools_tokens():
     swapped = cif_caf(S, H, U)
     assert swapped["CIF(u,alive)"] == pooled["CIF(h,alive)"]
     assert swapped["CAF(h,dead)"] == pooled["CAF(u,dead)"]
+
+
+def test_f1_score_by_hand():
+    from paper_2505_17701_amd.predictor import f1_score
+
+    # tp 1, fp 1, fn 1 -> 2/(2+1+1)
+    assert f1_score([1, 1, 0, 0], [1, 0, 1, 0]) == 0.5
+    assert f1_score([1, 1, 0], [1, 1, 0]) == 1.0
+    assert f1_score([0, 0, 1], [1, 1, 0]) == 0.0
+    # pooled over tokens, not averaged per token
+    assert f1_score([[1, 0], [1, 1]], [[1, 0], [0, 0]]) == 2 * 1 / (2 * 1 + 2 + 0)
+    assert f1_score([[0, 0]], [[0, 0]]) == 1.0
