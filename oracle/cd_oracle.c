@@ -17,6 +17,9 @@
  *   Sec. 4 "Constructing SP^Prac": layerwise constant threshold
  *     tau_hat = (1/T) sum_t Quantile(k, |u^(t)|) and the low-rank predictor
  *     s_hat = x.theta_A.theta_B with predicted set {i : s_hat[i] > tau};
+ *   Sec. 6 "Possible Predictor Candidate: TernaryLinear" (Table 4): the
+ *     predictor score s_hat = x.theta with theta in {-1, 0, +1}, thresholded
+ *     like the low-rank score;
  *   Limitations section: batch > 1 takes the union of the index sets;
  *   the per-token form of Eq. (6): each token's threshold is the quantile of
  *   its own coefficients (cdo_ffn_topk).
@@ -26,7 +29,8 @@
  * gets, widened to double. All arithmetic is double. Sums run in ascending
  * index order. Matrices are neuron-major [d_ff][d_model] row-major (row i is
  * the weight vector of intermediate neuron i); the predictor is A_t
- * [d_rank][d_model] and B_t [d_ff][d_rank].
+ * [d_rank][d_model] and B_t [d_ff][d_rank]; the ternary predictor is int8
+ * theta_t [d_ff][d_model] (theta transposed, entries -1, 0, +1).
  *
  * Readings of points the paper leaves open (strict '>' of Eq. (6) rather
  * than the listings' '>=', linear-interpolation quantiles, mean of
@@ -48,7 +52,13 @@
 #define CDO_EINVAL (-1)
 #define CDO_ENOMEM (-2)
 
-enum { CDO_COEF_ABS_U = 0, CDO_COEF_ABS_S = 1, CDO_COEF_SHAT = 2, CDO_COEF_ABS_H = 3 };
+enum {
+    CDO_COEF_ABS_U = 0,
+    CDO_COEF_ABS_S = 1,
+    CDO_COEF_SHAT = 2,
+    CDO_COEF_ABS_H = 3,
+    CDO_COEF_TERN = 4
+};
 
 /* exact widening of a bf16 bit pattern */
 static double wide(uint16_t b)
@@ -167,6 +177,30 @@ int cdo_predictor(const uint16_t *x, int B, const uint16_t *A_t, const uint16_t 
         project_f64(l, B_t, d_ff, d_rank, shat + (int64_t)b * d_ff);
     }
     free(l);
+    return CDO_OK;
+}
+
+/* Sec. 6, TernaryLinear: s_hat_b[i] = sum_j x_b[j] theta[j][i], theta in {-1, 0, +1},
+ * given transposed as theta_t [d_ff][d_model]; shat [B][d_ff]. Entries outside
+ * {-1, 0, +1} are rejected. */
+int cdo_ternary_predictor(const uint16_t *x, int B, const int8_t *theta_t, int d_model, int d_ff,
+                          double *shat)
+{
+    if (!x || !theta_t || !shat || B < 1 || d_model < 1 || d_ff < 1)
+        return CDO_EINVAL;
+    for (int64_t e = 0; e < (int64_t)d_ff * d_model; e++)
+        if (theta_t[e] < -1 || theta_t[e] > 1)
+            return CDO_EINVAL;
+    for (int b = 0; b < B; b++) {
+        const uint16_t *xb = x + (int64_t)b * d_model;
+#pragma omp parallel for schedule(static)
+        for (int64_t i = 0; i < d_ff; i++) {
+            double t = 0.0;
+            for (int64_t j = 0; j < d_model; j++)
+                t += wide(xb[j]) * (double)theta_t[i * d_model + j];
+            shat[(int64_t)b * d_ff + i] = t;
+        }
+    }
     return CDO_OK;
 }
 
@@ -394,6 +428,35 @@ int64_t cdo_ffn_dual_pred(const uint16_t *x, int B, const uint16_t *W_gate,
     return rc < 0 ? rc : n;
 }
 
+/* D-CountDown with the ternary predictor (Sec. 6): IDX = {i : exists b,
+ * s_hat_b[i] > thld} with s_hat = x.theta (signed); gate and up only on IDX;
+ * y by Eq. (5). coef (optional) receives s_hat [B][d_ff]. */
+int64_t cdo_ffn_dual_tern(const uint16_t *x, int B, const uint16_t *W_gate,
+                          const uint16_t *W_up, const uint16_t *W_down, const int8_t *theta_t,
+                          int d_model, int d_ff, double thld, int32_t *idx, double *y,
+                          double *coef)
+{
+    if (!x || !W_gate || !W_up || !W_down || !theta_t || !y || !idx || B < 1 || d_model < 1 ||
+        d_ff < 1 || isnan(thld))
+        return CDO_EINVAL;
+    double *sh = (double *)malloc(sizeof(double) * (size_t)B * (size_t)d_ff);
+    if (!sh)
+        return CDO_ENOMEM;
+    int rc = cdo_ternary_predictor(x, B, theta_t, d_model, d_ff, sh);
+    if (rc < 0) {
+        free(sh);
+        return rc;
+    }
+    if (coef)
+        memcpy(coef, sh, sizeof(double) * (size_t)B * (size_t)d_ff);
+    int64_t n = cdo_select(sh, B, d_ff, 0, thld, idx);
+    free(sh);
+    if (n < 0)
+        return n;
+    rc = cdo_ffn_on_idx(x, B, W_gate, W_up, W_down, d_model, d_ff, idx, n, y, NULL);
+    return rc < 0 ? rc : n;
+}
+
 static int cmp_double(const void *a, const void *b)
 {
     double x = *(const double *)a, y = *(const double *)b;
@@ -423,14 +486,17 @@ double cdo_quantile_linear(double k, const double *v, int64_t n)
 }
 
 /* Per-token coefficient vector for calibration: |u| (M, Eq. 6b), |s| (D ideal,
- * Eq. 6c), s_hat signed (predictor, Sec. 4) or |h| = |SiLU(x.W_gate)| (CATS, Eq. 6a). */
+ * Eq. 6c), s_hat signed (low-rank predictor, Sec. 4; ternary predictor, Sec. 6)
+ * or |h| = |SiLU(x.W_gate)| (CATS, Eq. 6a). */
 static int token_coef(int kind, const uint16_t *x, const uint16_t *W_gate, const uint16_t *W_up,
-                      const uint16_t *A_t, const uint16_t *B_t, int d_model, int d_rank, int d_ff,
-                      double *c)
+                      const uint16_t *A_t, const uint16_t *B_t, const int8_t *theta_t,
+                      int d_model, int d_rank, int d_ff, double *c)
 {
     int rc;
     if (kind == CDO_COEF_SHAT)
         return cdo_predictor(x, 1, A_t, B_t, d_model, d_rank, d_ff, NULL, c);
+    if (kind == CDO_COEF_TERN)
+        return cdo_ternary_predictor(x, 1, theta_t, d_model, d_ff, c);
     if (kind == CDO_COEF_ABS_U) {
         if (!W_up)
             return CDO_EINVAL;
@@ -459,7 +525,7 @@ static int token_coef(int kind, const uint16_t *x, const uint16_t *W_gate, const
  * order. Returns NAN on bad arguments. */
 double cdo_calibrate(int kind, const uint16_t *X, int T, const uint16_t *W_gate,
                      const uint16_t *W_up, const uint16_t *A_t, const uint16_t *B_t, int d_model,
-                     int d_rank, int d_ff, double k, double *q_out)
+                     int d_rank, int d_ff, double k, double *q_out, const int8_t *theta_t)
 {
     if (!X || T < 1 || d_model < 1 || d_ff < 1 || !(k >= 0.0 && k <= 1.0))
         return NAN;
@@ -468,8 +534,8 @@ double cdo_calibrate(int kind, const uint16_t *X, int T, const uint16_t *W_gate,
         return NAN;
     double sum = 0.0;
     for (int t = 0; t < T; t++) {
-        if (token_coef(kind, X + (int64_t)t * d_model, W_gate, W_up, A_t, B_t, d_model, d_rank,
-                       d_ff, c) < 0) {
+        if (token_coef(kind, X + (int64_t)t * d_model, W_gate, W_up, A_t, B_t, theta_t, d_model,
+                       d_rank, d_ff, c) < 0) {
             free(c);
             return NAN;
         }
@@ -487,13 +553,13 @@ double cdo_calibrate(int kind, const uint16_t *X, int T, const uint16_t *W_gate,
  * sparsity definition, Sec. 3; Sec. 4 replaces it by the calibrated mean):
  *   thld_b = Quantile(k, c_b),  IDX = {i : exists b, c_b[i] > thld_b},
  * c_b the variant's coefficient vector of token b (kind as in cdo_calibrate:
- * |u|, |s|, signed s_hat or |h|), union over the batch; y by Eq. (5) over IDX
+ * |u|, |s|, signed s_hat of either predictor, or |h|), union over the batch; y by Eq. (5) over IDX
  * with the dense-equivalent s. q_out (optional) receives the B thresholds.
  * Returns |IDX| or a negative status. */
 int64_t cdo_ffn_topk(int kind, const uint16_t *x, int B, const uint16_t *W_gate,
                      const uint16_t *W_up, const uint16_t *W_down, const uint16_t *A_t,
                      const uint16_t *B_t, int d_model, int d_rank, int d_ff, double k,
-                     int32_t *idx, double *y, double *q_out)
+                     int32_t *idx, double *y, double *q_out, const int8_t *theta_t)
 {
     if (!x || !W_gate || !W_up || !W_down || !idx || !y || B < 1 || d_model < 1 || d_ff < 1 ||
         !(k >= 0.0 && k <= 1.0))
@@ -507,8 +573,8 @@ int64_t cdo_ffn_topk(int kind, const uint16_t *x, int B, const uint16_t *W_gate,
     }
     for (int b = 0; b < B; b++) {
         double *cb = c + (int64_t)b * d_ff;
-        int rc = token_coef(kind, x + (int64_t)b * d_model, W_gate, W_up, A_t, B_t, d_model,
-                            d_rank, d_ff, cb);
+        int rc = token_coef(kind, x + (int64_t)b * d_model, W_gate, W_up, A_t, B_t, theta_t,
+                            d_model, d_rank, d_ff, cb);
         if (rc < 0) {
             free(c);
             free(q);

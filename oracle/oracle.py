@@ -17,15 +17,17 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 SRC = os.path.join(HERE, "cd_oracle.c")
 LIB = os.path.join(HERE, "libcdoracle.so")
 
-COEF_ABS_U, COEF_ABS_S, COEF_SHAT, COEF_ABS_H = 0, 1, 2, 3
-KIND = {"mono": COEF_ABS_U, "dual_ideal": COEF_ABS_S, "dual_pred": COEF_SHAT, "cats": COEF_ABS_H}
+COEF_ABS_U, COEF_ABS_S, COEF_SHAT, COEF_ABS_H, COEF_TERN = 0, 1, 2, 3, 4
+KIND = {"mono": COEF_ABS_U, "dual_ideal": COEF_ABS_S, "dual_pred": COEF_SHAT, "cats": COEF_ABS_H,
+        "dual_tern": COEF_TERN}
 
 _lib = None
 
 __all__ = [
     "build", "load", "num_threads", "silu", "coefficients", "predictor", "select", "combine",
     "dense", "ffn_on_idx", "ffn_mono", "ffn_dual_ideal", "ffn_dual_pred", "quantile_linear",
-    "calibrate", "ffn_topk", "ffn_cats", "residual_rmsnorm", "KIND",
+    "calibrate", "ffn_topk", "ffn_cats", "residual_rmsnorm", "ternary_predictor",
+    "ffn_dual_tern", "KIND",
 ]
 
 
@@ -49,6 +51,7 @@ def load():
         u16p = np.ctypeslib.ndpointer(np.uint16, flags="C_CONTIGUOUS")
         f64p = np.ctypeslib.ndpointer(np.float64, flags="C_CONTIGUOUS")
         i32p = np.ctypeslib.ndpointer(np.int32, flags="C_CONTIGUOUS")
+        i8p = np.ctypeslib.ndpointer(np.int8, flags="C_CONTIGUOUS")
         vp = C.c_void_p
         lib.cdo_num_threads.restype = C.c_int
         lib.cdo_silu.restype = C.c_double
@@ -78,11 +81,16 @@ def load():
         lib.cdo_quantile_linear.restype = C.c_double
         lib.cdo_quantile_linear.argtypes = [C.c_double, f64p, C.c_int64]
         lib.cdo_calibrate.restype = C.c_double
+        lib.cdo_ternary_predictor.restype = C.c_int
+        lib.cdo_ternary_predictor.argtypes = [u16p, C.c_int, i8p, C.c_int, C.c_int, f64p]
+        lib.cdo_ffn_dual_tern.restype = C.c_int64
+        lib.cdo_ffn_dual_tern.argtypes = [u16p, C.c_int, u16p, u16p, u16p, i8p, C.c_int, C.c_int,
+                                          C.c_double, i32p, f64p, vp]
         lib.cdo_calibrate.argtypes = [C.c_int, u16p, C.c_int, vp, vp, vp, vp, C.c_int, C.c_int,
-                                      C.c_int, C.c_double, vp]
+                                      C.c_int, C.c_double, vp, vp]
         lib.cdo_ffn_topk.restype = C.c_int64
         lib.cdo_ffn_topk.argtypes = [C.c_int, u16p, C.c_int, u16p, u16p, u16p, vp, vp, C.c_int,
-                                     C.c_int, C.c_int, C.c_double, i32p, f64p, f64p]
+                                     C.c_int, C.c_int, C.c_double, i32p, f64p, f64p, vp]
         lib.cdo_residual_rmsnorm.restype = C.c_int
         lib.cdo_residual_rmsnorm.argtypes = [f64p, vp, C.c_int, C.c_double, f64p]
         _lib = lib
@@ -224,33 +232,69 @@ def ffn_dual_pred(x, W_gate, W_up, W_down, A_t, B_t, thld, want_coef=False):
     return idx[:n].copy(), y, coef
 
 
+def _tern(theta_t) -> np.ndarray:
+    t = np.ascontiguousarray(theta_t)
+    if t.dtype != np.int8:
+        raise TypeError("theta_t must be int8 (-1, 0, +1)")
+    return t
+
+
+def ternary_predictor(x, theta_t):
+    """The TernaryLinear score of Sec. 6: ``s_hat = x . theta`` (``theta_t`` = theta
+    transposed, int8 ``[d_ff, d_model]``); returns ``[B, d_ff]`` float64."""
+    x = _tok(x)
+    t = _tern(theta_t)
+    B, dm = x.shape
+    out = np.empty((B, t.shape[0]))
+    _check(load().cdo_ternary_predictor(x, B, t, dm, t.shape[0], out), "ternary_predictor")
+    return out
+
+
+def ffn_dual_tern(x, W_gate, W_up, W_down, theta_t, thld, want_coef=False):
+    """D-CountDown with the ternary predictor (Sec. 6): returns ``(IDX, y, shat or None)``."""
+    x = _tok(x)
+    t = _tern(theta_t)
+    B, dm = x.shape
+    dff = t.shape[0]
+    idx = np.empty(dff, dtype=np.int32)
+    y = np.empty((B, dm))
+    coef = np.empty((B, dff)) if want_coef else None
+    n = _check(load().cdo_ffn_dual_tern(x, B, _u16(W_gate), _u16(W_up), _u16(W_down), t, dm, dff,
+                                        float(thld), idx, y, _ptr(coef)), "ffn_dual_tern")
+    return idx[:n].copy(), y, coef
+
+
 def quantile_linear(k: float, v) -> float:
     """``Quantile(k, v)`` with linear interpolation between order statistics."""
     v = np.ascontiguousarray(np.ravel(v), dtype=np.float64)
     return load().cdo_quantile_linear(float(k), v, len(v))
 
 
-def calibrate(variant: str, X, k: float, W_gate=None, W_up=None, A_t=None, B_t=None):
+def calibrate(variant: str, X, k: float, W_gate=None, W_up=None, A_t=None, B_t=None,
+              theta_t=None):
     """Sec. 4 calibration: mean over tokens of ``Quantile(k, c^(t))``.
 
     Returns ``(tau_hat as float64, per-token quantiles)``. ``variant`` is one
-    of ``mono`` (|u|), ``dual_ideal`` (|s|), ``dual_pred`` (signed s_hat), ``cats`` (|h|).
+    of ``mono`` (|u|), ``dual_ideal`` (|s|), ``dual_pred`` (signed s_hat),
+    ``dual_tern`` (signed ternary score, ``theta_t``), ``cats`` (|h|).
     """
     X = _tok(X)
     T, dm = X.shape
-    ref = W_up if W_up is not None else (W_gate if W_gate is not None else B_t)
-    dff = ref.shape[0]
+    refs = [a for a in (W_up, W_gate, B_t, theta_t) if a is not None]
+    dff = refs[0].shape[0]
     dr = A_t.shape[0] if A_t is not None else 0
     q = np.empty(T)
     keep = [None if a is None else _u16(a) for a in (W_gate, W_up, A_t, B_t)]
+    tt = None if theta_t is None else _tern(theta_t)
     t = load().cdo_calibrate(KIND[variant], X, T, *(_ptr(a) for a in keep), dm, dr, dff,
-                             float(k), _ptr(q))
+                             float(k), _ptr(q), _ptr(tt))
     if np.isnan(t):
         raise ValueError("oracle calibrate failed")
     return t, q
 
 
-def ffn_topk(variant: str, x, W_gate, W_up, W_down, k: float, A_t=None, B_t=None):
+def ffn_topk(variant: str, x, W_gate, W_up, W_down, k: float, A_t=None, B_t=None,
+             theta_t=None):
     """Per-token threshold (Eq. 6 with thld_b = Quantile(k, c_b) of each token's own
     coefficients, union over the batch): returns ``(IDX, y, per-token thresholds)``."""
     x = _tok(x)
@@ -260,10 +304,11 @@ def ffn_topk(variant: str, x, W_gate, W_up, W_down, k: float, A_t=None, B_t=None
     idx = np.empty(dff, dtype=np.int32)
     y = np.empty((B, dm))
     q = np.empty(B)
+    tt = None if theta_t is None else _tern(theta_t)
     n = _check(load().cdo_ffn_topk(KIND[variant], x, B, _u16(W_gate), _u16(W_up), _u16(W_down),
                                    _ptr(None if A_t is None else _u16(A_t)),
                                    _ptr(None if B_t is None else _u16(B_t)), dm, dr, dff,
-                                   float(k), idx, y, q), "ffn_topk")
+                                   float(k), idx, y, q, _ptr(tt)), "ffn_topk")
     return idx[:n].copy(), y, q
 
 

@@ -523,3 +523,108 @@ def test_cats_matches_brute_force(B):
     idx_t, _, q = oracle.ffn_topk("cats", x, L["W_gate"], L["W_up"], L["W_down"], 0.5)
     for b in range(B):
         assert q[b] == np.quantile(np.abs(h[b]), 0.5)
+
+
+# --------------------------------------- ternary predictor (Sec. 6, TernaryLinear)
+
+def _tern_small(B, seed=980, dm=8, dff=16):
+    from workloads import make_ternary
+
+    L = make_layer(seed, dm, dff, 0.5)
+    T = make_ternary(seed, dm, dff)
+    x = make_tokens(seed, B, dm)
+    return x, L, T
+
+
+@pytest.mark.parametrize("B", [1, 3])
+def test_ternary_matches_brute_force(B):
+    """s_hat = x . theta with theta in {-1, 0, +1}, then the predictor's signed
+    threshold and the gather, by pure-Python loops."""
+    x, L, T = _tern_small(B)
+    dm, dff = T.shape[1], T.shape[0]
+    X, G, U, D = (f64(a).tolist() for a in (x, L["W_gate"], L["W_up"], L["W_down"]))
+    th = T.tolist()  # theta_t[i][j] = theta[j][i]
+
+    def silu(z):
+        return z / (1.0 + math.exp(-z)) if z >= 0 else z * math.exp(z) / (1.0 + math.exp(z))
+
+    shat = []
+    for b in range(B):
+        row = []
+        for i in range(dff):
+            t = 0.0
+            for j in range(dm):
+                if th[i][j] == 1:
+                    t += X[b][j]
+                elif th[i][j] == -1:
+                    t -= X[b][j]
+            row.append(t)
+        shat.append(row)
+    thld = float(np.float32(np.quantile(shat[0], 0.6)))
+    idx_b = [i for i in range(dff) if any(shat[b][i] > thld for b in range(B))]
+    s = [[sum(X[b][j] * U[i][j] for j in range(dm)) * silu(sum(X[b][j] * G[i][j] for j in range(dm)))
+          for i in range(dff)] for b in range(B)]
+    y_b = [[sum(s[b][i] * D[i][j] for i in idx_b) for j in range(dm)] for b in range(B)]
+    idx, y, c = oracle.ffn_dual_tern(x, L["W_gate"], L["W_up"], L["W_down"], T, thld,
+                                     want_coef=True)
+    np.testing.assert_array_equal(idx, idx_b)
+    assert 0 < len(idx) < dff
+    np.testing.assert_array_equal(c, np.array(shat))
+    np.testing.assert_allclose(y, np.array(y_b), rtol=1e-12, atol=1e-13)
+
+
+def test_ternary_equals_low_rank_with_identity_and_theta():
+    """theta_A = I and theta_B = theta make the low-rank predictor the ternary one:
+    identical index sets, scores and outputs (the low-rank oracle is pinned above)."""
+    x, L, T = _tern_small(3, seed=981, dm=24, dff=40)
+    dm, dff = T.shape[1], T.shape[0]
+    A_t = bf16_round(np.eye(dm, dtype=np.float32))
+    B_t = bf16_round(T.astype(np.float32))          # [d_ff][d_rank = d_model]
+    sh_t = oracle.ternary_predictor(x, T)
+    _, sh_p = oracle.predictor(x, A_t, B_t)
+    np.testing.assert_array_equal(sh_t, sh_p)
+    thld = float(np.float32(np.median(sh_t)))
+    a = oracle.ffn_dual_tern(x, L["W_gate"], L["W_up"], L["W_down"], T, thld)
+    b = oracle.ffn_dual_pred(x, L["W_gate"], L["W_up"], L["W_down"], A_t, B_t, thld)
+    np.testing.assert_array_equal(a[0], b[0])
+    np.testing.assert_array_equal(a[1], b[1])
+
+
+def test_ternary_closed_forms():
+    x, L, _ = _tern_small(2, seed=982, dm=24, dff=40)
+    dm, dff = 24, 40
+    X = f64(x)
+    # one-hot theta columns: s_hat_i = x_{j(i)}; negated: -x_{j(i)}
+    T = np.zeros((dff, dm), dtype=np.int8)
+    cols = np.arange(dff) % dm
+    T[np.arange(dff), cols] = 1
+    np.testing.assert_array_equal(oracle.ternary_predictor(x, T), X[:, cols])
+    np.testing.assert_array_equal(oracle.ternary_predictor(x, -T), -X[:, cols])
+    # all +1: the sum of the token; all zero: 0, so thld 0 keeps nothing (strict)
+    ones = np.ones((dff, dm), dtype=np.int8)
+    np.testing.assert_allclose(oracle.ternary_predictor(x, ones),
+                               np.repeat(X.sum(axis=1, keepdims=True), dff, axis=1), rtol=1e-15)
+    zero = np.zeros((dff, dm), dtype=np.int8)
+    idx, y, _ = oracle.ffn_dual_tern(x, L["W_gate"], L["W_up"], L["W_down"], zero, 0.0)
+    assert len(idx) == 0 and not y.any()
+    with pytest.raises(ValueError):
+        bad = zero.copy()
+        bad[0, 0] = 2
+        oracle.ffn_dual_tern(x, L["W_gate"], L["W_up"], L["W_down"], bad, 0.0)
+
+
+def test_ternary_calibration_and_per_token_path():
+    """The ternary score through calibration (mean of per-token quantiles of the
+    signed score) and the per-token path, against numpy.quantile of brute-force scores."""
+    x, L, T = _tern_small(3, seed=983, dm=24, dff=40)
+    X = f64(x)
+    shat = X @ T.astype(np.float64).T
+    k = 0.7
+    qs = [np.quantile(shat[b], k) for b in range(3)]
+    tau, q = oracle.calibrate("dual_tern", x, k, theta_t=T)
+    np.testing.assert_allclose(q, qs, rtol=1e-14)
+    assert tau == pytest.approx(np.mean(qs), rel=1e-14)
+    idx, _, qo = oracle.ffn_topk("dual_tern", x, L["W_gate"], L["W_up"], L["W_down"], k, theta_t=T)
+    np.testing.assert_allclose(qo, qs, rtol=1e-14)
+    want = [i for i in range(40) if any(shat[b][i] > qs[b] for b in range(3))]
+    np.testing.assert_array_equal(idx, want)

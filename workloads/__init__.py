@@ -12,6 +12,7 @@ from .synth import (  # noqa: F401
     bf16_to_f32,
     make_layer,
     make_predictor,
+    make_ternary,
     make_tokens,
     outlier_channels,
     stream,

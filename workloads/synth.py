@@ -11,7 +11,9 @@ neuron-major, ``[d_ff, d_model]`` row-major, so row ``i`` is the contiguous
   linear combination of Eq. (5);
 * the low-rank predictor ``theta_A`` (``d_model x d_rank``) is stored as
   ``A_t [d_rank, d_model]`` and ``theta_B`` (``d_rank x d_inter``) as
-  ``B_t [d_ff, d_rank]`` (Sec. 4, "Constructing SP^Prac").
+  ``B_t [d_ff, d_rank]`` (Sec. 4, "Constructing SP^Prac");
+* the ternary predictor ``theta`` (``d_model x d_inter``, entries -1, 0, +1;
+  Sec. 6, TernaryLinear) as int8 ``theta_t [d_ff, d_model]``.
 
 bf16 tensors are carried as ``uint16`` bit patterns. Random streams come
 from numpy ``PCG64`` seeded by ``SeedSequence(42, spawn_key=...)`` (the
@@ -29,7 +31,7 @@ import numpy as np
 ROOT_SEED = 42
 
 # tensor ids inside a spawn key
-T_GATE, T_UP, T_DOWN, T_A, T_B = 0, 1, 2, 3, 4
+T_GATE, T_UP, T_DOWN, T_A, T_B, T_TERN = 0, 1, 2, 3, 4, 5
 T_CALIB, T_EVAL, T_OUTLIER, T_RESID = 10, 11, 12, 13
 
 
@@ -96,6 +98,20 @@ def make_predictor(wid: int, d_model: int, d_rank: int, d_ff: int, sigma: float,
     }
 
 
+def make_ternary(wid: int, d_model: int, d_ff: int, zero_frac: float = 1 / 3, layer: int = 0,
+                 copy: int = 0) -> np.ndarray:
+    """Seeded random ternary predictor ``theta_t [d_ff, d_model]`` int8: each entry is 0
+    with probability ``zero_frac``, else -1 or +1 with equal probability (about what an
+    absmean ternarisation of Gaussian weights gives at the default)."""
+    rng = stream(wid, layer, T_TERN, copy)
+    u = rng.random(size=(d_ff, d_model), dtype=np.float32)
+    half = np.float32((1.0 - zero_frac) / 2.0)
+    t = np.zeros((d_ff, d_model), dtype=np.int8)
+    t[u < half] = -1
+    t[u >= np.float32(1.0) - half] = 1
+    return t
+
+
 def outlier_channels(wid: int, d_model: int, frac: float) -> np.ndarray:
     """``round(frac * d_model)`` channel ids, drawn once per workload without replacement."""
     n = int(round(frac * d_model))
@@ -145,6 +161,9 @@ class Workload:
 
     def predictor(self, layer: int = 0, copy: int = 0):
         return make_predictor(self.wid, self.d_model, self.d_rank, self.d_ff, 0.02, layer, copy)
+
+    def ternary(self, layer: int = 0, copy: int = 0):
+        return make_ternary(self.wid, self.d_model, self.d_ff, layer=layer, copy=copy)
 
     def tokens(self, n: int, purpose: int = T_EVAL, layer: int = 0) -> np.ndarray:
         return make_tokens(self.wid, n, self.d_model, purpose, layer, self.outlier_frac)
