@@ -49,8 +49,9 @@ def parse():
     p.add_argument("--warmup", type=int, default=200)
     p.add_argument("--workload", default="llama7b_4096x11008")
     p.add_argument("--variant", default="mono",
-                   choices=["mono", "dual_ideal", "dual_pred", "dense", "cats", "mono_topk",
-                            "dual_ideal_topk", "dual_pred_topk", "cats_topk"])
+                   choices=["mono", "dual_ideal", "dual_pred", "dual_tern", "dense", "cats",
+                            "mono_topk", "dual_ideal_topk", "dual_pred_topk", "dual_tern_topk",
+                            "cats_topk"])
     p.add_argument("--batch", type=int, default=1, help="decode tokens per call (union IDX)")
     p.add_argument("--k", type=float, default=0.9)
     p.add_argument("--copies", type=int, default=4, help="independent weight copies rotated")
@@ -168,21 +169,27 @@ class Context:
         t = time.time()
         self.layers = []
         self.host0 = None
+        variants = variants or [v for v in w.variants if v != "dense"]
         for c in range(copies):
             L = w.layer(copy=c)
             if w.d_rank:
                 L.update(w.predictor(copy=c))
+            D = {k: dev_bf16(v) for k, v in L.items()}
+            if "dual_tern" in variants:  # the ternary predictor, packed for the kernels
+                T = w.ternary(copy=c)
+                packed = cd.countdown_ternary_pack(T)
+                D["theta_p"] = torch.from_numpy(packed.view(np.int32)).to("cuda")
+                L["theta_t"] = T
             if c == 0:
                 self.host0 = L
-            self.layers.append({k: dev_bf16(v) for k, v in L.items()})
+            self.layers.append(D)
         self.X_eval_h = w.tokens(ntok)
         self.X_eval = dev_bf16(self.X_eval_h)
         X_cal = dev_bf16(w.tokens(ncal, purpose=T_CALIB))
         torch.cuda.synchronize()
-        gb = sum(v.numel() * 2 for v in self.layers[0].values()) * copies / 1e9
+        gb = sum(v.numel() * v.element_size() for v in self.layers[0].values()) * copies / 1e9
         log(f"[bench] {copies} weight copies of {w.name} on device ({gb:.2f} GB) in "
             f"{time.time() - t:.1f}s")
-        variants = variants or [v for v in w.variants if v != "dense"]
         vids = {"mono": cd.CD_VARIANT_MONO, "dual_ideal": cd.CD_VARIANT_DUAL_IDEAL,
                 "dual_pred": cd.CD_VARIANT_DUAL_PRED, "cats": cd.CD_VARIANT_CATS}
         # tokens per calibration launch: the widest batch tile the shape allows
@@ -191,9 +198,12 @@ class Context:
         L0 = self.layers[0]
         for variant in variants:
             for k in ks:
-                th, _ = cd.countdown_calibrate(cal_plan, vids[variant], X_cal, k,
-                                               W_gate=L0["W_gate"], W_up=L0["W_up"],
-                                               A_t=L0.get("A_t"), B_t=L0.get("B_t"))
+                if variant == "dual_tern":
+                    th, _ = cd.countdown_calibrate_tern(cal_plan, X_cal, L0["theta_p"], k)
+                else:
+                    th, _ = cd.countdown_calibrate(cal_plan, vids[variant], X_cal, k,
+                                                   W_gate=L0["W_gate"], W_up=L0["W_up"],
+                                                   A_t=L0.get("A_t"), B_t=L0.get("B_t"))
                 self.thld[(variant, k)] = float(th.item())
         cal_plan.close()
         del X_cal
@@ -222,7 +232,10 @@ class Context:
         def step(i):
             L = layers[i % copies]
             x = X[i % ntok: i % ntok + B]
-            if topk:  # per-token threshold: the k-quantile of each token's own coefficients
+            if topk and base == "dual_tern":
+                cd.countdown_ffn_tern_topk(plan, x, L["W_gate"], L["W_up"], L["W_down"],
+                                           L["theta_p"], k, y=y)
+            elif topk:  # per-token threshold: the k-quantile of each token's own coefficients
                 cd.countdown_ffn_topk(plan, vid, x, L["W_gate"], L["W_up"], L["W_down"], k,
                                       A_t=L.get("A_t") if base == "dual_pred" else None,
                                       B_t=L.get("B_t") if base == "dual_pred" else None, y=y)
@@ -235,6 +248,9 @@ class Context:
             elif variant == "dual_pred":
                 cd.countdown_ffn_dual(plan, x, L["W_gate"], L["W_up"], L["W_down"], th,
                                       A_t=L["A_t"], B_t=L["B_t"], y=y)
+            elif variant == "dual_tern":
+                cd.countdown_ffn_tern(plan, x, L["W_gate"], L["W_up"], L["W_down"],
+                                      L["theta_p"], th, y=y)
             else:
                 cd.countdown_ffn_dense(plan, x, L["W_gate"], L["W_up"], L["W_down"], y=y)
         return step
@@ -304,7 +320,8 @@ def other_workloads(args):
 
     out = {}
     w = WORKLOADS["llama3_8b_4096x14336_pred"]
-    ctx = Context(w, 4, 64, args.calib_tokens, [0.9], max_batch=8)
+    ctx = Context(w, 4, 64, args.calib_tokens, [0.9], max_batch=8,
+                  variants=["dual_pred", "dual_tern"])
     r8 = {}
     for B in w.batches:
         r = ctx.measure("dual_pred", 0.9, B, max(200, args.steps // 4), 50)
@@ -313,9 +330,12 @@ def other_workloads(args):
     r = ctx.measure("dual_pred_topk", 0.9, 1, max(200, args.steps // 4), 50)
     r8["per-token k=0.9 B=1"] = brief(r)
     log(f"[bench] {w.name} dual_pred per-token B=1: {json.dumps(r8['per-token k=0.9 B=1'])}")
+    for B in w.batches:  # the ternary predictor (Sec. 6) in the low-rank one's place
+        r = ctx.measure("dual_tern", 0.9, B, max(200, args.steps // 4), 50)
+        r8[f"ternary B={B}"] = brief(r)
+        log(f"[bench] {w.name} dual_tern B={B}: {json.dumps(r8[f'ternary B={B}'])}")
     r = ctx.measure("dense", None, 1, max(200, args.steps // 4), 50)
     r8["dense B=1"] = brief(r)
-    dense_b = traffic.algorithmic_bytes("dense", w.d_model, w.d_ff, w.d_ff)["total"]
     for B in w.batches:
         r8[f"B={B}"]["speedup_vs_dense_B1"] = r["us_per_layer"] / r8[f"B={B}"]["us_per_layer"]
     ctx.free()
@@ -332,7 +352,6 @@ def other_workloads(args):
         r70[key]["speedup_vs_dense"] = r70["dense"]["us_per_layer"] / r70[key]["us_per_layer"]
     ctx.free()
     out[w.name] = r70
-    del dense_b
     return out
 
 
@@ -527,10 +546,14 @@ def main():
         torch.cuda.synchronize()
         del src, dst
 
+    base = args.variant[:-5] if args.variant.endswith("_topk") else args.variant
+    main_variants = (["mono", "dual_ideal", "cats"] if "mono" in w.variants
+                     else [v for v in w.variants if v != "dense"])
+    if base == "dual_tern":
+        main_variants.append("dual_tern")
     main_ctx = Context(w, args.copies, args.tokens, args.calib_tokens,
                        sorted(set((args.k,) + tuple(w.ks))), max_batch=args.batch,
-                       variants=(["mono", "dual_ideal", "cats"] if "mono" in w.variants
-                                 else None))
+                       variants=main_variants)
     main_res = main_ctx.measure(args.variant, args.k, args.batch, args.steps, args.warmup)
     log(f"[bench] {w.name} {args.variant} k={args.k}: {json.dumps(main_res)}")
 
@@ -582,11 +605,13 @@ def main():
                "dual_pred": lambda x: oracle.ffn_dual_pred(x, H["W_gate"], H["W_up"], H["W_down"],
                                                            H.get("A_t"), H.get("B_t"), th),
                "dense": lambda x: oracle.dense(x, H["W_gate"], H["W_up"], H["W_down"]),
-               "cats": lambda x: oracle.ffn_cats(x, H["W_gate"], H["W_up"], H["W_down"], th)}
-        for base in ("mono", "dual_ideal", "dual_pred", "cats"):
+               "cats": lambda x: oracle.ffn_cats(x, H["W_gate"], H["W_up"], H["W_down"], th),
+               "dual_tern": lambda x: oracle.ffn_dual_tern(x, H["W_gate"], H["W_up"],
+                                                           H["W_down"], H.get("theta_t"), th)}
+        for base in ("mono", "dual_ideal", "dual_pred", "cats", "dual_tern"):
             fns[base + "_topk"] = (lambda b: lambda x: oracle.ffn_topk(
                 b, x, H["W_gate"], H["W_up"], H["W_down"], args.k, A_t=H.get("A_t"),
-                B_t=H.get("B_t")))(base)
+                B_t=H.get("B_t"), theta_t=H.get("theta_t")))(base)
         fn = fns[args.variant]
         n_done, t0 = 0, time.perf_counter()
         nt = len(X_eval_h) - args.batch + 1
@@ -616,7 +641,11 @@ def main():
                                   "(per-token threshold)",
                 "cats": "k_coef_mono<CATS> (dense W_gate GEMV, SiLU, threshold, W_up gather)",
                 "cats_topk": "k_coef_mono<CATS> + k_topk_select + k_gather_topk "
-                             "(per-token threshold)"}[args.variant]
+                             "(per-token threshold)",
+                "dual_tern": "k_coef_tern (ternary predictor scores, threshold, block-local "
+                             "W_gate / W_up gather, s)",
+                "dual_tern_topk": "k_coef_tern + k_topk_select + k_gather_topk (per-token "
+                                  "threshold)"}[args.variant]
         roof = {"bound": "hbm", "kernel": desc,
                 "achieved": main_res[f"{dom}_kernel_GBs"], "peak": HBM_PEAK_GBS, "unit": "GB/s",
                 "frac": main_res[f"{dom}_kernel_GBs"] / HBM_PEAK_GBS,

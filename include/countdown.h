@@ -8,7 +8,9 @@
  *   M-CountDown  (countdown_ffn_mono):        IDX = {i : |u[i]| > thld}, u = x.W_up;
  *   D-CountDown  (countdown_ffn_dual, ideal): IDX = {i : |s[i]| > thld}, s computed densely;
  *   D-CountDown  (countdown_ffn_dual, pred):  IDX = {i : s_hat[i] > thld},
- *                                             s_hat = (x.theta_A).theta_B (signed score).
+ *                                             s_hat = (x.theta_A).theta_B (signed score);
+ *   D-CountDown  (countdown_ffn_tern):        the same with the ternary predictor
+ *                                             s_hat = x.theta, theta in {-1, 0, +1}.
  * For a batch of B tokens IDX is the union of the per-token sets and every
  * token uses all rows of IDX with its own coefficients.
  *
@@ -41,6 +43,7 @@
 #ifndef COUNTDOWN_H
 #define COUNTDOWN_H
 
+#include <stddef.h>
 #include <stdint.h>
 
 #ifdef __cplusplus
@@ -60,6 +63,7 @@ typedef int cd_status;
 #define CD_VARIANT_DUAL_PRED 2   /* D-CountDown, predictor score s_hat (Sec. 4) */
 #define CD_VARIANT_DENSE 3       /* dense Gated-MLP (Eq. 1) */
 #define CD_VARIANT_CATS 4        /* CATS, the comparison method: |SiLU(x.W_gate)| (Eq. 6a) */
+#define CD_VARIANT_DUAL_TERN 5   /* D-CountDown, ternary predictor score x.theta (Sec. 6) */
 
 /* Plan flags. */
 #define CD_PLAN_KEEP_COEF 1u  /* also store the dense coefficient vector of each call
@@ -145,6 +149,52 @@ cd_status countdown_ffn_topk(cd_plan *plan, int variant, const uint16_t *x, int 
                              float *y, void *stream);
 
 /*
+ * Ternary predictor (the TernaryLinear candidate of Sec. 6, Table 4; trained
+ * by Alg. 1): s_hat_b = x_b.theta with theta in {-1, 0, +1}^{d_model x d_ff}
+ * (no scale: a positive per-layer scale only rescales the threshold),
+ * IDX = {i : exists b, s_hat_b[i] > thld} (signed, strict), then gate and
+ * up on IDX and y by Eq. (5), as countdown_ffn_dual with a predictor.
+ * theta_packed is the DEVICE buffer written by countdown_ternary_pack
+ * (countdown_ternary_words(d_model, d_ff) uint32 words, 16-byte aligned).
+ * The plan's d_rank is not used. s_hat is accumulated in fp32.
+ */
+cd_status countdown_ffn_tern(cd_plan *plan, const uint16_t *x, int B, const uint16_t *W_gate,
+                             const uint16_t *W_up, const uint16_t *W_down,
+                             const uint32_t *theta_packed, float thld, float *y, void *stream);
+
+/* countdown_ffn_topk with the ternary predictor score (signed, per-token thresholds). */
+cd_status countdown_ffn_tern_topk(cd_plan *plan, const uint16_t *x, int B,
+                                  const uint16_t *W_gate, const uint16_t *W_up,
+                                  const uint16_t *W_down, const uint32_t *theta_packed, double k,
+                                  double *thld_out, float *y, void *stream);
+
+/* countdown_calibrate for the ternary predictor score (signed s_hat = x.theta). */
+cd_status countdown_calibrate_tern(cd_plan *plan, const uint16_t *X, int T,
+                                   const uint32_t *theta_packed, double k, float *thld_out,
+                                   double *q_out, void *stream);
+
+/*
+ * Size in uint32 words of the packed ternary predictor of a shape: d_ff rows
+ * of 64 * W words, W = max(1, C / 2), C the smallest of 1, 2, 4, 8, 16 with
+ * 512 C >= d_model. 0 for shapes countdown_check_shape rejects. Host only.
+ */
+size_t countdown_ternary_words(int d_model, int d_ff);
+
+/*
+ * Pack theta for the ternary predictor. HOST memory in and out, no device
+ * call. theta_t is int8 [d_ff][d_model] (theta transposed: row i is neuron
+ * i's weights), every entry -1, 0 or +1 (else CD_EINVAL, packed untouched
+ * beyond the rows already written). packed receives
+ * countdown_ternary_words(d_model, d_ff) words. Layout of row i (64 W words,
+ * unused columns zero): lane l = 0..63 owns words [l W, (l + 1) W); its unit
+ * j (j < C) holds the 8 weights of columns j * 512 + 8 l + e, e = 0..7; word
+ * k of the lane holds units 2k (A) and 2k + 1 (B). In a word, byte 1 bits
+ * 2m..2m+1 hold A's weight e = 2m, byte 3 A's e = 2m + 1, byte 0 B's e = 2m,
+ * byte 2 B's e = 2m + 1 (m = 0..3), coded 0 -> 0, 1 -> +1, 2 -> -1.
+ */
+cd_status countdown_ternary_pack(const int8_t *theta_t, int d_model, int d_ff, uint32_t *packed);
+
+/*
  * One layer of a stack of FFNs joined by a residual stream. The paper
  * evaluates single Gated-MLP layers (Sec. 3); the stack workload adds, per
  * token b, before the FFN of `variant` (CD_VARIANT_*, as in the calls above):
@@ -216,8 +266,9 @@ cd_status countdown_plan_set_phases(cd_plan *plan, unsigned phases);
  * Host-only validation of an FFN call's arguments against a shape, exactly
  * as the entry points perform it before launching: pointers non-NULL and
  * 16-byte aligned, 1 <= B <= max_batch, thld not NaN, predictor pointers
- * both NULL or both set (dual only, and d_rank > 0 when set). Touches no
- * device. variant is a CD_VARIANT_*.
+ * both NULL or both set (dual only, and d_rank > 0 when set). For
+ * CD_VARIANT_DUAL_TERN, A_t is the packed ternary predictor and B_t must be
+ * NULL. Touches no device. variant is a CD_VARIANT_*.
  */
 cd_status countdown_check_args(int variant, int d_model, int d_ff, int max_batch, int d_rank,
                                const void *x, int B, const void *W_gate, const void *W_up,
@@ -231,7 +282,7 @@ cd_status countdown_check_shape(int d_model, int d_ff, int max_batch, int d_rank
 const char *countdown_status_string(cd_status status);
 
 /* ABI version of this header (bumped on any signature change). */
-#define COUNTDOWN_ABI_VERSION 6
+#define COUNTDOWN_ABI_VERSION 7
 int countdown_abi_version(void);
 
 #ifdef __cplusplus

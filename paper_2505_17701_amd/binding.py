@@ -16,7 +16,7 @@ LIB_PATH = os.path.join(PKG, "libcountdown.so")
 
 CD_OK, CD_EINVAL, CD_EUNSUPPORTED, CD_EHIP, CD_ENOMEM = 0, -1, -2, -3, -4
 CD_VARIANT_MONO, CD_VARIANT_DUAL_IDEAL, CD_VARIANT_DUAL_PRED, CD_VARIANT_DENSE = 0, 1, 2, 3
-CD_VARIANT_CATS = 4
+CD_VARIANT_CATS, CD_VARIANT_DUAL_TERN = 4, 5
 CD_PLAN_KEEP_COEF = 1
 CD_PHASE_COEF, CD_PHASE_DOWN, CD_PHASE_ALL = 1, 2, 3
 
@@ -24,7 +24,8 @@ CD_PHASE_COEF, CD_PHASE_DOWN, CD_PHASE_ALL = 1, 2, 3
 EXPORTS = (
     "countdown_plan_create", "countdown_plan_destroy", "countdown_ffn_mono", "countdown_ffn_dual",
     "countdown_ffn_dense", "countdown_ffn_cats", "countdown_ffn_topk", "countdown_ffn_residual",
-    "countdown_calibrate",
+    "countdown_calibrate", "countdown_ffn_tern", "countdown_ffn_tern_topk",
+    "countdown_calibrate_tern", "countdown_ternary_words", "countdown_ternary_pack",
     "countdown_export_active",
     "countdown_plan_set_phases", "countdown_check_args",
     "countdown_check_shape", "countdown_status_string", "countdown_abi_version",
@@ -60,6 +61,11 @@ def load_library(path: str = LIB_PATH):
                                        vp]),
         "countdown_ffn_topk": (i, [vp, i, vp, i, vp, vp, vp, vp, vp, d, vp, vp, vp]),
         "countdown_calibrate": (i, [vp, i, vp, i, vp, vp, vp, vp, d, vp, vp, vp]),
+        "countdown_ffn_tern": (i, [vp, vp, i, vp, vp, vp, vp, f, vp, vp]),
+        "countdown_ffn_tern_topk": (i, [vp, vp, i, vp, vp, vp, vp, d, vp, vp, vp]),
+        "countdown_calibrate_tern": (i, [vp, vp, i, vp, d, vp, vp, vp]),
+        "countdown_ternary_words": (C.c_size_t, [i, i]),
+        "countdown_ternary_pack": (i, [vp, i, i, vp]),
         "countdown_export_active": (i, [vp, vp, vp, vp, vp, vp]),
         "countdown_plan_set_phases": (i, [vp, u]),
         "countdown_check_args": (i, [i, i, i, i, i, vp, i, vp, vp, vp, vp, vp, f, vp]),
@@ -264,6 +270,77 @@ def countdown_calibrate(plan: Plan, variant: int, X, k: float, W_gate=None, W_up
         plan.handle, int(variant), _ptr(_bf16(X)), T, _ptr(_bf16(W_gate)), _ptr(_bf16(W_up)),
         _ptr(_bf16(A_t)), _ptr(_bf16(B_t)), float(k), _ptr(thld), _ptr(q), _stream(stream)),
         "countdown_calibrate")
+    return thld, q
+
+
+def _u32(t):
+    import torch
+
+    if t.dtype not in (torch.int32, torch.uint32):
+        raise TypeError(f"expected a packed 32-bit tensor, got {t.dtype}")
+    return t
+
+
+def countdown_ternary_words(d_model: int, d_ff: int) -> int:
+    """uint32 words of the packed ternary predictor of a shape (0 if rejected)."""
+    return int(load_library().countdown_ternary_words(int(d_model), int(d_ff)))
+
+
+def countdown_ternary_pack(theta_t):
+    """Pack a host int8 ``theta_t [d_ff, d_model]`` (entries -1, 0, +1; theta transposed)
+    into the kernels' layout; returns a host numpy uint32 array (move it to the GPU)."""
+    import numpy as np
+
+    t = np.ascontiguousarray(theta_t, dtype=np.int8)
+    d_ff, d_model = t.shape
+    n = countdown_ternary_words(d_model, d_ff)
+    if n == 0:
+        raise CountdownError(CD_EINVAL, "countdown_ternary_words")
+    out = np.zeros(n, dtype=np.uint32)
+    _check(load_library().countdown_ternary_pack(t.ctypes.data, d_model, d_ff, out.ctypes.data),
+           "countdown_ternary_pack")
+    return out
+
+
+def countdown_ffn_tern(plan: Plan, x, W_gate, W_up, W_down, theta_packed, thld: float, y=None,
+                       stream=None):
+    """D-CountDown with the ternary predictor (``theta_packed``: device int32/uint32 tensor
+    from :func:`countdown_ternary_pack`)."""
+    B, y = _out(plan, x, y)
+    _check(load_library().countdown_ffn_tern(
+        plan.handle, _ptr(_bf16(x)), B, _ptr(_bf16(W_gate)), _ptr(_bf16(W_up)),
+        _ptr(_bf16(W_down)), _ptr(_u32(theta_packed)), float(thld), _ptr(y), _stream(stream)),
+        "countdown_ffn_tern")
+    plan.last_batch = B
+    return y
+
+
+def countdown_ffn_tern_topk(plan: Plan, x, W_gate, W_up, W_down, theta_packed, k: float, y=None,
+                            thld_out=None, stream=None):
+    """Per-token threshold on the ternary predictor score; returns y."""
+    import torch
+
+    B, y = _out(plan, x, y)
+    if thld_out is not None and (thld_out.dtype != torch.float64 or thld_out.numel() < B):
+        raise ValueError("thld_out must be a float64 device tensor with at least B entries")
+    _check(load_library().countdown_ffn_tern_topk(
+        plan.handle, _ptr(_bf16(x)), B, _ptr(_bf16(W_gate)), _ptr(_bf16(W_up)),
+        _ptr(_bf16(W_down)), _ptr(_u32(theta_packed)), float(k), _ptr(thld_out), _ptr(y),
+        _stream(stream)), "countdown_ffn_tern_topk")
+    plan.last_batch = B
+    return y
+
+
+def countdown_calibrate_tern(plan: Plan, X, theta_packed, k: float, stream=None):
+    """Layerwise threshold of the ternary predictor score; returns ``(thld [1], q [T])``."""
+    import torch
+
+    T = X.shape[0]
+    thld = torch.empty(1, dtype=torch.float32, device=X.device)
+    q = torch.empty(T, dtype=torch.float64, device=X.device)
+    _check(load_library().countdown_calibrate_tern(
+        plan.handle, _ptr(_bf16(X)), T, _ptr(_u32(theta_packed)), float(k), _ptr(thld), _ptr(q),
+        _stream(stream)), "countdown_calibrate_tern")
     return thld, q
 
 

@@ -71,7 +71,7 @@ cd_status check_args(int variant, int d_model, int d_ff, int max_batch, int d_ra
     cd_status st = check_shape(d_model, d_ff, max_batch, d_rank);
     if (st != CD_OK)
         return st;
-    if (variant < CD_VARIANT_MONO || variant > CD_VARIANT_CATS)
+    if (variant < CD_VARIANT_MONO || variant > CD_VARIANT_DUAL_TERN)
         return CD_EINVAL;
     if (B < 1 || B > max_batch)
         return CD_EINVAL;
@@ -84,6 +84,9 @@ cd_status check_args(int variant, int d_model, int d_ff, int max_batch, int d_ra
     if (variant == CD_VARIANT_DUAL_PRED) {
         if (!A_t || !B_t || !aligned16(A_t) || !aligned16(B_t) || d_rank == 0)
             return CD_EINVAL;
+    } else if (variant == CD_VARIANT_DUAL_TERN) {  // A_t: the packed ternary predictor
+        if (!A_t || !aligned16(A_t) || B_t)
+            return CD_EINVAL;
     } else if (A_t || B_t) {
         return CD_EINVAL;
     }
@@ -94,7 +97,8 @@ cd_status check_args(int variant, int d_model, int d_ff, int max_batch, int d_ra
 int kernel_variant(int variant) { return variant; }
 
 cdk::CoefArgs coef_args(cd_plan *p, const uint16_t *x, int B, const uint16_t *Wg,
-                        const uint16_t *Wu, const uint16_t *Bt, float thld, float *y)
+                        const uint16_t *Wu, const uint16_t *Bt, float thld, float *y,
+                        const uint32_t *Tp = nullptr)
 {
     cdk::CoefArgs a;
     a.x = x;
@@ -103,6 +107,7 @@ cdk::CoefArgs coef_args(cd_plan *p, const uint16_t *x, int B, const uint16_t *Wg
     a.Wu = Wu;
     a.Bt = Bt;
     a.lat = p->lat;
+    a.Tp = Tp;
     a.d_model = p->d_model;
     a.d_ff = p->d_ff;
     a.d_rank = p->d_rank;
@@ -128,14 +133,18 @@ cdk::DownArgs down_args(cd_plan *p, int B, const uint16_t *Wd, float *y)
     return a;
 }
 
+// Tp: the packed ternary predictor (CD_VARIANT_DUAL_TERN only)
 cd_status run_ffn(cd_plan *p, int variant, const uint16_t *x, int B, const uint16_t *Wg,
                   const uint16_t *Wu, const uint16_t *Wd, const uint16_t *At, const uint16_t *Bt,
-                  float thld, float *y, void *stream)
+                  float thld, float *y, void *stream, const uint32_t *Tp = nullptr)
 {
     if (!p)
         return CD_EINVAL;
+    const bool tern = variant == CD_VARIANT_DUAL_TERN;
+    if (tern && (At || Bt))
+        return CD_EINVAL;
     cd_status st = check_args(variant, p->d_model, p->d_ff, p->max_batch, p->d_rank, x, B, Wg, Wu,
-                              Wd, At, Bt, thld, y);
+                              Wd, tern ? static_cast<const void *>(Tp) : At, Bt, thld, y);
     if (st != CD_OK)
         return st;
     hipStream_t s = reinterpret_cast<hipStream_t>(stream);
@@ -148,7 +157,7 @@ cd_status run_ffn(cd_plan *p, int variant, const uint16_t *x, int B, const uint1
             if (st != CD_OK)
                 return st;
         }
-        const cdk::CoefArgs ca = coef_args(p, x, B, Wg, Wu, Bt, thld, y);
+        const cdk::CoefArgs ca = coef_args(p, x, B, Wg, Wu, Bt, thld, y, Tp);
         st = launched(cdk::launch_coef(kernel_variant(variant), ca, s));
         if (st != CD_OK)
             return st;
@@ -173,7 +182,7 @@ cd_status run_ffn_residual(cd_plan *p, int variant, const float *h_in, const flo
                            const uint16_t *Wu, const uint16_t *Wd, const uint16_t *At,
                            const uint16_t *Bt, float thld, float *y, void *stream)
 {
-    if (!p)
+    if (!p || variant == CD_VARIANT_DUAL_TERN)
         return CD_EINVAL;
     cd_status st = check_args(variant, p->d_model, p->d_ff, p->max_batch, p->d_rank, x_out, B, Wg,
                               Wu, Wd, At, Bt, thld, y);
@@ -225,17 +234,22 @@ cd_status run_ffn_residual(cd_plan *p, int variant, const float *h_in, const flo
 
 cd_status run_ffn_topk(cd_plan *p, int variant, const uint16_t *x, int B, const uint16_t *Wg,
                        const uint16_t *Wu, const uint16_t *Wd, const uint16_t *At,
-                       const uint16_t *Bt, double k, double *thld_out, float *y, void *stream)
+                       const uint16_t *Bt, double k, double *thld_out, float *y, void *stream,
+                       const uint32_t *Tp = nullptr)
 {
     if (!p)
         return CD_EINVAL;
     if (variant != CD_VARIANT_MONO && variant != CD_VARIANT_DUAL_IDEAL &&
-        variant != CD_VARIANT_DUAL_PRED && variant != CD_VARIANT_CATS)
+        variant != CD_VARIANT_DUAL_PRED && variant != CD_VARIANT_CATS &&
+        variant != CD_VARIANT_DUAL_TERN)
         return CD_EINVAL;
     if (!(k >= 0.0 && k <= 1.0) || (thld_out && (reinterpret_cast<uintptr_t>(thld_out) & 7u)))
         return CD_EINVAL;
+    const bool tern = variant == CD_VARIANT_DUAL_TERN;
+    if (tern && (At || Bt))
+        return CD_EINVAL;
     cd_status st = check_args(variant, p->d_model, p->d_ff, p->max_batch, p->d_rank, x, B, Wg, Wu,
-                              Wd, At, Bt, 0.0f, y);
+                              Wd, tern ? static_cast<const void *>(Tp) : At, Bt, 0.0f, y);
     if (st != CD_OK)
         return st;
     if (p->d_ff > cdk::kTopkMaxDff)
@@ -251,7 +265,7 @@ cd_status run_ffn_topk(cd_plan *p, int variant, const uint16_t *x, int B, const 
                 return st;
         }
         // dense coefficients of every neuron (threshold +inf: nothing is gathered yet)
-        cdk::CoefArgs ca = coef_args(p, x, B, Wg, Wu, Bt, INFINITY, y);
+        cdk::CoefArgs ca = coef_args(p, x, B, Wg, Wu, Bt, INFINITY, y, Tp);
         ca.coef = p->coef;
         st = launched(cdk::launch_coef(kernel_variant(variant), ca, s));
         if (st != CD_OK)
@@ -426,18 +440,26 @@ cd_status countdown_ffn_dense(cd_plan *plan, const uint16_t *x, int B, const uin
                    -INFINITY, y, stream);
 }
 
-cd_status countdown_calibrate(cd_plan *p, int variant, const uint16_t *X, int T,
-                              const uint16_t *W_gate, const uint16_t *W_up, const uint16_t *A_t,
-                              const uint16_t *B_t, double k, float *thld_out, double *q_out,
-                              void *stream)
+}  // extern "C"
+
+namespace {
+
+cd_status calibrate(cd_plan *p, int variant, const uint16_t *X, int T, const uint16_t *W_gate,
+                    const uint16_t *W_up, const uint16_t *A_t, const uint16_t *B_t,
+                    const uint32_t *Tp, double k, float *thld_out, double *q_out, void *stream)
 {
     if (!p || !X || !aligned16(X) || T < 1 || !thld_out || !(k >= 0.0 && k <= 1.0))
         return CD_EINVAL;
     if (variant != CD_VARIANT_MONO && variant != CD_VARIANT_DUAL_IDEAL &&
-        variant != CD_VARIANT_DUAL_PRED && variant != CD_VARIANT_CATS)
+        variant != CD_VARIANT_DUAL_PRED && variant != CD_VARIANT_CATS &&
+        variant != CD_VARIANT_DUAL_TERN)
         return CD_EINVAL;
     const bool pred = variant == CD_VARIANT_DUAL_PRED;
-    if (pred) {
+    const bool tern = variant == CD_VARIANT_DUAL_TERN;
+    if (tern) {
+        if (!Tp || !aligned16(Tp))
+            return CD_EINVAL;
+    } else if (pred) {
         if (!A_t || !B_t || !aligned16(A_t) || !aligned16(B_t) || p->d_rank == 0)
             return CD_EINVAL;
     } else if (variant == CD_VARIANT_CATS) {
@@ -466,12 +488,13 @@ cd_status countdown_calibrate(cd_plan *p, int variant, const uint16_t *X, int T,
             if (st != CD_OK)
                 break;
         }
-        cdk::CoefArgs a = coef_args(p, xb, nb, wg, wu, B_t, INFINITY, ybuf);
+        cdk::CoefArgs a = coef_args(p, xb, nb, wg, wu, B_t, INFINITY, ybuf, Tp);
         a.coef = coef;
         st = launched(cdk::launch_coef(variant, a, s));
         if (st != CD_OK)
             break;
-        st = launched(cdk::launch_select(coef, p->d_ff, p->d_ff, nb, pred ? 0 : 1, k, q + t0, s));
+        st = launched(cdk::launch_select(coef, p->d_ff, p->d_ff, nb, pred || tern ? 0 : 1, k,
+                                         q + t0, s));
     }
     // the act / s workspace now describes a calibration batch, not an FFN call
     p->last_batch = 0;
@@ -487,6 +510,80 @@ cd_status countdown_calibrate(cd_plan *p, int variant, const uint16_t *X, int T,
     if (ybuf) (void)hipFree(ybuf);
     if (q) (void)hipFree(q);
     return st;
+}
+
+}  // namespace
+
+extern "C" {
+
+cd_status countdown_calibrate(cd_plan *p, int variant, const uint16_t *X, int T,
+                              const uint16_t *W_gate, const uint16_t *W_up, const uint16_t *A_t,
+                              const uint16_t *B_t, double k, float *thld_out, double *q_out,
+                              void *stream)
+{
+    if (variant == CD_VARIANT_DUAL_TERN)  // countdown_calibrate_tern takes the packed predictor
+        return CD_EINVAL;
+    return calibrate(p, variant, X, T, W_gate, W_up, A_t, B_t, nullptr, k, thld_out, q_out,
+                     stream);
+}
+
+cd_status countdown_calibrate_tern(cd_plan *p, const uint16_t *X, int T,
+                                   const uint32_t *theta_packed, double k, float *thld_out,
+                                   double *q_out, void *stream)
+{
+    return calibrate(p, CD_VARIANT_DUAL_TERN, X, T, nullptr, nullptr, nullptr, nullptr,
+                     theta_packed, k, thld_out, q_out, stream);
+}
+
+cd_status countdown_ffn_tern(cd_plan *plan, const uint16_t *x, int B, const uint16_t *W_gate,
+                             const uint16_t *W_up, const uint16_t *W_down,
+                             const uint32_t *theta_packed, float thld, float *y, void *stream)
+{
+    return run_ffn(plan, CD_VARIANT_DUAL_TERN, x, B, W_gate, W_up, W_down, nullptr, nullptr, thld,
+                   y, stream, theta_packed);
+}
+
+cd_status countdown_ffn_tern_topk(cd_plan *plan, const uint16_t *x, int B,
+                                  const uint16_t *W_gate, const uint16_t *W_up,
+                                  const uint16_t *W_down, const uint32_t *theta_packed, double k,
+                                  double *thld_out, float *y, void *stream)
+{
+    return run_ffn_topk(plan, CD_VARIANT_DUAL_TERN, x, B, W_gate, W_up, W_down, nullptr, nullptr,
+                        k, thld_out, y, stream, theta_packed);
+}
+
+size_t countdown_ternary_words(int d_model, int d_ff)
+{
+    if (check_shape(d_model, d_ff, 1, 0) != CD_OK)
+        return 0;
+    return (size_t)d_ff * cdk::tern_row_words(d_model);
+}
+
+cd_status countdown_ternary_pack(const int8_t *theta_t, int d_model, int d_ff, uint32_t *packed)
+{
+    if (!theta_t || !packed || check_shape(d_model, d_ff, 1, 0) != CD_OK)
+        return CD_EINVAL;
+    const int row_words = cdk::tern_row_words(d_model);
+    const int lane_words = row_words / 64;
+    for (int i = 0; i < d_ff; ++i) {
+        uint32_t *row = packed + (size_t)i * row_words;
+        for (int w = 0; w < row_words; ++w)
+            row[w] = 0u;
+        const int8_t *t = theta_t + (size_t)i * d_model;
+        for (int c = 0; c < d_model; ++c) {
+            if (t[c] < -1 || t[c] > 1)
+                return CD_EINVAL;
+            if (t[c] == 0)
+                continue;
+            const uint32_t code = t[c] > 0 ? 1u : 2u;
+            const int j = c / 512, l = (c % 512) / 8, e = c % 8;  // unit, lane, position
+            const int m = e / 2;
+            // A (even unit): bytes 1 / 3; B (odd unit): bytes 0 / 2; e odd: the upper byte
+            const int byte = ((j & 1) ? 0 : 1) + ((e & 1) ? 2 : 0);
+            row[l * lane_words + j / 2] |= code << (8 * byte + 2 * m);
+        }
+    }
+    return CD_OK;
 }
 
 cd_status countdown_export_active(const cd_plan *p, int32_t *idx_dst, int32_t *n_dst,

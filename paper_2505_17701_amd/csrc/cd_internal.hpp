@@ -6,7 +6,7 @@
 
 namespace cdk {
 
-enum Variant { kMono = 0, kDualIdeal = 1, kDualPred = 2, kDense = 3, kCats = 4 };
+enum Variant { kMono = 0, kDualIdeal = 1, kDualPred = 2, kDense = 3, kCats = 4, kDualTern = 5 };
 
 // Arguments of the coefficient kernels: dense coefficient projection,
 // threshold, and (mono / pred) the gathered gate (mono) or gate+up (pred)
@@ -18,6 +18,7 @@ struct CoefArgs {
     const uint16_t *Wu;  // [d_ff][d_model]
     const uint16_t *Bt;  // [d_ff][d_rank] (pred only)
     const float *lat;    // [nb][d_rank] fp32 latent (pred only)
+    const uint32_t *Tp;  // packed ternary predictor (tern only)
     int d_model, d_ff, d_rank;
     float thld;
     int *act;            // [d_ff] 1 if the neuron is in IDX
@@ -47,6 +48,9 @@ struct NormArgs {
     int nb, d_model;
     float eps;
 };
+
+// 32-bit words of the packed ternary predictor per neuron row
+int tern_row_words(int d_model);
 
 // Smallest supported template widths for a call.
 int batch_tile(int B);        // 1, 2, 4 or 8

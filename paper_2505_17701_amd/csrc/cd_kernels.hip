@@ -495,46 +495,11 @@ __device__ __forceinline__ int pred_next(uint32_t &m)
     return r;
 }
 
-// Practical D-CountDown coefficient kernel (Sec. 4). A workgroup owns a block
-// of kPredRows neurons (kPredRowsPerWave per wave). One round of loads brings
-// the wave's B_t rows, the tokens (registers for batches of 1-2, this
-// thread's share of an LDS copy for 4-8) and the latent (staged in LDS).
-// Each wave scores its rows (s_hat = latent . B_t[row], signed threshold,
-// union over the batch); the block's active neurons are then dealt
-// round-robin to the four waves, which gather their W_gate and W_up rows
-// (the next row's loads in flight while the current one is reduced) and
-// write s = u * SiLU(g).
-template <int B, int NK, bool XREG, int LCPR>
-__global__ __launch_bounds__(kBlock) void k_coef_pred(const CoefArgs a)
+// This wave's share of the block's active neurons: the waves' masks are
+// joined (one barrier) and every fourth active neuron, starting at number
+// `wave`, is kept.
+__device__ __forceinline__ uint32_t block_share(uint32_t *wflag, uint32_t wmask, int wave, int lane)
 {
-    extern __shared__ __align__(16) uint32_t xs[];  // [tokens [B][NK * 256]], latent [B][d_rank]
-    __shared__ uint32_t wflag[kWavesPerBlock];
-    using S = PredShape<LCPR>;
-    constexpr bool kPrefetch = NK <= 8;  // two rows of W_gate + W_up in registers
-    const int lane = threadIdx.x % kWave, wave = threadIdx.x / kWave;
-    const int r0 = blockIdx.x * kPredRows;
-    const int wr0 = r0 + wave * kPredRowsPerWave;
-
-    using LR = LatentRegs<B, LCPR>;
-    u32x4 wb[S::kLoads];
-    pred_issue_bt<LCPR>(wb, a, wr0, lane);
-    Tokens<B, NK, XREG> tok;
-    tok.issue(a.x, a.nb, a.d_model, lane);
-    LR lr;
-    lr.issue(a.lat, a.nb, a.d_rank, lane);
-    LatentStage<LR::kRegs ? 1 : B> ls;  // the LDS copy, rank 1024 only
-    if constexpr (!LR::kRegs)
-        ls.issue(a.lat, a.nb, a.d_rank);
-    zero_y(a.y, a.nb * a.d_model);
-    tok.write(xs);
-    uint32_t *latw = xs + (XREG ? 0 : B * NK * kColsPerLoad / 2);
-    if constexpr (!LR::kRegs)
-        ls.write(reinterpret_cast<u32x4 *>(latw), a.lat, a.nb, a.d_rank);
-    if constexpr (!XREG || !LR::kRegs)
-        __syncthreads();
-
-    const uint32_t wmask = pred_score<B, LCPR>(wb, lr, reinterpret_cast<const float *>(latw), a,
-                                               wr0, lane);
     if (lane == 0)
         wflag[wave] = wmask;
     __syncthreads();
@@ -542,9 +507,19 @@ __global__ __launch_bounds__(kBlock) void k_coef_pred(const CoefArgs a)
 #pragma unroll
     for (int v = 0; v < kWavesPerBlock; ++v)
         m |= wflag[v] << (v * kPredRowsPerWave);
-    for (int v = 0; v < wave; ++v)  // this wave's share starts at active neuron number `wave`
+    for (int v = 0; v < wave; ++v)
         m &= m - 1;
+    return m;
+}
 
+// Gather of the wave's share m of the block's active neurons (block base r0):
+// W_gate and W_up rows, s = u * SiLU(g), the next neuron's rows in flight
+// while the current one is reduced.
+template <int B, int NK, bool XREG>
+__device__ __forceinline__ void gather_rr(const CoefArgs &a, const Tokens<B, NK, XREG> &tok,
+                                          uint32_t m, int r0, int lane)
+{
+    constexpr bool kPrefetch = NK <= 8;  // two rows of W_gate + W_up in registers
     int ra = pred_next(m);
     if (ra < 0)
         return;
@@ -581,6 +556,49 @@ __global__ __launch_bounds__(kBlock) void k_coef_pred(const CoefArgs a)
             load_row<NK>(ua, a.Wu + (size_t)(r0 + ra) * a.d_model, a.d_model, lane);
         }
     }
+}
+
+// Practical D-CountDown coefficient kernel (Sec. 4). A workgroup owns a block
+// of kPredRows neurons (kPredRowsPerWave per wave). One round of loads brings
+// the wave's B_t rows, the tokens (registers for batches of 1-2, this
+// thread's share of an LDS copy for 4-8) and the latent (staged in LDS).
+// Each wave scores its rows (s_hat = latent . B_t[row], signed threshold,
+// union over the batch); the block's active neurons are then dealt
+// round-robin to the four waves, which gather their W_gate and W_up rows
+// (the next row's loads in flight while the current one is reduced) and
+// write s = u * SiLU(g).
+template <int B, int NK, bool XREG, int LCPR>
+__global__ __launch_bounds__(kBlock) void k_coef_pred(const CoefArgs a)
+{
+    extern __shared__ __align__(16) uint32_t xs[];  // [tokens [B][NK * 256]], latent [B][d_rank]
+    __shared__ uint32_t wflag[kWavesPerBlock];
+    using S = PredShape<LCPR>;
+    const int lane = threadIdx.x % kWave, wave = threadIdx.x / kWave;
+    const int r0 = blockIdx.x * kPredRows;
+    const int wr0 = r0 + wave * kPredRowsPerWave;
+
+    using LR = LatentRegs<B, LCPR>;
+    u32x4 wb[S::kLoads];
+    pred_issue_bt<LCPR>(wb, a, wr0, lane);
+    Tokens<B, NK, XREG> tok;
+    tok.issue(a.x, a.nb, a.d_model, lane);
+    LR lr;
+    lr.issue(a.lat, a.nb, a.d_rank, lane);
+    LatentStage<LR::kRegs ? 1 : B> ls;  // the LDS copy, rank 1024 only
+    if constexpr (!LR::kRegs)
+        ls.issue(a.lat, a.nb, a.d_rank);
+    zero_y(a.y, a.nb * a.d_model);
+    tok.write(xs);
+    uint32_t *latw = xs + (XREG ? 0 : B * NK * kColsPerLoad / 2);
+    if constexpr (!LR::kRegs)
+        ls.write(reinterpret_cast<u32x4 *>(latw), a.lat, a.nb, a.d_rank);
+    if constexpr (!XREG || !LR::kRegs)
+        __syncthreads();
+
+    const uint32_t wmask = pred_score<B, LCPR>(wb, lr, reinterpret_cast<const float *>(latw), a,
+                                               wr0, lane);
+    uint32_t m = block_share(wflag, wmask, wave, lane);
+    gather_rr<B, NK, XREG>(a, tok, m, r0, lane);
 }
 
 // ------------------------------------------- MFMA gather for batches of 4-8
@@ -652,78 +670,65 @@ __device__ __forceinline__ void mfma_consume(const u32x4 (&ga)[kMfmaSteps],
     }
 }
 
-// Practical D-CountDown coefficient kernel for batches of 4-8 (Sec. 4): the
-// scoring of k_coef_pred, then the block's active neurons in tiles of 16 on MFMA.
-template <int B, int NK, int LCPR>
-__global__ __launch_bounds__(kBlock) void k_coef_pred_mfma(const CoefArgs a)
-{
-    // LDS: tokens [B][kStride] (+ zero chunk), then the latent [B][d_rank] fp32,
-    // whose space later holds the partial sums [4 waves][2][16 x 16] fp32
-    extern __shared__ __align__(16) uint32_t xs[];
-    __shared__ uint32_t wflag[kWavesPerBlock];
-    __shared__ int lrow[kPredRows];
-    using S = PredShape<LCPR>;
+// The tokens of the MFMA kernels: every thread's share of the LDS copy is
+// loaded with the kernel's first loads (issue) and written after (write);
+// the caller synchronises the workgroup before the copy is read.
+template <int B, int NK>
+struct MfmaTokens {
     using TL = MfmaTokLayout<NK>;
-    constexpr int kChunksPerTok = TL::kCols / 8;
-    constexpr int kTotal = B * kChunksPerTok;
-    constexpr int kIter = (kTotal + kBlock - 1) / kBlock;
-    const int lane = threadIdx.x % kWave, wave = threadIdx.x / kWave;
-    const int r0 = blockIdx.x * kPredRows;
-    const int wr0 = r0 + wave * kPredRowsPerWave;
-
-    using LR = LatentRegs<B, LCPR>;
-    u32x4 wb[S::kLoads];
-    pred_issue_bt<LCPR>(wb, a, wr0, lane);
+    static constexpr int kChunksPerTok = TL::kCols / 8;
+    static constexpr int kTotal = B * kChunksPerTok;
+    static constexpr int kIter = (kTotal + kBlock - 1) / kBlock;
     u32x4 stage[kIter];
-#pragma unroll
-    for (int t = 0; t < kIter; ++t) {
-        const int c = threadIdx.x + t * kBlock;
-        const int b = c / kChunksPerTok, col = (c % kChunksPerTok) * 8;
-        stage[t] = load16(or_zero(c < kTotal && b < a.nb && col < a.d_model,
-                                  a.x + (size_t)b * a.d_model + col));
-    }
-    LR lr;
-    lr.issue(a.lat, a.nb, a.d_rank, lane);
-    LatentStage<LR::kRegs ? 1 : B> ls;  // the LDS copy, rank 1024 only
-    if constexpr (!LR::kRegs)
-        ls.issue(a.lat, a.nb, a.d_rank);
-    __builtin_amdgcn_sched_barrier(0);
-    zero_y(a.y, a.nb * a.d_model);
-#pragma unroll
-    for (int t = 0; t < kIter; ++t) {
-        const int c = threadIdx.x + t * kBlock;
-        if (c < kTotal)
-            *reinterpret_cast<u32x4 *>(xs + (size_t)(c / kChunksPerTok) * TL::kStride +
-                                       (c % kChunksPerTok) * 4) = stage[t];
-    }
-    uint32_t *zchunk = xs + (size_t)B * TL::kStride;
-    if (threadIdx.x == 0)
-        *reinterpret_cast<u32x4 *>(zchunk) = zero16();
-    uint32_t *latw = xs + mfma_lds_tokens_u32<B, NK>();
-    if constexpr (!LR::kRegs)
-        ls.write(reinterpret_cast<u32x4 *>(latw), a.lat, a.nb, a.d_rank);
-    __syncthreads();
 
-    const uint32_t wmask = pred_score<B, LCPR>(wb, lr, reinterpret_cast<const float *>(latw), a,
-                                               wr0, lane);
-    if (lane == 0)
-        wflag[wave] = wmask;
-    __syncthreads();
-    uint32_t M = 0;
+    __device__ __forceinline__ void issue(const CoefArgs &a)
+    {
 #pragma unroll
-    for (int v = 0; v < kWavesPerBlock; ++v)
-        M |= wflag[v] << (v * kPredRowsPerWave);
+        for (int t = 0; t < kIter; ++t) {
+            const int c = threadIdx.x + t * kBlock;
+            const int b = c / kChunksPerTok, col = (c % kChunksPerTok) * 8;
+            stage[t] = load16(or_zero(c < kTotal && b < a.nb && col < a.d_model,
+                                      a.x + (size_t)b * a.d_model + col));
+        }
+    }
+
+    // the rows [B][kStride] and, after them, one zero chunk (returned)
+    __device__ __forceinline__ uint32_t *write(uint32_t *xs) const
+    {
+#pragma unroll
+        for (int t = 0; t < kIter; ++t) {
+            const int c = threadIdx.x + t * kBlock;
+            if (c < kTotal)
+                *reinterpret_cast<u32x4 *>(xs + (size_t)(c / kChunksPerTok) * TL::kStride +
+                                           (c % kChunksPerTok) * 4) = stage[t];
+        }
+        uint32_t *zchunk = xs + (size_t)B * TL::kStride;
+        if (threadIdx.x == 0)
+            *reinterpret_cast<u32x4 *>(zchunk) = zero16();
+        return zchunk;
+    }
+};
+
+// MFMA gather of the block's active neurons (block mask M, base r0) for
+// batches of 4-8: the tokens in LDS (rows of kStride u32, zero chunk after
+// them), part = LDS scratch [4 waves][2][16 x 16] fp32, lrow = LDS list of
+// kPredRows ints. Every thread of the workgroup must call this.
+template <int B, int NK>
+__device__ __forceinline__ void gather_mfma(const CoefArgs &a, const uint32_t *xs,
+                                            const uint32_t *zchunk, float *part, int *lrow,
+                                            uint32_t M, int r0, int wave, int lane)
+{
+    using TL = MfmaTokLayout<NK>;
     const int n = __builtin_popcount(M);
     if (threadIdx.x < kPredRows && ((M >> threadIdx.x) & 1u))
         lrow[__builtin_popcount(M & ((1u << threadIdx.x) - 1u))] = r0 + threadIdx.x;
-    __syncthreads();  // lrow visible; the latent is no longer read
+    __syncthreads();  // lrow visible; the LDS scratch is free
 
     // tiles of 16 active neurons: one tile takes the four waves, two tiles a pair each;
     // the waves of a tile split its 32-column steps into contiguous ranges
     const int ntiles = (n + kTile - 1) / kTile;  // 0, 1 or 2
     if (ntiles == 0)
         return;
-    float *part = reinterpret_cast<float *>(latw);  // [4 waves][2][16 x 16]
     const int wpt = kWavesPerBlock / ntiles;
     const int t0 = (wave / wpt) * kTile, kw = wave % wpt;
     const int i = lane % kTile, g = lane / kTile;
@@ -768,6 +773,263 @@ __global__ __launch_bounds__(kBlock) void k_coef_pred_mfma(const CoefArgs a)
         if (rank < n && tj < a.nb)
             a.s[(size_t)tj * a.d_ff + lrow[rank]] = us * silu(gs);
     }
+}
+
+// Practical D-CountDown coefficient kernel for batches of 4-8 (Sec. 4): the
+// scoring of k_coef_pred, then the block's active neurons in tiles of 16 on MFMA.
+template <int B, int NK, int LCPR>
+__global__ __launch_bounds__(kBlock) void k_coef_pred_mfma(const CoefArgs a)
+{
+    // LDS: tokens [B][kStride] (+ zero chunk), then the latent [B][d_rank] fp32,
+    // whose space later holds the partial sums [4 waves][2][16 x 16] fp32
+    extern __shared__ __align__(16) uint32_t xs[];
+    __shared__ uint32_t wflag[kWavesPerBlock];
+    __shared__ int lrow[kPredRows];
+    using S = PredShape<LCPR>;
+    const int lane = threadIdx.x % kWave, wave = threadIdx.x / kWave;
+    const int r0 = blockIdx.x * kPredRows;
+    const int wr0 = r0 + wave * kPredRowsPerWave;
+
+    using LR = LatentRegs<B, LCPR>;
+    u32x4 wb[S::kLoads];
+    pred_issue_bt<LCPR>(wb, a, wr0, lane);
+    MfmaTokens<B, NK> mt;
+    mt.issue(a);
+    LR lr;
+    lr.issue(a.lat, a.nb, a.d_rank, lane);
+    LatentStage<LR::kRegs ? 1 : B> ls;  // the LDS copy, rank 1024 only
+    if constexpr (!LR::kRegs)
+        ls.issue(a.lat, a.nb, a.d_rank);
+    __builtin_amdgcn_sched_barrier(0);
+    zero_y(a.y, a.nb * a.d_model);
+    const uint32_t *zchunk = mt.write(xs);
+    uint32_t *latw = xs + mfma_lds_tokens_u32<B, NK>();
+    if constexpr (!LR::kRegs)
+        ls.write(reinterpret_cast<u32x4 *>(latw), a.lat, a.nb, a.d_rank);
+    __syncthreads();
+
+    const uint32_t wmask = pred_score<B, LCPR>(wb, lr, reinterpret_cast<const float *>(latw), a,
+                                               wr0, lane);
+    if (lane == 0)
+        wflag[wave] = wmask;
+    __syncthreads();
+    uint32_t M = 0;
+#pragma unroll
+    for (int v = 0; v < kWavesPerBlock; ++v)
+        M |= wflag[v] << (v * kPredRowsPerWave);
+    // the latent is no longer read once gather_mfma's first barrier has passed
+    gather_mfma<B, NK>(a, xs, zchunk, reinterpret_cast<float *>(latw), lrow, M, r0, wave, lane);
+}
+
+// ------------------------------------------------ ternary predictor
+// The TernaryLinear predictor of the paper's appendix: s_hat = x . theta with
+// theta in {-1, 0, +1}^{d_model x d_ff}, thresholded like the low-rank score
+// (signed, union over the batch), then the same gather. theta is stored
+// neuron-major at 2 bits per weight in a layout that matches the token
+// chunks of the lanes: row i is 64 * kWords 32-bit words, lane l owning words
+// [l * kWords, (l + 1) * kWords). Unit j < NK of lane l holds the 8 weights
+// of columns j * 512 + 8 l + [0, 8) (the columns of the lane's token chunk
+// j); word k holds units 2k ("A") and 2k + 1 ("B"). In a word, bits 2m..2m+1
+// of byte 1 / byte 3 are A's weights 2m / 2m + 1, and of byte 0 / byte 2 are
+// B's weights 2m / 2m + 1 (m = 0..3). Codes: 0 -> 0, 1 -> +1, 2 -> -1.
+//
+// Decoding: a shift and a mask put the two codes of one weight pair in
+// bytes 1 and 3 of a v_perm_b32 selector (bytes 0 and 2 zero); the table
+// kTernLut maps code c to the high byte of a bf16 (0, +0.5, -0.5) and the
+// zero selectors give the low bytes, so one v_perm yields a packed bf16 pair
+// for v_dot2_f32_bf16. The products are half the weights', and doubling
+// the fp32 sum at the end is exact.
+template <int NK>
+struct TernShape {
+    static constexpr int kWords = NK >= 2 ? NK / 2 : 1;  // per lane and row
+};
+
+constexpr uint32_t kTernLut = 0x00BF3F00u;  // bytes: code 0 -> 0x00, 1 -> 0x3F, 2 -> 0xBF
+constexpr uint32_t kTernPairMask = 0x03000300u;
+
+template <int NK>
+struct TernRows {
+    static constexpr int kW = TernShape<NK>::kWords;
+    uint32_t w[kPredRowsPerWave][kW];
+
+    // the wave's kPredRowsPerWave rows starting at wr0 (rows past d_ff read zeros)
+    __device__ __forceinline__ void issue(const CoefArgs &a, int wr0, int lane)
+    {
+#pragma unroll
+        for (int r = 0; r < kPredRowsPerWave; ++r) {
+            const bool ok = wr0 + r < a.d_ff;
+            const uint32_t *p = a.Tp + ((size_t)(ok ? wr0 + r : 0) * kWave + lane) * kW;
+            if constexpr (kW >= 4) {
+#pragma unroll
+                for (int q = 0; q < kW / 4; ++q) {
+                    const u32x4 v = __builtin_nontemporal_load(
+                        reinterpret_cast<const u32x4 *>(or_zero(ok, p + 4 * q)));
+                    w[r][4 * q + 0] = v.x;
+                    w[r][4 * q + 1] = v.y;
+                    w[r][4 * q + 2] = v.z;
+                    w[r][4 * q + 3] = v.w;
+                }
+            } else if constexpr (kW == 2) {
+                const uint64_t v = __builtin_nontemporal_load(
+                    reinterpret_cast<const uint64_t *>(or_zero(ok, p)));
+                w[r][0] = (uint32_t)v;
+                w[r][1] = (uint32_t)(v >> 32);
+            } else {
+                w[r][0] = __builtin_nontemporal_load(or_zero(ok, p));
+            }
+        }
+    }
+};
+
+// bf16 pair (weights 2m, 2m + 1 of unit j's half of word W), each 0 or +-0.5
+// (j and m are compile-time constants after unrolling)
+__device__ __forceinline__ uint32_t tern_pair(uint32_t W, int j, int m)
+{
+    const uint32_t sel = (j & 1) ? (W << (8 - 2 * m)) & kTernPairMask : (W >> (2 * m)) & kTernPairMask;
+    return __builtin_amdgcn_perm(0u, kTernLut, sel);
+}
+
+// s_hat_b = x_b . theta[:, row] for the wave's rows (xget(b, j) = this lane's
+// 16-byte chunk j of token b), the signed threshold with the union over the
+// batch, act[] and (optionally) the coefficients. Returns the wave-uniform
+// mask of its active rows. With LDS tokens (SETTLE) the accumulators are
+// materialised after every chunk and xget addresses LDS through an opaque
+// offset, so the reads of chunk j + 1 cannot be hoisted above the products of
+// chunk j (hoisting them all costs 4 * B * NK registers).
+template <int B, int NK, bool SETTLE, class XF>
+__device__ __forceinline__ uint32_t tern_score(const TernRows<NK> &t, XF xget, const CoefArgs &a,
+                                               int wr0, int lane)
+{
+    constexpr int R = kPredRowsPerWave;
+    float acc[R][B];
+#pragma unroll
+    for (int r = 0; r < R; ++r)
+        zero_acc(acc[r]);
+#pragma unroll
+    for (int j = 0; j < NK; ++j) {
+        u32x4 xv[B];
+#pragma unroll
+        for (int b = 0; b < B; ++b)
+            xv[b] = xget(b, j);
+#pragma unroll
+        for (int r = 0; r < R; ++r) {
+            const uint32_t W = t.w[r][j >> 1];
+            const uint32_t p0 = tern_pair(W, j, 0), p1 = tern_pair(W, j, 1);
+            const uint32_t p2 = tern_pair(W, j, 2), p3 = tern_pair(W, j, 3);
+#pragma unroll
+            for (int b = 0; b < B; ++b) {
+                acc[r][b] = dot2_bf16(p0, xv[b].x, acc[r][b]);
+                acc[r][b] = dot2_bf16(p1, xv[b].y, acc[r][b]);
+                acc[r][b] = dot2_bf16(p2, xv[b].z, acc[r][b]);
+                acc[r][b] = dot2_bf16(p3, xv[b].w, acc[r][b]);
+            }
+        }
+        if constexpr (SETTLE) {
+#pragma unroll
+            for (int r = 0; r < R; ++r)
+#pragma unroll
+                for (int b = 0; b < B; ++b)
+                    asm volatile("" : "+v"(acc[r][b]));
+        }
+    }
+    uint32_t wmask = 0;
+#pragma unroll
+    for (int r = 0; r < R; ++r) {
+        const int row = wr0 + r;
+        bool act = false;
+#pragma unroll
+        for (int b = 0; b < B; ++b) {
+            const float v = 2.0f * wave_sum(acc[r][b]);
+            if (b < a.nb) {
+                act = act || (v > a.thld);
+                if (a.coef && lane == 0 && row < a.d_ff)
+                    a.coef[(size_t)b * a.d_ff + row] = v;
+            }
+        }
+        if (row < a.d_ff) {
+            if (lane == 0)
+                a.act[row] = act ? 1 : 0;
+            if (act)
+                wmask |= 1u << r;
+        }
+    }
+    return wmask;
+}
+
+// Ternary-predictor coefficient kernel for batches of 1-4: k_coef_pred with
+// the ternary score in place of the latent . B_t one (no latent kernel).
+template <int B, int NK, bool XREG>
+__global__ __launch_bounds__(kBlock) void k_coef_tern(const CoefArgs a)
+{
+    extern __shared__ __align__(16) uint32_t xs[];  // tokens [B][NK * 256] (LDS path)
+    __shared__ uint32_t wflag[kWavesPerBlock];
+    const int lane = threadIdx.x % kWave, wave = threadIdx.x / kWave;
+    const int r0 = blockIdx.x * kPredRows;
+    const int wr0 = r0 + wave * kPredRowsPerWave;
+
+    TernRows<NK> tr;
+    tr.issue(a, wr0, lane);
+    Tokens<B, NK, XREG> tok;
+    tok.issue(a.x, a.nb, a.d_model, lane);
+    zero_y(a.y, a.nb * a.d_model);
+    tok.commit(xs);
+    uint32_t wmask;
+    if constexpr (XREG) {
+        wmask = tern_score<B, NK, false>(tr, [&](int b, int j) { return tok.r[b][j]; }, a, wr0,
+                                         lane);
+    } else {
+        wmask = tern_score<B, NK, true>(
+            tr,
+            [&](int b, int j) {
+                return *tok.lds_chunk(b, j, lane, Tokens<B, NK, XREG>::opaque_zero());
+            },
+            a, wr0, lane);
+    }
+    const uint32_t m = block_share(wflag, wmask, wave, lane);
+    gather_rr<B, NK, XREG>(a, tok, m, r0, lane);
+}
+
+// Ternary-predictor coefficient kernel for batches of 5-8: the ternary score,
+// then the MFMA gather.
+template <int B, int NK>
+__global__ __launch_bounds__(kBlock) void k_coef_tern_mfma(const CoefArgs a)
+{
+    // LDS: tokens [B][kStride] (+ zero chunk), then the partial sums [4 waves][2][16 x 16]
+    extern __shared__ __align__(16) uint32_t xs[];
+    __shared__ uint32_t wflag[kWavesPerBlock];
+    __shared__ int lrow[kPredRows];
+    using TL = MfmaTokLayout<NK>;
+    const int lane = threadIdx.x % kWave, wave = threadIdx.x / kWave;
+    const int r0 = blockIdx.x * kPredRows;
+    const int wr0 = r0 + wave * kPredRowsPerWave;
+
+    TernRows<NK> tr;
+    tr.issue(a, wr0, lane);
+    MfmaTokens<B, NK> mt;
+    mt.issue(a);
+    __builtin_amdgcn_sched_barrier(0);
+    zero_y(a.y, a.nb * a.d_model);
+    const uint32_t *zchunk = mt.write(xs);
+    __syncthreads();
+
+    const uint32_t wmask = tern_score<B, NK, true>(
+        tr,
+        [&](int b, int j) {
+            return *reinterpret_cast<const u32x4 *>(xs + Tokens<B, NK, false>::opaque_zero() +
+                                                    (size_t)b * TL::kStride +
+                                                    (j * kColsPerLoad + lane * 8) / 2);
+        },
+        a, wr0, lane);
+    if (lane == 0)
+        wflag[wave] = wmask;
+    __syncthreads();
+    uint32_t M = 0;
+#pragma unroll
+    for (int v = 0; v < kWavesPerBlock; ++v)
+        M |= wflag[v] << (v * kPredRowsPerWave);
+    gather_mfma<B, NK>(a, xs, zchunk,
+                       reinterpret_cast<float *>(xs + mfma_lds_tokens_u32<B, NK>()), lrow, M, r0,
+                       wave, lane);
 }
 
 // latent = x . theta_A for the predictor: one workgroup per row of A_t, the
@@ -1489,6 +1751,12 @@ int col_tile(int d_model)
     return chunks <= 1 ? 1 : chunks <= 2 ? 2 : chunks <= 4 ? 4 : chunks <= 8 ? 8 : 16;
 }
 
+int tern_row_words(int d_model)
+{
+    const int nk = col_tile(d_model);
+    return kWave * (nk >= 2 ? nk / 2 : 1);
+}
+
 // tokens live in registers up to a batch of 2, in LDS beyond
 static size_t token_lds_bytes(int bt, int nk)
 {
@@ -1557,6 +1825,22 @@ static hipError_t coef_pred_launch(const CoefArgs &a, hipStream_t s)
     return hipGetLastError();
 }
 
+template <int B, int NK, bool XREG>
+static hipError_t coef_tern_launch(const CoefArgs &a, hipStream_t s)
+{
+    const int grid = (a.d_ff + kPredRows - 1) / kPredRows;
+    if constexpr (B >= 8) {  // MFMA gather, as for the low-rank predictor
+        const size_t lds = mfma_lds_tokens_u32<B, NK>() * 4 + (size_t)kWavesPerBlock * 2 * 256 * 4;
+        allow_lds(k_coef_tern_mfma<B, NK>, lds);
+        k_coef_tern_mfma<B, NK><<<grid, kBlock, lds, s>>>(a);
+    } else {
+        const size_t lds = token_lds_bytes(B, NK);
+        allow_lds(k_coef_tern<B, NK, XREG>, lds);
+        k_coef_tern<B, NK, XREG><<<grid, kBlock, lds, s>>>(a);
+    }
+    return hipGetLastError();
+}
+
 template <int B, int NK>
 static hipError_t coef_bn(int variant, const CoefArgs &a, hipStream_t s)
 {
@@ -1582,6 +1866,8 @@ static hipError_t coef_bn(int variant, const CoefArgs &a, hipStream_t s)
         break;
     case kDualPred:
         return coef_pred_launch<B, NK, XREG>(a, s);
+    case kDualTern:
+        return coef_tern_launch<B, NK, XREG>(a, s);
     default:
         return hipErrorInvalidValue;
     }
@@ -1761,6 +2047,8 @@ hipError_t launch_topk(int variant, const CoefArgs &a, double k, double *q, hipS
 {
     if (a.d_ff > kTopkThreads * kTopkPerThread)
         return hipErrorInvalidValue;
+    if (variant == kDualTern)  // a signed predictor score and the W_gate + W_up gather
+        variant = kDualPred;
     k_topk_select<<<a.nb, kTopkThreads, 0, s>>>(a.coef, a.d_ff, a.d_ff,
                                                  variant == kDualPred ? 0 : 1, k, q);
     hipError_t e = hipGetLastError();

@@ -82,6 +82,8 @@ def algorithmic_bytes(variant: str, d_model: int, d_ff: int, n_active: int, B: i
         k = {"latent": BF16 * d_rank * d_model + x + lat,
              "coef": BF16 * d_ff * d_rank + lat + 2 * n_active * row,
              "down": n_active * row + y}
+    elif variant == "dual_tern":  # theta at 2 bits per weight, no latent
+        k = {"coef": d_ff * d_model // 4 + x + 2 * n_active * row, "down": n_active * row + y}
     else:
         raise ValueError(variant)
     k["total"] = sum(k.values())
@@ -97,5 +99,6 @@ def algorithmic_flops(variant: str, d_model: int, d_ff: int, n_active: int, B: i
         "dual_ideal": 2 * d_ff * d_model + n_active * d_model,
         "dense": 3 * d_ff * d_model,
         "dual_pred": d_rank * d_model + d_ff * d_rank + 3 * n_active * d_model,
+        "dual_tern": d_ff * d_model + 3 * n_active * d_model,
     }[variant]
     return 2 * B * mac

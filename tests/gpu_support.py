@@ -18,7 +18,7 @@ def dev_bf16(a):
 def coef_max(variant, c):
     """Per-neuron union coefficient: max over the batch of |c| (signed for the predictor)."""
     c = np.atleast_2d(c)
-    return (c if variant == "dual_pred" else np.abs(c)).max(axis=0)
+    return (c if variant in ("dual_pred", "dual_tern") else np.abs(c)).max(axis=0)
 
 
 def check_idx(idx_gpu, idx_ref, cmax, thld, label=""):

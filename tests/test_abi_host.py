@@ -5,6 +5,7 @@ import os
 import re
 import subprocess
 
+import numpy as np
 import pytest
 
 from paper_2505_17701_amd import binding as cd
@@ -49,7 +50,7 @@ def test_header_compiles_as_c():
 
 
 def test_abi_version_and_status_strings(lib):
-    assert cd.countdown_abi_version() == 6
+    assert cd.countdown_abi_version() == 7
     for st in (cd.CD_OK, cd.CD_EINVAL, cd.CD_EUNSUPPORTED, cd.CD_EHIP, cd.CD_ENOMEM):
         assert cd.status_string(st).startswith(("CD_OK", "CD_E"))
     assert "unknown" in cd.status_string(12345)
@@ -129,3 +130,66 @@ def test_plan_create_rejects_bad_sizes_before_any_hip_call(lib):
     assert lib.countdown_plan_create(4096, 11008, 1, 0, 0x80, C.byref(h)) == cd.CD_EINVAL
     assert lib.countdown_plan_create(4096, 11008, 1, 0, 2, C.byref(h)) == cd.CD_EINVAL
     assert h.value is None
+
+
+def test_ternary_pointer_rules(lib):
+    tern = cd.CD_VARIANT_DUAL_TERN
+    assert check(tern, A_t=0x6000) == cd.CD_OK               # A_t carries the packed theta
+    assert check(tern, A_t=0x6000, d_rank=256) == cd.CD_OK   # the rank is not used
+    assert check(tern) == cd.CD_EINVAL
+    assert check(tern, A_t=0x6008) == cd.CD_EINVAL
+    assert check(tern, A_t=0x6000, B_t=0x7000) == cd.CD_EINVAL
+    assert check(6, A_t=0x6000) == cd.CD_EINVAL
+    assert lib.countdown_ffn_tern(None, 0x1000, 1, 0x2000, 0x3000, 0x4000, 0x6000, 1.0, 0x5000,
+                                  None) == cd.CD_EINVAL
+    assert lib.countdown_calibrate(None, tern, 0x1000, 4, 0x2000, 0x3000, None, None, 0.5,
+                                   0x5000, None, None) == cd.CD_EINVAL
+
+
+def _unpack_reference(packed, d_model, d_ff):
+    """The packed layout as the header states it, decoded by plain loops."""
+    C = 1
+    while 512 * C < d_model:
+        C *= 2
+    W = max(1, C // 2)
+    row_words = 64 * W
+    assert packed.size == d_ff * row_words
+    value = {0: 0, 1: 1, 2: -1}
+    out = np.zeros((d_ff, d_model), dtype=np.int8)
+    for i in range(d_ff):
+        for l in range(64):
+            for j in range(C):
+                word = int(packed[i * row_words + l * W + j // 2])
+                for e in range(8):
+                    m = e // 2
+                    byte = (1 if j % 2 == 0 else 0) + (2 if e % 2 else 0)
+                    code = (word >> (8 * byte + 2 * m)) & 3
+                    col = j * 512 + 8 * l + e
+                    assert code != 3
+                    if col < d_model:
+                        out[i, col] = value[code]
+                    else:
+                        assert code == 0
+    return out
+
+
+@pytest.mark.parametrize("d_model,d_ff", [(8, 16), (512, 24), (520, 8), (1032, 16), (4096, 8),
+                                          (8192, 8)])
+def test_ternary_pack_layout(lib, d_model, d_ff):
+    from workloads import make_ternary
+
+    T = make_ternary(990, d_model, d_ff)
+    packed = cd.countdown_ternary_pack(T)
+    assert packed.dtype == np.uint32
+    np.testing.assert_array_equal(_unpack_reference(packed, d_model, d_ff), T)
+
+
+def test_ternary_pack_rejects(lib):
+    assert cd.countdown_ternary_words(4100, 8) == 0
+    assert cd.countdown_ternary_words(4096, 11008) == 11008 * 256
+    assert cd.countdown_ternary_words(8192, 8) == 8 * 512
+    assert cd.countdown_ternary_words(256, 8) == 8 * 64
+    bad = np.zeros((8, 16), dtype=np.int8)
+    bad[3, 5] = 2
+    with pytest.raises(cd.CountdownError):
+        cd.countdown_ternary_pack(bad)

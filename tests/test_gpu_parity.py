@@ -38,15 +38,22 @@ def f64(a):
 
 
 class Layer:
-    """A layer's weights on host (bf16 bits) and device."""
+    """A layer's weights on host (bf16 bits) and device; T: an optional ternary
+    predictor theta_t (int8, kept on the host, packed on the device)."""
 
-    def __init__(self, L, P=None):
+    def __init__(self, L, P=None, T=None):
         self.h = dict(L)
         if P:
             self.h.update(P)
         self.d = {k: dev_bf16(v) for k, v in self.h.items()}
         self.d_ff, self.d_model = self.h["W_up"].shape
         self.d_rank = self.h["A_t"].shape[0] if P else 0
+        if T is not None:
+            from paper_2505_17701_amd import binding as cd
+
+            self.h["theta_t"] = T
+            packed = cd.countdown_ternary_pack(T)
+            self.d["theta_p"] = torch.from_numpy(packed.view(np.int32)).to("cuda")
 
 
 def run_gpu(plan, variant, layer, x, thld):
@@ -65,6 +72,9 @@ def run_gpu(plan, variant, layer, x, thld):
         y = cd.countdown_ffn_dense(plan, xd, D["W_gate"], D["W_up"], D["W_down"])
     elif variant == "cats":
         y = cd.countdown_ffn_cats(plan, xd, D["W_gate"], D["W_up"], D["W_down"], thld)
+    elif variant == "dual_tern":
+        y = cd.countdown_ffn_tern(plan, xd, D["W_gate"], D["W_up"], D["W_down"], D["theta_p"],
+                                  thld)
     else:
         raise ValueError(variant)
     idx, s_c, coef = cd.countdown_export_active(plan)
@@ -86,6 +96,9 @@ def run_oracle(variant, layer, x, thld):
         return idx, oracle.dense(x, H["W_gate"], H["W_up"], H["W_down"]), None
     if variant == "cats":
         return oracle.ffn_cats(x, H["W_gate"], H["W_up"], H["W_down"], thld, want_coef=True)
+    if variant == "dual_tern":
+        return oracle.ffn_dual_tern(x, H["W_gate"], H["W_up"], H["W_down"], H["theta_t"], thld,
+                                    want_coef=True)
     raise ValueError(variant)
 
 
@@ -127,6 +140,8 @@ def check_call(variant, layer, x, thld, gpu_out, label, check_coef=True):
         elif variant == "cats":
             # h = SiLU(g): |dh| <= max|SiLU'| |dg|, max|SiLU'| < 1.1
             bound = COEF_TOL * 1.1 * dot_bound(xf, f64(H["W_gate"]))
+        elif variant == "dual_tern":
+            bound = COEF_TOL * dot_bound(xf, H["theta_t"].astype(np.float64))
         else:
             lat = oracle.predictor(x, H["A_t"], H["B_t"])[0]
             bound = COEF_TOL * (np.abs(lat) @ np.abs(f64(H["B_t"])).T

@@ -31,6 +31,8 @@ def oracle_coef(variant, layer, x):
     H = layer.h
     if variant == "dual_pred":
         return oracle.predictor(x, H["A_t"], H["B_t"])[1]
+    if variant == "dual_tern":
+        return oracle.ternary_predictor(x, H["theta_t"])
     u, g, s = oracle.coefficients(x, H["W_gate"], H["W_up"])
     return np.abs({"mono": u, "dual_ideal": s, "cats": g / (1.0 + np.exp(-g))}[variant])
 
@@ -42,8 +44,12 @@ def run_topk(variant, layer, x, k):
     plan = cd.Plan(layer.d_model, layer.d_ff, max_batch=B, d_rank=layer.d_rank)
     q = torch.zeros(B, dtype=torch.float64, device="cuda")
     D = layer.d
-    y = cd.countdown_ffn_topk(plan, VID[variant], dev_bf16(x), D["W_gate"], D["W_up"],
-                              D["W_down"], k, A_t=D.get("A_t"), B_t=D.get("B_t"), thld_out=q)
+    if variant == "dual_tern":
+        y = cd.countdown_ffn_tern_topk(plan, dev_bf16(x), D["W_gate"], D["W_up"], D["W_down"],
+                                       D["theta_p"], k, thld_out=q)
+    else:
+        y = cd.countdown_ffn_topk(plan, VID[variant], dev_bf16(x), D["W_gate"], D["W_up"],
+                                  D["W_down"], k, A_t=D.get("A_t"), B_t=D.get("B_t"), thld_out=q)
     idx, s_c, _ = cd.countdown_export_active(plan)
     out = (y.cpu().numpy().astype(np.float64), idx.cpu().numpy(), s_c.cpu().numpy(),
            q.cpu().numpy())
@@ -57,7 +63,8 @@ def check_topk(variant, layer, x, k, label):
     y_g, idx_g, s_g, q_g = run_topk(variant, layer, x, k)
     H = layer.h
     idx_o, y_o, q_o = oracle.ffn_topk(variant, x, H["W_gate"], H["W_up"], H["W_down"], k,
-                                      A_t=H.get("A_t"), B_t=H.get("B_t"))
+                                      A_t=H.get("A_t"), B_t=H.get("B_t"),
+                                      theta_t=H.get("theta_t"))
     c = oracle_coef(variant, layer, x)
     scale = np.maximum(np.abs(q_o), np.sqrt(np.mean(c * c, axis=1)))
     assert np.all(np.abs(q_g - q_o) <= Q_TOL * scale), f"{label}: thresholds {q_g} vs {q_o}"
