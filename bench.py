@@ -365,8 +365,10 @@ def predictor_training_bench(args, n_train=8192, n_test=256, epochs=4):
     untrained start, not the paper's F1 values."""
     import torch
 
-    from paper_2505_17701_amd.predictor import (calibrated_threshold, f1_score, ideal_masks,
-                                                 predicted_masks, train_low_rank)
+    from paper_2505_17701_amd.predictor import (calibrated_threshold, calibrated_threshold_tern,
+                                                 f1_score, ideal_masks, packed_ternary,
+                                                 predicted_masks, predicted_masks_tern,
+                                                 train_low_rank, train_ternary)
     from workloads import WORKLOADS
     from workloads.synth import T_CALIB
 
@@ -395,6 +397,20 @@ def predictor_training_bench(args, n_train=8192, n_test=256, epochs=4):
                        "alive_frac_thld0": round(float(P_0.mean()), 4)}
         r.update({"epoch_loss": [round(v, 5) for v in tl["epoch_loss"]],
                   "train_seconds": round(tl["seconds"], 2), "mask_seconds": round(t_mask, 2)})
+        # the ternary predictor (Sec. 6) by the same procedure, straight-through estimator
+        T, tt = train_ternary(Xtr, Ytr, epochs=epochs)
+        tern = {}
+        for name, theta in (("random", w.ternary()), ("trained", T)):
+            tp = packed_ternary(theta)
+            th = calibrated_threshold_tern(tp, Xtr[:256], k, w.d_ff)
+            P = predicted_masks_tern(L, tp, Xte, th).cpu().numpy()
+            tern[name] = {"thld": round(th, 5), "f1": round(f1_score(P, ytrue), 4),
+                          "alive_frac": round(float(P.mean()), 4)}
+            del tp
+        tern.update({"epoch_loss": [round(v, 5) for v in tt["epoch_loss"]],
+                     "train_seconds": round(tt["seconds"], 2),
+                     "zero_frac": round(tt["zero_frac"], 4)})
+        r["ternary"] = tern
         out[f"k={k}"] = r
         log(f"[bench] predictor training k={k}: {json.dumps(out[f'k={k}'])}")
         del A0, B0, A, B, Ytr, Yte

@@ -10,6 +10,14 @@ logit). Training is plain PyTorch: only inference runs on the HIP kernels.
 
 Layout: the returned predictor is in the kernels' layout, A_t [d_rank][d_model]
 and B_t [d_ff][d_rank], bf16.
+
+The ternary predictor of Sec. 6 (TernaryLinear, trained by the same Alg. 1)
+keeps full-precision latent weights W and scores with their ternarisation
+gamma * RoundClip(W / gamma, -1, 1), gamma = mean |W| (the absmean rule of
+ternary "BitLinear" layers, whose name the paper's hyperparameter table
+uses); the rounding passes gradients straight through. The result is the
+int8 theta_t [d_ff][d_model] that countdown_ternary_pack takes (gamma > 0
+only rescales the score, which the threshold absorbs).
 """
 from __future__ import annotations
 
@@ -96,6 +104,92 @@ def calibrated_threshold(A_t, B_t, X, k: float) -> float:
     th, _ = cd.countdown_calibrate(plan, cd.CD_VARIANT_DUAL_PRED, X, k, A_t=A_t, B_t=B_t)
     plan.close()
     return float(th.item())
+
+
+def ternarize(W):
+    """(RoundClip(W / gamma, -1, 1), gamma) with gamma = mean |W|."""
+    import torch
+
+    gamma = W.abs().mean().clamp_min(1e-8)
+    return torch.clamp(torch.round(W / gamma), -1, 1), gamma
+
+
+def train_ternary(X, masks, epochs: int = 10, lr: float = 1e-3, batch: int = 16, seed: int = 42,
+                  weight_decay: float = 0.01):
+    """Fit s_hat = x . (gamma * ternary(W)) to the masks (BCE-with-logits, AdamW, the
+    straight-through estimator). X: [N, d_model] bf16 on the GPU; masks [N, d_ff] bool.
+    Returns (theta_t int8 numpy [d_ff, d_model], log dict)."""
+    import torch
+
+    g = torch.Generator(device=X.device).manual_seed(seed)
+    N, dm = X.shape
+    dff = masks.shape[1]
+    xf = X.float()
+    yf = masks.float()
+    W = (torch.randn(dff, dm, generator=g, device=X.device) / dm ** 0.5).requires_grad_()
+    opt = torch.optim.AdamW([W], lr=lr, weight_decay=weight_decay)
+    loss_fn = torch.nn.BCEWithLogitsLoss()
+    losses = []
+    t0 = time.time()
+    for _ in range(epochs):
+        perm = torch.randperm(N, generator=g, device=X.device)
+        tot, nb = 0.0, 0
+        for i in range(0, N, batch):
+            j = perm[i:i + batch]
+            q, gamma = ternarize(W)
+            Wq = W + (q * gamma - W).detach()  # straight-through estimator
+            loss = loss_fn(xf[j] @ Wq.t(), yf[j])
+            opt.zero_grad(set_to_none=True)
+            loss.backward()
+            opt.step()
+            tot += float(loss.detach())
+            nb += 1
+        losses.append(tot / nb)
+    torch.cuda.synchronize()
+    theta_t = ternarize(W.detach())[0].to(torch.int8).cpu().numpy()
+    return theta_t, {"epoch_loss": losses, "seconds": time.time() - t0,
+                     "zero_frac": float((theta_t == 0).mean())}
+
+
+def calibrated_threshold_tern(theta_p, X, k: float, d_ff: int) -> float:
+    """The Sec. 4 layerwise threshold of the ternary score at k over the tokens X
+    (theta_p: the packed predictor on the device)."""
+    from . import binding as cd
+
+    dm = X.shape[1]
+    plan = cd.Plan(dm, d_ff, max_batch=max(1, min(8, 32768 // dm)))
+    th, _ = cd.countdown_calibrate_tern(plan, X, theta_p, k)
+    plan.close()
+    return float(th.item())
+
+
+def packed_ternary(theta_t, device="cuda"):
+    """countdown_ternary_pack of theta_t, moved to the device."""
+    import torch
+
+    from . import binding as cd
+
+    return torch.from_numpy(cd.countdown_ternary_pack(theta_t).view(np.int32)).to(device)
+
+
+def predicted_masks_tern(layer: dict, theta_p, X, thld: float = 0.0):
+    """The ternary predictor's alive masks {s_hat > thld} of every token of X, from the
+    HIP ternary path (countdown_ffn_tern) at batch 1."""
+    import torch
+
+    from . import binding as cd
+
+    T, dm = X.shape
+    dff = layer["W_up"].shape[0]
+    plan = cd.Plan(dm, dff, max_batch=1)
+    masks = torch.zeros((T, dff), dtype=torch.bool, device=X.device)
+    for t in range(T):
+        cd.countdown_ffn_tern(plan, X[t:t + 1], layer["W_gate"], layer["W_up"], layer["W_down"],
+                              theta_p, thld)
+        idx, _, _ = cd.countdown_export_active(plan)
+        masks[t, idx.long()] = True
+    plan.close()
+    return masks
 
 
 def predicted_masks(layer: dict, A_t, B_t, X, thld: float = 0.0):
