@@ -1228,63 +1228,83 @@ __global__ __launch_bounds__(kBlock) void k_latent_norm(const NormArgs n,
     }
 }
 
-// Gathered down projection (Eq. 5). Workgroup (c, g) owns a 512-column chunk
-// c and a contiguous neuron range g: one round trip reads act and s of the
-// range, a wave ballot compacts the active neurons in ascending order into
-// LDS, each wave then keeps U rows in flight (1 KB of a row per load), the
-// four waves reduce in LDS and add the chunk to y with one fp32 atomic per
-// column and token.
-template <int B>
+// Gathered down projection (Eq. 5). Workgroup (c, g) owns a chunk c of
+// 512 / R columns and a contiguous neuron range g. Its threads first issue
+// the loads of act and s of all the range's neurons (up to kDownRowsPerThread
+// each), then a wave ballot compacts the active ones in ascending order into
+// LDS. Each wave load covers R rows of the chunk (64 / R lanes per row, 16 B
+// each), U loads in flight per wave; the 4 R partial sums of every column
+// are added in LDS and the chunk goes to y with one fp32 atomic per column
+// and token. The atomics into the small y are the expensive part at larger
+// batches (measured: a few 1e11 updates/s), so the launcher trades neuron
+// ranges, which multiply them, for narrower column chunks.
+constexpr int kDownRowsPerThread = 8;  // neurons per range <= 8 * kBlock
+
+template <int B, int R>
 __global__ __launch_bounds__(kBlock) void k_down(const DownArgs a)
 {
     constexpr int U = 8;
+    constexpr int LPR = kWave / R;  // lanes per row
+    constexpr int CW = LPR * 8;     // columns of the chunk
+    constexpr int T = kDownRowsPerThread;
     extern __shared__ __align__(16) int dsm[];
-    __shared__ int wcnt[kWavesPerBlock];
+    __shared__ int wcnt[T][kWavesPerBlock];
     const int cap = a.rows_per_group;
     int *lrow = dsm;                                                 // [cap]
     float *lsv = reinterpret_cast<float *>(dsm + cap);               // [B][cap]
-    float *red = reinterpret_cast<float *>(dsm + cap * (1 + B));     // [4][512]
+    float *red = reinterpret_cast<float *>(dsm + cap * (1 + B));     // [4 R][CW]
     const int lane = threadIdx.x % kWave, wave = threadIdx.x / kWave;
     const int c = blockIdx.x % a.gc, g = blockIdx.x / a.gc;
     const int r0 = g * cap;
     const int r1 = min(a.d_ff, r0 + cap);
 
-    int nl = 0;
-    for (int t0 = r0; t0 < r1; t0 += kBlock) {
-        const int row = t0 + threadIdx.x;
-        bool valid = false;
-        float sv[B];
+    // act and s of this thread's neurons r0 + t * kBlock + tid: every load first
+    int av[T];
+    float sv[T][B];
+#pragma unroll
+    for (int t = 0; t < T; ++t) {
+        av[t] = 0;
 #pragma unroll
         for (int b = 0; b < B; ++b)
-            sv[b] = 0.0f;
-        if (row < r1) {
-            valid = a.act[row] != 0;
+            sv[t][b] = 0.0f;
+        if (t * kBlock < cap) {  // uniform
+            const int row = r0 + t * kBlock + threadIdx.x;
+            const bool ok = row < r1;
+            av[t] = *or_zero(ok, a.act + row);
 #pragma unroll
             for (int b = 0; b < B; ++b)
-                if (b < a.nb)
-                    sv[b] = a.s[(size_t)b * a.d_ff + row];
+                sv[t][b] = *or_zero(ok && b < a.nb, a.s + (size_t)b * a.d_ff + row);
         }
-        const uint64_t m = ballot(valid);
+    }
+    uint64_t m[T];
+#pragma unroll
+    for (int t = 0; t < T; ++t) {
+        m[t] = ballot(av[t] != 0);
         if (lane == 0)
-            wcnt[wave] = __popcll(m);
-        __syncthreads();
+            wcnt[t][wave] = __popcll(m[t]);
+    }
+    __syncthreads();
+    int nl = 0;
+#pragma unroll
+    for (int t = 0; t < T; ++t) {
         int base = nl;
         for (int v = 0; v < wave; ++v)
-            base += wcnt[v];
-        if (valid) {
-            const int pos = base + lanes_below(m);
-            lrow[pos] = row;
+            base += wcnt[t][v];
+        if (av[t] != 0) {
+            const int pos = base + lanes_below(m[t]);
+            lrow[pos] = r0 + t * kBlock + threadIdx.x;
 #pragma unroll
             for (int b = 0; b < B; ++b)
-                lsv[b * cap + pos] = sv[b];
+                lsv[b * cap + pos] = sv[t][b];
         }
-        nl += wcnt[0] + wcnt[1] + wcnt[2] + wcnt[3];
-        __syncthreads();
+        nl += wcnt[t][0] + wcnt[t][1] + wcnt[t][2] + wcnt[t][3];
     }
+    __syncthreads();
     if (nl == 0)
         return;  // uniform for the workgroup
 
-    const int col = c * kColsPerLoad + lane * 8;
+    const int rs = lane / LPR, cl = lane % LPR;
+    const int col = c * CW + cl * 8;
     const bool colok = col < a.d_model;
     float acc[B][8];
 #pragma unroll
@@ -1293,27 +1313,26 @@ __global__ __launch_bounds__(kBlock) void k_down(const DownArgs a)
         for (int e = 0; e < 8; ++e)
             acc[b][e] = 0.0f;
 
-    for (int q0 = wave; q0 < nl; q0 += kWavesPerBlock * U) {
+    // list position of load q of step k0: ((k0 + q) * 4 + wave) * R + rs
+    for (int k0 = 0; k0 * kWavesPerBlock * R < nl; k0 += U) {
         u32x4 w[U];
 #pragma unroll
         for (int q = 0; q < U; ++q) {
-            const int r = q0 + q * kWavesPerBlock;
-            w[q] = (r < nl && colok) ? load16_stream(a.Wd + (size_t)lrow[r] * a.d_model + col)
+            const int p = ((k0 + q) * kWavesPerBlock + wave) * R + rs;
+            w[q] = (p < nl && colok) ? load16_stream(a.Wd + (size_t)lrow[p] * a.d_model + col)
                                      : zero16();
         }
 #pragma unroll
         for (int q = 0; q < U; ++q) {
-            const int r = q0 + q * kWavesPerBlock;
-            if (r >= nl)
-                break;
+            const int p = ((k0 + q) * kWavesPerBlock + wave) * R + rs;
             const float wf[8] = {bf16_lo(w[q].x), bf16_hi(w[q].x), bf16_lo(w[q].y), bf16_hi(w[q].y),
                                  bf16_lo(w[q].z), bf16_hi(w[q].z), bf16_lo(w[q].w), bf16_hi(w[q].w)};
 #pragma unroll
             for (int b = 0; b < B; ++b) {
-                const float sv = lsv[b * cap + r];
+                const float s = p < nl ? lsv[b * cap + p] : 0.0f;
 #pragma unroll
                 for (int e = 0; e < 8; ++e)
-                    acc[b][e] = fmaf(sv, wf[e], acc[b][e]);
+                    acc[b][e] = fmaf(s, wf[e], acc[b][e]);
             }
         }
     }
@@ -1325,17 +1344,199 @@ __global__ __launch_bounds__(kBlock) void k_down(const DownArgs a)
         __syncthreads();
 #pragma unroll
         for (int e = 0; e < 8; ++e)
-            red[wave * kColsPerLoad + lane * 8 + e] = acc[b][e];
+            red[(wave * R + rs) * CW + cl * 8 + e] = acc[b][e];
         __syncthreads();
-        for (int cc = threadIdx.x; cc < kColsPerLoad; cc += kBlock) {
-            const int gcol = c * kColsPerLoad + cc;
+        for (int cc = threadIdx.x; cc < CW; cc += kBlock) {
+            const int gcol = c * CW + cc;
             if (gcol < a.d_model) {
-                const float v = red[cc] + red[kColsPerLoad + cc] + red[2 * kColsPerLoad + cc] +
-                                red[3 * kColsPerLoad + cc];
+                float v = 0.0f;
+#pragma unroll
+                for (int k = 0; k < kWavesPerBlock * R; ++k)
+                    v += red[k * CW + cc];
                 unsafeAtomicAdd(a.y + (size_t)b * a.d_model + gcol, v);
             }
         }
     }
+}
+
+// Gathered down projection for batches of 2-8 on MFMA. The product
+// Y[B x d_model] = S[B x n] . W_down[IDX, :] is a dense contraction over the
+// active neurons: v_mfma_f32_16x16x32_bf16 with A = S (row i = token i, zero
+// rows past the batch) and B = the W_down rows. Workgroup (c, g) owns 128
+// columns c and neuron range g (compacted as in k_down); its waves take every
+// fourth step of 32 list positions and add their 16 x 128 results in LDS
+// before the atomics. In a step, lane l = j + 16 q loads rows
+// 8 q .. 8 q + 7 of the step at columns 8 j .. 8 j + 7 (one 16-byte load per
+// row); v_perm then regroups them per column e into the B operand of an
+// MFMA whose output columns are 8 j + e, so the loaded data needs no LDS
+// transpose. S enters as bf16 hi + lo (s - hi rounded again), two MFMAs per
+// operand, so each product keeps about 16 mantissa bits.
+template <int BT>
+__global__ __launch_bounds__(kBlock) void k_down_mfma(const DownArgs a)
+{
+    constexpr int T = kDownRowsPerThread;
+    extern __shared__ __align__(16) int dsm[];
+    __shared__ int wcnt[T][kWavesPerBlock];
+    const int cap = a.rows_per_group;
+    const int capp = (cap + 31) & ~31;                                     // padded list length
+    int *lrow = dsm;                                                       // [capp]
+    uint16_t *shi = reinterpret_cast<uint16_t *>(dsm + capp);              // [BT][capp] bf16
+    uint16_t *slo = shi + (size_t)BT * capp;                               // [BT][capp] bf16
+    uint32_t *zrow = reinterpret_cast<uint32_t *>(slo + (size_t)BT * capp);  // 16 zero bytes
+    float *out = reinterpret_cast<float *>(zrow + 4);                      // [4 waves][BT][128]
+    constexpr int kStep = 32, kWc = 128;  // list positions per step, columns per workgroup
+    const int lane = threadIdx.x % kWave, wave = threadIdx.x / kWave;
+    const int c = blockIdx.x % a.gc, g = blockIdx.x / a.gc;
+    const int r0 = g * cap;
+    const int r1 = min(a.d_ff, r0 + cap);
+
+    int av[T];
+    float sv[T][BT];
+#pragma unroll
+    for (int t = 0; t < T; ++t) {
+        av[t] = 0;
+#pragma unroll
+        for (int b = 0; b < BT; ++b)
+            sv[t][b] = 0.0f;
+        if (t * kBlock < cap) {  // uniform
+            const int row = r0 + t * kBlock + threadIdx.x;
+            const bool ok = row < r1;
+            av[t] = *or_zero(ok, a.act + row);
+#pragma unroll
+            for (int b = 0; b < BT; ++b)
+                sv[t][b] = *or_zero(ok && b < a.nb, a.s + (size_t)b * a.d_ff + row);
+        }
+    }
+    uint64_t m[T];
+#pragma unroll
+    for (int t = 0; t < T; ++t) {
+        m[t] = ballot(av[t] != 0);
+        if (lane == 0)
+            wcnt[t][wave] = __popcll(m[t]);
+    }
+    if (threadIdx.x < 4)
+        zrow[threadIdx.x] = 0u;
+    __syncthreads();
+    int nl = 0;
+#pragma unroll
+    for (int t = 0; t < T; ++t) {
+        int base = nl;
+        for (int v = 0; v < wave; ++v)
+            base += wcnt[t][v];
+        if (av[t] != 0) {
+            const int pos = base + lanes_below(m[t]);
+            lrow[pos] = r0 + t * kBlock + threadIdx.x;
+#pragma unroll
+            for (int b = 0; b < BT; ++b) {
+                const __bf16 h = (__bf16)sv[t][b];
+                const __bf16 l = (__bf16)(sv[t][b] - (float)h);
+                shi[b * capp + pos] = __builtin_bit_cast(uint16_t, h);
+                slo[b * capp + pos] = __builtin_bit_cast(uint16_t, l);
+            }
+        }
+        nl += wcnt[t][0] + wcnt[t][1] + wcnt[t][2] + wcnt[t][3];
+    }
+    // zero coefficients (and a valid row) for the padding of the last step
+    const int nlp = (nl + 31) & ~31;
+    for (int p = nl + threadIdx.x; p < nlp; p += kBlock) {
+        lrow[p] = r0;
+#pragma unroll
+        for (int b = 0; b < BT; ++b) {
+            shi[b * capp + p] = 0;
+            slo[b * capp + p] = 0;
+        }
+    }
+    __syncthreads();
+    if (nl == 0)
+        return;  // uniform for the workgroup
+
+    const int j = lane % 16, q = lane / 16;
+    const int col = c * kWc + j * 8;
+    const bool colok = col < a.d_model;
+    // A operand source: token j's coefficients (zero row past the batch)
+    const bool real = j < a.nb;
+    f32x4_t acc[8];
+#pragma unroll
+    for (int e = 0; e < 8; ++e)
+        acc[e] = f32x4_t{0.0f, 0.0f, 0.0f, 0.0f};
+
+    u32x4 cur[8], nxt[8];
+    auto load_step = [&](u32x4 (&w)[8], int p0) {
+#pragma unroll
+        for (int r = 0; r < 8; ++r) {
+            const int p = p0 + 8 * q + r;
+            w[r] = zero16();
+            if (p < nl && colok)
+                w[r] = load16_stream(a.Wd + (size_t)lrow[p] * a.d_model + col);
+        }
+    };
+    auto consume = [&](const u32x4 (&w)[8], int p0) {
+        const int pa = p0 + 8 * q;
+        const u32x4 ah = *reinterpret_cast<const u32x4 *>(real ? shi + (size_t)j * capp + pa
+                                                               : reinterpret_cast<uint16_t *>(zrow));
+        const u32x4 al = *reinterpret_cast<const u32x4 *>(real ? slo + (size_t)j * capp + pa
+                                                               : reinterpret_cast<uint16_t *>(zrow));
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+            // column 8 j + e of the lane's 8 rows: 16-bit halves of word e / 2
+            const uint32_t sel = (e & 1) ? 0x07060302u : 0x05040100u;
+            u32x4 bw;
+            bw.x = __builtin_amdgcn_perm(w[1][e / 2], w[0][e / 2], sel);
+            bw.y = __builtin_amdgcn_perm(w[3][e / 2], w[2][e / 2], sel);
+            bw.z = __builtin_amdgcn_perm(w[5][e / 2], w[4][e / 2], sel);
+            bw.w = __builtin_amdgcn_perm(w[7][e / 2], w[6][e / 2], sel);
+            acc[e] = mfma16(ah, bw, acc[e]);
+            acc[e] = mfma16(al, bw, acc[e]);
+        }
+    };
+    // this wave's steps start at positions wave * kStep + k * 4 * kStep
+    constexpr int kStride = kWavesPerBlock * kStep;
+    const int pw = wave * kStep;
+    if (pw < nl) {  // uniform per wave
+        load_step(cur, pw);
+        for (int p0 = pw; p0 < nl; p0 += 2 * kStride) {
+            const bool more = p0 + kStride < nl;  // uniform
+            if (more)
+                load_step(nxt, p0 + kStride);
+            consume(cur, p0);
+            if (!more)
+                break;
+            if (p0 + 2 * kStride < nl)
+                load_step(cur, p0 + 2 * kStride);
+            consume(nxt, p0 + kStride);
+        }
+    }
+
+    // D[token 4 q + r][column 8 j + e] of the four waves -> LDS, summed, then
+    // one contiguous fp32 atomic per column and token
+    float *ow = out + (size_t)wave * BT * kWc;
+#pragma unroll
+    for (int e = 0; e < 8; ++e)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+            const int tok = 4 * q + r;
+            if (tok < BT)
+                ow[tok * kWc + j * 8 + e] = acc[e][r];
+        }
+    __syncthreads();
+    for (int i = threadIdx.x; i < BT * kWc; i += kBlock) {
+        const int b = i / kWc, cc = i % kWc;
+        const int gcol = c * kWc + cc;
+        if (b < a.nb && gcol < a.d_model) {
+            const float v = out[i] + out[BT * kWc + i] + out[2 * BT * kWc + i] +
+                            out[3 * BT * kWc + i];
+            unsafeAtomicAdd(a.y + (size_t)b * a.d_model + gcol, v);
+        }
+    }
+}
+
+// batches from which the down projection runs on MFMA
+constexpr int kDownMfmaMinBatch = 4;
+
+size_t down_mfma_lds_bytes(int rows_per_group, int bt)
+{
+    const size_t capp = (size_t)((rows_per_group + 31) & ~31);
+    return capp * 4 + 2 * (size_t)bt * capp * 2 + 16 + (size_t)kWavesPerBlock * bt * 128 * 4;
 }
 
 constexpr int kExportThreads = 1024;
@@ -1768,23 +1969,27 @@ size_t down_lds_bytes(int rows_per_group, int bt)
     return (size_t)rows_per_group * 4 * (1 + bt) + (size_t)kWavesPerBlock * kColsPerLoad * 4;
 }
 
-// Down-kernel grid: 512-column chunks x 64 neuron ranges of at least 16
-// neurons (measured best at 4096 x 11008, 4096 x 14336 and 8192 x 28672 among
-// 16-128 ranges and 128-512-column chunks), more ranges when a range's lists
-// would not fit in 64 KB of LDS.
-void down_grid(int d_model, int d_ff, int bt, int *gc, int *gr, int *rows_per_group)
+// Down-kernel grid: R rows per wave load (chunks of 512 / R columns) and gr
+// neuron ranges of at least 16 neurons; the atomics into y number
+// gr * B * d_model. Measured best among R in {1, 2, 4, 8} and 8-64 ranges at
+// 4096 x 11008 and 4096 x 14336 (batches 1, 4, 8): 2 rows per load and 32
+// ranges; at 8192 x 28672: 1 row per load and 64 ranges. Ranges are raised
+// when a range's lists would not fit in 64 KB of LDS.
+void down_grid(int d_model, int d_ff, int bt, int *R, int *gc, int *gr, int *rows_per_group)
 {
-    *gc = (d_model + kColsPerLoad - 1) / kColsPerLoad;
-    int r = 64;
+    int r = d_model <= 4096 ? 32 : 64, rr = d_model <= 4096 ? 2 : 1;
     if (r > d_ff / 16)
         r = d_ff / 16;
     if (r < 1)
         r = 1;
     const int max_rows = (int)((65536 - down_lds_bytes(0, bt)) / (4 * (1 + bt)));
-    if ((d_ff + r - 1) / r > max_rows)
-        r = (d_ff + max_rows - 1) / max_rows;
+    const int lim = max_rows < kDownRowsPerThread * kBlock ? max_rows : kDownRowsPerThread * kBlock;
+    if ((d_ff + r - 1) / r > lim)
+        r = (d_ff + lim - 1) / lim;
+    *R = rr;
     *rows_per_group = (d_ff + r - 1) / r;
     *gr = (d_ff + *rows_per_group - 1) / *rows_per_group;
+    *gc = (d_model + kColsPerLoad / rr - 1) / (kColsPerLoad / rr);
 }
 
 template <int B, int NK, bool XREG, int LCPR>
@@ -1973,18 +2178,63 @@ hipError_t launch_latent_norm(const NormArgs &n, const uint16_t *At, int d_rank,
     return norm_dispatch(n, At, d_rank, lat, s);
 }
 
+template <int B>
+static void down_b(const DownArgs &a, int R, size_t lds, hipStream_t s)
+{
+    const int grid = a.gc * a.gr;
+    switch (R) {
+    case 1: allow_lds(k_down<B, 1>, lds); k_down<B, 1><<<grid, kBlock, lds, s>>>(a); break;
+    case 2: allow_lds(k_down<B, 2>, lds); k_down<B, 2><<<grid, kBlock, lds, s>>>(a); break;
+    case 4: allow_lds(k_down<B, 4>, lds); k_down<B, 4><<<grid, kBlock, lds, s>>>(a); break;
+    default: allow_lds(k_down<B, 8>, lds); k_down<B, 8><<<grid, kBlock, lds, s>>>(a); break;
+    }
+}
+
+// MFMA down kernel grid: 128-column chunks and gr neuron ranges, raised until
+// the range's lists fit in 64 KB of LDS
+static void down_grid_mfma(int d_model, int d_ff, int bt, int *gc, int *gr, int *rows_per_group)
+{
+    int r = 16;
+    if (r > d_ff / 16)
+        r = d_ff / 16;
+    if (r < 1)
+        r = 1;
+    for (;;) {
+        const int rows = (d_ff + r - 1) / r;
+        if (rows <= kDownRowsPerThread * kBlock && down_mfma_lds_bytes(rows, bt) <= 65536)
+            break;
+        ++r;
+    }
+    *rows_per_group = (d_ff + r - 1) / r;
+    *gr = (d_ff + *rows_per_group - 1) / *rows_per_group;
+    *gc = (d_model + 127) / 128;
+}
+
+bool down_uses_mfma(int bt) { return bt >= kDownMfmaMinBatch; }
+
 hipError_t launch_down(const DownArgs &args, hipStream_t s)
 {
     const int bt = batch_tile(args.nb);
     DownArgs a = args;
-    down_grid(a.d_model, a.d_ff, bt, &a.gc, &a.gr, &a.rows_per_group);
+    if (down_uses_mfma(bt)) {
+        down_grid_mfma(a.d_model, a.d_ff, bt, &a.gc, &a.gr, &a.rows_per_group);
+        const size_t lds = down_mfma_lds_bytes(a.rows_per_group, bt);
+        const int grid = a.gc * a.gr;
+        switch (bt) {
+        case 2: allow_lds(k_down_mfma<2>, lds); k_down_mfma<2><<<grid, kBlock, lds, s>>>(a); break;
+        case 4: allow_lds(k_down_mfma<4>, lds); k_down_mfma<4><<<grid, kBlock, lds, s>>>(a); break;
+        default: allow_lds(k_down_mfma<8>, lds); k_down_mfma<8><<<grid, kBlock, lds, s>>>(a); break;
+        }
+        return hipGetLastError();
+    }
+    int R = 1;
+    down_grid(a.d_model, a.d_ff, bt, &R, &a.gc, &a.gr, &a.rows_per_group);
     const size_t lds = down_lds_bytes(a.rows_per_group, bt);
-    const int grid = a.gc * a.gr;
     switch (bt) {
-    case 1: allow_lds(k_down<1>, lds); k_down<1><<<grid, kBlock, lds, s>>>(a); break;
-    case 2: allow_lds(k_down<2>, lds); k_down<2><<<grid, kBlock, lds, s>>>(a); break;
-    case 4: allow_lds(k_down<4>, lds); k_down<4><<<grid, kBlock, lds, s>>>(a); break;
-    default: allow_lds(k_down<8>, lds); k_down<8><<<grid, kBlock, lds, s>>>(a); break;
+    case 1: down_b<1>(a, R, lds, s); break;
+    case 2: down_b<2>(a, R, lds, s); break;
+    case 4: down_b<4>(a, R, lds, s); break;
+    default: down_b<8>(a, R, lds, s); break;
     }
     return hipGetLastError();
 }
