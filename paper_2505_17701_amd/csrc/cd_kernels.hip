@@ -1228,83 +1228,63 @@ __global__ __launch_bounds__(kBlock) void k_latent_norm(const NormArgs n,
     }
 }
 
-// Gathered down projection (Eq. 5). Workgroup (c, g) owns a chunk c of
-// 512 / R columns and a contiguous neuron range g. Its threads first issue
-// the loads of act and s of all the range's neurons (up to kDownRowsPerThread
-// each), then a wave ballot compacts the active ones in ascending order into
-// LDS. Each wave load covers R rows of the chunk (64 / R lanes per row, 16 B
-// each), U loads in flight per wave; the 4 R partial sums of every column
-// are added in LDS and the chunk goes to y with one fp32 atomic per column
-// and token. The atomics into the small y are the expensive part at larger
-// batches (measured: a few 1e11 updates/s), so the launcher trades neuron
-// ranges, which multiply them, for narrower column chunks.
-constexpr int kDownRowsPerThread = 8;  // neurons per range <= 8 * kBlock
-
-template <int B, int R>
+// Gathered down projection (Eq. 5). Workgroup (c, g) owns a 512-column chunk
+// c and a contiguous neuron range g: one round trip reads act and s of the
+// range, a wave ballot compacts the active neurons in ascending order into
+// LDS, each wave then keeps U rows in flight (1 KB of a row per load), the
+// four waves reduce in LDS and add the chunk to y with one fp32 atomic per
+// column and token.
+template <int B>
 __global__ __launch_bounds__(kBlock) void k_down(const DownArgs a)
 {
     constexpr int U = 8;
-    constexpr int LPR = kWave / R;  // lanes per row
-    constexpr int CW = LPR * 8;     // columns of the chunk
-    constexpr int T = kDownRowsPerThread;
     extern __shared__ __align__(16) int dsm[];
-    __shared__ int wcnt[T][kWavesPerBlock];
+    __shared__ int wcnt[kWavesPerBlock];
     const int cap = a.rows_per_group;
     int *lrow = dsm;                                                 // [cap]
     float *lsv = reinterpret_cast<float *>(dsm + cap);               // [B][cap]
-    float *red = reinterpret_cast<float *>(dsm + cap * (1 + B));     // [4 R][CW]
+    float *red = reinterpret_cast<float *>(dsm + cap * (1 + B));     // [4][512]
     const int lane = threadIdx.x % kWave, wave = threadIdx.x / kWave;
     const int c = blockIdx.x % a.gc, g = blockIdx.x / a.gc;
     const int r0 = g * cap;
     const int r1 = min(a.d_ff, r0 + cap);
 
-    // act and s of this thread's neurons r0 + t * kBlock + tid: every load first
-    int av[T];
-    float sv[T][B];
-#pragma unroll
-    for (int t = 0; t < T; ++t) {
-        av[t] = 0;
+    int nl = 0;
+    for (int t0 = r0; t0 < r1; t0 += kBlock) {
+        const int row = t0 + threadIdx.x;
+        bool valid = false;
+        float sv[B];
 #pragma unroll
         for (int b = 0; b < B; ++b)
-            sv[t][b] = 0.0f;
-        if (t * kBlock < cap) {  // uniform
-            const int row = r0 + t * kBlock + threadIdx.x;
-            const bool ok = row < r1;
-            av[t] = *or_zero(ok, a.act + row);
+            sv[b] = 0.0f;
+        if (row < r1) {
+            valid = a.act[row] != 0;
 #pragma unroll
             for (int b = 0; b < B; ++b)
-                sv[t][b] = *or_zero(ok && b < a.nb, a.s + (size_t)b * a.d_ff + row);
+                if (b < a.nb)
+                    sv[b] = a.s[(size_t)b * a.d_ff + row];
         }
-    }
-    uint64_t m[T];
-#pragma unroll
-    for (int t = 0; t < T; ++t) {
-        m[t] = ballot(av[t] != 0);
+        const uint64_t m = ballot(valid);
         if (lane == 0)
-            wcnt[t][wave] = __popcll(m[t]);
-    }
-    __syncthreads();
-    int nl = 0;
-#pragma unroll
-    for (int t = 0; t < T; ++t) {
+            wcnt[wave] = __popcll(m);
+        __syncthreads();
         int base = nl;
         for (int v = 0; v < wave; ++v)
-            base += wcnt[t][v];
-        if (av[t] != 0) {
-            const int pos = base + lanes_below(m[t]);
-            lrow[pos] = r0 + t * kBlock + threadIdx.x;
+            base += wcnt[v];
+        if (valid) {
+            const int pos = base + lanes_below(m);
+            lrow[pos] = row;
 #pragma unroll
             for (int b = 0; b < B; ++b)
-                lsv[b * cap + pos] = sv[t][b];
+                lsv[b * cap + pos] = sv[b];
         }
-        nl += wcnt[t][0] + wcnt[t][1] + wcnt[t][2] + wcnt[t][3];
+        nl += wcnt[0] + wcnt[1] + wcnt[2] + wcnt[3];
+        __syncthreads();
     }
-    __syncthreads();
     if (nl == 0)
         return;  // uniform for the workgroup
 
-    const int rs = lane / LPR, cl = lane % LPR;
-    const int col = c * CW + cl * 8;
+    const int col = c * kColsPerLoad + lane * 8;
     const bool colok = col < a.d_model;
     float acc[B][8];
 #pragma unroll
@@ -1313,26 +1293,27 @@ __global__ __launch_bounds__(kBlock) void k_down(const DownArgs a)
         for (int e = 0; e < 8; ++e)
             acc[b][e] = 0.0f;
 
-    // list position of load q of step k0: ((k0 + q) * 4 + wave) * R + rs
-    for (int k0 = 0; k0 * kWavesPerBlock * R < nl; k0 += U) {
+    for (int q0 = wave; q0 < nl; q0 += kWavesPerBlock * U) {
         u32x4 w[U];
 #pragma unroll
         for (int q = 0; q < U; ++q) {
-            const int p = ((k0 + q) * kWavesPerBlock + wave) * R + rs;
-            w[q] = (p < nl && colok) ? load16_stream(a.Wd + (size_t)lrow[p] * a.d_model + col)
+            const int r = q0 + q * kWavesPerBlock;
+            w[q] = (r < nl && colok) ? load16_stream(a.Wd + (size_t)lrow[r] * a.d_model + col)
                                      : zero16();
         }
 #pragma unroll
         for (int q = 0; q < U; ++q) {
-            const int p = ((k0 + q) * kWavesPerBlock + wave) * R + rs;
+            const int r = q0 + q * kWavesPerBlock;
+            if (r >= nl)
+                break;
             const float wf[8] = {bf16_lo(w[q].x), bf16_hi(w[q].x), bf16_lo(w[q].y), bf16_hi(w[q].y),
                                  bf16_lo(w[q].z), bf16_hi(w[q].z), bf16_lo(w[q].w), bf16_hi(w[q].w)};
 #pragma unroll
             for (int b = 0; b < B; ++b) {
-                const float s = p < nl ? lsv[b * cap + p] : 0.0f;
+                const float sv = lsv[b * cap + r];
 #pragma unroll
                 for (int e = 0; e < 8; ++e)
-                    acc[b][e] = fmaf(s, wf[e], acc[b][e]);
+                    acc[b][e] = fmaf(sv, wf[e], acc[b][e]);
             }
         }
     }
@@ -1344,22 +1325,23 @@ __global__ __launch_bounds__(kBlock) void k_down(const DownArgs a)
         __syncthreads();
 #pragma unroll
         for (int e = 0; e < 8; ++e)
-            red[(wave * R + rs) * CW + cl * 8 + e] = acc[b][e];
+            red[wave * kColsPerLoad + lane * 8 + e] = acc[b][e];
         __syncthreads();
-        for (int cc = threadIdx.x; cc < CW; cc += kBlock) {
-            const int gcol = c * CW + cc;
+        for (int cc = threadIdx.x; cc < kColsPerLoad; cc += kBlock) {
+            const int gcol = c * kColsPerLoad + cc;
             if (gcol < a.d_model) {
-                float v = 0.0f;
-#pragma unroll
-                for (int k = 0; k < kWavesPerBlock * R; ++k)
-                    v += red[k * CW + cc];
+                const float v = red[cc] + red[kColsPerLoad + cc] + red[2 * kColsPerLoad + cc] +
+                                red[3 * kColsPerLoad + cc];
                 unsafeAtomicAdd(a.y + (size_t)b * a.d_model + gcol, v);
             }
         }
     }
 }
 
-// Gathered down projection for batches of 2-8 on MFMA. The product
+// neurons per range read by each thread of the MFMA down kernel
+constexpr int kDownRowsPerThread = 8;
+
+// Gathered down projection for batches of 4-8 on MFMA. The product
 // Y[B x d_model] = S[B x n] . W_down[IDX, :] is a dense contraction over the
 // active neurons: v_mfma_f32_16x16x32_bf16 with A = S (row i = token i, zero
 // rows past the batch) and B = the W_down rows. Workgroup (c, g) owns 128
@@ -1530,7 +1512,8 @@ __global__ __launch_bounds__(kBlock) void k_down_mfma(const DownArgs a)
     }
 }
 
-// batches from which the down projection runs on MFMA
+// batches from which the down projection runs on MFMA (measured: at 2 the
+// VALU kernel is faster, at 4 and 8 the MFMA one)
 constexpr int kDownMfmaMinBatch = 4;
 
 size_t down_mfma_lds_bytes(int rows_per_group, int bt)
@@ -1969,27 +1952,23 @@ size_t down_lds_bytes(int rows_per_group, int bt)
     return (size_t)rows_per_group * 4 * (1 + bt) + (size_t)kWavesPerBlock * kColsPerLoad * 4;
 }
 
-// Down-kernel grid: R rows per wave load (chunks of 512 / R columns) and gr
-// neuron ranges of at least 16 neurons; the atomics into y number
-// gr * B * d_model. Measured best among R in {1, 2, 4, 8} and 8-64 ranges at
-// 4096 x 11008 and 4096 x 14336 (batches 1, 4, 8): 2 rows per load and 32
-// ranges; at 8192 x 28672: 1 row per load and 64 ranges. Ranges are raised
-// when a range's lists would not fit in 64 KB of LDS.
-void down_grid(int d_model, int d_ff, int bt, int *R, int *gc, int *gr, int *rows_per_group)
+// Down-kernel grid: 512-column chunks x 64 neuron ranges of at least 16
+// neurons (measured best at 4096 x 11008, 4096 x 14336 and 8192 x 28672 among
+// 16-128 ranges and 128-512-column chunks), more ranges when a range's lists
+// would not fit in 64 KB of LDS.
+void down_grid(int d_model, int d_ff, int bt, int *gc, int *gr, int *rows_per_group)
 {
-    int r = d_model <= 4096 ? 32 : 64, rr = d_model <= 4096 ? 2 : 1;
+    *gc = (d_model + kColsPerLoad - 1) / kColsPerLoad;
+    int r = 64;
     if (r > d_ff / 16)
         r = d_ff / 16;
     if (r < 1)
         r = 1;
     const int max_rows = (int)((65536 - down_lds_bytes(0, bt)) / (4 * (1 + bt)));
-    const int lim = max_rows < kDownRowsPerThread * kBlock ? max_rows : kDownRowsPerThread * kBlock;
-    if ((d_ff + r - 1) / r > lim)
-        r = (d_ff + lim - 1) / lim;
-    *R = rr;
+    if ((d_ff + r - 1) / r > max_rows)
+        r = (d_ff + max_rows - 1) / max_rows;
     *rows_per_group = (d_ff + r - 1) / r;
     *gr = (d_ff + *rows_per_group - 1) / *rows_per_group;
-    *gc = (d_model + kColsPerLoad / rr - 1) / (kColsPerLoad / rr);
 }
 
 template <int B, int NK, bool XREG, int LCPR>
@@ -2178,20 +2157,9 @@ hipError_t launch_latent_norm(const NormArgs &n, const uint16_t *At, int d_rank,
     return norm_dispatch(n, At, d_rank, lat, s);
 }
 
-template <int B>
-static void down_b(const DownArgs &a, int R, size_t lds, hipStream_t s)
-{
-    const int grid = a.gc * a.gr;
-    switch (R) {
-    case 1: allow_lds(k_down<B, 1>, lds); k_down<B, 1><<<grid, kBlock, lds, s>>>(a); break;
-    case 2: allow_lds(k_down<B, 2>, lds); k_down<B, 2><<<grid, kBlock, lds, s>>>(a); break;
-    case 4: allow_lds(k_down<B, 4>, lds); k_down<B, 4><<<grid, kBlock, lds, s>>>(a); break;
-    default: allow_lds(k_down<B, 8>, lds); k_down<B, 8><<<grid, kBlock, lds, s>>>(a); break;
-    }
-}
-
-// MFMA down kernel grid: 128-column chunks and gr neuron ranges, raised until
-// the range's lists fit in 64 KB of LDS
+// MFMA down kernel grid: 128-column chunks and 16 neuron ranges (measured best
+// among 4-32 at 4096 x 14336, batches 4 and 8), raised until a range's lists
+// fit in 64 KB of LDS
 static void down_grid_mfma(int d_model, int d_ff, int bt, int *gc, int *gr, int *rows_per_group)
 {
     int r = 16;
@@ -2210,7 +2178,7 @@ static void down_grid_mfma(int d_model, int d_ff, int bt, int *gc, int *gr, int 
     *gc = (d_model + 127) / 128;
 }
 
-bool down_uses_mfma(int bt) { return bt >= kDownMfmaMinBatch; }
+static bool down_uses_mfma(int bt) { return bt >= kDownMfmaMinBatch; }
 
 hipError_t launch_down(const DownArgs &args, hipStream_t s)
 {
@@ -2220,21 +2188,24 @@ hipError_t launch_down(const DownArgs &args, hipStream_t s)
         down_grid_mfma(a.d_model, a.d_ff, bt, &a.gc, &a.gr, &a.rows_per_group);
         const size_t lds = down_mfma_lds_bytes(a.rows_per_group, bt);
         const int grid = a.gc * a.gr;
-        switch (bt) {
-        case 2: allow_lds(k_down_mfma<2>, lds); k_down_mfma<2><<<grid, kBlock, lds, s>>>(a); break;
-        case 4: allow_lds(k_down_mfma<4>, lds); k_down_mfma<4><<<grid, kBlock, lds, s>>>(a); break;
-        default: allow_lds(k_down_mfma<8>, lds); k_down_mfma<8><<<grid, kBlock, lds, s>>>(a); break;
+        if (bt == 4) {
+            allow_lds(k_down_mfma<4>, lds);
+            k_down_mfma<4><<<grid, kBlock, lds, s>>>(a);
+        } else {
+            allow_lds(k_down_mfma<8>, lds);
+            k_down_mfma<8><<<grid, kBlock, lds, s>>>(a);
         }
         return hipGetLastError();
     }
-    int R = 1;
-    down_grid(a.d_model, a.d_ff, bt, &R, &a.gc, &a.gr, &a.rows_per_group);
+    down_grid(a.d_model, a.d_ff, bt, &a.gc, &a.gr, &a.rows_per_group);
     const size_t lds = down_lds_bytes(a.rows_per_group, bt);
-    switch (bt) {
-    case 1: down_b<1>(a, R, lds, s); break;
-    case 2: down_b<2>(a, R, lds, s); break;
-    case 4: down_b<4>(a, R, lds, s); break;
-    default: down_b<8>(a, R, lds, s); break;
+    const int grid = a.gc * a.gr;
+    if (bt == 1) {
+        allow_lds(k_down<1>, lds);
+        k_down<1><<<grid, kBlock, lds, s>>>(a);
+    } else {
+        allow_lds(k_down<2>, lds);
+        k_down<2><<<grid, kBlock, lds, s>>>(a);
     }
     return hipGetLastError();
 }
