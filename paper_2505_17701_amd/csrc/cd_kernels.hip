@@ -1659,39 +1659,78 @@ constexpr int kTopkThreads = 1024;
 constexpr int kTopkPerThread = 32;  // keys per thread: d_ff <= 32768
 
 // One workgroup per token: q = v[lo] + (h - lo)(v[lo + 1] - v[lo]), h = k (n - 1).
-// The order statistic of rank lo comes from 3 passes of radix select (11, 11
-// and 10 bits, most significant first) over order-preserving keys held in
-// registers: a shared LDS histogram of the keys that match the prefix so far,
-// a block-wide scan of its bins, and the bin that holds the rank. An 11-bit
-// top digit (sign, exponent, two mantissa bits) spreads typical coefficients
-// over tens of bins, so the atomics hardly contend. Rank lo + 1 is the same
-// key when it repeats, else the smallest key above it. fp64 interpolation.
+// Both order statistics (ranks lo and lo + 1) come from 3 passes of radix
+// select (11, 11 and 10 bits, most significant first) over order-preserving
+// keys held in registers, run in lockstep: each pass histograms in LDS the
+// keys that match a rank's prefix so far (one histogram while both ranks
+// share their prefix, two once they part), scans the bins and picks the bin
+// that holds each rank. The first pass puts every key into one of 8 padded
+// histogram copies (by lane) so that the atomics of a wave on the few busy
+// bins of the top digit (sign, exponent, two mantissa bits) land on different
+// banks; the scans use DPP within waves and one barrier across them. fp64
+// interpolation.
 constexpr int kSelBins = 2048;
+constexpr int kSelCopies = 8;
+constexpr int kSelCopyStride = kSelBins + 1;  // padding: copies of a bin on different banks
 
+// inclusive prefix sum over the 64 lanes (DPP row shifts, then row broadcasts)
+__device__ __forceinline__ uint32_t wave_incl_scan(uint32_t v)
+{
+    v += __builtin_amdgcn_update_dpp(0u, v, 0x111, 0xF, 0xF, false);  // row_shr:1
+    v += __builtin_amdgcn_update_dpp(0u, v, 0x112, 0xF, 0xF, false);  // row_shr:2
+    v += __builtin_amdgcn_update_dpp(0u, v, 0x114, 0xF, 0xF, false);  // row_shr:4
+    v += __builtin_amdgcn_update_dpp(0u, v, 0x118, 0xF, 0xF, false);  // row_shr:8
+    v += __builtin_amdgcn_update_dpp(0u, v, kDppBcast15, 0xA, 0xF, false);
+    v += __builtin_amdgcn_update_dpp(0u, v, kDppBcast31, 0xC, 0xF, false);
+    return v;
+}
+
+// Exclusive prefix of v over the workgroup (thread order) and the total; one barrier.
+// wsum: LDS [16]. Every thread must call this.
+__device__ __forceinline__ void block_scan(uint32_t v, uint32_t *wsum, uint32_t &excl,
+                                           uint32_t &total)
+{
+    const int lane = threadIdx.x % kWave, wave = threadIdx.x / kWave;
+    const uint32_t inc = wave_incl_scan(v);
+    if (lane == kWave - 1)
+        wsum[wave] = inc;
+    __syncthreads();
+    const uint32_t ws = lane < kTopkThreads / kWave ? wsum[lane] : 0u;
+    const uint32_t wi = wave_incl_scan(ws);
+    const uint32_t before = wave > 0 ? (uint32_t)__builtin_amdgcn_readlane((int)wi, wave - 1) : 0u;
+    total = (uint32_t)__builtin_amdgcn_readlane((int)wi, kTopkThreads / kWave - 1);
+    excl = before + inc - v;
+}
+
+template <int KPT>
 __global__ __launch_bounds__(kTopkThreads) void k_topk_select(const float *__restrict__ coef, int ld,
                                                               int n, int use_abs, double k,
                                                               double *__restrict__ q)
 {
     constexpr int kWaves = kTopkThreads / kWave;
-    __shared__ uint32_t hist[kSelBins];
-    __shared__ uint32_t wsum[kWaves];
-    __shared__ int sel[3];
-    __shared__ uint32_t umin[kWaves];
-    const int lane = threadIdx.x % kWave, wave = threadIdx.x / kWave;
+    extern __shared__ __align__(16) uint32_t sm[];
+    uint32_t *hA = sm;                                    // [kSelCopies][kSelCopyStride] rank lo
+    uint32_t *hB = hA + kSelCopies * kSelCopyStride;      // [kSelBins] rank lo + 1 once apart
+    uint32_t *sink = hB + kSelBins;                       // [64] counts of the other keys
+    __shared__ uint32_t wsum[2][kWaves];
+    __shared__ int sel[2][2];                             // [rank][bin, rank within bin]
+    const int lane = threadIdx.x % kWave;
     const float *c = coef + (size_t)blockIdx.x * ld;
     const int jn = (n + kTopkThreads - 1) / kTopkThreads;  // key slots in use (uniform)
-    float cv[kTopkPerThread];
+    float cv[KPT];
 #pragma unroll
-    for (int j = 0; j < kTopkPerThread; ++j) {
+    for (int j = 0; j < KPT; ++j) {
         const int i = threadIdx.x + j * kTopkThreads;
         cv[j] = 0.0f;
         if (j < jn)  // uniform
             cv[j] = *or_zero(i < n, c + i);
     }
-    uint32_t key[kTopkPerThread];
+    for (int i = threadIdx.x; i < kSelCopies * kSelCopyStride + kSelBins; i += kTopkThreads)
+        sm[i] = 0u;  // (the sink words are never read)
+    uint32_t key[KPT];
     uint32_t valid = 0u;  // bit j: slot j holds a key
 #pragma unroll
-    for (int j = 0; j < kTopkPerThread; ++j) {
+    for (int j = 0; j < KPT; ++j) {
         key[j] = order_key(cv[j], use_abs);
         if (j < jn && threadIdx.x + j * kTopkThreads < n)
             valid |= 1u << j;
@@ -1700,80 +1739,85 @@ __global__ __launch_bounds__(kTopkThreads) void k_topk_select(const float *__res
     int lo = (int)floor(h);
     if (lo > n - 1)
         lo = n - 1;
+    const bool two = lo + 1 < n;  // rank lo + 1 exists
+    uint32_t *hc = hA + (lane % kSelCopies) * kSelCopyStride;
+    __syncthreads();
 
-    uint32_t prefix = 0u, mask = 0u;
-    int r = lo;
-    int last_count = 0;  // keys equal to the selected key (after the last pass)
-#pragma unroll
-    for (int pass = 0; pass < 3; ++pass) {
+    uint32_t pA = 0u, pB = 0u, mask = 0u;  // prefixes of the two ranks, digits fixed so far
+    int rA = lo, rB = two ? lo + 1 : lo;   // ranks within the keys matching the prefixes
+#pragma unroll 1
+    for (int pass = 0; pass < 3; ++pass) {  // one copy of the pass code (instruction fetch)
         const int shift = pass == 0 ? 21 : pass == 1 ? 10 : 0;
         const uint32_t dmask = pass == 2 ? 0x3ffu : 0x7ffu;
-        hist[2 * threadIdx.x] = 0u;
-        hist[2 * threadIdx.x + 1] = 0u;
-        __syncthreads();
+        const bool apart = pA != pB;  // uniform
+        // branch-free: a key matching neither prefix (or no key) counts into this
+        // lane's own sink word
 #pragma unroll
-        for (int j = 0; j < kTopkPerThread; ++j)
-            if (j < jn && ((valid >> j) & 1u) && (key[j] & mask) == prefix)
-                atomicAdd(&hist[(key[j] >> shift) & dmask], 1u);
-        __syncthreads();
-        // block scan: thread t owns bins 2t and 2t + 1
-        const uint32_t h0 = hist[2 * threadIdx.x], h1 = hist[2 * threadIdx.x + 1];
-        const uint32_t tot = h0 + h1;
-        uint32_t inc = tot;
-#pragma unroll
-        for (int off = 1; off < kWave; off <<= 1) {
-            const uint32_t v = (uint32_t)__shfl_up((int)inc, off);
-            if (lane >= off)
-                inc += v;
-        }
-        if (lane == kWave - 1)
-            wsum[wave] = inc;
-        __syncthreads();
-        uint32_t cum = inc - tot;
-        for (int w = 0; w < wave; ++w)
-            cum += wsum[w];
-        const uint32_t rr = (uint32_t)r;
-        if (rr >= cum && rr < cum + h0) {
-            sel[0] = 2 * threadIdx.x;
-            sel[1] = (int)(rr - cum);
-            sel[2] = (int)h0;
-        } else if (rr >= cum + h0 && rr < cum + tot) {
-            sel[0] = 2 * threadIdx.x + 1;
-            sel[1] = (int)(rr - cum - h0);
-            sel[2] = (int)h1;
+        for (int j = 0; j < KPT; ++j) {
+            if (j < jn) {  // uniform
+                const uint32_t d = (key[j] >> shift) & dmask;
+                const uint32_t pk = key[j] & mask;
+                const bool v = (valid >> j) & 1u;
+                uint32_t *dst = sink + lane;
+                dst = v && apart && pk == pB ? hB + d : dst;
+                dst = v && pk == pA ? hc + d : dst;
+                atomicAdd(dst, 1u);
+            }
         }
         __syncthreads();
-        prefix |= (uint32_t)sel[0] << shift;
+        // thread t owns bins 2t and 2t + 1 (cleared for the next pass as they are read)
+        uint32_t a0 = 0u, a1 = 0u;
+#pragma unroll
+        for (int cpy = 0; cpy < kSelCopies; ++cpy) {
+            uint32_t *bin = hA + cpy * kSelCopyStride + 2 * threadIdx.x;
+            a0 += bin[0];
+            a1 += bin[1];
+            bin[0] = 0u;
+            bin[1] = 0u;
+        }
+        uint32_t ea, ta;
+        block_scan(a0 + a1, wsum[0], ea, ta);
+        uint32_t b0 = a0, b1 = a1, eb = ea;
+        if (apart) {
+            b0 = hB[2 * threadIdx.x];
+            b1 = hB[2 * threadIdx.x + 1];
+            hB[2 * threadIdx.x] = 0u;
+            hB[2 * threadIdx.x + 1] = 0u;
+            uint32_t tb;
+            block_scan(b0 + b1, wsum[1], eb, tb);
+        }
+        const uint32_t ra = (uint32_t)rA, rb = (uint32_t)rB;
+        if (ra >= ea && ra < ea + a0) {
+            sel[0][0] = 2 * threadIdx.x;
+            sel[0][1] = (int)(ra - ea);
+        } else if (ra >= ea + a0 && ra < ea + a0 + a1) {
+            sel[0][0] = 2 * threadIdx.x + 1;
+            sel[0][1] = (int)(ra - ea - a0);
+        }
+        if (rb >= eb && rb < eb + b0) {
+            sel[1][0] = 2 * threadIdx.x;
+            sel[1][1] = (int)(rb - eb);
+        } else if (rb >= eb + b0 && rb < eb + b0 + b1) {
+            sel[1][0] = 2 * threadIdx.x + 1;
+            sel[1][1] = (int)(rb - eb - b0);
+        }
+        __syncthreads();
+        pA |= (uint32_t)sel[0][0] << shift;
+        pB |= (uint32_t)sel[1][0] << shift;
         mask |= dmask << shift;
-        r = sel[1];
-        last_count = sel[2];
-    }
-    const uint32_t k0 = prefix;
-    uint32_t k1 = k0;
-    if (lo + 1 < n && r + 1 >= last_count) {
-        // rank lo + 1 is the smallest key above k0
-        uint32_t m = 0xffffffffu;
-#pragma unroll
-        for (int j = 0; j < kTopkPerThread; ++j)
-            if (j < jn && ((valid >> j) & 1u) && key[j] > k0)
-                m = min(m, key[j]);
-#pragma unroll
-        for (int off = 32; off >= 1; off >>= 1)
-            m = min(m, (uint32_t)__shfl_xor((int)m, off));
-        if (lane == 0)
-            umin[wave] = m;
-        __syncthreads();
-        m = 0xffffffffu;
-#pragma unroll
-        for (int w = 0; w < kWaves; ++w)
-            m = min(m, umin[w]);
-        k1 = m;
+        rA = sel[0][1];
+        rB = sel[1][1];
     }
     if (threadIdx.x == 0) {
-        const double v0 = (double)key_value(k0, use_abs);
-        const double v1 = (double)key_value(k1, use_abs);
+        const double v0 = (double)key_value(pA, use_abs);
+        const double v1 = (double)key_value(two ? pB : pA, use_abs);
         q[blockIdx.x] = v0 + (h - (double)lo) * (v1 - v0);
     }
+}
+
+static size_t topk_select_lds_bytes()
+{
+    return ((size_t)kSelCopies * kSelCopyStride + kSelBins + kWave) * 4;
 }
 
 // s of one active neuron of a single-projection variant from its second row
@@ -2264,14 +2308,29 @@ static hipError_t gather_topk_b(int variant, const CoefArgs &a, const double *q,
     }
 }
 
+// keys per thread of the select kernel for a row of n coefficients
+static int topk_kpt(int n) { return n <= 16 * kTopkThreads ? 16 : 32; }
+
+static void launch_topk_select(const float *coef, int ld, int n, int T, int use_abs, double k,
+                               double *q, size_t lds, hipStream_t s)
+{
+    if (topk_kpt(n) == 16) {
+        allow_lds(k_topk_select<16>, lds);
+        k_topk_select<16><<<T, kTopkThreads, lds, s>>>(coef, ld, n, use_abs, k, q);
+    } else {
+        allow_lds(k_topk_select<32>, lds);
+        k_topk_select<32><<<T, kTopkThreads, lds, s>>>(coef, ld, n, use_abs, k, q);
+    }
+}
+
 hipError_t launch_topk(int variant, const CoefArgs &a, double k, double *q, hipStream_t s)
 {
     if (a.d_ff > kTopkThreads * kTopkPerThread)
         return hipErrorInvalidValue;
     if (variant == kDualTern)  // a signed predictor score and the W_gate + W_up gather
         variant = kDualPred;
-    k_topk_select<<<a.nb, kTopkThreads, 0, s>>>(a.coef, a.d_ff, a.d_ff,
-                                                 variant == kDualPred ? 0 : 1, k, q);
+    launch_topk_select(a.coef, a.d_ff, a.d_ff, a.nb, variant == kDualPred ? 0 : 1, k, q,
+                       topk_select_lds_bytes(), s);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess)
         return e;
@@ -2294,7 +2353,7 @@ hipError_t launch_select(const float *coef, int ld, int n, int T, int use_abs, d
                          double *q_out, hipStream_t s)
 {
     if (n <= kTopkThreads * kTopkPerThread) {  // keys fit in registers: the faster select
-        k_topk_select<<<T, kTopkThreads, 0, s>>>(coef, ld, n, use_abs, k, q_out);
+        launch_topk_select(coef, ld, n, T, use_abs, k, q_out, topk_select_lds_bytes(), s);
     } else {
         allow_lds(k_select_quantile, (size_t)n * 4);
         k_select_quantile<<<T, kSelThreads, (size_t)n * 4, s>>>(coef, ld, n, use_abs, k, q_out);
