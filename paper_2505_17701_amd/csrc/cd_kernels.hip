@@ -1740,7 +1740,6 @@ __global__ __launch_bounds__(kTopkThreads) void k_topk_select(const float *__res
     if (lo > n - 1)
         lo = n - 1;
     const bool two = lo + 1 < n;  // rank lo + 1 exists
-    uint32_t *hc = hA + (lane % kSelCopies) * kSelCopyStride;
     __syncthreads();
 
     uint32_t pA = 0u, pB = 0u, mask = 0u;  // prefixes of the two ranks, digits fixed so far
@@ -1750,6 +1749,9 @@ __global__ __launch_bounds__(kTopkThreads) void k_topk_select(const float *__res
         const int shift = pass == 0 ? 21 : pass == 1 ? 10 : 0;
         const uint32_t dmask = pass == 2 ? 0x3ffu : 0x7ffu;
         const bool apart = pA != pB;  // uniform
+        // the first pass spreads over the copies; later passes see few keys per bin
+        const int ncopy = pass == 0 ? kSelCopies : 1;
+        uint32_t *hc = hA + (lane % ncopy) * kSelCopyStride;
         // branch-free: a key matching neither prefix (or no key) counts into this
         // lane's own sink word
 #pragma unroll
@@ -1767,8 +1769,7 @@ __global__ __launch_bounds__(kTopkThreads) void k_topk_select(const float *__res
         __syncthreads();
         // thread t owns bins 2t and 2t + 1 (cleared for the next pass as they are read)
         uint32_t a0 = 0u, a1 = 0u;
-#pragma unroll
-        for (int cpy = 0; cpy < kSelCopies; ++cpy) {
+        for (int cpy = 0; cpy < ncopy; ++cpy) {
             uint32_t *bin = hA + cpy * kSelCopyStride + 2 * threadIdx.x;
             a0 += bin[0];
             a1 += bin[1];
