@@ -1,0 +1,98 @@
+"""The per-token quantile selection on the GPU's own coefficients: for every
+row length the select kernels handle (16 or 32 keys per thread, and the
+LDS-keyed kernel past 32768), with distinct and with repeated values, |c| and
+signed, each quantile must be exactly the linear interpolation between the
+order statistics of the fp32 coefficients (numpy sort)."""
+import math
+
+import numpy as np
+import pytest
+
+from gpu_support import dev_bf16
+from test_gpu_parity import Layer
+from test_gpu_topk import check_topk
+from workloads import make_layer, make_predictor, make_tokens
+from workloads.synth import T_CALIB
+
+torch = pytest.importorskip("torch")
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+
+
+def exact_quantile(v, k):
+    v = np.sort(v)
+    n = len(v)
+    h = k * (n - 1)
+    lo = min(int(math.floor(h)), n - 1)
+    hi = min(lo + 1, n - 1)
+    return v[lo] + (h - lo) * (v[hi] - v[lo])
+
+
+@pytest.mark.parametrize("dm,dff,dup", [(256, 688, False), (64, 16384, False), (64, 16392, True),
+                                        (64, 32768, False), (64, 32776, False),
+                                        (128, 20000, True)])
+def test_select_exact_order_statistics(dm, dff, dup):
+    from paper_2505_17701_amd import binding as cd
+
+    L = make_layer(1900 + dff % 97, dm, dff, 0.05)
+    if dup:  # pairs of equal rows: every |u| value appears twice
+        L["W_up"][1::2] = L["W_up"][0::2][: dff // 2]
+    layer = Layer(L)
+    T = 5
+    X = make_tokens(1901, T, dm, purpose=T_CALIB)
+    plan = cd.Plan(dm, dff, 8, 0, keep_coef=True)
+    D = layer.d
+    xd = dev_bf16(X)
+    cd.countdown_ffn_mono(plan, xd, D["W_gate"], D["W_up"], D["W_down"], math.inf)
+    coef = cd.countdown_export_active(plan)[2].cpu().numpy().astype(np.float64)[:T]
+    if dup:
+        assert np.array_equal(np.abs(coef[:, 0::2][:, : dff // 2]), np.abs(coef[:, 1::2]))
+    for k in (0.0, 0.3, 0.9, 0.999, 1.0):
+        _, q = cd.countdown_calibrate(plan, cd.CD_VARIANT_MONO, xd, k, W_up=D["W_up"])
+        q = q.cpu().numpy()
+        for t in range(T):
+            assert q[t] == exact_quantile(np.abs(coef[t]), k), (dff, k, t)
+    plan.close()
+
+
+@pytest.mark.parametrize("dff", [688, 20000])
+def test_select_signed_scores(dff):
+    """The predictor's signed score: the quantile of the signed values."""
+    from paper_2505_17701_amd import binding as cd
+
+    dm, dr = 64, 8
+    L = make_layer(1950, dm, dff, 0.05)
+    P = make_predictor(1950, dm, dr, dff, 0.3)
+    layer = Layer(L, P)
+    T = 4
+    X = make_tokens(1951, T, dm, purpose=T_CALIB)
+    plan = cd.Plan(dm, dff, 8, dr, keep_coef=True)
+    D = layer.d
+    xd = dev_bf16(X)
+    cd.countdown_ffn_dual(plan, xd, D["W_gate"], D["W_up"], D["W_down"], math.inf,
+                          A_t=D["A_t"], B_t=D["B_t"])
+    coef = cd.countdown_export_active(plan)[2].cpu().numpy().astype(np.float64)[:T]
+    assert (coef < 0).any() and (coef > 0).any()
+    for k in (0.1, 0.5, 0.9):
+        _, q = cd.countdown_calibrate(plan, cd.CD_VARIANT_DUAL_PRED, xd, k, A_t=D["A_t"],
+                                      B_t=D["B_t"])
+        q = q.cpu().numpy()
+        for t in range(T):
+            assert q[t] == exact_quantile(coef[t], k), (dff, k, t)
+    plan.close()
+
+
+@pytest.mark.parametrize("shape", [(512, 24584, 2, 0.9), (256, 32768, 1, 0.7)])
+def test_topk_long_rows(shape):
+    """The per-token path with 32 keys per thread of the select (d_ff > 16384)."""
+    dm, dff, B, k = shape
+    layer = Layer(make_layer(1960 + B, dm, dff, 0.03))
+    x = make_tokens(1961, B, dm)
+    n, flips, rel = check_topk("mono", layer, x, k, f"long topk {shape}")
+    if B == 1 and flips == 0:
+        assert n == dff - 1 - math.floor(k * (dff - 1))
