@@ -577,26 +577,28 @@ __global__ __launch_bounds__(kBlock) void k_coef_pred(const CoefArgs a)
     const int r0 = blockIdx.x * kPredRows;
     const int wr0 = r0 + wave * kPredRowsPerWave;
 
+    // loads in the order they are needed: B_t and the latent for the scores,
+    // then the tokens, which only the gather reads
     using LR = LatentRegs<B, LCPR>;
     u32x4 wb[S::kLoads];
     pred_issue_bt<LCPR>(wb, a, wr0, lane);
-    Tokens<B, NK, XREG> tok;
-    tok.issue(a.x, a.nb, a.d_model, lane);
     LR lr;
     lr.issue(a.lat, a.nb, a.d_rank, lane);
     LatentStage<LR::kRegs ? 1 : B> ls;  // the LDS copy, rank 1024 only
     if constexpr (!LR::kRegs)
         ls.issue(a.lat, a.nb, a.d_rank);
+    Tokens<B, NK, XREG> tok;
+    tok.issue(a.x, a.nb, a.d_model, lane);
     zero_y(a.y, a.nb * a.d_model);
-    tok.write(xs);
     uint32_t *latw = xs + (XREG ? 0 : B * NK * kColsPerLoad / 2);
-    if constexpr (!LR::kRegs)
+    if constexpr (!LR::kRegs) {
         ls.write(reinterpret_cast<u32x4 *>(latw), a.lat, a.nb, a.d_rank);
-    if constexpr (!XREG || !LR::kRegs)
         __syncthreads();
+    }
 
     const uint32_t wmask = pred_score<B, LCPR>(wb, lr, reinterpret_cast<const float *>(latw), a,
                                                wr0, lane);
+    tok.write(xs);  // (block_share's barrier publishes the LDS copy)
     uint32_t m = block_share(wflag, wmask, wave, lane);
     gather_rr<B, NK, XREG>(a, tok, m, r0, lane);
 }
@@ -790,6 +792,8 @@ __global__ __launch_bounds__(kBlock) void k_coef_pred_mfma(const CoefArgs a)
     const int r0 = blockIdx.x * kPredRows;
     const int wr0 = r0 + wave * kPredRowsPerWave;
 
+    // (the tokens are staged before the scores: holding them in registers
+    // through the scoring costs occupancy, measured slower at 8 tokens)
     using LR = LatentRegs<B, LCPR>;
     u32x4 wb[S::kLoads];
     pred_issue_bt<LCPR>(wb, a, wr0, lane);
