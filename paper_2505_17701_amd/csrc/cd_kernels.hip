@@ -777,13 +777,142 @@ __device__ __forceinline__ void gather_mfma(const CoefArgs &a, const uint32_t *x
     }
 }
 
+// MFMA gather with the weight rows staged in LDS. Loads in the MFMA operand
+// layout (16 rows x 64 B per instruction) reach about 60% of the HBM rate of
+// row-contiguous loads on gathered rows (measured), so a wave loads each
+// batch of kWtSteps steps (128 columns) of its tile's 16 W_gate and W_up
+// rows four rows per instruction (256 B of a row per 16 lanes), writes them
+// to its own LDS tile (rows padded by 16 B) and reads the A operands back;
+// the token operand (L2-resident) is loaded with the batch. The next batch
+// is in flight while the current one is consumed.
+constexpr int kWtSteps = 4;
+constexpr int kWtCols = kWtSteps * 32;           // columns of a batch
+constexpr int kWtStride = kWtCols + 8;           // bf16 per tile row
+constexpr int kWtWave = 2 * kTile * kWtStride;   // bf16 per wave: W_gate and W_up tiles
+constexpr int kWtLoads = kTile / 4;              // loads per lane and matrix (4 rows each)
+
+struct WtBatch {
+    u32x4 w[2 * kWtLoads];  // [0, 4): W_gate rows 4q + (lane >> 4); [4, 8): W_up
+    u32x4 x[kWtSteps];
+};
+
+__device__ __forceinline__ void wt_load(WtBatch &bt, const CoefArgs &a, const int (&row)[kWtLoads],
+                                        uint32_t have, const uint16_t *xrow, bool xreal, int s,
+                                        int s1, int lane)
+{
+    const int g = lane / kTile;
+    const int col = s * 32 + (lane & 15) * 8;
+    const bool colok = col < s1 * 32 && col < a.d_model;
+#pragma unroll
+    for (int q = 0; q < kWtLoads; ++q) {
+        bt.w[q] = zero16();
+        bt.w[kWtLoads + q] = zero16();
+        if (((have >> q) & 1u) && colok) {
+            bt.w[q] = load16_stream(a.Wg + (size_t)row[q] * a.d_model + col);
+            bt.w[kWtLoads + q] = load16_stream(a.Wu + (size_t)row[q] * a.d_model + col);
+        }
+    }
+#pragma unroll
+    for (int q = 0; q < kWtSteps; ++q) {
+        const int xc = (s + q) * 32 + g * 8;
+        bt.x[q] = load16(or_zero(xreal && xc < a.d_model, xrow + xc));
+    }
+}
+
+__device__ __forceinline__ void wt_consume(uint16_t *wt, const WtBatch &bt, int s, int s1,
+                                           int lane, f32x4_t &dg, f32x4_t &du)
+{
+    const int i = lane % kTile, g = lane / kTile;
+    const int c = (lane & 15) * 8, rr0 = lane >> 4;
+#pragma unroll
+    for (int q = 0; q < kWtLoads; ++q) {
+        *reinterpret_cast<u32x4 *>(wt + (4 * q + rr0) * kWtStride + c) = bt.w[q];
+        *reinterpret_cast<u32x4 *>(wt + (kTile + 4 * q + rr0) * kWtStride + c) = bt.w[kWtLoads + q];
+    }
+#pragma unroll
+    for (int q = 0; q < kWtSteps; ++q) {
+        if (s + q < s1) {  // uniform
+            const u32x4 ga = *reinterpret_cast<const u32x4 *>(wt + i * kWtStride + q * 32 + g * 8);
+            const u32x4 ua =
+                *reinterpret_cast<const u32x4 *>(wt + (kTile + i) * kWtStride + q * 32 + g * 8);
+            dg = mfma16(ga, bt.x[q], dg);
+            du = mfma16(ua, bt.x[q], du);
+        }
+    }
+}
+
+// gather_mfma with LDS-staged weight rows and tokens from global memory.
+// wtiles: LDS [4 waves][kWtWave] bf16; part, lrow as in gather_mfma.
+template <int B, int NK>
+__device__ __forceinline__ void gather_mfma_lds(const CoefArgs &a, uint16_t *wtiles, float *part,
+                                                int *lrow, uint32_t M, int r0, int wave, int lane)
+{
+    const int n = __builtin_popcount(M);
+    if (threadIdx.x < kPredRows && ((M >> threadIdx.x) & 1u))
+        lrow[__builtin_popcount(M & ((1u << threadIdx.x) - 1u))] = r0 + threadIdx.x;
+    __syncthreads();  // lrow visible; the LDS scratch is free
+
+    const int ntiles = (n + kTile - 1) / kTile;  // 0, 1 or 2
+    if (ntiles == 0)
+        return;
+    const int wpt = kWavesPerBlock / ntiles;
+    const int t0 = (wave / wpt) * kTile, kw = wave % wpt;
+    const int i = lane % kTile, g = lane / kTile;
+    const int steps = (a.d_model + 31) / 32;
+    const int sw = (steps + wpt - 1) / wpt;
+    const int s0 = min(steps, kw * sw), s1 = min(steps, s0 + sw);
+    const bool xreal = i < a.nb;
+    const uint16_t *xrow = a.x + (size_t)(xreal ? i : 0) * a.d_model;
+    int row[kWtLoads];
+    uint32_t have = 0u;
+#pragma unroll
+    for (int q = 0; q < kWtLoads; ++q) {
+        const int k = t0 + 4 * q + (lane >> 4);
+        row[q] = k < n ? lrow[k] : r0;
+        have |= (k < n ? 1u : 0u) << q;
+    }
+    uint16_t *wt = wtiles + (size_t)wave * kWtWave;
+    f32x4_t dg = {0.0f, 0.0f, 0.0f, 0.0f}, du = {0.0f, 0.0f, 0.0f, 0.0f};
+    WtBatch b0, b1;
+    wt_load(b0, a, row, have, xrow, xreal, s0, s1, lane);
+    for (int s = s0; s < s1; s += 2 * kWtSteps) {
+        const int sb = s + kWtSteps;
+        if (sb < s1)
+            wt_load(b1, a, row, have, xrow, xreal, sb, s1, lane);
+        wt_consume(wt, b0, s, s1, lane, dg, du);
+        if (sb >= s1)
+            break;
+        if (sb + kWtSteps < s1)
+            wt_load(b0, a, row, have, xrow, xreal, sb + kWtSteps, s1, lane);
+        wt_consume(wt, b1, sb, s1, lane, dg, du);
+    }
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+        const int e = (4 * g + r) * kTile + i;  // D[4g + r][i]
+        part[(wave * 2 + 0) * 256 + e] = dg[r];
+        part[(wave * 2 + 1) * 256 + e] = du[r];
+    }
+    __syncthreads();
+    const int ti = threadIdx.x / kTile, tj = threadIdx.x % kTile;  // D[ti][tj] of each tile
+    for (int tile = 0; tile < ntiles; ++tile) {
+        float gs = 0.0f, us = 0.0f;
+        for (int v = tile * wpt; v < (tile + 1) * wpt; ++v) {
+            gs += part[(v * 2 + 0) * 256 + threadIdx.x];
+            us += part[(v * 2 + 1) * 256 + threadIdx.x];
+        }
+        const int rank = tile * kTile + ti;
+        if (rank < n && tj < a.nb)
+            a.s[(size_t)tj * a.d_ff + lrow[rank]] = us * silu(gs);
+    }
+}
+
 // Practical D-CountDown coefficient kernel for batches of 4-8 (Sec. 4): the
 // scoring of k_coef_pred, then the block's active neurons in tiles of 16 on MFMA.
 template <int B, int NK, int LCPR>
 __global__ __launch_bounds__(kBlock) void k_coef_pred_mfma(const CoefArgs a)
 {
-    // LDS: tokens [B][kStride] (+ zero chunk), then the latent [B][d_rank] fp32,
-    // whose space later holds the partial sums [4 waves][2][16 x 16] fp32
+    // LDS: the waves' weight tiles [4][kWtWave] bf16, then the latent [B][d_rank]
+    // fp32 (rank 1024 only), whose space later holds the partial sums [4][2][16 x 16]
     extern __shared__ __align__(16) uint32_t xs[];
     __shared__ uint32_t wflag[kWavesPerBlock];
     __shared__ int lrow[kPredRows];
@@ -792,13 +921,9 @@ __global__ __launch_bounds__(kBlock) void k_coef_pred_mfma(const CoefArgs a)
     const int r0 = blockIdx.x * kPredRows;
     const int wr0 = r0 + wave * kPredRowsPerWave;
 
-    // (the tokens are staged before the scores: holding them in registers
-    // through the scoring costs occupancy, measured slower at 8 tokens)
     using LR = LatentRegs<B, LCPR>;
     u32x4 wb[S::kLoads];
     pred_issue_bt<LCPR>(wb, a, wr0, lane);
-    MfmaTokens<B, NK> mt;
-    mt.issue(a);
     LR lr;
     lr.issue(a.lat, a.nb, a.d_rank, lane);
     LatentStage<LR::kRegs ? 1 : B> ls;  // the LDS copy, rank 1024 only
@@ -806,11 +931,12 @@ __global__ __launch_bounds__(kBlock) void k_coef_pred_mfma(const CoefArgs a)
         ls.issue(a.lat, a.nb, a.d_rank);
     __builtin_amdgcn_sched_barrier(0);
     zero_y(a.y, a.nb * a.d_model);
-    const uint32_t *zchunk = mt.write(xs);
-    uint32_t *latw = xs + mfma_lds_tokens_u32<B, NK>();
-    if constexpr (!LR::kRegs)
+    uint16_t *wtiles = reinterpret_cast<uint16_t *>(xs);
+    uint32_t *latw = xs + kWavesPerBlock * kWtWave / 2;
+    if constexpr (!LR::kRegs) {
         ls.write(reinterpret_cast<u32x4 *>(latw), a.lat, a.nb, a.d_rank);
-    __syncthreads();
+        __syncthreads();
+    }
 
     const uint32_t wmask = pred_score<B, LCPR>(wb, lr, reinterpret_cast<const float *>(latw), a,
                                                wr0, lane);
@@ -821,8 +947,8 @@ __global__ __launch_bounds__(kBlock) void k_coef_pred_mfma(const CoefArgs a)
 #pragma unroll
     for (int v = 0; v < kWavesPerBlock; ++v)
         M |= wflag[v] << (v * kPredRowsPerWave);
-    // the latent is no longer read once gather_mfma's first barrier has passed
-    gather_mfma<B, NK>(a, xs, zchunk, reinterpret_cast<float *>(latw), lrow, M, r0, wave, lane);
+    // the latent is no longer read once gather_mfma_lds's first barrier has passed
+    gather_mfma_lds<B, NK>(a, wtiles, reinterpret_cast<float *>(latw), lrow, M, r0, wave, lane);
 }
 
 // ------------------------------------------------ ternary predictor
@@ -2028,8 +2154,8 @@ static void coef_pred_lcpr(const CoefArgs &a, hipStream_t s)
     // MFMA tiles pay off at 8 tokens; at 4, a block's ~11 active neurons leave a
     // 16-row tile a third empty and the per-wave v_dot2 gather is faster (measured)
     if constexpr (B >= 8) {
-        // tokens (padded rows + zero chunk), then max(latent, 4 x 2 x 16 x 16 partial sums)
-        const size_t lds = mfma_lds_tokens_u32<B, NK>() * 4 +
+        // weight tiles, then max(latent, 4 x 2 x 16 x 16 partial sums)
+        const size_t lds = (size_t)kWavesPerBlock * kWtWave * 2 +
                            max(lat_lds, (size_t)kWavesPerBlock * 2 * 256 * 4);
         allow_lds(k_coef_pred_mfma<B, NK, LCPR>, lds);
         k_coef_pred_mfma<B, NK, LCPR><<<grid, kBlock, lds, s>>>(a);
