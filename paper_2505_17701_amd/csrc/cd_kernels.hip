@@ -603,7 +603,7 @@ __global__ __launch_bounds__(kBlock) void k_coef_pred(const CoefArgs a)
     gather_rr<B, NK, XREG>(a, tok, m, r0, lane);
 }
 
-// ------------------------------------------- MFMA gather for batches of 4-8
+// ------------------------------------------- MFMA gather for batches of 5-8
 // For 4-8 tokens the gathered products are small dense contractions: a tile
 // of 16 active neurons times the batch, on v_mfma_f32_16x16x32_bf16. Lane
 // l = i + 16 g (i = l % 16, g = l / 16) supplies row i of the tile (A operand)
@@ -616,7 +616,6 @@ typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
 typedef float f32x4_t __attribute__((ext_vector_type(4)));
 
 constexpr int kTile = 16;
-constexpr int kMfmaSteps = 8;  // 32-column steps per load batch (16 loads of 16 B per lane)
 
 __device__ __forceinline__ f32x4_t mfma16(const u32x4 &a, const u32x4 &b, f32x4_t c)
 {
@@ -636,40 +635,6 @@ template <int B, int NK>
 __host__ __device__ constexpr size_t mfma_lds_tokens_u32()
 {
     return (size_t)B * MfmaTokLayout<NK>::kStride + 4;
-}
-
-// one batch of kMfmaSteps steps of the tile's W_gate and W_up rows
-template <int NK>
-__device__ __forceinline__ void mfma_load(u32x4 (&ga)[kMfmaSteps], u32x4 (&ua)[kMfmaSteps],
-                                          const uint16_t *wg_row, const uint16_t *wu_row,
-                                          bool have, int s, int s1, int g, int d_model)
-{
-#pragma unroll
-    for (int q = 0; q < kMfmaSteps; ++q) {
-        const int col = (s + q) * 32 + g * 8;
-        ga[q] = zero16();
-        ua[q] = zero16();
-        if (have && s + q < s1 && col < d_model) {
-            ga[q] = load16_stream(wg_row + col);
-            ua[q] = load16_stream(wu_row + col);
-        }
-    }
-}
-
-__device__ __forceinline__ void mfma_consume(const u32x4 (&ga)[kMfmaSteps],
-                                             const u32x4 (&ua)[kMfmaSteps], const uint32_t *xrow,
-                                             bool xreal, int s, int s1, int g, f32x4_t &dg,
-                                             f32x4_t &du)
-{
-#pragma unroll
-    for (int q = 0; q < kMfmaSteps; ++q) {
-        if (s + q < s1) {  // uniform
-            const u32x4 xv =
-                *reinterpret_cast<const u32x4 *>(xrow + (xreal ? ((s + q) * 32 + g * 8) / 2 : 0));
-            dg = mfma16(ga[q], xv, dg);
-            du = mfma16(ua[q], xv, du);
-        }
-    }
 }
 
 // The tokens of the MFMA kernels: every thread's share of the LDS copy is
@@ -710,72 +675,6 @@ struct MfmaTokens {
         return zchunk;
     }
 };
-
-// MFMA gather of the block's active neurons (block mask M, base r0) for
-// batches of 4-8: the tokens in LDS (rows of kStride u32, zero chunk after
-// them), part = LDS scratch [4 waves][2][16 x 16] fp32, lrow = LDS list of
-// kPredRows ints. Every thread of the workgroup must call this.
-template <int B, int NK>
-__device__ __forceinline__ void gather_mfma(const CoefArgs &a, const uint32_t *xs,
-                                            const uint32_t *zchunk, float *part, int *lrow,
-                                            uint32_t M, int r0, int wave, int lane)
-{
-    using TL = MfmaTokLayout<NK>;
-    const int n = __builtin_popcount(M);
-    if (threadIdx.x < kPredRows && ((M >> threadIdx.x) & 1u))
-        lrow[__builtin_popcount(M & ((1u << threadIdx.x) - 1u))] = r0 + threadIdx.x;
-    __syncthreads();  // lrow visible; the LDS scratch is free
-
-    // tiles of 16 active neurons: one tile takes the four waves, two tiles a pair each;
-    // the waves of a tile split its 32-column steps into contiguous ranges
-    const int ntiles = (n + kTile - 1) / kTile;  // 0, 1 or 2
-    if (ntiles == 0)
-        return;
-    const int wpt = kWavesPerBlock / ntiles;
-    const int t0 = (wave / wpt) * kTile, kw = wave % wpt;
-    const int i = lane % kTile, g = lane / kTile;
-    const int steps = (a.d_model + 31) / 32;
-    const int sw = (steps + wpt - 1) / wpt;
-    const int s0 = min(steps, kw * sw), s1 = min(steps, s0 + sw);
-    const bool xreal = i < a.nb;
-    const uint32_t *xrow = xreal ? xs + (size_t)i * TL::kStride : zchunk;
-    const bool have = t0 + i < n;
-    const int row = have ? lrow[t0 + i] : r0;
-    const uint16_t *wg_row = a.Wg + (size_t)row * a.d_model;
-    const uint16_t *wu_row = a.Wu + (size_t)row * a.d_model;
-    f32x4_t dg = {0.0f, 0.0f, 0.0f, 0.0f}, du = {0.0f, 0.0f, 0.0f, 0.0f};
-    u32x4 ga[kMfmaSteps], ua[kMfmaSteps], gb[kMfmaSteps], ub[kMfmaSteps];
-    mfma_load<NK>(ga, ua, wg_row, wu_row, have, s0, s1, g, a.d_model);
-    for (int s = s0; s < s1; s += 2 * kMfmaSteps) {
-        const int sb = s + kMfmaSteps;
-        if (sb < s1)
-            mfma_load<NK>(gb, ub, wg_row, wu_row, have, sb, s1, g, a.d_model);
-        mfma_consume(ga, ua, xrow, xreal, s, s1, g, dg, du);
-        if (sb >= s1)
-            break;
-        if (sb + kMfmaSteps < s1)
-            mfma_load<NK>(ga, ua, wg_row, wu_row, have, sb + kMfmaSteps, s1, g, a.d_model);
-        mfma_consume(gb, ub, xrow, xreal, sb, s1, g, dg, du);
-    }
-#pragma unroll
-    for (int r = 0; r < 4; ++r) {
-        const int e = (4 * g + r) * kTile + i;  // D[4g + r][i]
-        part[(wave * 2 + 0) * 256 + e] = dg[r];
-        part[(wave * 2 + 1) * 256 + e] = du[r];
-    }
-    __syncthreads();
-    const int ti = threadIdx.x / kTile, tj = threadIdx.x % kTile;  // D[ti][tj] of each tile
-    for (int tile = 0; tile < ntiles; ++tile) {
-        float gs = 0.0f, us = 0.0f;
-        for (int v = tile * wpt; v < (tile + 1) * wpt; ++v) {
-            gs += part[(v * 2 + 0) * 256 + threadIdx.x];
-            us += part[(v * 2 + 1) * 256 + threadIdx.x];
-        }
-        const int rank = tile * kTile + ti;
-        if (rank < n && tj < a.nb)
-            a.s[(size_t)tj * a.d_ff + lrow[rank]] = us * silu(gs);
-    }
-}
 
 // MFMA gather with the weight rows staged in LDS. Loads in the MFMA operand
 // layout (16 rows x 64 B per instruction) reach about 60% of the HBM rate of
@@ -1119,12 +1018,23 @@ __global__ __launch_bounds__(kBlock) void k_coef_tern(const CoefArgs a)
     gather_rr<B, NK, XREG>(a, tok, m, r0, lane);
 }
 
+// LDS bytes of the ternary MFMA kernel: the token copy, which the gather's
+// weight tiles reuse once the scores are in, then the partial sums
+template <int B, int NK>
+__host__ __device__ constexpr size_t tern_mfma_front_u32()
+{
+    return mfma_lds_tokens_u32<B, NK>() > (size_t)kWavesPerBlock * kWtWave / 2
+               ? mfma_lds_tokens_u32<B, NK>()
+               : (size_t)kWavesPerBlock * kWtWave / 2;
+}
+
 // Ternary-predictor coefficient kernel for batches of 5-8: the ternary score,
-// then the MFMA gather.
+// then the MFMA gather with LDS-staged weight rows.
 template <int B, int NK>
 __global__ __launch_bounds__(kBlock) void k_coef_tern_mfma(const CoefArgs a)
 {
-    // LDS: tokens [B][kStride] (+ zero chunk), then the partial sums [4 waves][2][16 x 16]
+    // LDS: tokens [B][kStride] (+ zero chunk), overlaid by the weight tiles after
+    // the scores, then the partial sums [4 waves][2][16 x 16]
     extern __shared__ __align__(16) uint32_t xs[];
     __shared__ uint32_t wflag[kWavesPerBlock];
     __shared__ int lrow[kPredRows];
@@ -1157,9 +1067,11 @@ __global__ __launch_bounds__(kBlock) void k_coef_tern_mfma(const CoefArgs a)
 #pragma unroll
     for (int v = 0; v < kWavesPerBlock; ++v)
         M |= wflag[v] << (v * kPredRowsPerWave);
-    gather_mfma<B, NK>(a, xs, zchunk,
-                       reinterpret_cast<float *>(xs + mfma_lds_tokens_u32<B, NK>()), lrow, M, r0,
-                       wave, lane);
+    (void)zchunk;
+    // (the barrier above ends the token reads: the tiles may overwrite them)
+    gather_mfma_lds<B, NK>(a, reinterpret_cast<uint16_t *>(xs),
+                           reinterpret_cast<float *>(xs + tern_mfma_front_u32<B, NK>()), lrow, M,
+                           r0, wave, lane);
 }
 
 // latent = x . theta_A for the predictor: one workgroup per row of A_t, the
@@ -2189,7 +2101,7 @@ static hipError_t coef_tern_launch(const CoefArgs &a, hipStream_t s)
 {
     const int grid = (a.d_ff + kPredRows - 1) / kPredRows;
     if constexpr (B >= 8) {  // MFMA gather, as for the low-rank predictor
-        const size_t lds = mfma_lds_tokens_u32<B, NK>() * 4 + (size_t)kWavesPerBlock * 2 * 256 * 4;
+        const size_t lds = tern_mfma_front_u32<B, NK>() * 4 + (size_t)kWavesPerBlock * 2 * 256 * 4;
         allow_lds(k_coef_tern_mfma<B, NK>, lds);
         k_coef_tern_mfma<B, NK><<<grid, kBlock, lds, s>>>(a);
     } else {
