@@ -408,3 +408,54 @@ def test_graph_replay_matches_eager(tiny):
         torch.cuda.synchronize()
         for y, e in zip(ys, eager):
             torch.testing.assert_close(y, e, rtol=0, atol=1e-6 * float(e.abs().max()) + 1e-30)
+
+
+def test_graph_replay_all_paths():
+    """Graph replay of the batch-8 predictor (MFMA gather and MFMA down projection),
+    the ternary predictor and the per-token path, against their eager results."""
+    from paper_2505_17701_amd import binding as cd
+    from workloads import make_ternary
+
+    dm, dff = 1024, 2056
+    L = make_layer(830, dm, dff, 0.03)
+    P = make_predictor(830, dm, 64, dff, 0.05)
+    T = make_ternary(830, dm, dff)
+    layer = Layer(L, P, T)
+    D = layer.d
+    X = dev_bf16(make_tokens(830, 16, dm))
+    th_p = calibrated("dual_pred", layer, 830, 0.7, T=32)
+    th_t = float(np.float32(oracle.calibrate("dual_tern", make_tokens(830, 32, dm, purpose=T_CALIB),
+                                             0.7, theta_t=T)[0]))
+    plans = [cd.Plan(dm, dff, 8, 64) for _ in range(4)]
+    ys = [torch.empty((8, dm), dtype=torch.float32, device="cuda") for _ in range(4)]
+
+    def calls():
+        cd.countdown_ffn_dual(plans[0], X[:8], D["W_gate"], D["W_up"], D["W_down"], th_p,
+                              A_t=D["A_t"], B_t=D["B_t"], y=ys[0])
+        cd.countdown_ffn_tern(plans[1], X[8:16], D["W_gate"], D["W_up"], D["W_down"],
+                              D["theta_p"], th_t, y=ys[1])
+        cd.countdown_ffn_topk(plans[2], cd.CD_VARIANT_MONO, X[2:6], D["W_gate"], D["W_up"],
+                              D["W_down"], 0.9, y=ys[2][:4])
+        cd.countdown_ffn_tern_topk(plans[3], X[5:6], D["W_gate"], D["W_up"], D["W_down"],
+                                   D["theta_p"], 0.8, y=ys[3][:1])
+
+    calls()
+    torch.cuda.synchronize()
+    eager = [y.clone() for y in ys]
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        calls()
+    for rep in range(3):
+        for y in ys:
+            y.fill_(float("nan"))
+        cd.countdown_ffn_dual(plans[0], X[8:16], D["W_gate"], D["W_up"], D["W_down"], th_p,
+                              A_t=D["A_t"], B_t=D["B_t"])  # eager work between replays
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        for k, (y, e) in enumerate(zip(ys, eager)):
+            rows = (8, 8, 4, 1)[k]
+            torch.testing.assert_close(y[:rows], e[:rows], rtol=0,
+                                       atol=1e-6 * float(e[:rows].abs().max()) + 1e-30)
+    for p in plans:
+        p.close()
