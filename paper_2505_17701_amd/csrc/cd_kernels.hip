@@ -14,12 +14,18 @@
 //   predictor (practical D-CountDown): the latent x . theta_A (one workgroup
 //     per A_t row), then a coefficient kernel over blocks of 32 neurons: B_t
 //     scores, signed threshold, and the block's active neurons dealt to its
-//     waves for the W_gate / W_up gather.
-//   down kernel: workgroup (c, g) owns a 512-column chunk c and a
-//     contiguous neuron range g. One round trip reads act and s of the
-//     range, a wave ballot compacts the active neurons in ascending order
-//     into LDS, each wave then keeps 8 W_down rows in flight, the four waves
-//     reduce in LDS and add the chunk to y with one fp32 atomic per column.
+//     waves for the W_gate / W_up gather (v_dot2 up to 4 tokens, MFMA tiles
+//     of 16 neurons with the rows staged through LDS for 5-8). The ternary
+//     predictor scores from its 2-bit packed theta instead, with no latent.
+//   down kernel: workgroup (c, g) owns a column chunk c and a contiguous
+//     neuron range g. One round trip reads act and s of the range, a wave
+//     ballot compacts the active neurons in ascending order into LDS; for 1-2
+//     tokens each wave then keeps 8 W_down rows in flight on the VALU, for
+//     4-8 the rows feed MFMA (S as bf16 hi + lo); partial sums are added in
+//     LDS and go to y with one fp32 atomic per column and token.
+//   per-token threshold: the coefficient kernel writes the dense
+//     coefficients, one workgroup per token selects its quantile by radix
+//     select, a gather kernel thresholds and gathers.
 // The residual stream of a layer stack (h += y, x = bf16(RMSNorm(h))) is a
 // small kernel of its own, or part of the latent kernel with the predictor.
 #include "cd_device.hpp"
