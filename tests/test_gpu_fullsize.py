@@ -72,3 +72,29 @@ def test_llama70b_layer(llama70b, k):
     n, flips, rel = compare(plan, "mono", layer, w.tokens(1), thld, f"70b mono k={k}")
     print(f"70b mono k={k}: n={n} flips={flips} rel_err={rel:.2e}", flush=True)
     compare(plan, "dense", layer, w.tokens(1), 0.0, "70b dense", check_coef=False)
+
+
+def test_llama70b_per_token_and_calibration(llama70b):
+    """The 70B-shaped layer (d_ff 28672: the select with 32 keys per thread): the
+    per-token path at batch 2 and the GPU calibration against the oracle."""
+    import math
+
+    import numpy as np
+
+    import oracle
+    from gpu_support import dev_bf16
+    from paper_2505_17701_amd import binding as cd
+    from test_gpu_topk import check_topk
+    from workloads.synth import T_CALIB
+
+    w, layer = llama70b
+    n, flips, rel = check_topk("mono", layer, w.tokens(2), 0.9, "70b mono topk B=2")
+    print(f"70b mono topk B=2: n={n} flips={flips} rel={rel:.2e}", flush=True)
+    X = w.tokens(4, purpose=T_CALIB)
+    plan = cd.Plan(w.d_model, w.d_ff, 4)
+    th, q = cd.countdown_calibrate(plan, cd.CD_VARIANT_MONO, dev_bf16(X), 0.7,
+                                   W_up=layer.d["W_up"])
+    plan.close()
+    t_o, q_o = oracle.calibrate("mono", X, 0.7, W_up=layer.h["W_up"])
+    np.testing.assert_allclose(q.cpu().numpy(), q_o, rtol=2e-5)
+    assert abs(float(th.item()) - t_o) <= 2e-5 * abs(t_o)
