@@ -77,8 +77,6 @@ def test_llama70b_layer(llama70b, k):
 def test_llama70b_per_token_and_calibration(llama70b):
     """The 70B-shaped layer (d_ff 28672: the select with 32 keys per thread): the
     per-token path at batch 2 and the GPU calibration against the oracle."""
-    import math
-
     import numpy as np
 
     import oracle
