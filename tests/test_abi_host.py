@@ -193,3 +193,23 @@ def test_ternary_pack_rejects(lib):
     bad[3, 5] = 2
     with pytest.raises(cd.CountdownError):
         cd.countdown_ternary_pack(bad)
+
+
+def test_missing_library_fails_loudly(tmp_path):
+    """No fallback: loading a library that is not there raises, naming the build step."""
+    import subprocess
+    import sys
+
+    code = (
+        "import sys; sys.path.insert(0, %r)\n"
+        "from paper_2505_17701_amd import binding as cd\n"
+        "cd.LIB_PATH = %r\n"
+        "try:\n"
+        "    cd.load_library(cd.LIB_PATH)\n"
+        "except RuntimeError as e:\n"
+        "    print('raised:', e)\n"
+        "    sys.exit(0)\n"
+        "sys.exit(1)\n" % (ROOT, str(tmp_path / "absent.so")))
+    res = subprocess.run([sys.executable, "-c", code], capture_output=True, text=True)
+    assert res.returncode == 0, res.stdout + res.stderr
+    assert "build" in res.stdout
