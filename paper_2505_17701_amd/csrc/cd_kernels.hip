@@ -1707,19 +1707,33 @@ constexpr int kTopkThreads = 1024;
 constexpr int kTopkPerThread = 32;  // keys per thread: d_ff <= 32768
 
 // One workgroup per token: q = v[lo] + (h - lo)(v[lo + 1] - v[lo]), h = k (n - 1).
-// Both order statistics (ranks lo and lo + 1) come from 3 passes of radix
-// select (11, 11 and 10 bits, most significant first) over order-preserving
-// keys held in registers, run in lockstep: each pass histograms in LDS the
-// keys that match a rank's prefix so far (one histogram while both ranks
-// share their prefix, two once they part), scans the bins and picks the bin
-// that holds each rank. The first pass puts every key into one of 8 padded
-// histogram copies (by lane) so that the atomics of a wave on the few busy
-// bins of the top digit (sign, exponent, two mantissa bits) land on different
-// banks; the scans use DPP within waves and one barrier across them. fp64
-// interpolation.
-constexpr int kSelBins = 2048;
-constexpr int kSelCopies = 8;
-constexpr int kSelCopyStride = kSelBins + 1;  // padding: copies of a bin on different banks
+// Both order statistics (ranks lo and lo + 1) are found together from
+// order-preserving keys held in registers. The first radix pass histograms the
+// top 15 significant key bits (sign, exponent and the leading mantissa bits)
+// into 32768 LDS bins, so a bin spans a relative width of 2^-7 (2^-6 for
+// signed keys) and the bins of the two ranks typically hold a few dozen keys.
+// The count each key's atomic returns is its slot within its bin, so those
+// keys are placed into an LDS list without a second scan, and the thread
+// holding each candidate counts the candidates below it and equal to it: the
+// rank of every candidate is exact, ties included. When the two bins hold more
+// than kSelList keys (many equal values, or a narrow cluster), two radix passes
+// of 11 bits and of the rest fix every remaining bit instead, with one
+// histogram per rank once the ranks part. Slots past the row hold a key above
+// every finite value, which lands in the top bin. Every VALU instruction per
+// key costs the one CU about 16 cycles at 1024 threads, so the per-key work is
+// kept to the first pass and the placement. Scans use DPP within waves and
+// one barrier across them; fp64 interpolation.
+constexpr int kSelBits0 = 15;
+constexpr int kSelBins0 = 1 << kSelBits0;               // first pass
+constexpr int kSelPer0 = kSelBins0 / kTopkThreads;      // 32 consecutive bins per thread
+constexpr int kSelPad0 = kSelPer0 + 4;                  // their LDS words: lanes on different banks
+constexpr int kSelWords0 = kSelPad0 * kTopkThreads;
+constexpr int kSelBins = 2048;                          // later passes (11 bits)
+constexpr int kSelList = 512;                           // candidates ranked by counting
+constexpr uint32_t kSelNoKey = 0xffffffffu;             // slot past the row: above every finite key
+
+// LDS word of first-pass bin d
+__device__ __forceinline__ uint32_t sel_word(uint32_t d) { return d + 4u * (d >> 5); }
 
 // inclusive prefix sum over the 64 lanes (DPP row shifts, then row broadcasts)
 __device__ __forceinline__ uint32_t wave_incl_scan(uint32_t v)
@@ -1750,6 +1764,38 @@ __device__ __forceinline__ void block_scan(uint32_t v, uint32_t *wsum, uint32_t 
     excl = before + inc - v;
 }
 
+// The bin that holds rank r among this thread's 32 first-pass bins (LDS words
+// mine[0, 36), groups of 4 at 4 g summing to gs[g]), given base <= r < base +
+// sum(gs): out = {bin, rank within it, its count}. Only the group found is
+// read back.
+__device__ __forceinline__ void find_bin(const uint32_t *mine, const uint32_t (&gs)[kSelPer0 / 4],
+                                         uint32_t base, uint32_t r, uint32_t *out)
+{
+    uint32_t cum = base, gbase = base;
+    int gi = kSelPer0 / 4 - 1;
+    bool found = false;
+#pragma unroll
+    for (int i = 0; i < kSelPer0 / 4; ++i) {
+        const bool here = !found && r < cum + gs[i];
+        gi = here ? i : gi;
+        gbase = here ? cum : gbase;
+        found = found || here;
+        cum += gs[i];
+    }
+    const uint4 v = *reinterpret_cast<const uint4 *>(mine + 4 * gi);
+    uint32_t o = 3, before = gbase + v.x + v.y + v.z, cnt = v.w;
+    if (r < gbase + v.x) {
+        o = 0, before = gbase, cnt = v.x;
+    } else if (r < gbase + v.x + v.y) {
+        o = 1, before = gbase + v.x, cnt = v.y;
+    } else if (r < gbase + v.x + v.y + v.z) {
+        o = 2, before = gbase + v.x + v.y, cnt = v.z;
+    }
+    out[0] = kSelPer0 * threadIdx.x + 4 * gi + o;
+    out[1] = r - before;
+    out[2] = cnt;
+}
+
 template <int KPT>
 __global__ __launch_bounds__(kTopkThreads) void k_topk_select(const float *__restrict__ coef, int ld,
                                                               int n, int use_abs, double k,
@@ -1757,11 +1803,13 @@ __global__ __launch_bounds__(kTopkThreads) void k_topk_select(const float *__res
 {
     constexpr int kWaves = kTopkThreads / kWave;
     extern __shared__ __align__(16) uint32_t sm[];
-    uint32_t *hA = sm;                                    // [kSelCopies][kSelCopyStride] rank lo
-    uint32_t *hB = hA + kSelCopies * kSelCopyStride;      // [kSelBins] rank lo + 1 once apart
-    uint32_t *sink = hB + kSelBins;                       // [64] counts of the other keys
-    __shared__ uint32_t wsum[2][kWaves];
-    __shared__ int sel[2][2];                             // [rank][bin, rank within bin]
+    uint32_t *hA = sm;                    // first pass: bin d at word sel_word(d); later: [kSelBins] rank lo
+    uint32_t *hB = sm + kSelBins;         // later passes: [kSelBins] rank lo + 1, once apart
+    uint32_t *list = sm + kSelWords0;     // [kSelList] candidate keys, then kSelNoKey
+    uint32_t *dump = list + kSelList;     // [64] stores of the other keys (never read)
+    __shared__ uint32_t wsum[kWaves];
+    __shared__ uint32_t sel[2][3];        // [rank][bin, rank within bin, keys in bin]
+    __shared__ uint32_t val[2];
     const int lane = threadIdx.x % kWave;
     const float *c = coef + (size_t)blockIdx.x * ld;
     const int jn = (n + kTopkThreads - 1) / kTopkThreads;  // key slots in use (uniform)
@@ -1773,100 +1821,166 @@ __global__ __launch_bounds__(kTopkThreads) void k_topk_select(const float *__res
         if (j < jn)  // uniform
             cv[j] = *or_zero(i < n, c + i);
     }
-    for (int i = threadIdx.x; i < kSelCopies * kSelCopyStride + kSelBins; i += kTopkThreads)
-        sm[i] = 0u;  // (the sink words are never read)
+    for (int i = threadIdx.x; i < kSelWords0 / 4; i += kTopkThreads)
+        reinterpret_cast<uint4 *>(sm)[i] = make_uint4(0u, 0u, 0u, 0u);
+    if (threadIdx.x < kSelList)
+        list[threadIdx.x] = kSelNoKey;
     uint32_t key[KPT];
-    uint32_t valid = 0u;  // bit j: slot j holds a key
+    const uint32_t am = use_abs ? ~0u : 0u;  // order_key without a branch per slot
 #pragma unroll
     for (int j = 0; j < KPT; ++j) {
-        key[j] = order_key(cv[j], use_abs);
-        if (j < jn && threadIdx.x + j * kTopkThreads < n)
-            valid |= 1u << j;
+        const uint32_t u = __float_as_uint(cv[j]);
+        const uint32_t sk = u ^ ((uint32_t)((int32_t)u >> 31) | 0x80000000u);
+        key[j] = threadIdx.x + j * kTopkThreads < n ? ((u & 0x7fffffffu) & am) | (sk & ~am)
+                                                    : kSelNoKey;
     }
     const double h = k * (double)(n - 1);
     int lo = (int)floor(h);
     if (lo > n - 1)
         lo = n - 1;
     const bool two = lo + 1 < n;  // rank lo + 1 exists
+    const uint32_t rlo = (uint32_t)lo, rhi = two ? rlo + 1u : rlo;
+    const int sh0 = use_abs ? 16 : 17;  // |c| keys have bit 31 clear
     __syncthreads();
 
-    uint32_t pA = 0u, pB = 0u, mask = 0u;  // prefixes of the two ranks, digits fixed so far
-    int rA = lo, rB = two ? lo + 1 : lo;   // ranks within the keys matching the prefixes
-#pragma unroll 1
-    for (int pass = 0; pass < 3; ++pass) {  // one copy of the pass code (instruction fetch)
-        const int shift = pass == 0 ? 21 : pass == 1 ? 10 : 0;
-        const uint32_t dmask = pass == 2 ? 0x3ffu : 0x7ffu;
-        const bool apart = pA != pB;  // uniform
-        // the first pass spreads over the copies; later passes see few keys per bin
-        const int ncopy = pass == 0 ? kSelCopies : 1;
-        uint32_t *hc = hA + (lane % ncopy) * kSelCopyStride;
-        // branch-free: a key matching neither prefix (or no key) counts into this
-        // lane's own sink word
+    // first pass; the returned count is the key's slot within its bin
+    uint32_t pos[KPT];
+#pragma unroll
+    for (int j = 0; j < KPT; ++j) {
+        pos[j] = 0u;
+        if (j < jn)  // uniform
+            pos[j] = atomicAdd(hA + sel_word((key[j] >> sh0) & (uint32_t)(kSelBins0 - 1)), 1u);
+    }
+    __syncthreads();
+    {
+        const uint32_t *mine = hA + kSelPad0 * threadIdx.x;
+        uint32_t gs[kSelPer0 / 4];
+        uint32_t sum = 0u;
+#pragma unroll
+        for (int i = 0; i < kSelPer0 / 4; ++i) {
+            const uint4 g = reinterpret_cast<const uint4 *>(mine)[i];
+            gs[i] = g.x + g.y + g.z + g.w;
+            sum += gs[i];
+        }
+        uint32_t e, tot;
+        block_scan(sum, wsum, e, tot);
+        if (rlo >= e && rlo < e + sum)
+            find_bin(mine, gs, e, rlo, sel[0]);
+        if (rhi >= e && rhi < e + sum)
+            find_bin(mine, gs, e, rhi, sel[1]);
+        __syncthreads();
+    }
+    const uint32_t binA = sel[0][0], binB = sel[1][0];
+    uint32_t rA = sel[0][1], rB = sel[1][1];
+    const uint32_t cA = sel[0][2];
+    const bool apart = binA != binB;  // then rank lo is the last of its bin, lo + 1 the first of its
+    const uint32_t cnt = cA + (apart ? sel[1][2] : 0u);
+    uint32_t kA, kB;
+    if (cnt <= (uint32_t)kSelList) {  // uniform
+        // bin A's keys fill list[0, cA), bin B's follow
 #pragma unroll
         for (int j = 0; j < KPT; ++j) {
             if (j < jn) {  // uniform
-                const uint32_t d = (key[j] >> shift) & dmask;
-                const uint32_t pk = key[j] & mask;
-                const bool v = (valid >> j) & 1u;
-                uint32_t *dst = sink + lane;
-                dst = v && apart && pk == pB ? hB + d : dst;
-                dst = v && pk == pA ? hc + d : dst;
-                atomicAdd(dst, 1u);
+                const uint32_t d = (key[j] >> sh0) & (uint32_t)(kSelBins0 - 1);
+                const uint32_t at = d == binA ? pos[j] : cA + pos[j];
+                const bool m = (d == binA || d == binB) && at < (uint32_t)kSelList;
+                *(m ? list + at : dump + lane) = key[j];
             }
         }
         __syncthreads();
-        // thread t owns bins 2t and 2t + 1 (cleared for the next pass as they are read)
-        uint32_t a0 = 0u, a1 = 0u;
-        for (int cpy = 0; cpy < ncopy; ++cpy) {
-            uint32_t *bin = hA + cpy * kSelCopyStride + 2 * threadIdx.x;
-            a0 += bin[0];
-            a1 += bin[1];
-            bin[0] = 0u;
-            bin[1] = 0u;
-        }
-        uint32_t ea, ta;
-        block_scan(a0 + a1, wsum[0], ea, ta);
-        uint32_t b0 = a0, b1 = a1, eb = ea;
-        if (apart) {
-            b0 = hB[2 * threadIdx.x];
-            b1 = hB[2 * threadIdx.x + 1];
-            hB[2 * threadIdx.x] = 0u;
-            hB[2 * threadIdx.x + 1] = 0u;
-            uint32_t tb;
-            block_scan(b0 + b1, wsum[1], eb, tb);
-        }
-        const uint32_t ra = (uint32_t)rA, rb = (uint32_t)rB;
-        if (ra >= ea && ra < ea + a0) {
-            sel[0][0] = 2 * threadIdx.x;
-            sel[0][1] = (int)(ra - ea);
-        } else if (ra >= ea + a0 && ra < ea + a0 + a1) {
-            sel[0][0] = 2 * threadIdx.x + 1;
-            sel[0][1] = (int)(ra - ea - a0);
-        }
-        if (rb >= eb && rb < eb + b0) {
-            sel[1][0] = 2 * threadIdx.x;
-            sel[1][1] = (int)(rb - eb);
-        } else if (rb >= eb + b0 && rb < eb + b0 + b1) {
-            sel[1][0] = 2 * threadIdx.x + 1;
-            sel[1][1] = (int)(rb - eb - b0);
+        const uint32_t tA = rA, tB = apart ? cA + rB : rB;
+        if (threadIdx.x < cnt) {
+            const uint32_t me = list[threadIdx.x];
+            const uint4 *l4 = reinterpret_cast<const uint4 *>(list);
+            uint32_t less = 0u, leq = 0u;
+#pragma unroll 1
+            for (uint32_t j = 0; j < cnt; j += 8) {  // the list is kSelNoKey past cnt
+                const uint4 o = l4[j / 4], p = l4[j / 4 + 1];
+                less += (o.x < me ? 1u : 0u) + (o.y < me ? 1u : 0u) + (o.z < me ? 1u : 0u) +
+                        (o.w < me ? 1u : 0u) + (p.x < me ? 1u : 0u) + (p.y < me ? 1u : 0u) +
+                        (p.z < me ? 1u : 0u) + (p.w < me ? 1u : 0u);
+                leq += (o.x <= me ? 1u : 0u) + (o.y <= me ? 1u : 0u) + (o.z <= me ? 1u : 0u) +
+                       (o.w <= me ? 1u : 0u) + (p.x <= me ? 1u : 0u) + (p.y <= me ? 1u : 0u) +
+                       (p.z <= me ? 1u : 0u) + (p.w <= me ? 1u : 0u);
+            }
+            if (less <= tA && tA < leq)
+                val[0] = me;
+            if (less <= tB && tB < leq)
+                val[1] = me;
         }
         __syncthreads();
-        pA |= (uint32_t)sel[0][0] << shift;
-        pB |= (uint32_t)sel[1][0] << shift;
-        mask |= dmask << shift;
-        rA = sel[0][1];
-        rB = sel[1][1];
+        kA = val[0];
+        kB = val[1];
+    } else {
+        // many keys in the bins: radix passes over the remaining bits (11, then
+        // the rest); the bins of both histograms are cleared as they are read
+        reinterpret_cast<uint4 *>(sm)[threadIdx.x] = make_uint4(0u, 0u, 0u, 0u);  // hA, hB
+        __syncthreads();
+        uint32_t pA = binA << sh0, pB = binB << sh0;
+        uint32_t mask = (uint32_t)(kSelBins0 - 1) << sh0;
+#pragma unroll 1
+        for (int pass = 1; pass < 3; ++pass) {
+            const bool ap = pA != pB;  // uniform
+            const int shift = pass == 1 ? sh0 - 11 : 0;
+            const uint32_t dmask = pass == 1 ? 0x7ffu : (1u << (sh0 - 11)) - 1u;
+#pragma unroll
+            for (int j = 0; j < KPT; ++j) {
+                if (j < jn) {  // uniform
+                    const uint32_t d = (key[j] >> shift) & dmask;
+                    const uint32_t pk = key[j] & mask;
+                    uint32_t *dst = dump + lane;
+                    dst = ap && pk == pB ? hB + d : dst;
+                    dst = pk == pA ? hA + d : dst;
+                    atomicAdd(dst, 1u);
+                }
+            }
+            __syncthreads();
+            // thread t owns bins 2t and 2t + 1
+            const uint32_t a0 = hA[2 * threadIdx.x], a1 = hA[2 * threadIdx.x + 1];
+            hA[2 * threadIdx.x] = 0u;
+            hA[2 * threadIdx.x + 1] = 0u;
+            uint32_t ea, ta;
+            block_scan(a0 + a1, wsum, ea, ta);
+            uint32_t b0 = a0, b1 = a1, eb = ea;
+            if (ap) {
+                b0 = hB[2 * threadIdx.x];
+                b1 = hB[2 * threadIdx.x + 1];
+                hB[2 * threadIdx.x] = 0u;
+                hB[2 * threadIdx.x + 1] = 0u;
+                uint32_t tb;
+                __syncthreads();  // wsum is read by every thread before it is rewritten
+                block_scan(b0 + b1, wsum, eb, tb);
+            }
+            if (rA >= ea && rA < ea + a0) {
+                sel[0][0] = 2 * threadIdx.x, sel[0][1] = rA - ea;
+            } else if (rA >= ea + a0 && rA < ea + a0 + a1) {
+                sel[0][0] = 2 * threadIdx.x + 1, sel[0][1] = rA - ea - a0;
+            }
+            if (rB >= eb && rB < eb + b0) {
+                sel[1][0] = 2 * threadIdx.x, sel[1][1] = rB - eb;
+            } else if (rB >= eb + b0 && rB < eb + b0 + b1) {
+                sel[1][0] = 2 * threadIdx.x + 1, sel[1][1] = rB - eb - b0;
+            }
+            __syncthreads();
+            pA |= sel[0][0] << shift;
+            pB |= sel[1][0] << shift;
+            mask |= dmask << shift;
+            rA = sel[0][1];
+            rB = sel[1][1];
+        }
+        kA = pA;  // every bit is fixed
+        kB = pB;
     }
     if (threadIdx.x == 0) {
-        const double v0 = (double)key_value(pA, use_abs);
-        const double v1 = (double)key_value(two ? pB : pA, use_abs);
+        const double v0 = (double)key_value(kA, use_abs);
+        const double v1 = (double)key_value(two ? kB : kA, use_abs);
         q[blockIdx.x] = v0 + (h - (double)lo) * (v1 - v0);
     }
 }
 
 static size_t topk_select_lds_bytes()
 {
-    return ((size_t)kSelCopies * kSelCopyStride + kSelBins + kWave) * 4;
+    return ((size_t)kSelWords0 + kSelList + kWave) * 4;
 }
 
 // s of one active neuron of a single-projection variant from its second row

@@ -12,7 +12,7 @@ from gpu_support import dev_bf16
 from test_gpu_parity import Layer
 from test_gpu_topk import check_topk
 from workloads import make_layer, make_predictor, make_tokens
-from workloads.synth import T_CALIB
+from workloads.synth import T_CALIB, bf16_round
 
 torch = pytest.importorskip("torch")
 pytestmark = pytest.mark.gpu
@@ -33,15 +33,32 @@ def exact_quantile(v, k):
     return v[lo] + (h - lo) * (v[hi] - v[lo])
 
 
-@pytest.mark.parametrize("dm,dff,dup", [(256, 688, False), (64, 16384, False), (64, 16392, True),
-                                        (64, 32768, False), (64, 32776, False),
-                                        (128, 20000, True)])
+@pytest.mark.parametrize("dm,dff,dup", [(256, 688, None), (64, 16384, None), (64, 16392, "pairs"),
+                                        (64, 32768, None), (64, 32776, None),
+                                        (128, 20000, "pairs"), (64, 11008, "all"),
+                                        (64, 11008, "cluster"), (64, 28672, "cluster")])
 def test_select_exact_order_statistics(dm, dff, dup):
+    """dup: "pairs" makes every |u| value appear twice; "all" makes every row
+    equal, so all coefficients of a token tie; "cluster" gives 15/16 of the
+    rows one shared body and a small varying first weight, so most
+    coefficients of a token lie within a relative 2^-8 of each other, with
+    many ties: both put far more keys than the candidate list holds into the
+    select's first-pass bins, and the exact result then comes from its later
+    radix passes."""
     from paper_2505_17701_amd import binding as cd
 
     L = make_layer(1900 + dff % 97, dm, dff, 0.05)
-    if dup:  # pairs of equal rows: every |u| value appears twice
-        L["W_up"][1::2] = L["W_up"][0::2][: dff // 2]
+    W = L["W_up"]
+    if dup == "pairs":
+        W[1::2] = W[0::2][: dff // 2]
+    elif dup == "all":
+        W[:] = W[0]
+    elif dup == "cluster":
+        rows = np.arange(dff) % 16 != 0
+        W[rows] = W[0]
+        # first weight of each clustered row: 64 distinct bf16 values in [-2^-13, 2^-13)
+        small = (np.arange(dff) % 64 - 32).astype(np.float32) * np.float32(2.0 ** -18)
+        W[rows, 0] = bf16_round(small[rows])
     layer = Layer(L)
     T = 5
     X = make_tokens(1901, T, dm, purpose=T_CALIB)
@@ -50,13 +67,19 @@ def test_select_exact_order_statistics(dm, dff, dup):
     xd = dev_bf16(X)
     cd.countdown_ffn_mono(plan, xd, D["W_gate"], D["W_up"], D["W_down"], math.inf)
     coef = cd.countdown_export_active(plan)[2].cpu().numpy().astype(np.float64)[:T]
-    if dup:
+    if dup == "pairs":
         assert np.array_equal(np.abs(coef[:, 0::2][:, : dff // 2]), np.abs(coef[:, 1::2]))
-    for k in (0.0, 0.3, 0.9, 0.999, 1.0):
+    elif dup == "all":
+        assert (np.abs(coef) == np.abs(coef[:, :1])).all()
+    elif dup == "cluster":
+        c = np.abs(coef[:, rows])
+        assert (c.max(axis=1) - c.min(axis=1) < 2.0 ** -8 * c.max(axis=1)).all()
+        assert all(len(np.unique(r)) > 16 for r in c)
+    for k in (0.0, 0.3, 0.5, 0.9, 0.999, 1.0):
         _, q = cd.countdown_calibrate(plan, cd.CD_VARIANT_MONO, xd, k, W_up=D["W_up"])
         q = q.cpu().numpy()
         for t in range(T):
-            assert q[t] == exact_quantile(np.abs(coef[t]), k), (dff, k, t)
+            assert q[t] == exact_quantile(np.abs(coef[t]), k), (dff, dup, k, t)
     plan.close()
 
 
