@@ -24,8 +24,9 @@
 //     4-8 the rows feed MFMA (S as bf16 hi + lo); partial sums are added in
 //     LDS and go to y with one fp32 atomic per column and token.
 //   per-token threshold: the coefficient kernel writes the dense
-//     coefficients, one workgroup per token selects its quantile by radix
-//     select, a gather kernel thresholds and gathers.
+//     coefficients, one workgroup per token selects its quantile (one wide
+//     radix pass, then the few keys of the two bins ranked by counting), a
+//     gather kernel thresholds and gathers.
 // The residual stream of a layer stack (h += y, x = bf16(RMSNorm(h))) is a
 // small kernel of its own, or part of the latent kernel with the predictor.
 #include "cd_device.hpp"
