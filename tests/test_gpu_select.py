@@ -83,14 +83,24 @@ def test_select_exact_order_statistics(dm, dff, dup):
     plan.close()
 
 
-@pytest.mark.parametrize("dff", [688, 20000])
-def test_select_signed_scores(dff):
-    """The predictor's signed score: the quantile of the signed values."""
+@pytest.mark.parametrize("dff,cluster", [(688, False), (20000, False), (11008, True),
+                                         (20000, True)])
+def test_select_signed_scores(dff, cluster):
+    """The predictor's signed score: the quantile of the signed values. With
+    cluster, 15/16 of the B_t rows share one body and differ in a small first
+    entry, so most scores of a token lie within a relative 2^-8 of each other
+    (with ties): the select's later radix passes on signed keys."""
     from paper_2505_17701_amd import binding as cd
 
     dm, dr = 64, 8
     L = make_layer(1950, dm, dff, 0.05)
     P = make_predictor(1950, dm, dr, dff, 0.3)
+    if cluster:
+        Bt = P["B_t"]
+        rows = np.arange(dff) % 16 != 0
+        Bt[rows] = Bt[0]
+        small = (np.arange(dff) % 64 - 32).astype(np.float32) * np.float32(2.0 ** -19)
+        Bt[rows, 0] = bf16_round(small[rows])
     layer = Layer(L, P)
     T = 4
     X = make_tokens(1951, T, dm, purpose=T_CALIB)
@@ -100,13 +110,18 @@ def test_select_signed_scores(dff):
     cd.countdown_ffn_dual(plan, xd, D["W_gate"], D["W_up"], D["W_down"], math.inf,
                           A_t=D["A_t"], B_t=D["B_t"])
     coef = cd.countdown_export_active(plan)[2].cpu().numpy().astype(np.float64)[:T]
-    assert (coef < 0).any() and (coef > 0).any()
+    if cluster:
+        c = coef[:, rows]
+        assert (c.max(axis=1) - c.min(axis=1) < 2.0 ** -8 * np.abs(c).max(axis=1)).all()
+        assert all(len(np.unique(r)) > 8 for r in c)
+    else:
+        assert (coef < 0).any() and (coef > 0).any()
     for k in (0.1, 0.5, 0.9):
         _, q = cd.countdown_calibrate(plan, cd.CD_VARIANT_DUAL_PRED, xd, k, A_t=D["A_t"],
                                       B_t=D["B_t"])
         q = q.cpu().numpy()
         for t in range(T):
-            assert q[t] == exact_quantile(coef[t], k), (dff, k, t)
+            assert q[t] == exact_quantile(coef[t], k), (dff, cluster, k, t)
     plan.close()
 
 
