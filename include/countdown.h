@@ -39,6 +39,12 @@
  *    on error nothing is launched. A launch failure returns CD_EHIP.
  *  - A plan is not thread-safe: calls on one plan must not overlap (use one
  *    plan per stream).
+ *  - A plan belongs to the device that was current when it was created:
+ *    every call on it must be made with that device current (else
+ *    CD_EINVAL); countdown_plan_destroy switches to it by itself.
+ *  - The outputs of a call (y, and thld_out of the per-token calls) must not
+ *    share memory with its inputs (x, the weights, the predictor) or with
+ *    each other: CD_EINVAL. The residual step states its own rules.
  */
 #ifndef COUNTDOWN_H
 #define COUNTDOWN_H
@@ -204,7 +210,8 @@ cd_status countdown_ternary_pack(const int8_t *theta_t, int d_model, int d_ff, u
  * then y = FFN(x). x is written to x_out [B][d_model] bf16 (the FFN input).
  * h_in, y_prev, h_out are [B][d_model] fp32. Only y_prev and y may share
  * memory (y_prev is read before y is written); any other overlap among h_in,
- * h_out, x_out, y and y_prev is CD_EINVAL. eps must be finite and >= 0.
+ * h_out, x_out, y and y_prev, or of h_out, x_out or y with the weights or the
+ * predictor, is CD_EINVAL. eps must be finite and >= 0.
  * thld is ignored for CD_VARIANT_DENSE; A_t / B_t as for countdown_ffn_dual
  * (both set exactly for CD_VARIANT_DUAL_PRED, else NULL). With the predictor
  * the normalisation is computed inside the latent product's kernel.

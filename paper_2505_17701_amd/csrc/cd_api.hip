@@ -96,6 +96,52 @@ cd_status check_args(int variant, int d_model, int d_ff, int max_batch, int d_ra
 // CD_VARIANT_* and cdk::Variant share their numbering
 int kernel_variant(int variant) { return variant; }
 
+// [a, a + na) and [b, b + nb) share a byte
+bool overlaps(const void *a, size_t na, const void *b, size_t nb)
+{
+    const uintptr_t x = reinterpret_cast<uintptr_t>(a), y = reinterpret_cast<uintptr_t>(b);
+    return x < y + nb && y < x + na;
+}
+
+// A plan's workspace lives on the device current at its creation; a call made
+// with another device current would hand that device foreign pointers.
+cd_status plan_device_ok(const cd_plan *p)
+{
+    int dev = -1;
+    if (hipGetDevice(&dev) != hipSuccess)
+        return CD_EHIP;
+    return dev == p->device ? CD_OK : CD_EINVAL;
+}
+
+// The outputs of a call (y, and the per-token thresholds q when given) share
+// no memory with what it reads: the coefficient kernel zeroes y while other
+// workgroups still read x and the weights. Null inputs are skipped.
+bool outputs_disjoint(const cd_plan *p, int B, const void *x, const void *Wg, const void *Wu,
+                      const void *Wd, const void *At, const void *Bt, const void *Tp,
+                      const void *y, const void *q)
+{
+    const size_t xb = (size_t)B * p->d_model * sizeof(uint16_t);
+    const size_t wb = (size_t)p->d_ff * p->d_model * sizeof(uint16_t);
+    const size_t yb = (size_t)B * p->d_model * sizeof(float);
+    const struct {
+        const void *ptr;
+        size_t n;
+    } in[] = {{x, xb},
+              {Wg, wb},
+              {Wu, wb},
+              {Wd, wb},
+              {At, (size_t)p->d_rank * p->d_model * sizeof(uint16_t)},
+              {Bt, (size_t)p->d_ff * p->d_rank * sizeof(uint16_t)},
+              {Tp, (size_t)p->d_ff * cdk::tern_row_words(p->d_model) * sizeof(uint32_t)}};
+    for (const auto &t : in) {
+        if (!t.ptr)
+            continue;
+        if (overlaps(t.ptr, t.n, y, yb) || (q && overlaps(t.ptr, t.n, q, (size_t)B * sizeof(double))))
+            return false;
+    }
+    return !(q && overlaps(q, (size_t)B * sizeof(double), y, yb));
+}
+
 cdk::CoefArgs coef_args(cd_plan *p, const uint16_t *x, int B, const uint16_t *Wg,
                         const uint16_t *Wu, const uint16_t *Bt, float thld, float *y,
                         const uint32_t *Tp = nullptr)
@@ -147,6 +193,10 @@ cd_status run_ffn(cd_plan *p, int variant, const uint16_t *x, int B, const uint1
                               Wd, tern ? static_cast<const void *>(Tp) : At, Bt, thld, y);
     if (st != CD_OK)
         return st;
+    if (!outputs_disjoint(p, B, x, Wg, Wu, Wd, At, Bt, Tp, y, nullptr))
+        return CD_EINVAL;
+    if ((st = plan_device_ok(p)) != CD_OK)
+        return st;
     hipStream_t s = reinterpret_cast<hipStream_t>(stream);
     if (!(p->phases & CD_PHASE_COEF) && !p->has_state)
         return CD_EINVAL;  // a down-only call needs a previous coefficient kernel's output
@@ -168,13 +218,6 @@ cd_status run_ffn(cd_plan *p, int variant, const uint16_t *x, int B, const uint1
         st = launched(cdk::launch_down(da, s));
     }
     return st;
-}
-
-// [a, a + na) and [b, b + nb) share a byte
-bool overlaps(const void *a, size_t na, const void *b, size_t nb)
-{
-    const uintptr_t x = reinterpret_cast<uintptr_t>(a), y = reinterpret_cast<uintptr_t>(b);
-    return x < y + nb && y < x + na;
 }
 
 cd_status run_ffn_residual(cd_plan *p, int variant, const float *h_in, const float *y_prev,
@@ -200,6 +243,18 @@ cd_status run_ffn_residual(cd_plan *p, int variant, const float *h_in, const flo
         overlaps(x_out, xb, y, fb) || overlaps(h_in, fb, y, fb) ||
         (y_prev && (overlaps(y_prev, fb, h_out, fb) || overlaps(y_prev, fb, x_out, xb))))
         return CD_EINVAL;
+    if (!outputs_disjoint(p, B, nullptr, Wg, Wu, Wd, At, Bt, nullptr, y, nullptr))
+        return CD_EINVAL;
+    const void *weights[] = {Wg, Wu, Wd, At, Bt};
+    const size_t wsz[] = {(size_t)p->d_ff * p->d_model * 2, (size_t)p->d_ff * p->d_model * 2,
+                          (size_t)p->d_ff * p->d_model * 2, (size_t)p->d_rank * p->d_model * 2,
+                          (size_t)p->d_ff * p->d_rank * 2};
+    for (int i = 0; i < 5; ++i)
+        if (weights[i] && (overlaps(weights[i], wsz[i], h_out, fb) ||
+                           overlaps(weights[i], wsz[i], x_out, xb)))
+            return CD_EINVAL;
+    if ((st = plan_device_ok(p)) != CD_OK)
+        return st;
     hipStream_t s = reinterpret_cast<hipStream_t>(stream);
     if (!(p->phases & CD_PHASE_COEF) && !p->has_state)
         return CD_EINVAL;
@@ -254,6 +309,10 @@ cd_status run_ffn_topk(cd_plan *p, int variant, const uint16_t *x, int B, const 
         return st;
     if (p->d_ff > cdk::kTopkMaxDff)
         return CD_EUNSUPPORTED;
+    if (!outputs_disjoint(p, B, x, Wg, Wu, Wd, At, Bt, Tp, y, thld_out))
+        return CD_EINVAL;
+    if ((st = plan_device_ok(p)) != CD_OK)
+        return st;
     hipStream_t s = reinterpret_cast<hipStream_t>(stream);
     if (!(p->phases & CD_PHASE_COEF) && !p->has_state)
         return CD_EINVAL;
@@ -408,8 +467,16 @@ cd_status countdown_plan_destroy(cd_plan *plan)
 {
     if (!plan)
         return CD_OK;
-    const hipError_t e = hipDeviceSynchronize();
+    int cur = -1;
+    hipError_t e = hipGetDevice(&cur);
+    const bool other = e == hipSuccess && cur != plan->device;
+    if (other)
+        e = hipSetDevice(plan->device);
+    if (e == hipSuccess)
+        e = hipDeviceSynchronize();
     release(plan);
+    if (other)
+        (void)hipSetDevice(cur);
     return hip_status(e);
 }
 
@@ -469,11 +536,14 @@ cd_status calibrate(cd_plan *p, int variant, const uint16_t *X, int T, const uin
                (variant == CD_VARIANT_DUAL_IDEAL && (!W_gate || !aligned16(W_gate)))) {
         return CD_EINVAL;
     }
+    cd_status st = plan_device_ok(p);
+    if (st != CD_OK)
+        return st;
     hipStream_t s = reinterpret_cast<hipStream_t>(stream);
     const int tb = p->max_batch;
     float *coef = nullptr, *ybuf = nullptr;
     double *q = nullptr;
-    cd_status st = dalloc(&coef, (size_t)tb * p->d_ff);
+    st = dalloc(&coef, (size_t)tb * p->d_ff);
     if (st == CD_OK) st = dalloc(&ybuf, (size_t)tb * p->d_model);
     if (st == CD_OK) st = dalloc(&q, (size_t)T);
     // The coefficient kernels run with thld = +inf (no neuron active) and
@@ -591,6 +661,9 @@ cd_status countdown_export_active(const cd_plan *p, int32_t *idx_dst, int32_t *n
 {
     if (!p || (coef_dst && !(p->flags & CD_PLAN_KEEP_COEF)) || p->last_batch < 1)
         return CD_EINVAL;
+    const cd_status st = plan_device_ok(p);
+    if (st != CD_OK)
+        return st;
     hipStream_t s = reinterpret_cast<hipStream_t>(stream);
     hipError_t e = hipSuccess;
     if (idx_dst || n_dst || s_dst)

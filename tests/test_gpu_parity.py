@@ -323,6 +323,44 @@ def test_bad_calls_raise(tiny):
                               A_t=D["W_up"], B_t=None)
 
 
+def test_outputs_overlapping_inputs_are_rejected(tiny):
+    """y sharing memory with x or a weight matrix, and per-token thresholds sharing
+    memory with y, are rejected on the host: nothing is launched."""
+    from paper_2505_17701_amd import binding as cd
+
+    w, layer = tiny
+    plan = plan_for(layer, max_batch=2)
+    D = layer.d
+    dm = plan.d_model
+    x = dev_bf16(w.tokens(2))
+    raw = torch.zeros(2 * dm * 4, dtype=torch.uint8, device="cuda")
+    y_over_x = raw.view(torch.float32).view(2, dm)
+    x_in = raw[: 2 * dm * 2].view(torch.bfloat16).view(2, dm)
+    x_in.copy_(x)
+    with pytest.raises(cd.CountdownError):
+        cd.countdown_ffn_mono(plan, x_in, D["W_gate"], D["W_up"], D["W_down"], 0.5, y=y_over_x)
+    up_before = D["W_up"].clone()
+    y_in_up = D["W_up"].view(-1).view(torch.float32)[dm: 3 * dm].view(2, dm)
+    for call in (lambda: cd.countdown_ffn_mono(plan, x, D["W_gate"], D["W_up"], D["W_down"],
+                                               0.5, y=y_in_up),
+                 lambda: cd.countdown_ffn_dense(plan, x, D["W_gate"], D["W_up"], D["W_down"],
+                                                y=y_in_up),
+                 lambda: cd.countdown_ffn_topk(plan, 0, x, D["W_gate"], D["W_up"], D["W_down"],
+                                               0.9, y=y_in_up)):
+        with pytest.raises(cd.CountdownError):
+            call()
+    y = torch.empty(2, dm, dtype=torch.float32, device="cuda")
+    with pytest.raises(cd.CountdownError):
+        cd.countdown_ffn_topk(plan, 0, x, D["W_gate"], D["W_up"], D["W_down"], 0.9, y=y,
+                              thld_out=y.view(-1).view(torch.float64)[:2])
+    torch.cuda.synchronize()
+    assert torch.equal(D["W_up"], up_before)
+    # the same call with separate outputs goes through
+    q = torch.empty(2, dtype=torch.float64, device="cuda")
+    cd.countdown_ffn_topk(plan, 0, x, D["W_gate"], D["W_up"], D["W_down"], 0.9, y=y, thld_out=q)
+    torch.cuda.synchronize()
+
+
 # ------------------------------------------------------------- calibration
 
 @pytest.mark.parametrize("variant", ["mono", "dual_ideal", "dual_pred", "cats"])
