@@ -146,6 +146,75 @@ def time_steps_graph(fn, steps, warmup):
     return ms
 
 
+def pooled_thresholds(dm, dff, dr, L, X_cal, variants, ks):
+    """The other reading of the calibration rule, reported beside the one used (the
+    mean of per-token quantiles): one linear quantile of the coefficients of all
+    calibration tokens pooled. The coefficients come from the HIP coefficient kernels
+    (threshold +inf, coefficient phase only); the quantile is numpy's."""
+    import torch
+
+    from paper_2505_17701_amd import binding as cd
+
+    mb = min(8, 32768 // dm)
+    plan = cd.Plan(dm, dff, max_batch=mb, d_rank=dr, keep_coef=True)
+    cd.countdown_plan_set_phases(plan, cd.CD_PHASE_COEF)
+    inf = float("inf")
+    out = {}
+    for variant in variants:
+        chunks = []
+        for t0 in range(0, X_cal.shape[0], mb):
+            x = X_cal[t0:t0 + mb]
+            y = torch.empty((x.shape[0], dm), dtype=torch.float32, device="cuda")
+            if variant == "mono":
+                cd.countdown_ffn_mono(plan, x, L["W_gate"], L["W_up"], L["W_down"], inf, y=y)
+            elif variant == "dual_ideal":
+                cd.countdown_ffn_dual(plan, x, L["W_gate"], L["W_up"], L["W_down"], inf, y=y)
+            elif variant == "cats":
+                cd.countdown_ffn_cats(plan, x, L["W_gate"], L["W_up"], L["W_down"], inf, y=y)
+            elif variant == "dual_pred":
+                cd.countdown_ffn_dual(plan, x, L["W_gate"], L["W_up"], L["W_down"], inf,
+                                      A_t=L["A_t"], B_t=L["B_t"], y=y)
+            elif variant == "dual_tern":
+                cd.countdown_ffn_tern(plan, x, L["W_gate"], L["W_up"], L["W_down"],
+                                      L["theta_p"], inf, y=y)
+            else:
+                continue
+            chunks.append(cd.countdown_export_active(plan)[2].cpu().numpy().astype(np.float64))
+        if not chunks:
+            continue
+        c = np.concatenate(chunks).ravel()
+        if variant not in ("dual_pred", "dual_tern"):  # signed scores keep their sign
+            c = np.abs(c)
+        for k in ks:
+            out[(variant, k)] = float(np.float32(np.quantile(c, k)))
+    plan.close()
+    return out
+
+
+def stream_ceiling(ctx, nk):
+    """Plain streaming reads (countdown_stream_read), timed like the kernels with one
+    event pair around a graph-replayed loop: the W_up matrices of the rotated weight
+    copies (the bytes the M coefficient kernel streams densely, one launch each) and a
+    1 GiB buffer (the asymptotic read rate)."""
+    import torch
+
+    from paper_2505_17701_amd import binding as cd
+
+    sink = torch.zeros(1, dtype=torch.int32, device="cuda")
+    ups = [L["W_up"] for L in ctx.layers]
+    nb = ups[0].numel() * ups[0].element_size()
+    ms = time_steps_graph(lambda i: cd.countdown_stream_read(ups[i % len(ups)], sink), nk, 20)
+    out = {"W_up": {"bytes": nb, "us": ms * 1e3, "GBs": nb / (ms * 1e-3) / 1e9}}
+    big = torch.zeros(1 << 29, dtype=torch.bfloat16, device="cuda")  # 1 GiB
+    nb = big.numel() * 2
+    ms = time_steps_graph(lambda i: cd.countdown_stream_read(big, sink), 40, 5)
+    out["1GiB"] = {"bytes": nb, "us": ms * 1e3, "GBs": nb / (ms * 1e-3) / 1e9}
+    del big
+    torch.cuda.synchronize()
+    torch.cuda.empty_cache()
+    return out
+
+
 def brief(r):
     return {kk: r[kk] for kk in ("us_per_layer", "us_per_layer_eager", "tokens_per_s",
                                  "achieved_GBs", "frac_hbm_peak", "n_active_mean",
@@ -206,9 +275,12 @@ class Context:
                                                    A_t=L0.get("A_t"), B_t=L0.get("B_t"))
                 self.thld[(variant, k)] = float(th.item())
         cal_plan.close()
+        self.thld_pooled = pooled_thresholds(self.dm, self.dff, self.dr, L0, X_cal, variants, ks)
         del X_cal
         log(f"[bench] thresholds: " + ", ".join(f"{v}@{k}={t:.4f}"
                                                  for (v, k), t in self.thld.items()))
+        log(f"[bench] pooled-quantile thresholds (reported only): " + ", ".join(
+            f"{v}@{k}={t:.4f}" for (v, k), t in self.thld_pooled.items()))
 
     def free(self):
         import torch
@@ -572,6 +644,8 @@ def main():
                        variants=main_variants)
     main_res = main_ctx.measure(args.variant, args.k, args.batch, args.steps, args.warmup)
     log(f"[bench] {w.name} {args.variant} k={args.k}: {json.dumps(main_res)}")
+    ceiling = stream_ceiling(main_ctx, min(args.steps, 512))
+    log(f"[bench] plain streaming read: {json.dumps(ceiling)}")
 
     extra = {}
     if not args.no_extra and "mono" in w.variants:
@@ -598,6 +672,7 @@ def main():
     host0 = main_ctx.host0
     X_eval_h = main_ctx.X_eval_h
     thld = main_ctx.thld
+    thld_pooled = main_ctx.thld_pooled
     main_ctx.free()
 
     others = {}
@@ -624,10 +699,10 @@ def main():
                "cats": lambda x: oracle.ffn_cats(x, H["W_gate"], H["W_up"], H["W_down"], th),
                "dual_tern": lambda x: oracle.ffn_dual_tern(x, H["W_gate"], H["W_up"],
                                                            H["W_down"], H.get("theta_t"), th)}
-        for base in ("mono", "dual_ideal", "dual_pred", "cats", "dual_tern"):
-            fns[base + "_topk"] = (lambda b: lambda x: oracle.ffn_topk(
+        for vb in ("mono", "dual_ideal", "dual_pred", "cats", "dual_tern"):
+            fns[vb + "_topk"] = (lambda b: lambda x: oracle.ffn_topk(
                 b, x, H["W_gate"], H["W_up"], H["W_down"], args.k, A_t=H.get("A_t"),
-                B_t=H.get("B_t"), theta_t=H.get("theta_t")))(base)
+                B_t=H.get("B_t"), theta_t=H.get("theta_t")))(vb)
         fn = fns[args.variant]
         n_done, t0 = 0, time.perf_counter()
         nt = len(X_eval_h) - args.batch + 1
@@ -640,6 +715,21 @@ def main():
                "cores": oracle.num_threads(), "kind": "oracle",
                "sample": f"{n_done} calls of {w.name} {args.variant} k={args.k}, "
                          f"batch {args.batch}, one weight copy, fp64 C oracle ({el:.1f} s)"}
+        # beside it: the oracle's dense path on the same threads, and the same sparse
+        # path on one thread (a few seconds each)
+        def rate(f, secs):
+            n, t = 0, time.perf_counter()
+            while n < 2 or time.perf_counter() - t < secs:
+                f(X_eval_h[n % nt:n % nt + args.batch])
+                n += 1
+            return n * args.batch / (time.perf_counter() - t)
+
+        secs = max(1.0, args.cpu_seconds / 4)
+        cpu["detail"] = {"dense_tokens_per_s": rate(fns["dense"], secs)}
+        nthreads = oracle.num_threads()
+        oracle.set_num_threads(1)
+        cpu["detail"]["one_thread_tokens_per_s"] = rate(fn, secs)
+        oracle.set_num_threads(nthreads)
         log(f"[bench] cpu baseline: {json.dumps(cpu)}")
 
     roof = None
@@ -668,7 +758,12 @@ def main():
                 "traffic": measured_traffic() if (args.workload, args.variant, args.k) ==
                 ("llama7b_4096x11008", "mono", 0.9) else None,
                 "bytes_per_launch": main_res[f"{dom}_kernel_bytes"],
-                "avg_launch_us": main_res[f"{dom}_kernel_us"]}
+                "avg_launch_us": main_res[f"{dom}_kernel_us"],
+                # measured ceilings: a plain read of the same W_up bytes per launch, and
+                # of 1 GiB (countdown_stream_read)
+                "stream_same_bytes_GBs": ceiling["W_up"]["GBs"],
+                "frac_of_stream_same_bytes": main_res[f"{dom}_kernel_GBs"] / ceiling["W_up"]["GBs"],
+                "stream_1GiB_GBs": ceiling["1GiB"]["GBs"]}
 
     out = {
         "metric": "sparse-FFN decode tokens/s and \u00b5s/layer; achieved HBM GB/s vs peak at 90% "
@@ -694,7 +789,9 @@ def main():
                 + (f" with {w.outlier_frac:.0%} outlier channels x20)" if w.outlier_frac else ")"),
         "config": {"workload": w.name, "d_model": dm, "d_ff": dff, "batch": args.batch,
                    "variant": args.variant, "k": args.k,
-                   "thld": thld.get((args.variant, args.k)), "weight_copies": args.copies,
+                   "thld": thld.get((args.variant, args.k)),
+                   "thld_pooled_reading": thld_pooled.get((base, args.k)),
+                   "weight_copies": args.copies,
                    "n_active_mean": main_res["n_active_mean"],
                    "realised_sparsity": main_res["realised_sparsity"],
                    "algorithmic_bytes_per_step": main_res["algorithmic_bytes"],

@@ -270,6 +270,19 @@ cd_status countdown_export_active(const cd_plan *plan, int32_t *idx_dst, int32_t
 cd_status countdown_plan_set_phases(cd_plan *plan, unsigned phases);
 
 /*
+ * Measurement aid, not part of the method: a plain streaming read of `bytes`
+ * bytes at `src` with the coefficient kernel's load pattern (one wave per
+ * 8 KB, non-temporal 16-byte loads) and no arithmetic but an xor per load.
+ * Timed by the caller, it gives the read bandwidth that a kernel reading the
+ * same number of bytes can reach: the measured ceiling beside the 8 TB/s
+ * peak. src: device, 16-byte aligned; bytes: a positive multiple of 16.
+ * sink: one device uint32, written only when the xor of a lane's data equals
+ * 0x9E3779B9 (which keeps the loads from being optimised away). Enqueued on
+ * `stream`; CD_EINVAL for bad arguments.
+ */
+cd_status countdown_stream_read(const void *src, size_t bytes, uint32_t *sink, void *stream);
+
+/*
  * Host-only validation of an FFN call's arguments against a shape, exactly
  * as the entry points perform it before launching: pointers non-NULL and
  * 16-byte aligned, 1 <= B <= max_batch, thld not NaN, predictor pointers
@@ -289,7 +302,7 @@ cd_status countdown_check_shape(int d_model, int d_ff, int max_batch, int d_rank
 const char *countdown_status_string(cd_status status);
 
 /* ABI version of this header (bumped on any signature change). */
-#define COUNTDOWN_ABI_VERSION 7
+#define COUNTDOWN_ABI_VERSION 8
 int countdown_abi_version(void);
 
 #ifdef __cplusplus

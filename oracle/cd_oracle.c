@@ -78,6 +78,17 @@ int cdo_num_threads(void)
 #endif
 }
 
+/* threads of the following calls (timing only; results do not depend on it) */
+void cdo_set_num_threads(int n)
+{
+#ifdef _OPENMP
+    if (n > 0)
+        omp_set_num_threads(n);
+#else
+    (void)n;
+#endif
+}
+
 /* SiLU(z) = z * sigmoid(z) = z / (1 + e^-z), the activation of Sec. 3
  * (sigma = SiLU). For z < 0 the form z e^z / (1 + e^z) avoids e^-z overflow. */
 double cdo_silu(double z)

@@ -24,7 +24,7 @@ KIND = {"mono": COEF_ABS_U, "dual_ideal": COEF_ABS_S, "dual_pred": COEF_SHAT, "c
 _lib = None
 
 __all__ = [
-    "build", "load", "num_threads", "silu", "coefficients", "predictor", "select", "combine",
+    "build", "load", "num_threads", "set_num_threads", "silu", "coefficients", "predictor", "select", "combine",
     "dense", "ffn_on_idx", "ffn_mono", "ffn_dual_ideal", "ffn_dual_pred", "quantile_linear",
     "calibrate", "ffn_topk", "ffn_cats", "residual_rmsnorm", "ternary_predictor",
     "ffn_dual_tern", "KIND",
@@ -54,6 +54,8 @@ def load():
         i8p = np.ctypeslib.ndpointer(np.int8, flags="C_CONTIGUOUS")
         vp = C.c_void_p
         lib.cdo_num_threads.restype = C.c_int
+        lib.cdo_set_num_threads.restype = None
+        lib.cdo_set_num_threads.argtypes = [C.c_int]
         lib.cdo_silu.restype = C.c_double
         lib.cdo_silu.argtypes = [C.c_double]
         lib.cdo_coefficients.restype = C.c_int
@@ -121,6 +123,11 @@ def _check(rc, what):
 
 def num_threads() -> int:
     return load().cdo_num_threads()
+
+
+def set_num_threads(n: int) -> None:
+    """OpenMP threads of the following oracle calls (timing only)."""
+    load().cdo_set_num_threads(int(n))
 
 
 def silu(z: float) -> float:

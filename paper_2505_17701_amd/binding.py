@@ -27,7 +27,7 @@ EXPORTS = (
     "countdown_calibrate", "countdown_ffn_tern", "countdown_ffn_tern_topk",
     "countdown_calibrate_tern", "countdown_ternary_words", "countdown_ternary_pack",
     "countdown_export_active",
-    "countdown_plan_set_phases", "countdown_check_args",
+    "countdown_plan_set_phases", "countdown_stream_read", "countdown_check_args",
     "countdown_check_shape", "countdown_status_string", "countdown_abi_version",
 )
 
@@ -68,6 +68,7 @@ def load_library(path: str = LIB_PATH):
         "countdown_ternary_pack": (i, [vp, i, i, vp]),
         "countdown_export_active": (i, [vp, vp, vp, vp, vp, vp]),
         "countdown_plan_set_phases": (i, [vp, u]),
+        "countdown_stream_read": (i, [vp, C.c_size_t, vp, vp]),
         "countdown_check_args": (i, [i, i, i, i, i, vp, i, vp, vp, vp, vp, vp, f, vp]),
         "countdown_check_shape": (i, [i, i, i, i]),
         "countdown_status_string": (C.c_char_p, [i]),
@@ -366,6 +367,15 @@ def countdown_plan_set_phases(plan: Plan, phases: int) -> None:
     """Launch only the kernels in ``phases`` (CD_PHASE_*) on later calls (measurement aid)."""
     _check(load_library().countdown_plan_set_phases(plan.handle, int(phases)),
            "countdown_plan_set_phases")
+
+
+def countdown_stream_read(src, sink, stream=None) -> None:
+    """Measurement aid: a plain streaming read of the whole of ``src`` (a contiguous
+    device tensor) with the coefficient kernel's load pattern; ``sink`` is a one-word
+    int32 / uint32 device tensor. Enqueued on ``stream``."""
+    _check(load_library().countdown_stream_read(
+        _ptr(src), src.numel() * src.element_size(), _ptr(sink), _stream(stream)),
+        "countdown_stream_read")
 
 
 def countdown_check_args(variant, d_model, d_ff, max_batch, d_rank, x, B, W_gate, W_up, W_down,

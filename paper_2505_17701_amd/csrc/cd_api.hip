@@ -674,6 +674,15 @@ cd_status countdown_export_active(const cd_plan *p, int32_t *idx_dst, int32_t *n
     return hip_status(e);
 }
 
+cd_status countdown_stream_read(const void *src, size_t bytes, uint32_t *sink, void *stream)
+{
+    if (!src || !aligned16(src) || bytes == 0 || bytes % 16 || !sink ||
+        (reinterpret_cast<uintptr_t>(sink) & 3u) ||
+        bytes / 16 > (size_t)0x7fffffff * 256 * 8)  // the grid of 256-thread workgroups
+        return CD_EINVAL;
+    return hip_status(cdk::launch_stream_read(src, bytes, sink, reinterpret_cast<hipStream_t>(stream)));
+}
+
 cd_status countdown_plan_set_phases(cd_plan *p, unsigned phases)
 {
     if (!p || phases == 0 || (phases & ~CD_PHASE_ALL))

@@ -78,5 +78,7 @@ constexpr int kTopkMaxDff = 32768;
 hipError_t launch_select(const float *coef, int ld, int n, int T, int use_abs, double k,
                          double *q_out, hipStream_t s);
 hipError_t launch_mean(const double *q, int T, float *out, hipStream_t s);
+// Measurement aid: plain streaming read of bytes (a multiple of 16) at src.
+hipError_t launch_stream_read(const void *src, size_t bytes, uint32_t *sink, hipStream_t s);
 
 } // namespace cdk

@@ -2525,6 +2525,42 @@ hipError_t launch_select(const float *coef, int ld, int n, int T, int use_abs, d
     return hipGetLastError();
 }
 
+// Plain streaming read, a measurement aid: the bandwidth a kernel that reads
+// n16 16-byte chunks can reach with the coefficient kernel's load pattern (one
+// wave per 8 KB, all eight non-temporal 16-byte loads of a lane issued before
+// any use) and no arithmetic but an xor per chunk. A lane stores its fold only
+// if it equals a fixed value, which keeps the loads live without a store each.
+__global__ __launch_bounds__(kBlock) void k_stream_read(const uint16_t *__restrict__ src,
+                                                        size_t n16, uint32_t *sink)
+{
+    constexpr int kLoads = 8;
+    const int lane = threadIdx.x % kWave, wave = threadIdx.x / kWave;
+    const size_t first = ((size_t)blockIdx.x * kWavesPerBlock + wave) * (kWave * kLoads);
+    u32x4 w[kLoads];
+#pragma unroll
+    for (int k = 0; k < kLoads; ++k) {
+        const size_t i = first + (size_t)k * kWave + lane;
+        w[k] = load16_stream(or_zero(i < n16, src + i * 8));
+    }
+    uint32_t f = 0u;
+#pragma unroll
+    for (int k = 0; k < kLoads; ++k)
+        f ^= w[k].x ^ w[k].y ^ w[k].z ^ w[k].w;
+    if (f == 0x9e3779b9u)
+        sink[0] = f;
+}
+
+hipError_t launch_stream_read(const void *src, size_t bytes, uint32_t *sink, hipStream_t s)
+{
+    const size_t n16 = bytes / 16;
+    const size_t per_block = (size_t)kBlock * 8;  // 16-byte chunks per workgroup
+    const size_t grid = (n16 + per_block - 1) / per_block;
+    if (grid == 0 || grid > 0x7fffffffu)
+        return hipErrorInvalidValue;
+    k_stream_read<<<(unsigned)grid, kBlock, 0, s>>>(static_cast<const uint16_t *>(src), n16, sink);
+    return hipGetLastError();
+}
+
 hipError_t launch_mean(const double *q, int T, float *out, hipStream_t s)
 {
     k_mean<<<1, 64, 0, s>>>(q, T, out);

@@ -497,3 +497,20 @@ def test_graph_replay_all_paths():
                                        atol=1e-6 * float(e[:rows].abs().max()) + 1e-30)
     for p in plans:
         p.close()
+
+
+def test_stream_read_measurement_aid():
+    """countdown_stream_read reads a buffer without touching it or the sink (all-zero
+    data folds to 0) and rejects sizes that are not whole 16-byte chunks."""
+    from paper_2505_17701_amd import binding as cd
+
+    sink = torch.zeros(1, dtype=torch.int32, device="cuda")
+    for n in (8, 4096 * 8 + 8, 3 << 20):  # bf16 elements: one chunk, a ragged wave, 6 MiB
+        buf = torch.zeros(n, dtype=torch.bfloat16, device="cuda")
+        cd.countdown_stream_read(buf, sink)
+        torch.cuda.synchronize()
+        assert int(sink.item()) == 0 and not buf.any()
+    with pytest.raises(cd.CountdownError):
+        cd.countdown_stream_read(torch.zeros(7, dtype=torch.uint8, device="cuda"), sink)
+    with pytest.raises(cd.CountdownError):
+        cd.countdown_stream_read(torch.zeros(64, dtype=torch.uint8, device="cuda")[1:17], sink)

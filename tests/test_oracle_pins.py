@@ -628,3 +628,22 @@ def test_ternary_calibration_and_per_token_path():
     np.testing.assert_allclose(qo, qs, rtol=1e-14)
     want = [i for i in range(40) if any(shat[b][i] > qs[b] for b in range(3))]
     np.testing.assert_array_equal(idx, want)
+
+
+def test_thread_count_does_not_change_results():
+    """The oracle's OpenMP loops split independent rows and columns, each summed by
+    one thread in ascending order: one thread and many give the same bits."""
+    L = make_layer(2200, 64, 264, 0.05)
+    X = make_tokens(2201, 3, 64)
+    n = oracle.num_threads()
+    try:
+        outs = []
+        for t in (1, max(n, 2)):
+            oracle.set_num_threads(t)
+            assert oracle.num_threads() == t
+            outs.append(oracle.ffn_mono(X, L["W_gate"], L["W_up"], L["W_down"], np.float32(0.3)))
+            outs.append(oracle.dense(X, L["W_gate"], L["W_up"], L["W_down"]))
+    finally:
+        oracle.set_num_threads(n)
+    (i1, y1, _), d1, (i2, y2, _), d2 = outs
+    assert np.array_equal(i1, i2) and np.array_equal(y1, y2) and np.array_equal(d1, d2)
