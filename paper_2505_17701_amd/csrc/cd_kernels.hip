@@ -2237,16 +2237,22 @@ template <int B, int NK>
 static hipError_t coef_bn(int variant, const CoefArgs &a, hipStream_t s)
 {
     constexpr bool XREG = B <= 2;
+    // The one-row kernel keeps the tokens in registers for one token only: at
+    // two they cost it 114 VGPRs (4 waves per SIMD), and the LDS copy measured
+    // 8-10% faster at 2 tokens (7B and 70B shapes); the two-row kernel gained
+    // nothing from it.
+    constexpr bool XREG1 = B <= 1;
     const size_t lds = token_lds_bytes(B, NK);
+    const size_t lds1 = XREG1 ? 0 : (size_t)B * NK * kColsPerLoad * 2;
     const int grid = (a.d_ff + kWavesPerBlock - 1) / kWavesPerBlock;
     switch (variant) {
     case kMono:
-        allow_lds(k_coef_mono<B, NK, XREG, false>, lds);
-        k_coef_mono<B, NK, XREG, false><<<grid, kBlock, lds, s>>>(a);
+        allow_lds(k_coef_mono<B, NK, XREG1, false>, lds1);
+        k_coef_mono<B, NK, XREG1, false><<<grid, kBlock, lds1, s>>>(a);
         break;
     case kCats:
-        allow_lds(k_coef_mono<B, NK, XREG, true>, lds);
-        k_coef_mono<B, NK, XREG, true><<<grid, kBlock, lds, s>>>(a);
+        allow_lds(k_coef_mono<B, NK, XREG1, true>, lds1);
+        k_coef_mono<B, NK, XREG1, true><<<grid, kBlock, lds1, s>>>(a);
         break;
     case kDualIdeal:
         allow_lds(k_coef_dual<B, NK, XREG, false>, lds);
