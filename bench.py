@@ -383,6 +383,29 @@ class Context:
         return res
 
 
+def optimal_dense_us(ctx, k, steps):
+    """The dense layer with only int(d_ff (1 - k)) neurons (rounded down to a multiple
+    of 8): the first rows of the rotated weight copies, through the dense path."""
+    import torch
+
+    from paper_2505_17701_amd import binding as cd
+
+    n = max(8, int(ctx.dff * (1 - k)) // 8 * 8)
+    plan = cd.Plan(ctx.dm, n, max_batch=1)
+    y = torch.empty((1, ctx.dm), dtype=torch.float32, device="cuda")
+    views = [{m: L[m][:n] for m in ("W_gate", "W_up", "W_down")} for L in ctx.layers]
+    X, nt = ctx.X_eval, ctx.X_eval.shape[0]
+
+    def step(i):
+        L = views[i % len(views)]
+        cd.countdown_ffn_dense(plan, X[i % nt:i % nt + 1], L["W_gate"], L["W_up"], L["W_down"],
+                               y=y)
+
+    ms = time_steps_graph(step, steps, 30)
+    plan.close()
+    return ms * 1e3
+
+
 def other_workloads(args):
     """The remaining single-layer shapes: Llama-3-8B-shaped layer with the low-rank
     predictor at batch 1/4/8, and the 70B-shaped layer (M-CountDown k 0.9 / 0.7
@@ -392,8 +415,9 @@ def other_workloads(args):
 
     out = {}
     w = WORKLOADS["llama3_8b_4096x14336_pred"]
-    ctx = Context(w, 4, 64, args.calib_tokens, [0.9], max_batch=8,
-                  variants=["dual_pred", "dual_tern"])
+    sweep_ks = (0.5, 0.6, 0.7, 0.8, 0.9)
+    ctx = Context(w, 4, 64, args.calib_tokens, list(sweep_ks), max_batch=8,
+                  variants=["dual_pred", "dual_tern", "mono", "cats"])
     r8 = {}
     for B in w.batches:
         r = ctx.measure("dual_pred", 0.9, B, max(200, args.steps // 4), 50)
@@ -410,6 +434,17 @@ def other_workloads(args):
     r8["dense B=1"] = brief(r)
     for B in w.batches:
         r8[f"B={B}"]["speedup_vs_dense_B1"] = r["us_per_layer"] / r8[f"B={B}"]["us_per_layer"]
+    # the paper's kernel-speed comparison at this shape (its Llama-3.1-8B figure): CATS,
+    # M-CountDown and practical D-CountDown at calibrated thresholds across sparsity,
+    # beside the dense layer ("Full") and a dense layer of the active count ("Optimal")
+    sweep = {"dense_us": r["us_per_layer"]}
+    for k in sweep_ks:
+        row = {v: ctx.measure(v, k, 1, max(200, args.steps // 8), 30)["us_per_layer"]
+               for v in ("cats", "mono", "dual_pred")}
+        row["optimal_us"] = optimal_dense_us(ctx, k, max(200, args.steps // 8))
+        sweep[f"k={k}"] = row
+        log(f"[bench] {w.name} kernel speed k={k} (us per layer): {json.dumps(row)}")
+    r8["kernel_speed_sweep"] = sweep
     ctx.free()
     out[w.name] = r8
 
