@@ -166,17 +166,42 @@ def countdown_plan_destroy(plan: Plan) -> None:
     plan.close()
 
 
+def _shape(t, shape, name):
+    """ValueError unless ``t`` (None is skipped) has exactly ``shape``."""
+    if t is not None and tuple(t.shape) != tuple(shape):
+        raise ValueError(f"{name} must have shape {tuple(shape)}, got {tuple(t.shape)}")
+
+
+def _layer_shapes(plan, x, W_gate=None, W_up=None, W_down=None, A_t=None, B_t=None,
+                  theta_packed=None):
+    """Check a call's tensors against the plan before any pointer is taken: the C ABI
+    sees only pointers, and the kernels read exactly these extents."""
+    if x.dim() != 2 or x.shape[1] != plan.d_model:
+        raise ValueError(f"x must be [B, {plan.d_model}], got {tuple(x.shape)}")
+    for t, name in ((W_gate, "W_gate"), (W_up, "W_up"), (W_down, "W_down")):
+        _shape(t, (plan.d_ff, plan.d_model), name)
+    _shape(A_t, (plan.d_rank, plan.d_model), "A_t")
+    _shape(B_t, (plan.d_ff, plan.d_rank), "B_t")
+    if theta_packed is not None:
+        words = countdown_ternary_words(plan.d_model, plan.d_ff)
+        if theta_packed.numel() * theta_packed.element_size() != 4 * words:
+            raise ValueError(f"theta_packed must hold {words} 32-bit words "
+                             f"(countdown_ternary_words), got {theta_packed.numel()} elements")
+
+
 def _out(plan: Plan, x, y):
     import torch
 
     B = x.shape[0]
     if y is None:
         y = torch.empty((B, plan.d_model), dtype=torch.float32, device=x.device)
+    _shape(y, (B, plan.d_model), "y")
     return B, _f32(y)
 
 
 def countdown_ffn_mono(plan: Plan, x, W_gate, W_up, W_down, thld: float, y=None, stream=None):
     """M-CountDown FFN; returns y ``[B, d_model]`` fp32 (enqueued on ``stream``)."""
+    _layer_shapes(plan, x, W_gate, W_up, W_down)
     B, y = _out(plan, x, y)
     _check(load_library().countdown_ffn_mono(
         plan.handle, _ptr(_bf16(x)), B, _ptr(_bf16(W_gate)), _ptr(_bf16(W_up)),
@@ -188,6 +213,7 @@ def countdown_ffn_mono(plan: Plan, x, W_gate, W_up, W_down, thld: float, y=None,
 def countdown_ffn_dual(plan: Plan, x, W_gate, W_up, W_down, thld: float, A_t=None, B_t=None,
                        y=None, stream=None):
     """D-CountDown FFN (ideal without a predictor, practical with ``A_t``/``B_t``)."""
+    _layer_shapes(plan, x, W_gate, W_up, W_down, A_t, B_t)
     B, y = _out(plan, x, y)
     _check(load_library().countdown_ffn_dual(
         plan.handle, _ptr(_bf16(x)), B, _ptr(_bf16(W_gate)), _ptr(_bf16(W_up)),
@@ -199,6 +225,7 @@ def countdown_ffn_dual(plan: Plan, x, W_gate, W_up, W_down, thld: float, A_t=Non
 
 def countdown_ffn_cats(plan: Plan, x, W_gate, W_up, W_down, thld: float, y=None, stream=None):
     """CATS (Eq. 6a): keep |SiLU(x.W_gate)| > thld, gather W_up on the kept neurons."""
+    _layer_shapes(plan, x, W_gate, W_up, W_down)
     B, y = _out(plan, x, y)
     _check(load_library().countdown_ffn_cats(
         plan.handle, _ptr(_bf16(x)), B, _ptr(_bf16(W_gate)), _ptr(_bf16(W_up)),
@@ -214,6 +241,7 @@ def countdown_ffn_topk(plan: Plan, variant: int, x, W_gate, W_up, W_down, k: flo
     tensor for the thresholds. Returns y."""
     import torch
 
+    _layer_shapes(plan, x, W_gate, W_up, W_down, A_t, B_t)
     B, y = _out(plan, x, y)
     if thld_out is not None and (thld_out.dtype != torch.float64 or thld_out.numel() < B):
         raise ValueError("thld_out must be a float64 device tensor with at least B entries")
@@ -240,6 +268,7 @@ def countdown_ffn_residual(plan: Plan, variant: int, h_in, y_prev, h_out, x_out,
             raise ValueError("h_in, y_prev, h_out and y must be contiguous fp32 [B, d_model]")
     if tuple(x_out.shape) != (B, plan.d_model) or not x_out.is_contiguous():
         raise ValueError("x_out must be a contiguous [B, d_model] bf16 tensor")
+    _layer_shapes(plan, x_out, W_gate, W_up, W_down, A_t, B_t)
     _check(load_library().countdown_ffn_residual(
         plan.handle, int(variant), _ptr(h_in), _ptr(y_prev), _ptr(h_out), float(eps),
         _ptr(_bf16(x_out)), B, _ptr(_bf16(W_gate)), _ptr(_bf16(W_up)), _ptr(_bf16(W_down)),
@@ -251,6 +280,7 @@ def countdown_ffn_residual(plan: Plan, variant: int, h_in, y_prev, h_out, x_out,
 
 def countdown_ffn_dense(plan: Plan, x, W_gate, W_up, W_down, y=None, stream=None):
     """Dense Gated-MLP through the same kernels."""
+    _layer_shapes(plan, x, W_gate, W_up, W_down)
     B, y = _out(plan, x, y)
     _check(load_library().countdown_ffn_dense(
         plan.handle, _ptr(_bf16(x)), B, _ptr(_bf16(W_gate)), _ptr(_bf16(W_up)),
@@ -264,6 +294,7 @@ def countdown_calibrate(plan: Plan, variant: int, X, k: float, W_gate=None, W_up
     """Layerwise threshold; returns ``(thld fp32 tensor [1], per-token quantiles fp64 [T])``."""
     import torch
 
+    _layer_shapes(plan, X, W_gate, W_up, None, A_t, B_t)
     T = X.shape[0]
     thld = torch.empty(1, dtype=torch.float32, device=X.device)
     q = torch.empty(T, dtype=torch.float64, device=X.device)
@@ -307,6 +338,7 @@ def countdown_ffn_tern(plan: Plan, x, W_gate, W_up, W_down, theta_packed, thld: 
                        stream=None):
     """D-CountDown with the ternary predictor (``theta_packed``: device int32/uint32 tensor
     from :func:`countdown_ternary_pack`)."""
+    _layer_shapes(plan, x, W_gate, W_up, W_down, theta_packed=theta_packed)
     B, y = _out(plan, x, y)
     _check(load_library().countdown_ffn_tern(
         plan.handle, _ptr(_bf16(x)), B, _ptr(_bf16(W_gate)), _ptr(_bf16(W_up)),
@@ -321,6 +353,7 @@ def countdown_ffn_tern_topk(plan: Plan, x, W_gate, W_up, W_down, theta_packed, k
     """Per-token threshold on the ternary predictor score; returns y."""
     import torch
 
+    _layer_shapes(plan, x, W_gate, W_up, W_down, theta_packed=theta_packed)
     B, y = _out(plan, x, y)
     if thld_out is not None and (thld_out.dtype != torch.float64 or thld_out.numel() < B):
         raise ValueError("thld_out must be a float64 device tensor with at least B entries")
@@ -336,6 +369,7 @@ def countdown_calibrate_tern(plan: Plan, X, theta_packed, k: float, stream=None)
     """Layerwise threshold of the ternary predictor score; returns ``(thld [1], q [T])``."""
     import torch
 
+    _layer_shapes(plan, X, theta_packed=theta_packed)
     T = X.shape[0]
     thld = torch.empty(1, dtype=torch.float32, device=X.device)
     q = torch.empty(T, dtype=torch.float64, device=X.device)
@@ -373,6 +407,8 @@ def countdown_stream_read(src, sink, stream=None) -> None:
     """Measurement aid: a plain streaming read of the whole of ``src`` (a contiguous
     device tensor) with the coefficient kernel's load pattern; ``sink`` is a one-word
     int32 / uint32 device tensor. Enqueued on ``stream``."""
+    if sink.numel() * sink.element_size() < 4:
+        raise ValueError("sink must hold at least one 32-bit word")
     _check(load_library().countdown_stream_read(
         _ptr(src), src.numel() * src.element_size(), _ptr(sink), _stream(stream)),
         "countdown_stream_read")

@@ -213,3 +213,38 @@ def test_missing_library_fails_loudly(tmp_path):
     res = subprocess.run([sys.executable, "-c", code], capture_output=True, text=True)
     assert res.returncode == 0, res.stdout + res.stderr
     assert "build" in res.stdout
+
+
+def test_binding_checks_shapes_before_pointers():
+    """The C ABI sees only pointers, so the binding checks every tensor's shape against
+    the plan first: an undersized x, weight, predictor, packed theta or y raises
+    ValueError before any pointer is taken (CPU tensors suffice to show it)."""
+    import types
+
+    import torch
+
+    plan = types.SimpleNamespace(d_model=64, d_ff=128, d_rank=8, max_batch=2)
+    x = torch.zeros(2, 64, dtype=torch.bfloat16)
+    W = torch.zeros(128, 64, dtype=torch.bfloat16)
+    A = torch.zeros(8, 64, dtype=torch.bfloat16)
+    Bt = torch.zeros(128, 8, dtype=torch.bfloat16)
+    cd._layer_shapes(plan, x, W, W, W, A, Bt)  # the right shapes pass
+    bad = [dict(x=torch.zeros(2, 32, dtype=torch.bfloat16)),
+           dict(x=torch.zeros(128, dtype=torch.bfloat16)),
+           dict(W_gate=W[:64]), dict(W_up=W[:, :32]), dict(W_down=W.reshape(64, 128)),
+           dict(A_t=A[:4]), dict(B_t=Bt[:, :4])]
+    for b in bad:
+        kw = dict(x=x, W_gate=W, W_up=W, W_down=W, A_t=A, B_t=Bt)
+        kw.update(b)
+        with pytest.raises(ValueError):
+            cd._layer_shapes(plan, **kw)
+    words = cd.countdown_ternary_words(64, 128)
+    cd._layer_shapes(plan, x, W, W, W, theta_packed=torch.zeros(words, dtype=torch.int32))
+    with pytest.raises(ValueError):
+        cd._layer_shapes(plan, x, W, W, W, theta_packed=torch.zeros(words - 1, dtype=torch.int32))
+    B, y = cd._out(plan, x, None)
+    assert B == 2 and tuple(y.shape) == (2, 64)
+    with pytest.raises(ValueError):
+        cd._out(plan, x, torch.zeros(1, 64))
+    with pytest.raises(TypeError):
+        cd._out(plan, x, torch.zeros(2, 64, dtype=torch.float64))
