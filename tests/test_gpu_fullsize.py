@@ -23,7 +23,7 @@ def llama7b():
     return w, Layer(w.layer())
 
 
-@pytest.mark.parametrize("variant", ["mono", "dual_ideal"])
+@pytest.mark.parametrize("variant", ["mono", "dual_ideal", "cats"])
 @pytest.mark.parametrize("k", [0.9, 0.5])
 def test_llama7b_layer(llama7b, variant, k):
     w, layer = llama7b
@@ -35,6 +35,16 @@ def test_llama7b_layer(llama7b, variant, k):
                                 f"7b {variant} k={k} tok{t}")
         assert abs(n / w.d_ff - (1 - k)) < 0.15, n
         print(f"7b {variant} k={k} tok{t}: n={n} flips={flips} rel_err={rel:.2e}", flush=True)
+
+
+@pytest.mark.parametrize("variant", ["mono", "cats"])
+def test_llama7b_batch2(llama7b, variant):
+    """Two tokens: the one-row kernel stages them in LDS (union over the batch)."""
+    w, layer = llama7b
+    thld = calibrated(variant, layer, w.wid, 0.9, T=32, outlier_frac=w.outlier_frac)
+    plan = plan_for(layer, max_batch=2)
+    n, flips, rel = compare(plan, variant, layer, w.tokens(2), thld, f"7b {variant} B=2")
+    print(f"7b {variant} B=2: n={n} flips={flips} rel_err={rel:.2e}", flush=True)
 
 
 @pytest.fixture(scope="module")
@@ -53,6 +63,17 @@ def test_llama3_predictor_batch_union(llama3_pred, B):
     expect = 1 - 0.9 ** B
     assert abs(n / w.d_ff - expect) < 0.1, (n, expect)
     print(f"8b pred B={B}: n={n} flips={flips} rel_err={rel:.2e}", flush=True)
+
+
+@pytest.mark.parametrize("variant", ["mono", "cats"])
+def test_llama3_shape_mono_and_cats(llama3_pred, variant):
+    """The kernel-speed sweep's M and CATS lines at the 8B shape (k 0.6)."""
+    w, layer = llama3_pred
+    thld = calibrated(variant, layer, w.wid, 0.6, T=16)
+    plan = plan_for(layer, max_batch=8)
+    n, flips, rel = compare(plan, variant, layer, w.tokens(1), thld, f"8b {variant} k=0.6")
+    assert abs(n / w.d_ff - 0.4) < 0.15, n
+    print(f"8b {variant} k=0.6: n={n} flips={flips} rel_err={rel:.2e}", flush=True)
 
 
 @pytest.fixture(scope="module")
