@@ -1282,11 +1282,12 @@ __global__ __launch_bounds__(kBlock) void k_latent_norm(const NormArgs n,
 // range, a wave ballot compacts the active neurons in ascending order into
 // LDS, each wave then keeps U rows in flight (1 KB of a row per load), the
 // four waves reduce in LDS and add the chunk to y with one fp32 atomic per
-// column and token.
+// column and token. U = 16 against 8: the same time at 90% sparsity, 5% less
+// at 50% (7B shape), where a wave has about 20 rows to read.
 template <int B>
 __global__ __launch_bounds__(kBlock) void k_down(const DownArgs a)
 {
-    constexpr int U = 8;
+    constexpr int U = 16;
     extern __shared__ __align__(16) int dsm[];
     __shared__ int wcnt[kWavesPerBlock];
     const int cap = a.rows_per_group;
