@@ -246,6 +246,24 @@ def test_ragged_shapes(d_model, d_ff, B, variant):
     compare(plan, variant, layer, x, thld, f"ragged {d_model}x{d_ff} B={B} {variant}")
 
 
+@pytest.mark.parametrize("d_rank", [8, 32, 128, 512, 1024])
+@pytest.mark.parametrize("B", [1, 4, 8])
+def test_predictor_ranks(d_rank, B):
+    """Every predictor rank the plan accepts, through the v_dot2 (B <= 4) and MFMA
+    (B 8) predictor kernels; rank 1024 stages the latent in LDS instead of
+    registers. Signed 0.8-quantile threshold of the oracle's scores."""
+    dm, dff = 512, 1040
+    L = make_layer(900 + d_rank, dm, dff, 0.05)
+    P = make_predictor(900 + d_rank, dm, d_rank, dff, 0.05)
+    layer = Layer(L, P)
+    x = make_tokens(901 + d_rank, B, dm)
+    thld = float(np.float32(np.quantile(oracle.predictor(x, P["A_t"], P["B_t"])[1], 0.8)))
+    plan = plan_for(layer, max_batch=8)
+    n, flips, rel = compare(plan, "dual_pred", layer, x, thld, f"rank {d_rank} B={B}")
+    assert n > 0
+    print(f"rank {d_rank} B={B}: n={n} flips={flips} rel_err={rel:.2e}", flush=True)
+
+
 def test_plan_reuse_with_shrinking_batch(tiny):
     w, layer = tiny
     thld = calibrated("mono", layer, w.wid, 0.9, T=64)
