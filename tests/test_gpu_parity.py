@@ -264,6 +264,34 @@ def test_predictor_ranks(d_rank, B):
     print(f"rank {d_rank} B={B}: n={n} flips={flips} rel_err={rel:.2e}", flush=True)
 
 
+@pytest.mark.parametrize("B", [3, 4])
+@pytest.mark.parametrize("variant", ["mono", "dual_ideal", "dual_pred", "cats", "dual_tern"])
+def test_widest_token_tile(variant, B):
+    """d_model 8192 at 3-4 tokens: batch x d_model at the plan's limit of 32768, the
+    token copy of the coefficient kernels at its largest (64 KB of LDS), and the MFMA
+    down kernel at its widest rows."""
+    from workloads import make_ternary
+
+    dm, dff = 8192, 1048
+    L = make_layer(960 + B, dm, dff, 0.02)
+    P = make_predictor(960 + B, dm, 64, dff, 0.02) if variant == "dual_pred" else None
+    T = make_ternary(960 + B, dm, dff) if variant == "dual_tern" else None
+    layer = Layer(L, P, T)
+    x = make_tokens(961 + B, B, dm)
+    if variant == "dual_pred":
+        c = oracle.predictor(x, P["A_t"], P["B_t"])[1]
+    elif variant == "dual_tern":
+        c = oracle.ternary_predictor(x, T)
+    else:
+        u, g, s = oracle.coefficients(x, L["W_gate"], L["W_up"])
+        c = np.abs({"mono": u, "dual_ideal": s, "cats": g / (1.0 + np.exp(-g))}[variant])
+    thld = float(np.float32(np.quantile(c, 0.85)))
+    plan = plan_for(layer, max_batch=4)
+    n, flips, rel = compare(plan, variant, layer, x, thld, f"8192 B={B} {variant}")
+    assert n > 0
+    print(f"8192 B={B} {variant}: n={n} flips={flips} rel_err={rel:.2e}", flush=True)
+
+
 def test_plan_reuse_with_shrinking_batch(tiny):
     w, layer = tiny
     thld = calibrated("mono", layer, w.wid, 0.9, T=64)
