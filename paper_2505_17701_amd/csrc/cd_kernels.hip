@@ -2151,9 +2151,17 @@ int tern_row_words(int d_model)
 }
 
 // tokens live in registers up to a batch of 2, in LDS beyond
+// Whether the coefficient kernels keep the tokens in registers (else one LDS
+// copy per workgroup). Registers hold 4 * B * NK VGPRs of tokens: at two tokens
+// of d_model 8192 that left the two-row and predictor kernels one wave per SIMD,
+// and the LDS copy measured 8-20% faster there (70B shape: ideal D, low-rank and
+// ternary predictors, dense); at one token, and two of d_model <= 4096, the
+// registers are as fast or faster.
+constexpr bool tokens_in_regs(int bt, int nk) { return bt == 1 || (bt == 2 && nk <= 8); }
+
 static size_t token_lds_bytes(int bt, int nk)
 {
-    return bt <= 2 ? 0 : (size_t)bt * nk * kColsPerLoad * 2;
+    return tokens_in_regs(bt, nk) ? 0 : (size_t)bt * nk * kColsPerLoad * 2;
 }
 
 size_t down_lds_bytes(int rows_per_group, int bt)
@@ -2237,7 +2245,7 @@ static hipError_t coef_tern_launch(const CoefArgs &a, hipStream_t s)
 template <int B, int NK>
 static hipError_t coef_bn(int variant, const CoefArgs &a, hipStream_t s)
 {
-    constexpr bool XREG = B <= 2;
+    constexpr bool XREG = tokens_in_regs(B, NK);
     // The one-row kernel keeps the tokens in registers for one token only: at
     // two they cost it 114 VGPRs (4 waves per SIMD), and the LDS copy measured
     // 8-10% faster at 2 tokens (7B and 70B shapes); the two-row kernel gained

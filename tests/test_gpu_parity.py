@@ -264,11 +264,11 @@ def test_predictor_ranks(d_rank, B):
     print(f"rank {d_rank} B={B}: n={n} flips={flips} rel_err={rel:.2e}", flush=True)
 
 
-@pytest.mark.parametrize("B", [3, 4])
+@pytest.mark.parametrize("B", [2, 3, 4])
 @pytest.mark.parametrize("variant", ["mono", "dual_ideal", "dual_pred", "cats", "dual_tern"])
 def test_widest_token_tile(variant, B):
-    """d_model 8192 at 3-4 tokens: batch x d_model at the plan's limit of 32768, the
-    token copy of the coefficient kernels at its largest (64 KB of LDS), and the MFMA
+    """d_model 8192 at 2-4 tokens: the LDS token copy that two tokens of this width
+    take, batch x d_model at the plan's limit of 32768 (64 KB of LDS), and the MFMA
     down kernel at its widest rows."""
     from workloads import make_ternary
 
