@@ -5,7 +5,8 @@
 //     neuron. The wave streams the neuron's coefficient row(s) -- W_up, or
 //     W_gate and W_up -- with non-temporal 16-byte loads (64 lanes x 16 B =
 //     one contiguous 1 KB segment per instruction), takes the dot products
-//     against x (registers for batches of 1-2, an LDS copy for 4-8) with
+//     against x (registers for one token, and for two of d_model <= 4096 in
+//     the two-row kernel; otherwise an LDS copy per workgroup) with
 //     v_dot2_f32_bf16, reduces across the wave with DPP and applies the
 //     strict threshold (union over the batch). For M-CountDown an active
 //     neuron's wave immediately reads its W_gate row and forms s = u *
@@ -20,7 +21,7 @@
 //   down kernel: workgroup (c, g) owns a column chunk c and a contiguous
 //     neuron range g. One round trip reads act and s of the range, a wave
 //     ballot compacts the active neurons in ascending order into LDS; for 1-2
-//     tokens each wave then keeps 8 W_down rows in flight on the VALU, for
+//     tokens each wave then keeps 16 W_down rows in flight on the VALU, for
 //     4-8 the rows feed MFMA (S as bf16 hi + lo); partial sums are added in
 //     LDS and go to y with one fp32 atomic per column and token.
 //   per-token threshold: the coefficient kernel writes the dense
