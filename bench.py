@@ -121,9 +121,11 @@ def time_steps(fn, steps, warmup, stream):
     return t0.elapsed_time(t1) / steps  # ms per step
 
 
-def time_steps_graph(fn, steps, warmup):
+def time_steps_graph(fn, steps, warmup, extra=None):
     """Warm up eagerly, capture exactly `steps` calls into one HIP graph, replay it once
-    untimed and once timed between two synchronisations."""
+    untimed and once timed between two synchronisations; returns ms per call of that
+    replay. With a list `extra`, a few more timed replays append their ms per call to it
+    (spread statistics only)."""
     import torch
 
     for i in range(warmup):
@@ -142,6 +144,13 @@ def time_steps_graph(fn, steps, warmup):
     t1.record()
     torch.cuda.synchronize()
     ms = t0.elapsed_time(t1) / steps
+    if extra is not None:
+        for _ in range(5):
+            t0.record()
+            g.replay()
+            t1.record()
+            torch.cuda.synchronize()
+            extra.append(t0.elapsed_time(t1) / steps)
     del g
     return ms
 
@@ -327,7 +336,7 @@ class Context:
                 cd.countdown_ffn_dense(plan, x, L["W_gate"], L["W_up"], L["W_down"], y=y)
         return step
 
-    def measure(self, variant, k, B, steps, warmup):
+    def measure(self, variant, k, B, steps, warmup, replays=False):
         import torch
 
         from paper_2505_17701_amd import binding as cd
@@ -341,7 +350,8 @@ class Context:
                        d_rank=dr if base == "dual_pred" else 0)
         step = self.make_step(plan, variant, k, B, y)
         ms_eager = time_steps(step, steps, warmup, stream)
-        ms = time_steps_graph(step, steps, warmup)
+        rep = [] if replays else None
+        ms = time_steps_graph(step, steps, warmup, rep)
         # per-kernel averages: graph-replayed loops of a single kernel (the plan's phase
         # selection), each bracketed by one HIP event pair on the launch stream
         nk = min(steps, 512)
@@ -366,6 +376,9 @@ class Context:
         dr_v = dr if base == "dual_pred" else 0
         per = [traffic.algorithmic_bytes(base, dm, dff, int(v), B=B, d_rank=dr_v) for v in n]
         res = {"batch": B, "ms_per_step": ms, "us_per_layer": ms * 1e3,
+               **({"us_per_layer_5_more_replays": [r * 1e3 for r in rep],
+                   "us_per_layer_median_of_6": float(np.median([ms] + rep)) * 1e3,
+                   "us_per_layer_mean_of_6": float(np.mean([ms] + rep)) * 1e3} if rep else {}),
                "tokens_per_s": B * 1e3 / ms, "us_per_layer_eager": ms_eager * 1e3,
                "n_active_mean": float(n.mean()), "realised_sparsity": float(1 - n.mean() / dff)}
         # the coefficient loop includes the predictor's latent kernel (one launch each)
@@ -677,7 +690,8 @@ def main():
     main_ctx = Context(w, args.copies, args.tokens, args.calib_tokens,
                        sorted(set((args.k,) + tuple(w.ks))), max_batch=args.batch,
                        variants=main_variants)
-    main_res = main_ctx.measure(args.variant, args.k, args.batch, args.steps, args.warmup)
+    main_res = main_ctx.measure(args.variant, args.k, args.batch, args.steps, args.warmup,
+                                replays=True)
     log(f"[bench] {w.name} {args.variant} k={args.k}: {json.dumps(main_res)}")
     ceiling = stream_ceiling(main_ctx, min(args.steps, 512))
     log(f"[bench] plain streaming read: {json.dumps(ceiling)}")
@@ -812,6 +826,8 @@ def main():
         "ms_per_step": main_res["ms_per_step"],
         "us_per_layer": main_res["us_per_layer"],
         "us_per_layer_eager": main_res["us_per_layer_eager"],
+        "us_per_layer_median_of_6": main_res["us_per_layer_median_of_6"],
+        "us_per_layer_mean_of_6": main_res["us_per_layer_mean_of_6"],
         "launch": "one HIP graph of exactly `steps` layer calls, replayed once (timed)",
         "achieved_GBs": main_res["achieved_GBs"],
         "frac_hbm_peak": main_res["frac_hbm_peak"],
