@@ -751,8 +751,10 @@ __device__ __forceinline__ void wt_consume(uint16_t *wt, const WtBatch &bt, int 
     }
 }
 
-// gather_mfma with LDS-staged weight rows and tokens from global memory.
-// wtiles: LDS [4 waves][kWtWave] bf16; part, lrow as in gather_mfma.
+// The block's active neurons (bits of M, rows r0 + bit) in tiles of 16 on MFMA:
+// each tile's column steps are split among 4 / ntiles waves, which add their
+// 16 x 16 partial sums in `part` (LDS [4][2][256] fp32) and write s = u * SiLU(g).
+// wtiles: LDS [4 waves][kWtWave] bf16; lrow: LDS [32] rows of the active neurons.
 template <int B, int NK>
 __device__ __forceinline__ void gather_mfma_lds(const CoefArgs &a, uint16_t *wtiles, float *part,
                                                 int *lrow, uint32_t M, int r0, int wave, int lane)
