@@ -15,7 +15,9 @@ import numpy as np
 
 HERE = os.path.dirname(os.path.abspath(__file__))
 SRC = os.path.join(HERE, "cd_oracle.c")
-LIB = os.path.join(HERE, "libcdoracle.so")
+# CD_ORACLE_LIB names another build of the oracle to load (the mutation test of
+# the pins loads deliberately broken copies this way); build() leaves it alone
+LIB = os.environ.get("CD_ORACLE_LIB") or os.path.join(HERE, "libcdoracle.so")
 
 COEF_ABS_U, COEF_ABS_S, COEF_SHAT, COEF_ABS_H, COEF_TERN = 0, 1, 2, 3, 4
 KIND = {"mono": COEF_ABS_U, "dual_ideal": COEF_ABS_S, "dual_pred": COEF_SHAT, "cats": COEF_ABS_H,
@@ -33,6 +35,8 @@ __all__ = [
 
 def build(force: bool = True) -> str:
     """Compile ``cd_oracle.c`` with gcc (fp64, no fast-math, OpenMP over rows)."""
+    if os.environ.get("CD_ORACLE_LIB"):
+        return LIB
     if force or not os.path.exists(LIB):
         tmp = LIB + ".tmp"
         cmd = ["gcc", "-O2", "-fopenmp", "-fPIC", "-shared", "-std=c11", "-Wall", "-Wextra",

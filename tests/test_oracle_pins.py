@@ -388,6 +388,9 @@ def test_residual_rmsnorm_closed_form():
     h = np.array([3.0, -4.0])
     _, r = oracle.residual_rmsnorm(h, None, eps=0.0)
     np.testing.assert_allclose(r, h / math.sqrt(12.5), rtol=1e-15)
+    # eps inside the root, comparable to mean(h^2): 1 / sqrt(1 + 3) = 1/2 exactly
+    _, r = oracle.residual_rmsnorm(np.ones(16), None, eps=3.0)
+    np.testing.assert_array_equal(r, 0.5)
 
 
 def test_bad_arguments_are_rejected():
