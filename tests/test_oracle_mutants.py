@@ -69,6 +69,17 @@ MUTANTS = {
     "per-token path: quantile at 1 - k": (
         "        q[b] = cdo_quantile_linear(k, cb, d_ff);",
         "        q[b] = cdo_quantile_linear(1.0 - k, cb, d_ff);"),
+    "dense path: last neuron dropped": (
+        "            for (int64_t i = 0; i < d_ff; i++)\n                acc += s[i] * wide(W_down[i * d_model + j]);",
+        "            for (int64_t i = 0; i < d_ff - 1; i++)\n                acc += s[i] * wide(W_down[i * d_model + j]);"),
+    "dense path: W_down read transposed": (
+        "acc += s[i] * wide(W_down[i * d_model + j]);", "acc += s[i] * wide(W_down[j * d_ff + i]);"),
+    "index-restricted FFN: gate from W_up": (
+        "            double gg = row_dot(xb, W_gate, i, d_model);\n            s[(int64_t)b * d_ff + i] = uu * cdo_silu(gg);",
+        "            double gg = row_dot(xb, W_up, i, d_model);\n            s[(int64_t)b * d_ff + i] = uu * cdo_silu(gg);"),
+    "index-restricted FFN: compact s of token 0 for every token": (
+        "s_c[(int64_t)b * n + t] = s[(int64_t)b * d_ff + idx[t]];",
+        "s_c[(int64_t)b * n + t] = s[idx[t]];"),
     # the low-rank predictor's call (the first of two identical lines; the second is the
     # ternary predictor's)
     "low-rank predictor score thresholded as |s_hat|": (
