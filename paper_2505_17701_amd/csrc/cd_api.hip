@@ -37,6 +37,7 @@ struct cd_plan {
     float *lat;                   // [max_batch][d_rank] predictor latent
     unsigned phases;              // kernels launched per call (CD_PHASE_*)
     bool has_state;               // act / s hold a coefficient kernel's output
+    bool s_in_coef;               // the last call's s is coef (ideal D, per-token thresholds)
 };
 
 namespace {
@@ -169,7 +170,7 @@ cdk::DownArgs down_args(cd_plan *p, int B, const uint16_t *Wd, float *y)
 {
     cdk::DownArgs a;
     a.act = p->act;
-    a.s = p->s;
+    a.s = p->s_in_coef ? p->coef : p->s;
     a.nb = B;
     a.Wd = Wd;
     a.d_model = p->d_model;
@@ -212,6 +213,7 @@ cd_status run_ffn(cd_plan *p, int variant, const uint16_t *x, int B, const uint1
         if (st != CD_OK)
             return st;
         p->has_state = true;
+        p->s_in_coef = false;
     }
     if (p->phases & CD_PHASE_DOWN) {
         const cdk::DownArgs da = down_args(p, B, Wd, y);
@@ -279,6 +281,7 @@ cd_status run_ffn_residual(cd_plan *p, int variant, const float *h_in, const flo
         if (st != CD_OK)
             return st;
         p->has_state = true;
+        p->s_in_coef = false;
     }
     if (p->phases & CD_PHASE_DOWN) {
         const cdk::DownArgs da = down_args(p, B, Wd, y);
@@ -333,6 +336,7 @@ cd_status run_ffn_topk(cd_plan *p, int variant, const uint16_t *x, int B, const 
         if (st != CD_OK)
             return st;
         p->has_state = true;
+        p->s_in_coef = variant == CD_VARIANT_DUAL_IDEAL;
     }
     if (p->phases & CD_PHASE_DOWN) {
         const cdk::DownArgs da = down_args(p, B, Wd, y);
@@ -449,6 +453,7 @@ cd_status countdown_plan_create(int d_model, int d_ff, int max_batch, int d_rank
     p->last_batch = 0;
     p->phases = CD_PHASE_ALL;
     p->has_state = false;
+    p->s_in_coef = false;
     const size_t mb = (size_t)max_batch;
     st = dalloc(&p->act, (size_t)d_ff);
     if (st == CD_OK) st = dalloc(&p->s, mb * d_ff);
@@ -667,7 +672,8 @@ cd_status countdown_export_active(const cd_plan *p, int32_t *idx_dst, int32_t *n
     hipStream_t s = reinterpret_cast<hipStream_t>(stream);
     hipError_t e = hipSuccess;
     if (idx_dst || n_dst || s_dst)
-        e = cdk::launch_export(p->act, p->s, p->last_batch, p->d_ff, idx_dst, n_dst, s_dst, s);
+        e = cdk::launch_export(p->act, p->s_in_coef ? p->coef : p->s, p->last_batch, p->d_ff,
+                               idx_dst, n_dst, s_dst, s);
     if (coef_dst && e == hipSuccess)
         e = hipMemcpyAsync(coef_dst, p->coef, sizeof(float) * (size_t)p->last_batch * p->d_ff,
                            hipMemcpyDeviceToDevice, s);

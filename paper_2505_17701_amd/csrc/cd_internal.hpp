@@ -71,7 +71,8 @@ hipError_t launch_export(const int *act, const float *s_rows, int nb, int d_ff, 
                          int *n_dst, float *s_dst, hipStream_t s);
 // Per-token threshold path after a dense coefficient kernel (a.coef holds
 // [nb][d_ff]): q[b] = Quantile(k, c_b), then act / s of the neurons above
-// their tokens' thresholds (gathering W_gate, or W_gate and W_up). d_ff <= 32768.
+// their tokens' thresholds (gathering W_gate, or W_gate and W_up). For ideal
+// D-CountDown the select sets act and s stays in a.coef. d_ff <= 32768.
 hipError_t launch_topk(int variant, const CoefArgs &a, double k, double *q, hipStream_t s);
 constexpr int kTopkMaxDff = 32768;
 // Per-token linear-interpolation quantile of coef rows [T][ld] (n used entries).

@@ -1804,10 +1804,15 @@ __device__ __forceinline__ void find_bin(const uint32_t *mine, const uint32_t (&
     out[2] = cnt;
 }
 
+// With act set (ideal D-CountDown, |s| keys), the workgroup also flags its
+// token's neurons with |c| > q: act starts at 0 (the coefficient kernel with
+// threshold +inf wrote it) and every token stores the same 1, so the union
+// needs no atomics and no gather kernel follows (s is the coefficient itself).
 template <int KPT>
 __global__ __launch_bounds__(kTopkThreads) void k_topk_select(const float *__restrict__ coef, int ld,
                                                               int n, int use_abs, double k,
-                                                              double *__restrict__ q)
+                                                              double *__restrict__ q,
+                                                              int *__restrict__ act)
 {
     constexpr int kWaves = kTopkThreads / kWave;
     extern __shared__ __align__(16) uint32_t sm[];
@@ -1979,10 +1984,22 @@ __global__ __launch_bounds__(kTopkThreads) void k_topk_select(const float *__res
         kA = pA;  // every bit is fixed
         kB = pB;
     }
+    __shared__ double qs;
     if (threadIdx.x == 0) {
         const double v0 = (double)key_value(kA, use_abs);
         const double v1 = (double)key_value(two ? kB : kA, use_abs);
-        q[blockIdx.x] = v0 + (h - (double)lo) * (v1 - v0);
+        qs = v0 + (h - (double)lo) * (v1 - v0);
+        q[blockIdx.x] = qs;
+    }
+    if (act) {  // uniform; |s| keys (use_abs): the key's bits are |c|
+        __syncthreads();
+        const double qv = qs;
+#pragma unroll
+        for (int j = 0; j < KPT; ++j) {
+            const int i = threadIdx.x + j * kTopkThreads;
+            if (j < jn && i < n && (double)__uint_as_float(key[j]) > qv)
+                act[i] = 1;
+        }
     }
 }
 
@@ -2497,14 +2514,14 @@ static hipError_t gather_topk_b(int variant, const CoefArgs &a, const double *q,
 static int topk_kpt(int n) { return n <= 16 * kTopkThreads ? 16 : 32; }
 
 static void launch_topk_select(const float *coef, int ld, int n, int T, int use_abs, double k,
-                               double *q, size_t lds, hipStream_t s)
+                               double *q, size_t lds, hipStream_t s, int *act = nullptr)
 {
     if (topk_kpt(n) == 16) {
         allow_lds(k_topk_select<16>, lds);
-        k_topk_select<16><<<T, kTopkThreads, lds, s>>>(coef, ld, n, use_abs, k, q);
+        k_topk_select<16><<<T, kTopkThreads, lds, s>>>(coef, ld, n, use_abs, k, q, act);
     } else {
         allow_lds(k_topk_select<32>, lds);
-        k_topk_select<32><<<T, kTopkThreads, lds, s>>>(coef, ld, n, use_abs, k, q);
+        k_topk_select<32><<<T, kTopkThreads, lds, s>>>(coef, ld, n, use_abs, k, q, act);
     }
 }
 
@@ -2514,10 +2531,13 @@ hipError_t launch_topk(int variant, const CoefArgs &a, double k, double *q, hipS
         return hipErrorInvalidValue;
     if (variant == kDualTern)  // a signed predictor score and the W_gate + W_up gather
         variant = kDualPred;
+    // ideal D: s is the dense coefficient, so the select sets the flags itself and
+    // the down kernel reads s from a.coef (no gather kernel)
+    const bool ideal = variant == kDualIdeal;
     launch_topk_select(a.coef, a.d_ff, a.d_ff, a.nb, variant == kDualPred ? 0 : 1, k, q,
-                       topk_select_lds_bytes(), s);
+                       topk_select_lds_bytes(), s, ideal ? a.act : nullptr);
     hipError_t e = hipGetLastError();
-    if (e != hipSuccess)
+    if (e != hipSuccess || ideal)
         return e;
     switch (batch_tile(a.nb)) {
     case 1: return gather_topk_b<1>(variant, a, q, s);
