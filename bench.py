@@ -790,8 +790,8 @@ def main():
                              "W_gate / W_up gather, s)",
                 "dense": "k_coef_dual (dense W_gate + W_up GEMV, s)",
                 "mono_topk": "k_coef_mono + k_topk_select + k_gather_topk (per-token threshold)",
-                "dual_ideal_topk": "k_coef_dual + k_topk_select + k_gather_topk (per-token "
-                                   "threshold)",
+                "dual_ideal_topk": "k_coef_dual + k_topk_select (per-token threshold; the "
+                                   "select sets the flags, s is the coefficient)",
                 "dual_pred_topk": "k_latent + k_coef_pred + k_topk_select + k_gather_topk "
                                   "(per-token threshold)",
                 "cats": "k_coef_mono<CATS> (dense W_gate GEMV, SiLU, threshold, W_up gather)",
