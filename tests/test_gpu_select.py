@@ -134,3 +134,54 @@ def test_topk_long_rows(shape):
     n, flips, rel = check_topk("mono", layer, x, k, f"long topk {shape}")
     if B == 1 and flips == 0:
         assert n == dff - 1 - math.floor(k * (dff - 1))
+
+
+@pytest.mark.parametrize("variant", ["mono", "cats", "dual_ideal", "dual_pred"])
+@pytest.mark.parametrize("dup", [None, "pairs", "all", "cluster"])
+def test_per_token_call_exact_order_statistics(variant, dup):
+    """The per-token FFN call's own select (|c| keys, or signed keys for the
+    predictor score): on five calls in a row of one plan, with batch sizes and
+    k that change from call to call, every token's threshold is exactly the
+    interpolated order statistic of the coefficients the call wrote. "all"
+    (every coefficient of a token equal) and "cluster" (most within a relative
+    2^-8, with ties) put thousands of keys into one first-pass bin, so the
+    radix passes finish those."""
+    from paper_2505_17701_amd import binding as cd
+
+    dm, dff, dr = 64, 11008, 8
+    L = make_layer(1970, dm, dff, 0.05)
+    P = make_predictor(1970, dm, dr, dff, 0.3) if variant == "dual_pred" else None
+    # the matrix whose rows set the coefficient (for ideal D both factors)
+    mats = {"mono": [L["W_up"]], "cats": [L["W_gate"]], "dual_ideal": [L["W_up"], L["W_gate"]],
+            "dual_pred": [P["B_t"] if P is not None else None]}[variant]
+    rows = np.arange(dff) % 16 != 0
+    for W in mats:
+        if dup == "pairs":
+            W[1::2] = W[0::2][: dff // 2]
+        elif dup == "all":
+            W[:] = W[0]
+        elif dup == "cluster":
+            W[rows] = W[0]
+    if dup == "cluster":  # a small varying first weight in the coefficient's own matrix
+        W = mats[0]
+        small = (np.arange(dff) % 64 - 32).astype(np.float32) * np.float32(2.0 ** -18)
+        W[rows, 0] = bf16_round(small[rows])
+    layer = Layer(L, P)
+    D = layer.d
+    vid = {"mono": cd.CD_VARIANT_MONO, "cats": cd.CD_VARIANT_CATS,
+           "dual_ideal": cd.CD_VARIANT_DUAL_IDEAL, "dual_pred": cd.CD_VARIANT_DUAL_PRED}[variant]
+    plan = cd.Plan(dm, dff, 8, dr if variant == "dual_pred" else 0, keep_coef=True)
+    signed = variant == "dual_pred"
+    for call, (B, k) in enumerate([(5, 0.9), (3, 0.5), (8, 0.0), (1, 1.0), (2, 0.999)]):
+        X = make_tokens(1971 + call, B, dm, purpose=T_CALIB)
+        q = torch.empty(B, dtype=torch.float64, device="cuda")
+        cd.countdown_ffn_topk(plan, vid, dev_bf16(X), D["W_gate"], D["W_up"], D["W_down"], k,
+                              A_t=D.get("A_t"), B_t=D.get("B_t"), thld_out=q)
+        coef = cd.countdown_export_active(plan)[2].cpu().numpy().astype(np.float64)[:B]
+        q = q.cpu().numpy()
+        if dup == "all" and variant != "dual_ideal":
+            assert (coef == coef[:, :1]).all()
+        for t in range(B):
+            v = coef[t] if signed else np.abs(coef[t])
+            assert q[t] == exact_quantile(v, k), (variant, dup, call, B, k, t)
+    plan.close()
