@@ -658,8 +658,9 @@ def stack_bench(args, steps_tokens=128, warmup_tokens=8):
 def main():
     args = parse()
     if args.gpus != 1:
-        print(f"bench.py measures one GPU only (got --gpus {args.gpus}); the sparse FFN is "
-              "built and timed on a single MI355X in this build.", file=sys.stderr)
+        print(f"bench.py measures one GPU only (got --gpus {args.gpus}): the sparse FFN layer "
+              "runs and is timed on a single MI355X; sharding it across GPUs is not "
+              "implemented.", file=sys.stderr)
         sys.exit(2)
 
     import torch

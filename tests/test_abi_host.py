@@ -248,3 +248,15 @@ def test_binding_checks_shapes_before_pointers():
         cd._out(plan, x, torch.zeros(1, 64))
     with pytest.raises(TypeError):
         cd._out(plan, x, torch.zeros(2, 64, dtype=torch.float64))
+
+
+def test_bench_refuses_more_than_one_gpu():
+    """bench.py times one GPU: --gpus N > 1 exits with status 2 and says why,
+    before it touches a device."""
+    import sys
+
+    root = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+    r = subprocess.run([sys.executable, os.path.join(root, "bench.py"), "--gpus", "2"], cwd=root,
+                       capture_output=True, text=True, timeout=120)
+    assert r.returncode == 2
+    assert "one GPU only" in r.stderr and r.stdout == ""
