@@ -262,7 +262,8 @@ cd_status countdown_export_active(const cd_plan *plan, int32_t *idx_dst, int32_t
  * alone launch only that kernel, so a loop of calls times one kernel in
  * isolation; y is then not the FFN output. A down-only call uses the flags
  * and coefficients left by the plan's last coefficient kernel (CD_EINVAL if
- * there is none). Plans start at CD_PHASE_ALL.
+ * there is none, or if it ran on another batch size). Plans start at
+ * CD_PHASE_ALL.
  */
 #define CD_PHASE_COEF 1u
 #define CD_PHASE_DOWN 2u

@@ -180,6 +180,14 @@ cdk::DownArgs down_args(cd_plan *p, int B, const uint16_t *Wd, float *y)
     return a;
 }
 
+// A down-only call reads the flags and coefficients left by the plan's last
+// coefficient kernel: there must be one, and it must have run on the same
+// batch (its coefficients of later tokens were never written).
+bool down_state_ok(const cd_plan *p, int B)
+{
+    return (p->phases & CD_PHASE_COEF) || (p->has_state && B == p->last_batch);
+}
+
 // Tp: the packed ternary predictor (CD_VARIANT_DUAL_TERN only)
 cd_status run_ffn(cd_plan *p, int variant, const uint16_t *x, int B, const uint16_t *Wg,
                   const uint16_t *Wu, const uint16_t *Wd, const uint16_t *At, const uint16_t *Bt,
@@ -199,8 +207,8 @@ cd_status run_ffn(cd_plan *p, int variant, const uint16_t *x, int B, const uint1
     if ((st = plan_device_ok(p)) != CD_OK)
         return st;
     hipStream_t s = reinterpret_cast<hipStream_t>(stream);
-    if (!(p->phases & CD_PHASE_COEF) && !p->has_state)
-        return CD_EINVAL;  // a down-only call needs a previous coefficient kernel's output
+    if (!down_state_ok(p, B))
+        return CD_EINVAL;
     p->last_batch = B;
     if (p->phases & CD_PHASE_COEF) {
         if (variant == CD_VARIANT_DUAL_PRED) {
@@ -258,7 +266,7 @@ cd_status run_ffn_residual(cd_plan *p, int variant, const float *h_in, const flo
     if ((st = plan_device_ok(p)) != CD_OK)
         return st;
     hipStream_t s = reinterpret_cast<hipStream_t>(stream);
-    if (!(p->phases & CD_PHASE_COEF) && !p->has_state)
+    if (!down_state_ok(p, B))
         return CD_EINVAL;
     p->last_batch = B;
     if (p->phases & CD_PHASE_COEF) {
@@ -317,7 +325,7 @@ cd_status run_ffn_topk(cd_plan *p, int variant, const uint16_t *x, int B, const 
     if ((st = plan_device_ok(p)) != CD_OK)
         return st;
     hipStream_t s = reinterpret_cast<hipStream_t>(stream);
-    if (!(p->phases & CD_PHASE_COEF) && !p->has_state)
+    if (!down_state_ok(p, B))
         return CD_EINVAL;
     p->last_batch = B;
     if (p->phases & CD_PHASE_COEF) {

@@ -321,7 +321,7 @@ def test_nondefault_stream_and_repeatability(tiny):
 
 def test_phase_selection(tiny):
     """Coefficient-only then down-only calls reproduce the full call; a down-only call
-    needs a previous coefficient kernel on the plan."""
+    needs a previous coefficient kernel on the plan, run on the same batch."""
     from paper_2505_17701_amd import binding as cd
 
     w, layer = tiny
@@ -340,6 +340,9 @@ def test_phase_selection(tiny):
         y_d = torch.zeros_like(y_full)
         cd.countdown_ffn_mono(plan, X, D["W_gate"], D["W_up"], D["W_down"], thld, y=y_d)
         torch.testing.assert_close(y_d, y_full, rtol=0, atol=1e-6 * float(y_full.abs().max()))
+    # the coefficient kernel ran on two tokens: a down-only call on one is refused
+    with pytest.raises(cd.CountdownError):
+        cd.countdown_ffn_mono(plan, X[:1], D["W_gate"], D["W_up"], D["W_down"], thld)
     cd.countdown_plan_set_phases(plan, cd.CD_PHASE_ALL)
     torch.testing.assert_close(
         cd.countdown_ffn_mono(plan, X, D["W_gate"], D["W_up"], D["W_down"], thld), y_full,
