@@ -13,6 +13,7 @@ import numpy as np
 import pytest
 
 from workloads import WORKLOADS, bf16_to_f32, make_layer, make_predictor, make_tokens
+from workloads.synth import bf16_round
 from workloads.synth import T_CALIB
 
 from gpu_support import (COEF_TOL, check_idx, check_s, check_y, coef_max, dev_bf16, dot_bound)
@@ -214,6 +215,48 @@ def test_dense_parity(tiny, B):
     w, layer = tiny
     plan = plan_for(layer, max_batch=4)
     compare(plan, "dense", layer, w.tokens(B), 0.0, f"dense B={B}")
+
+
+def _summation_atol(layer, idx, x):
+    """fp32 bound on the difference of two orders of the sum of y over the active rows:
+    2 (n + 8) units of 2^-24 of the largest sum of |s_i W_down[i, j]| (n terms, plus
+    the lane and workgroup sums; each order within half of it)."""
+    H = layer.h
+    _, s_on = oracle.ffn_on_idx(np.atleast_2d(x), H["W_gate"], H["W_up"], H["W_down"], idx)
+    yabs = np.abs(s_on) @ np.abs(f64(H["W_down"])[idx])
+    return 2 * (len(idx) + 8) * 2.0 ** -24 * float(yabs.max()) + 1e-30
+
+
+@pytest.mark.parametrize("variant", ["mono", "dual_ideal"])
+def test_metamorphic_relations(tiny, variant):
+    """Exact relations of the method, checked on the kernels alone (Eq. 5 and 6): W_down
+    doubled gives the same IDX and 2y; W_up negated gives the same IDX and -y (|u| and
+    |s| are unchanged bit for bit); a permutation of the neurons permutes IDX and leaves
+    y unchanged up to the order of the sum."""
+    w, layer = tiny
+    thld = calibrated(variant, layer, w.wid, 0.9, T=64)
+    X = w.tokens(2)
+    plan = plan_for(layer, max_batch=2)
+    y, idx, _, _ = run_gpu(plan, variant, layer, X, thld)
+    assert 0 < len(idx) < layer.d_ff
+    atol = _summation_atol(layer, idx, X)
+    H = layer.h
+
+    doubled = Layer(dict(H, W_down=bf16_round(2.0 * bf16_to_f32(H["W_down"]))))
+    y2, idx2, _, _ = run_gpu(plan, variant, doubled, X, thld)
+    np.testing.assert_array_equal(idx2, idx)
+    np.testing.assert_allclose(y2, 2.0 * y, rtol=0, atol=2.0 * atol)
+
+    negated = Layer(dict(H, W_up=H["W_up"] ^ np.uint16(0x8000)))
+    yn, idxn, _, _ = run_gpu(plan, variant, negated, X, thld)
+    np.testing.assert_array_equal(idxn, idx)
+    np.testing.assert_allclose(yn, -y, rtol=0, atol=atol)
+
+    perm = np.random.default_rng(17).permutation(layer.d_ff)  # new row j = old row perm[j]
+    permuted = Layer({k: np.ascontiguousarray(v[perm]) for k, v in H.items()})
+    yp, idxp, _, _ = run_gpu(plan, variant, permuted, X, thld)
+    np.testing.assert_array_equal(np.sort(perm[idxp]), idx)
+    np.testing.assert_allclose(yp, y, rtol=0, atol=atol)
 
 
 def test_single_active_row(tiny):
