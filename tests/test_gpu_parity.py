@@ -227,13 +227,15 @@ def _summation_atol(layer, idx, x):
     return 2 * (len(idx) + 8) * 2.0 ** -24 * float(yabs.max()) + 1e-30
 
 
-@pytest.mark.parametrize("variant", ["mono", "dual_ideal"])
+@pytest.mark.parametrize("variant", ["mono", "dual_ideal", "cats", "dual_pred"])
 def test_metamorphic_relations(tiny, variant):
     """Exact relations of the method, checked on the kernels alone (Eq. 5 and 6): W_down
-    doubled gives the same IDX and 2y; W_up negated gives the same IDX and -y (|u| and
-    |s| are unchanged bit for bit); a permutation of the neurons permutes IDX and leaves
+    doubled gives the same IDX and 2y; W_up negated gives the same IDX and -y (|u|, |s|,
+    |SiLU(g)| and the predictor score are unchanged bit for bit); a permutation of the neurons permutes IDX and leaves
     y unchanged up to the order of the sum."""
     w, layer = tiny
+    if variant == "dual_pred":  # the predictor reads neither W_up nor W_down
+        layer = Layer(w.layer(), make_predictor(w.wid, layer.d_model, 64, layer.d_ff, 0.02))
     thld = calibrated(variant, layer, w.wid, 0.9, T=64)
     X = w.tokens(2)
     plan = plan_for(layer, max_batch=2)
@@ -253,7 +255,8 @@ def test_metamorphic_relations(tiny, variant):
     np.testing.assert_allclose(yn, -y, rtol=0, atol=atol)
 
     perm = np.random.default_rng(17).permutation(layer.d_ff)  # new row j = old row perm[j]
-    permuted = Layer({k: np.ascontiguousarray(v[perm]) for k, v in H.items()})
+    permuted = Layer({k: np.ascontiguousarray(v[perm]) if v.shape[0] == layer.d_ff else v
+                      for k, v in H.items()})  # neuron-major matrices (A_t is not)
     yp, idxp, _, _ = run_gpu(plan, variant, permuted, X, thld)
     np.testing.assert_array_equal(np.sort(perm[idxp]), idx)
     np.testing.assert_allclose(yp, y, rtol=0, atol=atol)
