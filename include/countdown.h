@@ -83,7 +83,10 @@ typedef struct cd_plan cd_plan;
  * predictor latent and, with CD_PLAN_KEEP_COEF, the dense coefficients) on
  * the current device. d_model and d_ff must be positive multiples of 8 with
  * d_model <= 8192; 1 <= max_batch <= 8; d_rank is 0 (no predictor) or a
- * power of two in [8, 1024]; max_batch * d_model <= 32768. Returns CD_EINVAL
+ * power of two in [8, 1024]; T * C <= 32768, where T is max_batch rounded up
+ * to 1, 2, 4 or 8 and C is d_model rounded up to 512, 1024, 2048, 4096 or
+ * 8192 (the widest token tile a call stages; d_model 4096 takes up to 8
+ * tokens, d_model 4097..8192 up to 4). Returns CD_EINVAL
  * for malformed sizes and CD_EUNSUPPORTED for well-formed sizes beyond those
  * limits (both checked before any HIP call), CD_ENOMEM / CD_EHIP when the
  * device is missing or allocation fails. *out is set only on success.

@@ -425,5 +425,13 @@ def countdown_check_shape(d_model, d_ff, max_batch, d_rank) -> int:
     return load_library().countdown_check_shape(d_model, d_ff, max_batch, d_rank)
 
 
+def max_batch_for(d_model: int, d_ff: int = 8, d_rank: int = 0) -> int:
+    """Largest max_batch countdown_check_shape accepts for this shape (0 if none)."""
+    for b in range(8, 0, -1):
+        if countdown_check_shape(d_model, d_ff, b, d_rank) == CD_OK:
+            return b
+    return 0
+
+
 def countdown_abi_version() -> int:
     return load_library().countdown_abi_version()

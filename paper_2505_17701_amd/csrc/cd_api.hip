@@ -16,7 +16,10 @@ namespace {
 constexpr int kMaxDModel = 8192;
 constexpr int kMaxBatch = 8;
 constexpr int kMaxRank = 1024;
-constexpr int kMaxBatchCols = 32768;  // max_batch * d_model (batch tiles of 4 and 8 stage x in LDS)
+// Token columns of the widest tile a call launches: the batch rounded up to
+// 1, 2, 4 or 8 tokens times d_model rounded up to 1, 2, 4, 8 or 16 chunks of
+// 512 (batch tiles of 4 and 8 stage x in LDS).
+constexpr int kMaxTileCols = 32768;
 
 bool aligned16(const void *p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
 
@@ -60,7 +63,7 @@ cd_status check_shape(int d_model, int d_ff, int max_batch, int d_rank)
         return CD_EINVAL;
     if (d_rank > 0 && (!is_pow2(d_rank) || d_rank < 8 || d_rank > kMaxRank))
         return CD_EUNSUPPORTED;
-    if ((long long)max_batch * d_model > kMaxBatchCols)
+    if ((long long)cdk::batch_tile(max_batch) * cdk::col_tile(d_model) * 512 > kMaxTileCols)
         return CD_EUNSUPPORTED;
     return CD_OK;
 }
@@ -180,6 +183,24 @@ cdk::DownArgs down_args(cd_plan *p, int B, const uint16_t *Wd, float *y)
     return a;
 }
 
+// The per-neuron workspace no longer describes a finished coefficient kernel
+// (a coefficient phase is starting, or a launch of it failed).
+void forget_state(cd_plan *p)
+{
+    p->has_state = false;
+    p->last_batch = 0;
+    p->s_in_coef = false;
+}
+
+// The coefficient phase of a B-token call was enqueued: a down-only call of the
+// same batch, and countdown_export_active, may read its workspace.
+void keep_state(cd_plan *p, int B, bool s_in_coef)
+{
+    p->has_state = true;
+    p->last_batch = B;
+    p->s_in_coef = s_in_coef;
+}
+
 // A down-only call reads the flags and coefficients left by the plan's last
 // coefficient kernel: there must be one, and it must have run on the same
 // batch (its coefficients of later tokens were never written).
@@ -209,8 +230,8 @@ cd_status run_ffn(cd_plan *p, int variant, const uint16_t *x, int B, const uint1
     hipStream_t s = reinterpret_cast<hipStream_t>(stream);
     if (!down_state_ok(p, B))
         return CD_EINVAL;
-    p->last_batch = B;
     if (p->phases & CD_PHASE_COEF) {
+        forget_state(p);
         if (variant == CD_VARIANT_DUAL_PRED) {
             st = launched(cdk::launch_latent(x, B, At, p->d_model, p->d_rank, p->lat, s));
             if (st != CD_OK)
@@ -220,8 +241,7 @@ cd_status run_ffn(cd_plan *p, int variant, const uint16_t *x, int B, const uint1
         st = launched(cdk::launch_coef(kernel_variant(variant), ca, s));
         if (st != CD_OK)
             return st;
-        p->has_state = true;
-        p->s_in_coef = false;
+        keep_state(p, B, false);
     }
     if (p->phases & CD_PHASE_DOWN) {
         const cdk::DownArgs da = down_args(p, B, Wd, y);
@@ -268,8 +288,8 @@ cd_status run_ffn_residual(cd_plan *p, int variant, const float *h_in, const flo
     hipStream_t s = reinterpret_cast<hipStream_t>(stream);
     if (!down_state_ok(p, B))
         return CD_EINVAL;
-    p->last_batch = B;
     if (p->phases & CD_PHASE_COEF) {
+        forget_state(p);
         cdk::NormArgs n;
         n.h_in = h_in;
         n.y_prev = y_prev;
@@ -288,8 +308,7 @@ cd_status run_ffn_residual(cd_plan *p, int variant, const float *h_in, const flo
         st = launched(cdk::launch_coef(kernel_variant(variant), ca, s));
         if (st != CD_OK)
             return st;
-        p->has_state = true;
-        p->s_in_coef = false;
+        keep_state(p, B, false);
     }
     if (p->phases & CD_PHASE_DOWN) {
         const cdk::DownArgs da = down_args(p, B, Wd, y);
@@ -327,8 +346,8 @@ cd_status run_ffn_topk(cd_plan *p, int variant, const uint16_t *x, int B, const 
     hipStream_t s = reinterpret_cast<hipStream_t>(stream);
     if (!down_state_ok(p, B))
         return CD_EINVAL;
-    p->last_batch = B;
     if (p->phases & CD_PHASE_COEF) {
+        forget_state(p);
         if (variant == CD_VARIANT_DUAL_PRED) {
             st = launched(cdk::launch_latent(x, B, At, p->d_model, p->d_rank, p->lat, s));
             if (st != CD_OK)
@@ -343,8 +362,7 @@ cd_status run_ffn_topk(cd_plan *p, int variant, const uint16_t *x, int B, const 
         st = launched(cdk::launch_topk(kernel_variant(variant), ca, k, thld_out ? thld_out : p->q, s));
         if (st != CD_OK)
             return st;
-        p->has_state = true;
-        p->s_in_coef = variant == CD_VARIANT_DUAL_IDEAL;
+        keep_state(p, B, variant == CD_VARIANT_DUAL_IDEAL);
     }
     if (p->phases & CD_PHASE_DOWN) {
         const cdk::DownArgs da = down_args(p, B, Wd, y);
@@ -580,8 +598,7 @@ cd_status calibrate(cd_plan *p, int variant, const uint16_t *X, int T, const uin
                                          q + t0, s));
     }
     // the act / s workspace now describes a calibration batch, not an FFN call
-    p->last_batch = 0;
-    p->has_state = false;
+    forget_state(p);
     if (st == CD_OK)
         st = hip_status(cdk::launch_mean(q, T, thld_out, s));
     if (st == CD_OK && q_out)

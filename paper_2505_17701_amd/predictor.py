@@ -45,6 +45,14 @@ def ideal_masks(layer: dict, X, k: float):
     return masks
 
 
+def random_mask_f1(true_frac: float, pred_frac: float) -> float:
+    """Expected F1 of a predicted mask drawn independently of the true one, with the
+    given alive fractions: precision is true_frac and recall is pred_frac, so
+    F1 = 2 t p / (t + p). At a matched fraction (p = t) it equals t."""
+    t, p = float(true_frac), float(pred_frac)
+    return 2.0 * t * p / (t + p) if t + p > 0 else 0.0
+
+
 def f1_score(pred, true) -> float:
     """F1 of predicted against true alive masks (bool arrays of one shape), pooled."""
     pred = np.asarray(pred, dtype=bool)
@@ -96,11 +104,14 @@ def train_low_rank(X, masks, d_rank: int, epochs: int = 10, lr: float = 1e-3, ba
 
 def calibrated_threshold(A_t, B_t, X, k: float) -> float:
     """The Sec. 4 layerwise threshold of the predictor score s_hat at k over the
-    calibration tokens X (mean of the per-token k-quantiles of s_hat)."""
+    calibration tokens X (mean of the per-token k-quantiles of s_hat). X must be
+    held out from the predictor's training tokens: a trained predictor scores its
+    own training tokens differently, and a threshold taken there misses the target
+    alive fraction on new tokens."""
     from . import binding as cd
 
     dm = X.shape[1]
-    plan = cd.Plan(dm, B_t.shape[0], max_batch=max(1, min(8, 32768 // dm)), d_rank=A_t.shape[0])
+    plan = cd.Plan(dm, B_t.shape[0], max_batch=cd.max_batch_for(dm), d_rank=A_t.shape[0])
     th, _ = cd.countdown_calibrate(plan, cd.CD_VARIANT_DUAL_PRED, X, k, A_t=A_t, B_t=B_t)
     plan.close()
     return float(th.item())
@@ -157,7 +168,7 @@ def calibrated_threshold_tern(theta_p, X, k: float, d_ff: int) -> float:
     from . import binding as cd
 
     dm = X.shape[1]
-    plan = cd.Plan(dm, d_ff, max_batch=max(1, min(8, 32768 // dm)))
+    plan = cd.Plan(dm, d_ff, max_batch=cd.max_batch_for(dm))
     th, _ = cd.countdown_calibrate_tern(plan, X, theta_p, k)
     plan.close()
     return float(th.item())
@@ -210,3 +221,57 @@ def predicted_masks(layer: dict, A_t, B_t, X, thld: float = 0.0):
         masks[t, idx.long()] = True
     plan.close()
     return masks
+
+
+def topk_masks(layer: dict, X, k: float, A_t=None, B_t=None, theta_p=None):
+    """The predictor's alive masks at exactly the target fraction: each token keeps
+    its neurons with s_hat above its own k-quantile of s_hat (the per-token form of
+    the threshold, countdown_ffn_topk / countdown_ffn_tern_topk at batch 1), so the
+    predicted and the true masks have the same alive count. Pass A_t and B_t for the
+    low-rank predictor, theta_p (packed) for the ternary one."""
+    import torch
+
+    from . import binding as cd
+
+    T, dm = X.shape
+    dff = layer["W_up"].shape[0]
+    plan = cd.Plan(dm, dff, max_batch=1, d_rank=A_t.shape[0] if A_t is not None else 0)
+    masks = torch.zeros((T, dff), dtype=torch.bool, device=X.device)
+    for t in range(T):
+        if theta_p is not None:
+            cd.countdown_ffn_tern_topk(plan, X[t:t + 1], layer["W_gate"], layer["W_up"],
+                                       layer["W_down"], theta_p, k)
+        else:
+            cd.countdown_ffn_topk(plan, cd.CD_VARIANT_DUAL_PRED, X[t:t + 1], layer["W_gate"],
+                                  layer["W_up"], layer["W_down"], k, A_t=A_t, B_t=B_t)
+        idx, _, _ = cd.countdown_export_active(plan)
+        masks[t, idx.long()] = True
+    plan.close()
+    return masks
+
+
+def evaluate(layer: dict, X_cal, X_test, Y_test, k: float, A_t=None, B_t=None, theta_p=None):
+    """A predictor's masks on the test tokens against their ideal masks Y_test:
+
+    - at the Sec. 4 layerwise threshold calibrated on X_cal (held out from the
+      training tokens): the threshold, the realised alive fraction and F1;
+    - at the matched alive fraction (each token's own top 1 - k of s_hat): F1;
+    - beside each, the F1 a random mask of the same alive fraction would score.
+
+    Pass A_t and B_t for the low-rank predictor, theta_p for the packed ternary one."""
+    ytrue = Y_test.cpu().numpy()
+    t_frac = float(ytrue.mean())
+    d_ff = layer["W_up"].shape[0]
+    if theta_p is not None:
+        th = calibrated_threshold_tern(theta_p, X_cal, k, d_ff)
+        P = predicted_masks_tern(layer, theta_p, X_test, th).cpu().numpy()
+    else:
+        th = calibrated_threshold(A_t, B_t, X_cal, k)
+        P = predicted_masks(layer, A_t, B_t, X_test, th).cpu().numpy()
+    Pk = topk_masks(layer, X_test, k, A_t=A_t, B_t=B_t, theta_p=theta_p).cpu().numpy()
+    alive = float(P.mean())
+    return {"thld": round(th, 5), "alive_frac": round(alive, 4), "f1": round(f1_score(P, ytrue), 4),
+            "f1_random_same_alive": round(random_mask_f1(t_frac, alive), 4),
+            "matched_alive_frac": round(float(Pk.mean()), 4),
+            "f1_matched": round(f1_score(Pk, ytrue), 4),
+            "f1_random_matched": round(random_mask_f1(t_frac, float(Pk.mean())), 4)}

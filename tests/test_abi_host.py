@@ -68,6 +68,10 @@ def test_abi_version_and_status_strings(lib):
     ((4096, 11008, 0, 0), cd.CD_EINVAL),
     ((4096, 11008, 9, 0), cd.CD_EUNSUPPORTED),
     ((8192, 28672, 8, 0), cd.CD_EUNSUPPORTED),   # batch x d_model > 32768
+    ((4160, 1024, 4, 0), cd.CD_OK),              # 4 tokens x 16 chunks of 512
+    ((4160, 1024, 5, 0), cd.CD_EUNSUPPORTED),    # tile of 8 tokens x 16 chunks
+    ((4160, 1024, 7, 0), cd.CD_EUNSUPPORTED),
+    ((2056, 4104, 8, 0), cd.CD_OK),              # 8 tokens x 8 chunks
     ((4096, 14336, 1, 200), cd.CD_EUNSUPPORTED), # rank not a power of two
     ((4096, 14336, 1, -8), cd.CD_EINVAL),
 ])
@@ -260,3 +264,19 @@ def test_bench_refuses_more_than_one_gpu():
                        capture_output=True, text=True, timeout=120)
     assert r.returncode == 2
     assert "one GPU only" in r.stderr and r.stdout == ""
+
+
+@pytest.mark.parametrize("d_model,expect", [(4096, 8), (4160, 4), (8192, 4), (256, 8), (2056, 8)])
+def test_max_batch_for(lib, d_model, expect):
+    """The widest batch a plan accepts: the batch tile (1, 2, 4 or 8 tokens) times
+    d_model rounded up to a power-of-two number of 512-column chunks stays within
+    32768 token columns."""
+    assert cd.max_batch_for(d_model) == expect
+
+
+def test_plan_create_refuses_unsupported_tile_before_hip(lib):
+    """d_model 4160 at 5 tokens would need an 8-token tile of 16 chunks; plan creation
+    refuses it on the host, before any HIP call."""
+    with pytest.raises(cd.CountdownError) as e:
+        cd.Plan(4160, 1024, max_batch=5)
+    assert e.value.status == cd.CD_EUNSUPPORTED

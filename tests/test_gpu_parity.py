@@ -275,7 +275,7 @@ def test_single_active_row(tiny):
 
 @pytest.mark.parametrize("d_model,d_ff,B", [(264, 1000, 3), (1032, 520, 2), (8, 8, 1),
                                             (2056, 4104, 7), (512, 16, 4), (8192, 1048, 1),
-                                            (1544, 2056, 2), (4096, 776, 1)])
+                                            (1544, 2056, 2), (4096, 776, 1), (4160, 1000, 4)])
 @pytest.mark.parametrize("variant", ["mono", "dual_ideal", "dual_pred", "cats"])
 def test_ragged_shapes(d_model, d_ff, B, variant):
     L = make_layer(700 + d_model, d_model, d_ff, 0.05)
@@ -288,7 +288,9 @@ def test_ragged_shapes(d_model, d_ff, B, variant):
         u, g, s = oracle.coefficients(x, L["W_gate"], L["W_up"])
         c = np.abs({"mono": u, "dual_ideal": s, "cats": g / (1.0 + np.exp(-g))}[variant])
     thld = float(np.float32(np.quantile(c, 0.7)))
-    plan = plan_for(layer, max_batch=min(8, 32768 // d_model))
+    from paper_2505_17701_amd import binding as cd
+
+    plan = plan_for(layer, max_batch=cd.max_batch_for(d_model))
     compare(plan, variant, layer, x, thld, f"ragged {d_model}x{d_ff} B={B} {variant}")
 
 

@@ -1,16 +1,24 @@
 """Predictor training (Sec. 4, Alg. 1) on synthetic activations: targets from
 the HIP per-token ideal-D path, BCE + AdamW in PyTorch, inference through the
-HIP predictor path. With random synthetic weights the masks carry no low-rank
-structure, so only learning (against the untrained start) is asserted, and
-the trained predictor's index sets are checked against the oracle."""
+HIP predictor path.
+
+Each predictor is evaluated on test tokens at the Sec. 4 threshold calibrated on
+held-out tokens (neither training nor test), which must give an alive fraction
+near 1 - k, and at exactly the target alive fraction (each token's own top
+1 - k of the score), where a random mask scores F1 = 1 - k. A linear predictor
+of rank r can follow the gate only within an r-dimensional subspace, so the
+low-rank test layer gets a W_gate of rank below the predictor's; the ternary
+predictor is full rank and trains on a plain random layer. Both train for 20
+epochs (the paper's table lists 10 to 80). The trained
+predictors' index sets through the HIP path are checked against the oracle."""
 import numpy as np
 import pytest
 
 import oracle
 from gpu_support import IDX_BAND, dev_bf16
 from test_gpu_parity import Layer
-from workloads import make_layer, make_tokens
-from workloads.synth import T_CALIB
+from workloads import make_layer, make_low_rank, make_tokens
+from workloads.synth import T_CALIB, T_HELDOUT
 
 torch = pytest.importorskip("torch")
 pytestmark = pytest.mark.gpu
@@ -23,27 +31,32 @@ def _gpu():
 
 
 def test_train_low_rank_predictor():
-    from paper_2505_17701_amd.predictor import (calibrated_threshold, f1_score, ideal_masks,
-                                                 predicted_masks, train_low_rank)
+    from paper_2505_17701_amd.predictor import (evaluate, ideal_masks, predicted_masks,
+                                                 train_low_rank)
 
-    dm, dff, k = 512, 1376, 0.7
-    layer = Layer(make_layer(1600, dm, dff, 0.03))
+    dm, dff, k, rank = 512, 1376, 0.7, 64
+    L = make_layer(1600, dm, dff, 0.03)
+    L["W_gate"] = make_low_rank(1600, dff, dm, 16, 0.03)
+    layer = Layer(L)
     Xtr = dev_bf16(make_tokens(1600, 1024, dm, purpose=T_CALIB))
+    Xcal = dev_bf16(make_tokens(1600, 256, dm, purpose=T_HELDOUT))
     Xte_h = make_tokens(1601, 64, dm)
     Xte = dev_bf16(Xte_h)
     Ytr = ideal_masks(layer.d, Xtr, k)
     Yte = ideal_masks(layer.d, Xte, k)
     assert abs(Ytr.float().mean().item() - (1 - k)) < 0.01
-    A0, B0, _ = train_low_rank(Xtr, Ytr, 64, epochs=0)
-    A, B, log = train_low_rank(Xtr, Ytr, 64, epochs=6)
+    A0, B0, _ = train_low_rank(Xtr, Ytr, rank, epochs=0)
+    A, B, log = train_low_rank(Xtr, Ytr, rank, epochs=20)
     assert log["epoch_loss"][-1] < log["epoch_loss"][0]
-    scores = {}
-    for name, (At, Bt) in (("start", (A0, B0)), ("trained", (A, B))):
-        th = calibrated_threshold(At, Bt, Xtr[:256], k)
-        P = predicted_masks(layer.d, At, Bt, Xte, th)
-        scores[name] = f1_score(P.cpu().numpy(), Yte.cpu().numpy())
-    print(f"F1 on S^{k}: start {scores['start']:.3f} trained {scores['trained']:.3f}", flush=True)
-    assert scores["trained"] > scores["start"] + 0.02
+    r = {name: evaluate(layer.d, Xcal, Xte, Yte, k, A_t=At, B_t=Bt)
+         for name, (At, Bt) in (("start", (A0, B0)), ("trained", (A, B)))}
+    print(f"low-rank on S^{k}: {r}", flush=True)
+    for v in r.values():  # the held-out threshold lands near the target alive fraction
+        assert abs(v["alive_frac"] - (1 - k)) < 0.05
+        assert abs(v["matched_alive_frac"] - (1 - k)) < 0.002
+    assert r["trained"]["f1_matched"] > r["trained"]["f1_random_matched"] + 0.05
+    assert r["trained"]["f1_matched"] > r["start"]["f1_matched"] + 0.05
+    assert r["trained"]["f1"] > r["trained"]["f1_random_same_alive"] + 0.05
     # the HIP predictor path on the trained weights matches the oracle's index sets
     Ah = A.view(torch.int16).cpu().numpy().view(np.uint16)
     Bh = B.view(torch.int16).cpu().numpy().view(np.uint16)
@@ -61,30 +74,30 @@ def test_train_low_rank_predictor():
 def test_train_ternary_predictor():
     """The ternary predictor (Sec. 6) trained by Alg. 1 with the straight-through
     estimator; inference through the HIP ternary path."""
-    from paper_2505_17701_amd.predictor import (calibrated_threshold_tern, f1_score, ideal_masks,
-                                                 packed_ternary, predicted_masks_tern,
-                                                 train_ternary)
+    from paper_2505_17701_amd.predictor import (evaluate, ideal_masks, packed_ternary,
+                                                 predicted_masks_tern, train_ternary)
     from workloads import make_ternary
 
     dm, dff, k = 512, 1376, 0.7
     layer = Layer(make_layer(1610, dm, dff, 0.03))
     Xtr = dev_bf16(make_tokens(1610, 1024, dm, purpose=T_CALIB))
+    Xcal = dev_bf16(make_tokens(1610, 256, dm, purpose=T_HELDOUT))
     Xte_h = make_tokens(1611, 64, dm)
     Xte = dev_bf16(Xte_h)
     Ytr = ideal_masks(layer.d, Xtr, k)
     Yte = ideal_masks(layer.d, Xte, k)
-    T, log = train_ternary(Xtr, Ytr, epochs=6)
+    T, log = train_ternary(Xtr, Ytr, epochs=20)
     assert T.dtype == np.int8 and set(np.unique(T)) <= {-1, 0, 1}
     assert log["epoch_loss"][-1] < log["epoch_loss"][0]
-    scores = {}
-    for name, theta in (("random", make_ternary(1610, dm, dff)), ("trained", T)):
-        tp = packed_ternary(theta)
-        th = calibrated_threshold_tern(tp, Xtr[:256], k, dff)
-        P = predicted_masks_tern(layer.d, tp, Xte, th)
-        scores[name] = f1_score(P.cpu().numpy(), Yte.cpu().numpy())
-    print(f"ternary F1 on S^{k}: random {scores['random']:.3f} trained {scores['trained']:.3f} "
-          f"zeros {log['zero_frac']:.2f}", flush=True)
-    assert scores["trained"] > scores["random"] + 0.02
+    r = {name: evaluate(layer.d, Xcal, Xte, Yte, k, theta_p=packed_ternary(theta))
+         for name, theta in (("random", make_ternary(1610, dm, dff)), ("trained", T))}
+    print(f"ternary on S^{k}: {r} zeros {log['zero_frac']:.2f}", flush=True)
+    for v in r.values():
+        assert abs(v["alive_frac"] - (1 - k)) < 0.05
+        assert abs(v["matched_alive_frac"] - (1 - k)) < 0.002
+    # ternarisation leaves less to learn (CPU runs of the same recipe: 0.35 against 0.30)
+    assert r["trained"]["f1_matched"] > r["trained"]["f1_random_matched"] + 0.025
+    assert r["trained"]["f1_matched"] > r["random"]["f1_matched"] + 0.025
     tp = packed_ternary(T)
     P0 = predicted_masks_tern(layer.d, tp, Xte[:4], 0.0).cpu().numpy()
     for t in range(4):

@@ -11,6 +11,7 @@ from .synth import (  # noqa: F401
     bf16_round,
     bf16_to_f32,
     make_layer,
+    make_low_rank,
     make_predictor,
     make_ternary,
     make_tokens,

@@ -33,6 +33,9 @@ ROOT_SEED = 42
 # tensor ids inside a spawn key
 T_GATE, T_UP, T_DOWN, T_A, T_B, T_TERN = 0, 1, 2, 3, 4, 5
 T_CALIB, T_EVAL, T_OUTLIER, T_RESID = 10, 11, 12, 13
+# held-out calibration tokens of a trained predictor (neither its training nor its test set)
+T_HELDOUT = 14
+T_LOWRANK = 15
 
 
 def stream(*key: int) -> np.random.Generator:
@@ -96,6 +99,18 @@ def make_predictor(wid: int, d_model: int, d_rank: int, d_ff: int, sigma: float,
         "A_t": _normal_bf16(stream(wid, layer, T_A, copy), (d_rank, d_model), sigma),
         "B_t": _normal_bf16(stream(wid, layer, T_B, copy), (d_ff, d_rank), sigma),
     }
+
+
+def make_low_rank(wid: int, rows: int, cols: int, rank: int, sigma: float, layer: int = 0,
+                  tensor: int = T_GATE) -> np.ndarray:
+    """A seeded ``[rows, cols]`` bf16 matrix of rank at most ``rank`` (before rounding):
+    ``P @ Q`` with ``P [rows, rank]`` and ``Q [rank, cols]`` i.i.d. normal, scaled so that
+    entries have standard deviation ``sigma``. A layer whose W_gate has low rank gives a
+    predictor of matching rank something it can represent."""
+    rng = stream(wid, layer, T_LOWRANK, tensor)
+    P = rng.standard_normal(size=(rows, rank), dtype=np.float32)
+    Q = rng.standard_normal(size=(rank, cols), dtype=np.float32)
+    return bf16_round((P @ Q) * np.float32(sigma / np.sqrt(rank)))
 
 
 def make_ternary(wid: int, d_model: int, d_ff: int, zero_frac: float = 1 / 3, layer: int = 0,
