@@ -119,6 +119,27 @@ cd_status countdown_ffn_dual(cd_plan *plan, const uint16_t *x, int B, const uint
                              const uint16_t *W_up, const uint16_t *W_down, const uint16_t *A_t,
                              const uint16_t *B_t, float thld, float *y, void *stream);
 
+/*
+ * countdown_ffn_mono without a plan, for callers that cannot allocate device
+ * memory (code under HIP graph capture, tight serving loops, harnesses that
+ * forbid hipMalloc). It computes exactly what countdown_ffn_mono computes, with
+ * the same kernels, and allocates nothing: the per-neuron workspace (active
+ * flags and s) lives in a static device array of the library, 1.125 MiB per
+ * device (d_ff <= 32768 at up to 8 tokens), held on each device the library
+ * runs on until the process ends. Its device address is looked up on the first
+ * call made with that device current.
+ * x [B][d_model], W_gate / W_up / W_down [d_ff][d_model] bf16; y [B][d_model]
+ * fp32, overwritten; all device pointers owned by the caller, 16-byte aligned.
+ * Shape rules as countdown_plan_create with max_batch = B and d_rank = 0, plus
+ * d_ff <= 32768 (CD_EUNSUPPORTED beyond); argument errors as countdown_ffn_mono.
+ * All calls on one device share the array: calls that overlap in time on one
+ * device (two streams, two host threads) race and must not be made. Enqueued
+ * on `stream`; no host synchronisation.
+ */
+cd_status countdown_ffn_mono_noalloc(const uint16_t *x, int B, const uint16_t *W_gate,
+                                     const uint16_t *W_up, const uint16_t *W_down, int d_model,
+                                     int d_ff, float thld, float *y, void *stream);
+
 /* Dense Gated-MLP (Eq. 1) through the same kernels with every row active:
  * the reference the sparse variants are timed against. */
 cd_status countdown_ffn_dense(cd_plan *plan, const uint16_t *x, int B, const uint16_t *W_gate,
@@ -306,7 +327,7 @@ cd_status countdown_check_shape(int d_model, int d_ff, int max_batch, int d_rank
 const char *countdown_status_string(cd_status status);
 
 /* ABI version of this header (bumped on any signature change). */
-#define COUNTDOWN_ABI_VERSION 8
+#define COUNTDOWN_ABI_VERSION 9
 int countdown_abi_version(void);
 
 #ifdef __cplusplus

@@ -23,6 +23,7 @@ CD_PHASE_COEF, CD_PHASE_DOWN, CD_PHASE_ALL = 1, 2, 3
 # every symbol include/countdown.h declares
 EXPORTS = (
     "countdown_plan_create", "countdown_plan_destroy", "countdown_ffn_mono", "countdown_ffn_dual",
+    "countdown_ffn_mono_noalloc",
     "countdown_ffn_dense", "countdown_ffn_cats", "countdown_ffn_topk", "countdown_ffn_residual",
     "countdown_calibrate", "countdown_ffn_tern", "countdown_ffn_tern_topk",
     "countdown_calibrate_tern", "countdown_ternary_words", "countdown_ternary_pack",
@@ -55,6 +56,7 @@ def load_library(path: str = LIB_PATH):
         "countdown_plan_destroy": (i, [vp]),
         "countdown_ffn_mono": (i, [vp, vp, i, vp, vp, vp, f, vp, vp]),
         "countdown_ffn_dual": (i, [vp, vp, i, vp, vp, vp, vp, vp, f, vp, vp]),
+        "countdown_ffn_mono_noalloc": (i, [vp, i, vp, vp, vp, i, i, f, vp, vp]),
         "countdown_ffn_dense": (i, [vp, vp, i, vp, vp, vp, vp, vp]),
         "countdown_ffn_cats": (i, [vp, vp, i, vp, vp, vp, f, vp, vp]),
         "countdown_ffn_residual": (i, [vp, i, vp, vp, vp, f, vp, i, vp, vp, vp, vp, vp, f, vp,
@@ -207,6 +209,25 @@ def countdown_ffn_mono(plan: Plan, x, W_gate, W_up, W_down, thld: float, y=None,
         plan.handle, _ptr(_bf16(x)), B, _ptr(_bf16(W_gate)), _ptr(_bf16(W_up)),
         _ptr(_bf16(W_down)), float(thld), _ptr(y), _stream(stream)), "countdown_ffn_mono")
     plan.last_batch = B
+    return y
+
+
+def countdown_ffn_mono_noalloc(x, W_gate, W_up, W_down, thld: float, y, stream=None):
+    """M-CountDown without a plan (the library's static workspace); y [B, d_model] fp32
+    must be given (nothing is allocated). Returns y."""
+    for t, name in ((x, "x"), (W_gate, "W_gate"), (W_up, "W_up"), (W_down, "W_down")):
+        if t is None or t.dim() != 2:
+            raise ValueError(f"{name} must be a 2-D tensor")
+    if y is None:
+        raise ValueError("y must be given: countdown_ffn_mono_noalloc allocates nothing")
+    B, dm = x.shape
+    dff = W_up.shape[0]
+    for t, name in ((W_gate, "W_gate"), (W_up, "W_up"), (W_down, "W_down")):
+        _shape(t, (dff, dm), name)
+    _shape(_f32(y), (B, dm), "y")
+    _check(load_library().countdown_ffn_mono_noalloc(
+        _ptr(_bf16(x)), B, _ptr(_bf16(W_gate)), _ptr(_bf16(W_up)), _ptr(_bf16(W_down)), dm, dff,
+        float(thld), _ptr(y), _stream(stream)), "countdown_ffn_mono_noalloc")
     return y
 
 

@@ -5,6 +5,7 @@
 #include <cmath>
 #include <cstdint>
 #include <cstdlib>
+#include <mutex>
 #include <new>
 #include <vector>
 
@@ -723,3 +724,82 @@ cd_status countdown_plan_set_phases(cd_plan *p, unsigned phases)
 }
 
 }  // extern "C"
+
+// ------------------------------------------------- entry point without allocation
+// countdown_ffn_mono_noalloc keeps the per-neuron workspace of a call (the
+// active flags and the coefficients s of the active neurons) in this
+// file-scope device array instead of a plan's hipMalloc'd buffers. Each device
+// the library runs on holds its own copy until the process ends; its address
+// on the current device comes from hipGetSymbolAddress on the first call made
+// there (the name itself is a host-side stand-in, never passed to a kernel).
+namespace {
+
+constexpr int kNoallocMaxDff = 32768;
+constexpr size_t kNoallocActBytes = (size_t)kNoallocMaxDff * sizeof(int);
+constexpr size_t kNoallocBytes = kNoallocActBytes + (size_t)kMaxBatch * kNoallocMaxDff * sizeof(float);
+constexpr int kNoallocMaxDevices = 64;
+
+}  // namespace
+
+static __device__ __align__(256) unsigned char scratch[kNoallocBytes];
+
+namespace {
+
+std::mutex g_scratch_mutex;
+void *g_scratch_ptr[kNoallocMaxDevices];  // per device, set once
+
+// Device address of the scratch array on the current device.
+cd_status scratch_on_current_device(int *dev_out, void **out)
+{
+    int dev = -1;
+    if (hipGetDevice(&dev) != hipSuccess)
+        return CD_EHIP;
+    if (dev < 0 || dev >= kNoallocMaxDevices)
+        return CD_EUNSUPPORTED;
+    std::lock_guard<std::mutex> lock(g_scratch_mutex);
+    if (!g_scratch_ptr[dev]) {
+        void *p = nullptr;
+        const hipError_t e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+        if (e != hipSuccess || !p)
+            return CD_EHIP;
+        g_scratch_ptr[dev] = p;
+    }
+    *dev_out = dev;
+    *out = g_scratch_ptr[dev];
+    return CD_OK;
+}
+
+}  // namespace
+
+extern "C" cd_status countdown_ffn_mono_noalloc(const uint16_t *x, int B, const uint16_t *W_gate,
+                                                const uint16_t *W_up, const uint16_t *W_down,
+                                                int d_model, int d_ff, float thld, float *y,
+                                                void *stream)
+{
+    // the shape and arguments first, on the host (run_ffn checks them again)
+    cd_status st = check_args(CD_VARIANT_MONO, d_model, d_ff, B < 1 ? 1 : B, 0, x, B, W_gate,
+                              W_up, W_down, nullptr, nullptr, thld, y);
+    if (st != CD_OK)
+        return st;
+    if (d_ff > kNoallocMaxDff)
+        return CD_EUNSUPPORTED;
+    int dev = -1;
+    void *ws = nullptr;
+    if ((st = scratch_on_current_device(&dev, &ws)) != CD_OK)
+        return st;
+    // A plan on the stack whose workspace is the scratch array: act [d_ff], then
+    // s [B][d_ff]. The coefficient kernel writes every act and zeroes y, and s is
+    // read only where act is set, so nothing needs clearing between calls.
+    cd_plan p{};
+    p.d_model = d_model;
+    p.d_ff = d_ff;
+    p.max_batch = B;
+    p.d_rank = 0;
+    p.flags = 0;
+    p.device = dev;
+    p.act = static_cast<int *>(ws);
+    p.s = reinterpret_cast<float *>(static_cast<unsigned char *>(ws) + kNoallocActBytes);
+    p.phases = CD_PHASE_ALL;
+    return run_ffn(&p, CD_VARIANT_MONO, x, B, W_gate, W_up, W_down, nullptr, nullptr, thld, y,
+                   stream);
+}

@@ -50,7 +50,7 @@ def test_header_compiles_as_c():
 
 
 def test_abi_version_and_status_strings(lib):
-    assert cd.countdown_abi_version() == 8
+    assert cd.countdown_abi_version() == 9
     for st in (cd.CD_OK, cd.CD_EINVAL, cd.CD_EUNSUPPORTED, cd.CD_EHIP, cd.CD_ENOMEM):
         assert cd.status_string(st).startswith(("CD_OK", "CD_E"))
     assert "unknown" in cd.status_string(12345)
