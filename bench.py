@@ -3,13 +3,16 @@
 
 A step is one decode token through one FFN layer on the HIP path: the
 coefficient kernel (dense W_up projection, threshold, compaction, gathered
-gate rows) and the gathered down projection. Default workload: the
-Llama-7B-shaped layer (d_model 4096, d_ff 11008, bf16 weights N(0, 0.02^2),
-1% outlier input channels x20, batch 1), M-CountDown at sparsity k = 0.9 with
-the layerwise threshold calibrated on the GPU from 256 seeded tokens.
-Weights are rotated over several independent copies (> 1 GB in total) so
-the 256 MB Infinity Cache cannot serve them; inputs are resident in HBM
-before the timed region starts.
+gate rows) and the gathered down projection. Default workload (the largest
+single-GPU configuration): the 70B-shaped layer (d_model 8192, d_ff 28672,
+bf16 weights N(0, 0.015^2), 1.41 GB, batch 1), M-CountDown at sparsity k = 0.9
+with the layerwise threshold calibrated on the GPU from 256 seeded tokens.
+Secondary lines: the Llama-7B-shaped layer (M, ideal D, CATS, per-token
+thresholds, dense), the Llama-3-8B-shaped layer with the low-rank and ternary
+predictors at batch 1/4/8, the 32-layer stack, predictor training. Weights
+are rotated over enough independent copies (> 1 GB in total) that the 256 MB
+Infinity Cache cannot serve them; inputs are resident in HBM before the timed
+region starts.
 
 Prints ONE JSON line on stdout; progress goes to stderr.
 """
@@ -29,7 +32,16 @@ sys.path.insert(0, ROOT)
 HBM_PEAK_GBS = 8000.0  # MI355X HBM3E peak, GB/s
 KERNEL_SRCS = [os.path.join(ROOT, "paper_2505_17701_amd", "csrc", f)
                for f in ("cd_kernels.hip", "cd_device.hpp", "cd_internal.hpp")]
-TRAFFIC_SUMMARY = os.path.join(ROOT, "profiles", "k_coef_mono_llama7b_4096x11008_k0.9_traffic.md")
+# committed FETCH_SIZE / WRITE_SIZE summaries of a line's dominant kernel(s), by
+# (workload, variant, k, batch)
+TRAFFIC_SUMMARIES = {
+    ("llama70b_8192x28672", "mono", 0.9, 1): "k_coef_mono_llama70b_8192x28672_k0.9_traffic.md",
+    ("llama7b_4096x11008", "mono", 0.9, 1): "k_coef_mono_llama7b_4096x11008_k0.9_traffic.md",
+    ("llama3_8b_4096x14336_pred", "dual_pred", 0.9, 1):
+        "k_coef_pred_llama3_8b_4096x14336_k0.9_b1_traffic.md",
+    ("llama3_8b_4096x14336_pred", "dual_pred", 0.9, 8):
+        "k_coef_pred_mfma_llama3_8b_4096x14336_k0.9_b8_traffic.md",
+}
 
 
 def log(*a):
@@ -47,14 +59,15 @@ def parse():
     p.add_argument("--gpus", type=int, default=1)
     p.add_argument("--steps", type=int, default=2000)
     p.add_argument("--warmup", type=int, default=200)
-    p.add_argument("--workload", default="llama7b_4096x11008")
+    p.add_argument("--workload", default="llama70b_8192x28672")
     p.add_argument("--variant", default="mono",
                    choices=["mono", "dual_ideal", "dual_pred", "dual_tern", "dense", "cats",
                             "mono_topk", "dual_ideal_topk", "dual_pred_topk", "dual_tern_topk",
                             "cats_topk"])
     p.add_argument("--batch", type=int, default=1, help="decode tokens per call (union IDX)")
     p.add_argument("--k", type=float, default=0.9)
-    p.add_argument("--copies", type=int, default=4, help="independent weight copies rotated")
+    p.add_argument("--copies", type=int, default=0,
+                   help="independent weight copies rotated (0: enough for more than 1 GB)")
     p.add_argument("--tokens", type=int, default=64, help="distinct eval tokens rotated")
     p.add_argument("--calib-tokens", type=int, default=256)
     p.add_argument("--cpu-seconds", type=float, default=12.0,
@@ -62,7 +75,9 @@ def parse():
     p.add_argument("--no-extra", action="store_true",
                    help="skip the secondary variants and the other workloads")
     p.add_argument("--no-other", action="store_true",
-                   help="skip the 8B-predictor, 70B and 32-layer stack workloads")
+                   help="skip the other workloads (7B, 8B-predictor, 70B, stack, training)")
+    p.add_argument("--no-7b", action="store_true", help="skip the 7B-shaped layer's lines")
+    p.add_argument("--no-8b", action="store_true", help="skip the 8B predictor layer's lines")
     p.add_argument("--no-stack", action="store_true", help="skip the 32-layer stack")
     p.add_argument("--no-train", action="store_true", help="skip the predictor-training run")
     p.add_argument("--traffic-probe", action="store_true",
@@ -86,13 +101,16 @@ def kernel_source_digest():
     return h.hexdigest()
 
 
-def measured_traffic():
-    """HBM bytes per launch of the dominant kernel from the committed FETCH_SIZE /
-    WRITE_SIZE summary, or None when the kernel source changed since it was taken."""
-    if not os.path.exists(TRAFFIC_SUMMARY):
+def measured_traffic(key):
+    """HBM bytes per launch of a line's dominant kernel(s) from the committed
+    FETCH_SIZE / WRITE_SIZE summary, or None when there is none or the kernel
+    source changed since it was taken."""
+    name = TRAFFIC_SUMMARIES.get(key)
+    path = os.path.join(ROOT, "profiles", name) if name else None
+    if not path or not os.path.exists(path):
         return None
     fields = {}
-    for line in open(TRAFFIC_SUMMARY):
+    for line in open(path):
         if ":" in line and line.startswith("- "):
             k, v = line[2:].split(":", 1)
             fields[k.strip()] = v.strip().strip("`")
@@ -419,31 +437,149 @@ def optimal_dense_us(ctx, k, steps):
     return ms * 1e3
 
 
-def other_workloads(args):
-    """The remaining single-layer shapes: Llama-3-8B-shaped layer with the low-rank
-    predictor at batch 1/4/8, and the 70B-shaped layer (M-CountDown k 0.9 / 0.7
-    beside the dense FFN)."""
+def kernel_desc(variant, B=1):
+    """The kernel(s) of a line's coefficient phase, the dominant part of every call."""
+    pred = "k_coef_pred_mfma" if B >= 5 else "k_coef_pred"
+    tern = "k_coef_tern_mfma" if B >= 5 else "k_coef_tern"
+    return {"mono": "k_coef_mono (dense W_up GEMV, threshold, wave-local W_gate gather, s)",
+            "dual_ideal": "k_coef_dual (dense W_gate + W_up GEMV, s, threshold)",
+            "dual_pred": f"k_latent + {pred} (predictor latent, scores, threshold, block-local "
+                         "W_gate / W_up gather, s)",
+            "dense": "k_coef_dual (dense W_gate + W_up GEMV, s)",
+            "mono_topk": "k_coef_mono + k_topk_select + k_gather_topk (per-token threshold)",
+            "dual_ideal_topk": "k_coef_dual + k_topk_select (per-token threshold; the select "
+                               "sets the flags, s is the coefficient)",
+            "dual_pred_topk": f"k_latent + {pred} + k_topk_select + k_gather_topk (per-token "
+                              "threshold)",
+            "cats": "k_coef_mono<CATS> (dense W_gate GEMV, SiLU, threshold, W_up gather)",
+            "cats_topk": "k_coef_mono<CATS> + k_topk_select + k_gather_topk (per-token "
+                         "threshold)",
+            "dual_tern": f"{tern} (ternary predictor scores, threshold, block-local W_gate / "
+                         "W_up gather, s)",
+            "dual_tern_topk": f"{tern} + k_topk_select + k_gather_topk (per-token threshold)"
+            }[variant]
+
+
+def roofline(res, variant, key, ceiling=None):
+    """Roofline object of a line: the coefficient phase (its dominant kernel, with the
+    predictor's latent launch where there is one): algorithmic bytes per launch over
+    the launch's average duration, both measured in this run; traffic from the
+    committed PMC summary of the same kernel source, or None."""
+    kb, kus = res["coef_kernel_bytes"], res["coef_kernel_us"]
+    ach = kb / (kus * 1e-6) / 1e9
+    obj = {"bound": "hbm", "kernel": kernel_desc(variant, res["batch"]), "achieved": ach,
+           "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": ach / HBM_PEAK_GBS,
+           "traffic": measured_traffic(key), "bytes_per_launch": kb, "avg_launch_us": kus}
+    if ceiling:
+        # measured read ceilings: a plain read of one rotated W_up per launch, and of 1 GiB
+        obj.update({"stream_W_up_GBs": ceiling["W_up"]["GBs"],
+                    "stream_1GiB_GBs": ceiling["1GiB"]["GBs"],
+                    "frac_of_stream_1GiB": ach / ceiling["1GiB"]["GBs"]})
+    return obj
+
+
+def auto_copies(w):
+    """Weight copies to rotate: enough that they exceed 1 GB (the 256 MB Infinity Cache
+    then serves none of a call's weight bytes)."""
+    per = 3 * w.d_ff * w.d_model * 2 + (w.d_rank * (w.d_model + w.d_ff) * 2 if w.d_rank else 0)
+    return max(1, -(-1_000_000_000 // per))
+
+
+def workload_lines(ctx, args, skip):
+    """The secondary lines of the 7B- and 70B-shaped layers (batch 1): the dense FFN and
+    the other variants and sparsities of the workload, with speedups over dense beside
+    the ideal byte ratio."""
     from paper_2505_17701_amd import traffic
+
+    w = ctx.w
+    if w.name == "llama7b_4096x11008":
+        todo = (("mono", 0.9), ("dense", None), ("dual_ideal", 0.9), ("mono", 0.7), ("mono", 0.5),
+                ("cats", 0.9), ("mono_topk", 0.9), ("dual_ideal_topk", 0.9), ("cats_topk", 0.9))
+    elif w.name == "llama70b_8192x28672":
+        todo = (("mono", 0.9), ("mono", 0.7), ("dense", None))
+    else:
+        return {}, {}
+    n = max(100 if w.d_model > 4096 else 200, args.steps // 4)
+    lines, res = {}, {}
+    for variant, k in todo:
+        name = variant + ("" if k is None else f"@k={k}")
+        if (variant, k) == skip:
+            continue
+        res[name] = ctx.measure(variant, k, 1, n, 30)
+        lines[name] = brief(res[name])
+        log(f"[bench] {w.name} {name}: {json.dumps(lines[name])}")
+    dense = res.get("dense")
+    if dense:
+        dense_b = traffic.algorithmic_bytes("dense", w.d_model, w.d_ff, w.d_ff)["total"]
+        for name, r in res.items():
+            if name != "dense":
+                lines[name]["speedup_vs_dense"] = dense["us_per_layer"] / r["us_per_layer"]
+                lines[name]["ideal_byte_ratio"] = dense_b / r["algorithmic_bytes"]
+    if w.name == "llama7b_4096x11008":
+        # mask agreement of u and h with s (CIF / CAF) on the layer's eval tokens
+        from paper_2505_17701_amd.metrics import cif_caf, masks_on_gpu
+
+        lines["cif_caf"] = {}
+        for k in (0.5, 0.7, 0.9):
+            m = cif_caf(*masks_on_gpu(ctx.layers[0], ctx.X_eval[:32], k))
+            lines["cif_caf"][f"k={k}"] = {kk: round(v, 4) for kk, v in m.items()}
+        log(f"[bench] CIF/CAF: {json.dumps(lines['cif_caf'])}")
+    return lines, res
+
+
+def layer_block(args, wname):
+    """A single-layer workload that is not the headline: its M-CountDown k 0.9 line
+    with a roofline object and the read ceilings, then its other lines."""
     from workloads import WORKLOADS
 
-    out = {}
+    w = WORKLOADS[wname]
+    variants = ["mono", "dual_ideal", "cats"] if w.name == "llama7b_4096x11008" else ["mono"]
+    ctx = Context(w, auto_copies(w), args.tokens, args.calib_tokens, list(w.ks),
+                  max_batch=1, variants=variants)
+    r = ctx.measure("mono", 0.9, 1, max(200 if w.d_model <= 4096 else 100, args.steps), 30,
+                    replays=True)
+    ceiling = stream_ceiling(ctx, min(max(args.steps, 64), 512))
+    lines, res = workload_lines(ctx, args, ("mono", 0.9))
+    dense = res.get("dense")
+    out = {"mono@k=0.9": {**brief(r), "us_per_layer_median_of_6": r["us_per_layer_median_of_6"],
+                          "roofline": roofline(r, "mono", (w.name, "mono", 0.9, 1), ceiling)},
+           **lines, "stream_ceiling": ceiling}
+    if dense:
+        from paper_2505_17701_amd import traffic
+
+        out["mono@k=0.9"]["speedup_vs_dense"] = dense["us_per_layer"] / r["us_per_layer"]
+        out["mono@k=0.9"]["ideal_byte_ratio"] = (traffic.algorithmic_bytes(
+            "dense", w.d_model, w.d_ff, w.d_ff)["total"] / r["algorithmic_bytes"])
+    log(f"[bench] {w.name} mono@k=0.9: {json.dumps(out['mono@k=0.9'])}")
+    ctx.free()
+    return out
+
+
+def eight_b_block(args):
+    """The Llama-3-8B-shaped layer with the low-rank predictor at batch 1/4/8 (each with
+    a roofline object), the per-token form, the ternary predictor, dense, and the
+    paper's kernel-speed comparison across sparsity at this shape."""
+    from workloads import WORKLOADS
+
     w = WORKLOADS["llama3_8b_4096x14336_pred"]
     sweep_ks = (0.5, 0.6, 0.7, 0.8, 0.9)
-    ctx = Context(w, 4, 64, args.calib_tokens, list(sweep_ks), max_batch=8,
+    ctx = Context(w, auto_copies(w), 64, args.calib_tokens, list(sweep_ks), max_batch=8,
                   variants=["dual_pred", "dual_tern", "mono", "cats"])
     r8 = {}
+    n = max(200, args.steps // 4)
     for B in w.batches:
-        r = ctx.measure("dual_pred", 0.9, B, max(200, args.steps // 4), 50)
-        r8[f"B={B}"] = brief(r)
+        r = ctx.measure("dual_pred", 0.9, B, n, 50)
+        r8[f"B={B}"] = {**brief(r), "roofline": roofline(r, "dual_pred",
+                                                         (w.name, "dual_pred", 0.9, B))}
         log(f"[bench] {w.name} dual_pred B={B}: {json.dumps(r8[f'B={B}'])}")
-    r = ctx.measure("dual_pred_topk", 0.9, 1, max(200, args.steps // 4), 50)
+    r = ctx.measure("dual_pred_topk", 0.9, 1, n, 50)
     r8["per-token k=0.9 B=1"] = brief(r)
     log(f"[bench] {w.name} dual_pred per-token B=1: {json.dumps(r8['per-token k=0.9 B=1'])}")
     for B in w.batches:  # the ternary predictor (Sec. 6) in the low-rank one's place
-        r = ctx.measure("dual_tern", 0.9, B, max(200, args.steps // 4), 50)
+        r = ctx.measure("dual_tern", 0.9, B, n, 50)
         r8[f"ternary B={B}"] = brief(r)
         log(f"[bench] {w.name} dual_tern B={B}: {json.dumps(r8[f'ternary B={B}'])}")
-    r = ctx.measure("dense", None, 1, max(200, args.steps // 4), 50)
+    r = ctx.measure("dense", None, 1, n, 50)
     r8["dense B=1"] = brief(r)
     for B in w.batches:
         r8[f"B={B}"]["speedup_vs_dense_B1"] = r["us_per_layer"] / r8[f"B={B}"]["us_per_layer"]
@@ -459,20 +595,7 @@ def other_workloads(args):
         log(f"[bench] {w.name} kernel speed k={k} (us per layer): {json.dumps(row)}")
     r8["kernel_speed_sweep"] = sweep
     ctx.free()
-    out[w.name] = r8
-
-    w = WORKLOADS["llama70b_8192x28672"]
-    ctx = Context(w, 1, 16, args.calib_tokens, list(w.ks), max_batch=1)
-    r70 = {}
-    for variant, k in (("mono", 0.9), ("mono", 0.7), ("dense", None)):
-        r = ctx.measure(variant, k, 1, max(100, args.steps // 8), 20)
-        r70[variant + ("" if k is None else f"@k={k}")] = brief(r)
-        log(f"[bench] {w.name} {variant} k={k}: {json.dumps(brief(r))}")
-    for key in ("mono@k=0.9", "mono@k=0.7"):
-        r70[key]["speedup_vs_dense"] = r70["dense"]["us_per_layer"] / r70[key]["us_per_layer"]
-    ctx.free()
-    out[w.name] = r70
-    return out
+    return r8
 
 
 def predictor_training_bench(args, n_train=8192, n_cal=256, n_test=256, epochs=4):
@@ -541,7 +664,7 @@ def predictor_training_bench(args, n_train=8192, n_cal=256, n_test=256, epochs=4
     return out
 
 
-def stack_bench(args, steps_tokens=128, warmup_tokens=8):
+def stack_bench(args, steps_tokens=128, warmup_tokens=8, dense_layer_us=None):
     """The 32-layer stack of 7B-shaped predictor layers joined by the residual stream
     (h += y, x = bf16(RMSNorm(h))): per-layer thresholds calibrated at k on 256 seeded
     tokens propagated through the dense stack, then 128 independent decode tokens at
@@ -638,8 +761,8 @@ def stack_bench(args, steps_tokens=128, warmup_tokens=8):
     n = n_arr.cpu().numpy()
     from paper_2505_17701_amd import traffic
 
-    tok_bytes = sum(traffic.algorithmic_bytes("dual_pred", dm, dff, int(v), d_rank=dr)["total"]
-                    for v in n)
+    per = [traffic.algorithmic_bytes("dual_pred", dm, dff, int(v), d_rank=dr) for v in n]
+    tok_bytes = sum(p["total"] for p in per)
     dense_bytes = nl * traffic.algorithmic_bytes("dense", dm, dff, dff)["total"]
     r = res["dual_pred"]
     r["algorithmic_bytes_per_token"] = tok_bytes
@@ -649,12 +772,101 @@ def stack_bench(args, steps_tokens=128, warmup_tokens=8):
     r["realised_sparsity"] = float(1 - n.mean() / dff)
     r["speedup_vs_dense"] = res["dense"]["us_per_token"] / r["us_per_token"]
     r["ideal_byte_ratio"] = dense_bytes / tok_bytes
+    # the dense stack runs its residual RMSNorm as a kernel of its own, while the
+    # predictor path folds it into the latent kernel: the speedup is also given against
+    # 32 single dense layers (no residual stream) timed in this run
+    if dense_layer_us:
+        r["dense_layer_us"] = dense_layer_us
+        r["speedup_vs_32_dense_layers"] = nl * dense_layer_us / r["us_per_token"]
+
+    # the coefficient phase alone (k_latent_norm + k_coef_pred of every layer) and the
+    # down kernel alone (on the last coefficient call's rows), each as one graph of
+    # tokens x layers with the plan's phase selection and one event pair
+    def phase_us(phases, ntok):
+        cd.countdown_plan_set_phases(plan, phases)
+        for i in range(2):
+            token(i, cd.CD_VARIANT_DUAL_PRED)
+        torch.cuda.synchronize()
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g):
+            for i in range(ntok):
+                token(i, cd.CD_VARIANT_DUAL_PRED)
+        g.replay()
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        g.replay()
+        e1.record()
+        torch.cuda.synchronize()
+        del g
+        cd.countdown_plan_set_phases(plan, cd.CD_PHASE_ALL)
+        return e0.elapsed_time(e1) * 1e3 / (ntok * nl)
+
+    coef_us = phase_us(cd.CD_PHASE_COEF, 32)
+    down_us = phase_us(cd.CD_PHASE_DOWN, 32)
+    coef_b = float(np.mean([p["coef"] + p["latent"] for p in per]))
+    ach = coef_b / (coef_us * 1e-6) / 1e9
+    r["coef_phase_us_per_layer"] = coef_us
+    r["down_kernel_us_per_layer"] = down_us
+    r["roofline"] = {"bound": "hbm", "kernel": "k_latent_norm + k_coef_pred (residual + "
+                     "RMSNorm, predictor latent, scores, threshold, W_gate / W_up gather, s)",
+                     "achieved": ach, "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                     "frac": ach / HBM_PEAK_GBS, "traffic": None, "bytes_per_launch": coef_b,
+                     "avg_launch_us": coef_us}
     plan.close()
     del layers
     torch.cuda.empty_cache()
     log(f"[bench] stack: {json.dumps(res)}")
     return {"workload": w.name, "layers": nl, "k": k, "batch": 1,
             "thld_first_last": [thld[0], thld[-1]], **res}
+
+
+def cpu_baseline(args, w, host0, X_eval_h, thld):
+    """The fp64 oracle on the host cores, timed on a bounded sample of the headline
+    workload (same weights, thresholds and eval tokens), with its dense path on the
+    same threads and the same sparse path on one thread beside it."""
+    import oracle
+
+    th = np.float32(thld.get((args.variant, args.k), 0.0))
+    H = host0
+    fns = {"mono": lambda x: oracle.ffn_mono(x, H["W_gate"], H["W_up"], H["W_down"], th),
+           "dual_ideal": lambda x: oracle.ffn_dual_ideal(x, H["W_gate"], H["W_up"],
+                                                         H["W_down"], th),
+           "dual_pred": lambda x: oracle.ffn_dual_pred(x, H["W_gate"], H["W_up"], H["W_down"],
+                                                       H.get("A_t"), H.get("B_t"), th),
+           "dense": lambda x: oracle.dense(x, H["W_gate"], H["W_up"], H["W_down"]),
+           "cats": lambda x: oracle.ffn_cats(x, H["W_gate"], H["W_up"], H["W_down"], th),
+           "dual_tern": lambda x: oracle.ffn_dual_tern(x, H["W_gate"], H["W_up"],
+                                                       H["W_down"], H.get("theta_t"), th)}
+    for vb in ("mono", "dual_ideal", "dual_pred", "cats", "dual_tern"):
+        fns[vb + "_topk"] = (lambda b: lambda x: oracle.ffn_topk(
+            b, x, H["W_gate"], H["W_up"], H["W_down"], args.k, A_t=H.get("A_t"),
+            B_t=H.get("B_t"), theta_t=H.get("theta_t")))(vb)
+    fn = fns[args.variant]
+    nt = len(X_eval_h) - args.batch + 1
+
+    def rate(f, secs):
+        n, t = 0, time.perf_counter()
+        while n < 2 or time.perf_counter() - t < secs:
+            f(X_eval_h[n % nt:n % nt + args.batch])
+            n += 1
+        return n, time.perf_counter() - t
+
+    n_done, el = rate(fn, args.cpu_seconds)
+    cpu = {"value": n_done * args.batch / el, "unit": "tokens/s",
+           "cores": oracle.num_threads(), "kind": "oracle",
+           "sample": f"{n_done} calls of {w.name} {args.variant} k={args.k}, "
+                     f"batch {args.batch}, one weight copy, fp64 C oracle ({el:.1f} s)"}
+    secs = max(1.0, args.cpu_seconds / 4)
+    n, el = rate(fns["dense"], secs)
+    cpu["detail"] = {"dense_tokens_per_s": n * args.batch / el}
+    nthreads = oracle.num_threads()
+    oracle.set_num_threads(1)
+    n, el = rate(fn, secs)
+    cpu["detail"]["one_thread_tokens_per_s"] = n * args.batch / el
+    oracle.set_num_threads(nthreads)
+    log(f"[bench] cpu baseline: {json.dumps(cpu)}")
+    return cpu
 
 
 def main():
@@ -668,7 +880,6 @@ def main():
     import torch
 
     from paper_2505_17701_amd import binding as cd
-    from paper_2505_17701_amd import traffic
     from workloads import WORKLOADS
 
     cd.load_library()
@@ -677,6 +888,7 @@ def main():
     torch.cuda.set_device(0)
     w = WORKLOADS[args.workload]
     dm, dff = w.d_model, w.d_ff
+    copies = args.copies or auto_copies(w)
     if args.traffic_probe:
         src = torch.ones(64 << 20, dtype=torch.float32, device="cuda")  # 256 MiB
         dst = torch.empty_like(src)
@@ -688,134 +900,51 @@ def main():
     base = args.variant[:-5] if args.variant.endswith("_topk") else args.variant
     main_variants = (["mono", "dual_ideal", "cats"] if "mono" in w.variants
                      else [v for v in w.variants if v != "dense"])
+    if w.name == "llama70b_8192x28672":
+        main_variants = ["mono"]
     if base == "dual_tern":
         main_variants.append("dual_tern")
-    main_ctx = Context(w, args.copies, args.tokens, args.calib_tokens,
+    main_ctx = Context(w, copies, args.tokens, args.calib_tokens,
                        sorted(set((args.k,) + tuple(w.ks))), max_batch=args.batch,
                        variants=main_variants)
     main_res = main_ctx.measure(args.variant, args.k, args.batch, args.steps, args.warmup,
                                 replays=True)
     log(f"[bench] {w.name} {args.variant} k={args.k}: {json.dumps(main_res)}")
-    ceiling = stream_ceiling(main_ctx, min(args.steps, 512))
+    ceiling = stream_ceiling(main_ctx, min(max(args.steps, 64), 512))
     log(f"[bench] plain streaming read: {json.dumps(ceiling)}")
 
     extra = {}
-    if not args.no_extra and "mono" in w.variants:
-        for variant, k in (("dense", None), ("dual_ideal", 0.9), ("mono", 0.7), ("mono", 0.5),
-                           ("cats", 0.9), ("mono_topk", 0.9), ("dual_ideal_topk", 0.9),
-                           ("cats_topk", 0.9)):
-            if variant == args.variant and k == args.k:
-                continue
-            r = main_ctx.measure(variant, k, 1, max(200, args.steps // 4), 50)
-            extra[f"{variant}" + ("" if k is None else f"@k={k}")] = brief(r)
-            log(f"[bench] {variant} k={k}: {json.dumps(extra[list(extra)[-1]])}")
-        # mask agreement of u and h with s (CIF / CAF) on the layer's eval tokens
-        from paper_2505_17701_amd.metrics import cif_caf, masks_on_gpu
-
-        extra["cif_caf"] = {}
-        for k in (0.5, 0.7, 0.9):
-            m = cif_caf(*masks_on_gpu(main_ctx.layers[0], main_ctx.X_eval[:32], k))
-            extra["cif_caf"][f"k={k}"] = {kk: round(v, 4) for kk, v in m.items()}
-        log(f"[bench] CIF/CAF: {json.dumps(extra['cif_caf'])}")
+    if not args.no_extra:
+        extra, _ = workload_lines(main_ctx, args, (args.variant, args.k))
         if "dense" in extra:
+            from paper_2505_17701_amd import traffic
+
             extra["speedup_vs_dense"] = extra["dense"]["us_per_layer"] / main_res["us_per_layer"]
-            dense_b = traffic.algorithmic_bytes("dense", dm, dff, dff)["total"]
-            extra["ideal_byte_ratio"] = dense_b / main_res["algorithmic_bytes"]
-    host0 = main_ctx.host0
-    X_eval_h = main_ctx.X_eval_h
-    thld = main_ctx.thld
-    thld_pooled = main_ctx.thld_pooled
+            extra["ideal_byte_ratio"] = (traffic.algorithmic_bytes("dense", dm, dff, dff)["total"]
+                                         / main_res["algorithmic_bytes"])
+    host0, X_eval_h = main_ctx.host0, main_ctx.X_eval_h
+    thld, thld_pooled = main_ctx.thld, main_ctx.thld_pooled
     main_ctx.free()
 
     others = {}
     if not args.no_extra and not args.no_other:
-        others = other_workloads(args)
+        seven_dense_us = None
+        for name in ("llama7b_4096x11008", "llama70b_8192x28672"):
+            if name != w.name and not (args.no_7b and name == "llama7b_4096x11008"):
+                others[name] = layer_block(args, name)
+        if "llama7b_4096x11008" in others:
+            seven_dense_us = others["llama7b_4096x11008"].get("dense", {}).get("us_per_layer")
+        elif w.name == "llama7b_4096x11008":
+            seven_dense_us = extra.get("dense", {}).get("us_per_layer")
+        if not args.no_8b:
+            others["llama3_8b_4096x14336_pred"] = eight_b_block(args)
         if not args.no_stack:
-            others["stack32_llama7b_pred"] = stack_bench(args)
+            others["stack32_llama7b_pred"] = stack_bench(args, dense_layer_us=seven_dense_us)
         if not args.no_train:
             others["predictor_training_llama3_8b"] = predictor_training_bench(args)
 
-    # CPU baseline: the fp64 oracle on host cores, bounded sample of the same workload
-    cpu = None
-    if args.cpu_seconds > 0:
-        import oracle
-
-        th = np.float32(thld.get((args.variant, args.k), 0.0))
-        H = host0
-        fns = {"mono": lambda x: oracle.ffn_mono(x, H["W_gate"], H["W_up"], H["W_down"], th),
-               "dual_ideal": lambda x: oracle.ffn_dual_ideal(x, H["W_gate"], H["W_up"],
-                                                             H["W_down"], th),
-               "dual_pred": lambda x: oracle.ffn_dual_pred(x, H["W_gate"], H["W_up"], H["W_down"],
-                                                           H.get("A_t"), H.get("B_t"), th),
-               "dense": lambda x: oracle.dense(x, H["W_gate"], H["W_up"], H["W_down"]),
-               "cats": lambda x: oracle.ffn_cats(x, H["W_gate"], H["W_up"], H["W_down"], th),
-               "dual_tern": lambda x: oracle.ffn_dual_tern(x, H["W_gate"], H["W_up"],
-                                                           H["W_down"], H.get("theta_t"), th)}
-        for vb in ("mono", "dual_ideal", "dual_pred", "cats", "dual_tern"):
-            fns[vb + "_topk"] = (lambda b: lambda x: oracle.ffn_topk(
-                b, x, H["W_gate"], H["W_up"], H["W_down"], args.k, A_t=H.get("A_t"),
-                B_t=H.get("B_t"), theta_t=H.get("theta_t")))(vb)
-        fn = fns[args.variant]
-        n_done, t0 = 0, time.perf_counter()
-        nt = len(X_eval_h) - args.batch + 1
-        while n_done < 3 or time.perf_counter() - t0 < args.cpu_seconds:
-            i = n_done % nt
-            fn(X_eval_h[i:i + args.batch])
-            n_done += 1
-        el = time.perf_counter() - t0
-        cpu = {"value": n_done * args.batch / el, "unit": "tokens/s",
-               "cores": oracle.num_threads(), "kind": "oracle",
-               "sample": f"{n_done} calls of {w.name} {args.variant} k={args.k}, "
-                         f"batch {args.batch}, one weight copy, fp64 C oracle ({el:.1f} s)"}
-        # beside it: the oracle's dense path on the same threads, and the same sparse
-        # path on one thread (a few seconds each)
-        def rate(f, secs):
-            n, t = 0, time.perf_counter()
-            while n < 2 or time.perf_counter() - t < secs:
-                f(X_eval_h[n % nt:n % nt + args.batch])
-                n += 1
-            return n * args.batch / (time.perf_counter() - t)
-
-        secs = max(1.0, args.cpu_seconds / 4)
-        cpu["detail"] = {"dense_tokens_per_s": rate(fns["dense"], secs)}
-        nthreads = oracle.num_threads()
-        oracle.set_num_threads(1)
-        cpu["detail"]["one_thread_tokens_per_s"] = rate(fn, secs)
-        oracle.set_num_threads(nthreads)
-        log(f"[bench] cpu baseline: {json.dumps(cpu)}")
-
-    roof = None
-    dom = "coef"
-    if main_res.get(f"{dom}_kernel_us"):
-        desc = {"mono": "k_coef_mono (dense W_up GEMV, threshold, wave-local W_gate gather, s)",
-                "dual_ideal": "k_coef_dual (dense W_gate + W_up GEMV, s, threshold)",
-                "dual_pred": "k_latent + k_coef_pred (predictor scores, threshold, block-local "
-                             "W_gate / W_up gather, s)",
-                "dense": "k_coef_dual (dense W_gate + W_up GEMV, s)",
-                "mono_topk": "k_coef_mono + k_topk_select + k_gather_topk (per-token threshold)",
-                "dual_ideal_topk": "k_coef_dual + k_topk_select (per-token threshold; the "
-                                   "select sets the flags, s is the coefficient)",
-                "dual_pred_topk": "k_latent + k_coef_pred + k_topk_select + k_gather_topk "
-                                  "(per-token threshold)",
-                "cats": "k_coef_mono<CATS> (dense W_gate GEMV, SiLU, threshold, W_up gather)",
-                "cats_topk": "k_coef_mono<CATS> + k_topk_select + k_gather_topk "
-                             "(per-token threshold)",
-                "dual_tern": "k_coef_tern (ternary predictor scores, threshold, block-local "
-                             "W_gate / W_up gather, s)",
-                "dual_tern_topk": "k_coef_tern + k_topk_select + k_gather_topk (per-token "
-                                  "threshold)"}[args.variant]
-        roof = {"bound": "hbm", "kernel": desc,
-                "achieved": main_res[f"{dom}_kernel_GBs"], "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                "frac": main_res[f"{dom}_kernel_GBs"] / HBM_PEAK_GBS,
-                "traffic": measured_traffic() if (args.workload, args.variant, args.k) ==
-                ("llama7b_4096x11008", "mono", 0.9) else None,
-                "bytes_per_launch": main_res[f"{dom}_kernel_bytes"],
-                "avg_launch_us": main_res[f"{dom}_kernel_us"],
-                # measured ceilings: a plain read of the same W_up bytes per launch, and
-                # of 1 GiB (countdown_stream_read)
-                "stream_same_bytes_GBs": ceiling["W_up"]["GBs"],
-                "frac_of_stream_same_bytes": main_res[f"{dom}_kernel_GBs"] / ceiling["W_up"]["GBs"],
-                "stream_1GiB_GBs": ceiling["1GiB"]["GBs"]}
+    cpu = cpu_baseline(args, w, host0, X_eval_h, thld) if args.cpu_seconds > 0 else None
+    roof = roofline(main_res, args.variant, (w.name, args.variant, args.k, args.batch), ceiling)
 
     out = {
         "metric": "sparse-FFN decode tokens/s and \u00b5s/layer; achieved HBM GB/s vs peak at 90% "
@@ -845,7 +974,7 @@ def main():
                    "variant": args.variant, "k": args.k,
                    "thld": thld.get((args.variant, args.k)),
                    "thld_pooled_reading": thld_pooled.get((base, args.k)),
-                   "weight_copies": args.copies,
+                   "weight_copies": copies,
                    "n_active_mean": main_res["n_active_mean"],
                    "realised_sparsity": main_res["realised_sparsity"],
                    "algorithmic_bytes_per_step": main_res["algorithmic_bytes"],
@@ -853,6 +982,9 @@ def main():
         "kernels": {k: main_res.get(k) for k in ("coef_kernel_us", "coef_kernel_GBs",
                                                   "down_kernel_us", "down_kernel_GBs")
                     if main_res.get(k) is not None},
+        "roofline_traffic_source": "profiles/ PMC summary of the same kernel source (FETCH_SIZE "
+                                   "+ WRITE_SIZE scaled by a 256 MiB copy), null when absent "
+                                   "or stale; not read in this run",
         "variants": extra,
         "other_workloads": others,
         "roofline": roof,
