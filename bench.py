@@ -354,7 +354,7 @@ class Context:
                 cd.countdown_ffn_dense(plan, x, L["W_gate"], L["W_up"], L["W_down"], y=y)
         return step
 
-    def measure(self, variant, k, B, steps, warmup, replays=False):
+    def measure(self, variant, k, B, steps, warmup, replays=False, deterministic=False):
         import torch
 
         from paper_2505_17701_amd import binding as cd
@@ -365,7 +365,7 @@ class Context:
         y = torch.empty((B, dm), dtype=torch.float32, device="cuda")
         base = variant[:-5] if variant.endswith("_topk") else variant
         plan = cd.Plan(dm, dff, max_batch=max(B, self.max_batch),
-                       d_rank=dr if base == "dual_pred" else 0)
+                       d_rank=dr if base == "dual_pred" else 0, deterministic=deterministic)
         step = self.make_step(plan, variant, k, B, y)
         ms_eager = time_steps(step, steps, warmup, stream)
         rep = [] if replays else None
@@ -540,6 +540,13 @@ def layer_block(args, wname):
                     replays=True)
     ceiling = stream_ceiling(ctx, min(max(args.steps, 64), 512))
     lines, res = workload_lines(ctx, args, ("mono", 0.9))
+    # the same call with the fixed-order reduction of y (CD_PLAN_DETERMINISTIC)
+    rd = ctx.measure("mono", 0.9, 1, max(200 if w.d_model <= 4096 else 100, args.steps // 4),
+                     30, deterministic=True)
+    lines["mono@k=0.9 deterministic"] = {**brief(rd), "cost_us": rd["us_per_layer"] -
+                                         r["us_per_layer"]}
+    log(f"[bench] {w.name} mono@k=0.9 deterministic: "
+        f"{json.dumps(lines['mono@k=0.9 deterministic'])}")
     dense = res.get("dense")
     out = {"mono@k=0.9": {**brief(r), "us_per_layer_median_of_6": r["us_per_layer_median_of_6"],
                           "roofline": roofline(r, "mono", (w.name, "mono", 0.9, 1), ceiling)},
@@ -572,6 +579,12 @@ def eight_b_block(args):
         r8[f"B={B}"] = {**brief(r), "roofline": roofline(r, "dual_pred",
                                                          (w.name, "dual_pred", 0.9, B))}
         log(f"[bench] {w.name} dual_pred B={B}: {json.dumps(r8[f'B={B}'])}")
+    for B in (1, 8):  # the fixed-order reduction of y (CD_PLAN_DETERMINISTIC)
+        r = ctx.measure("dual_pred", 0.9, B, n, 50, deterministic=True)
+        r8[f"B={B} deterministic"] = {**brief(r), "cost_us": r["us_per_layer"] -
+                                      r8[f"B={B}"]["us_per_layer"]}
+        log(f"[bench] {w.name} dual_pred B={B} deterministic: "
+            f"{json.dumps(r8[f'B={B} deterministic'])}")
     r = ctx.measure("dual_pred_topk", 0.9, 1, n, 50)
     r8["per-token k=0.9 B=1"] = brief(r)
     log(f"[bench] {w.name} dual_pred per-token B=1: {json.dumps(r8['per-token k=0.9 B=1'])}")

@@ -74,6 +74,11 @@ typedef int cd_status;
 /* Plan flags. */
 #define CD_PLAN_KEEP_COEF 1u  /* also store the dense coefficient vector of each call
                                  (u for mono, s for dual ideal, s_hat for dual pred) */
+#define CD_PLAN_DETERMINISTIC 2u  /* bit-reproducible y: the down projection stores one
+                                 partial sum per neuron range (plan workspace, about
+                                 64 x max_batch x d_model floats) and a second kernel
+                                 adds them in ascending range order, instead of fp32
+                                 atomics in arrival order; costs one more launch */
 
 typedef struct cd_plan cd_plan;
 

@@ -17,7 +17,7 @@ LIB_PATH = os.path.join(PKG, "libcountdown.so")
 CD_OK, CD_EINVAL, CD_EUNSUPPORTED, CD_EHIP, CD_ENOMEM = 0, -1, -2, -3, -4
 CD_VARIANT_MONO, CD_VARIANT_DUAL_IDEAL, CD_VARIANT_DUAL_PRED, CD_VARIANT_DENSE = 0, 1, 2, 3
 CD_VARIANT_CATS, CD_VARIANT_DUAL_TERN = 4, 5
-CD_PLAN_KEEP_COEF = 1
+CD_PLAN_KEEP_COEF, CD_PLAN_DETERMINISTIC = 1, 2
 CD_PHASE_COEF, CD_PHASE_DOWN, CD_PHASE_ALL = 1, 2, 3
 
 # every symbol include/countdown.h declares
@@ -132,9 +132,10 @@ class Plan:
     """Owns a ``cd_plan``: shape, workspace, and optional timing/coefficient capture."""
 
     def __init__(self, d_model: int, d_ff: int, max_batch: int = 1, d_rank: int = 0,
-                 keep_coef: bool = False):
+                 keep_coef: bool = False, deterministic: bool = False):
         self.d_model, self.d_ff, self.max_batch, self.d_rank = d_model, d_ff, max_batch, d_rank
-        flags = CD_PLAN_KEEP_COEF if keep_coef else 0
+        flags = (CD_PLAN_KEEP_COEF if keep_coef else 0) | (
+            CD_PLAN_DETERMINISTIC if deterministic else 0)
         h = C.c_void_p()
         _check(load_library().countdown_plan_create(d_model, d_ff, max_batch, d_rank, flags,
                                                     C.byref(h)), "countdown_plan_create")
@@ -160,8 +161,9 @@ class Plan:
         self.close()
 
 
-def countdown_plan_create(d_model, d_ff, max_batch=1, d_rank=0, keep_coef=False):
-    return Plan(d_model, d_ff, max_batch, d_rank, keep_coef)
+def countdown_plan_create(d_model, d_ff, max_batch=1, d_rank=0, keep_coef=False,
+                          deterministic=False):
+    return Plan(d_model, d_ff, max_batch, d_rank, keep_coef, deterministic)
 
 
 def countdown_plan_destroy(plan: Plan) -> None:

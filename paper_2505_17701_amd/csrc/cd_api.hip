@@ -39,6 +39,7 @@ struct cd_plan {
                                   // call with CD_PLAN_KEEP_COEF, by the per-token path always)
     double *q;                    // [max_batch] per-token thresholds of the last per-token call
     float *lat;                   // [max_batch][d_rank] predictor latent
+    float *part;                  // per-range partial sums of y (CD_PLAN_DETERMINISTIC)
     unsigned phases;              // kernels launched per call (CD_PHASE_*)
     bool has_state;               // act / s hold a coefficient kernel's output
     bool s_in_coef;               // the last call's s is coef (ideal D, per-token thresholds)
@@ -181,6 +182,7 @@ cdk::DownArgs down_args(cd_plan *p, int B, const uint16_t *Wd, float *y)
     a.d_ff = p->d_ff;
     a.gc = a.gr = a.rows_per_group = 0;  // chosen per batch tile by launch_down
     a.y = y;
+    a.part = p->part;
     return a;
 }
 
@@ -387,7 +389,7 @@ cd_status dalloc(T **ptr, size_t count)
 
 void release(cd_plan *p)
 {
-    void *bufs[] = {p->act, p->s, p->coef, p->lat, p->q};
+    void *bufs[] = {p->act, p->s, p->coef, p->lat, p->q, p->part};
     for (void *b : bufs)
         if (b)
             (void)hipFree(b);
@@ -463,7 +465,7 @@ cd_status countdown_plan_create(int d_model, int d_ff, int max_batch, int d_rank
     cd_status st = check_shape(d_model, d_ff, max_batch, d_rank);
     if (st != CD_OK)
         return st;
-    if (flags & ~CD_PLAN_KEEP_COEF)
+    if (flags & ~(CD_PLAN_KEEP_COEF | CD_PLAN_DETERMINISTIC))
         return CD_EINVAL;
     int dev = 0;
     if (hipGetDevice(&dev) != hipSuccess)
@@ -487,6 +489,15 @@ cd_status countdown_plan_create(int d_model, int d_ff, int max_batch, int d_rank
     if (st == CD_OK) st = dalloc(&p->coef, mb * d_ff);
     if (st == CD_OK) st = dalloc(&p->q, mb);
     if (st == CD_OK && d_rank > 0) st = dalloc(&p->lat, mb * d_rank);
+    if (st == CD_OK && (flags & CD_PLAN_DETERMINISTIC)) {
+        // the largest partial-sum array of any batch tile up to max_batch's
+        size_t n = 0;
+        for (int bt = 1; bt <= cdk::batch_tile(max_batch); bt *= 2) {
+            const size_t f = cdk::down_part_floats(d_model, d_ff, bt);
+            n = f > n ? f : n;
+        }
+        st = dalloc(&p->part, n);
+    }
     if (st != CD_OK) {
         release(p);
         return st;

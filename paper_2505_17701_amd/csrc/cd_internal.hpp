@@ -35,7 +35,10 @@ struct DownArgs {
     int d_model, d_ff;
     int gc, gr;          // column chunks x neuron ranges (set by launch_down)
     int rows_per_group;  // ceil(d_ff / gr)
-    float *y;            // [nb][d_model], accumulated
+    float *y;            // [nb][d_model], accumulated (or written from part)
+    float *part;         // [gr][nb][d_model] per-range partial sums, summed into y in
+                         // ascending range order by a second kernel (bit-reproducible
+                         // y); NULL: each range adds into y with fp32 atomics
 };
 
 // Residual stream between stacked layers (not part of the paper's method):
@@ -61,6 +64,8 @@ hipError_t launch_coef(int variant, const CoefArgs &a, hipStream_t s);
 hipError_t launch_latent(const uint16_t *x, int nb, const uint16_t *At, int d_model, int d_rank,
                          float *lat, hipStream_t s);
 hipError_t launch_down(const DownArgs &a, hipStream_t s);
+// floats of DownArgs::part a call of batch tile bt needs at this shape
+size_t down_part_floats(int d_model, int d_ff, int bt);
 // x_out / h_out of the residual stream (one workgroup)
 hipError_t launch_norm(const NormArgs &n, hipStream_t s);
 // the same fused with the predictor latent: every workgroup normalises, the first writes

@@ -1283,6 +1283,42 @@ __global__ __launch_bounds__(kBlock) void k_latent_norm(const NormArgs n,
     }
 }
 
+// A range without active neurons still owns its slice of the per-range partial
+// sums in deterministic mode: zeros for columns [c0, c0 + w) of every token.
+__device__ __forceinline__ void zero_part(const DownArgs &a, int g, int c0, int w)
+{
+    for (int i = threadIdx.x; i < a.nb * w; i += kBlock) {
+        const int b = i / w, col = c0 + i % w;
+        if (col < a.d_model)
+            a.part[((size_t)g * a.nb + b) * a.d_model + col] = 0.0f;
+    }
+}
+
+// y[b][col] = sum over the gr ranges, in ascending order, of their partial sums:
+// the down projection's reduction in a fixed order (deterministic mode).
+__global__ __launch_bounds__(kBlock) void k_reduce_parts(const float *__restrict__ part, int gr,
+                                                         int n, float *__restrict__ y)
+{
+    const int i = blockIdx.x * kBlock + threadIdx.x;
+    if (i >= n)
+        return;
+    constexpr int U = 8;  // loads in flight; the additions stay in range order
+    float v = 0.0f;
+    int g = 0;
+    for (; g + U <= gr; g += U) {
+        float t[U];
+#pragma unroll
+        for (int q = 0; q < U; ++q)
+            t[q] = part[(size_t)(g + q) * n + i];
+#pragma unroll
+        for (int q = 0; q < U; ++q)
+            v += t[q];
+    }
+    for (; g < gr; ++g)
+        v += part[(size_t)g * n + i];
+    y[i] = v;
+}
+
 // Gathered down projection (Eq. 5). Workgroup (c, g) owns a 512-column chunk
 // c and a contiguous neuron range g: one round trip reads act and s of the
 // range, a wave ballot compacts the active neurons in ascending order into
@@ -1337,8 +1373,11 @@ __global__ __launch_bounds__(kBlock) void k_down(const DownArgs a)
         nl += wcnt[0] + wcnt[1] + wcnt[2] + wcnt[3];
         __syncthreads();
     }
-    if (nl == 0)
-        return;  // uniform for the workgroup
+    if (nl == 0) {  // uniform for the workgroup
+        if (a.part)
+            zero_part(a, g, c * kColsPerLoad, kColsPerLoad);
+        return;
+    }
 
     const int col = c * kColsPerLoad + lane * 8;
     const bool colok = col < a.d_model;
@@ -1388,7 +1427,10 @@ __global__ __launch_bounds__(kBlock) void k_down(const DownArgs a)
             if (gcol < a.d_model) {
                 const float v = red[cc] + red[kColsPerLoad + cc] + red[2 * kColsPerLoad + cc] +
                                 red[3 * kColsPerLoad + cc];
-                unsafeAtomicAdd(a.y + (size_t)b * a.d_model + gcol, v);
+                if (a.part)
+                    a.part[((size_t)g * a.nb + b) * a.d_model + gcol] = v;
+                else
+                    unsafeAtomicAdd(a.y + (size_t)b * a.d_model + gcol, v);
             }
         }
     }
@@ -1485,8 +1527,11 @@ __global__ __launch_bounds__(kBlock) void k_down_mfma(const DownArgs a)
         }
     }
     __syncthreads();
-    if (nl == 0)
-        return;  // uniform for the workgroup
+    if (nl == 0) {  // uniform for the workgroup
+        if (a.part)
+            zero_part(a, g, c * kWc, kWc);
+        return;
+    }
 
     const int j = lane % 16, q = lane / 16;
     const int col = c * kWc + j * 8;
@@ -1563,7 +1608,10 @@ __global__ __launch_bounds__(kBlock) void k_down_mfma(const DownArgs a)
         if (b < a.nb && gcol < a.d_model) {
             const float v = out[i] + out[BT * kWc + i] + out[2 * BT * kWc + i] +
                             out[3 * BT * kWc + i];
-            unsafeAtomicAdd(a.y + (size_t)b * a.d_model + gcol, v);
+            if (a.part)
+                a.part[((size_t)g * a.nb + b) * a.d_model + gcol] = v;
+            else
+                unsafeAtomicAdd(a.y + (size_t)b * a.d_model + gcol, v);
         }
     }
 }
@@ -2426,6 +2474,26 @@ static void down_grid_mfma(int d_model, int d_ff, int bt, int *gc, int *gr, int 
 
 static bool down_uses_mfma(int bt) { return bt >= kDownMfmaMinBatch; }
 
+// the per-range partial sums of a deterministic call, added into y in range order
+static hipError_t reduce_parts(const DownArgs &a, hipStream_t s)
+{
+    if (!a.part)
+        return hipGetLastError();
+    const int n = a.nb * a.d_model;
+    k_reduce_parts<<<(n + kBlock - 1) / kBlock, kBlock, 0, s>>>(a.part, a.gr, n, a.y);
+    return hipGetLastError();
+}
+
+size_t down_part_floats(int d_model, int d_ff, int bt)
+{
+    int gc = 0, gr = 0, rows = 0;
+    if (down_uses_mfma(bt))
+        down_grid_mfma(d_model, d_ff, bt, &gc, &gr, &rows);
+    else
+        down_grid(d_model, d_ff, bt, &gc, &gr, &rows);
+    return (size_t)gr * bt * d_model;
+}
+
 hipError_t launch_down(const DownArgs &args, hipStream_t s)
 {
     const int bt = batch_tile(args.nb);
@@ -2441,7 +2509,8 @@ hipError_t launch_down(const DownArgs &args, hipStream_t s)
             allow_lds(k_down_mfma<8>, lds);
             k_down_mfma<8><<<grid, kBlock, lds, s>>>(a);
         }
-        return hipGetLastError();
+        const hipError_t e = hipGetLastError();
+        return e != hipSuccess ? e : reduce_parts(a, s);
     }
     down_grid(a.d_model, a.d_ff, bt, &a.gc, &a.gr, &a.rows_per_group);
     const size_t lds = down_lds_bytes(a.rows_per_group, bt);
@@ -2453,7 +2522,8 @@ hipError_t launch_down(const DownArgs &args, hipStream_t s)
         allow_lds(k_down<2>, lds);
         k_down<2><<<grid, kBlock, lds, s>>>(a);
     }
-    return hipGetLastError();
+    const hipError_t e = hipGetLastError();
+    return e != hipSuccess ? e : reduce_parts(a, s);
 }
 
 template <int B, int NK>

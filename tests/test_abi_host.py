@@ -132,7 +132,7 @@ def test_plan_create_rejects_bad_sizes_before_any_hip_call(lib):
     h = C.c_void_p()
     assert lib.countdown_plan_create(4100, 11008, 1, 0, 0, C.byref(h)) == cd.CD_EINVAL
     assert lib.countdown_plan_create(4096, 11008, 1, 0, 0x80, C.byref(h)) == cd.CD_EINVAL
-    assert lib.countdown_plan_create(4096, 11008, 1, 0, 2, C.byref(h)) == cd.CD_EINVAL
+    assert lib.countdown_plan_create(4096, 11008, 1, 0, 4, C.byref(h)) == cd.CD_EINVAL
     assert h.value is None
 
 
