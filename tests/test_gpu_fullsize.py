@@ -24,7 +24,7 @@ def llama7b():
 
 
 @pytest.mark.parametrize("variant", ["mono", "dual_ideal", "cats"])
-@pytest.mark.parametrize("k", [0.9, 0.5])
+@pytest.mark.parametrize("k", [0.9, 0.7, 0.5])
 def test_llama7b_layer(llama7b, variant, k):
     w, layer = llama7b
     thld = calibrated(variant, layer, w.wid, k, T=32, outlier_frac=w.outlier_frac)

@@ -115,29 +115,87 @@ def test_residual_rejects_overlap():
 
 
 def test_stack_teacher_forced():
-    """Three stacked 7B-shaped predictor layers run back to back on the GPU (the
-    residual stream passed from layer to layer); every layer is checked against
-    the oracle on the inputs the GPU layer received."""
+    """All 32 layers of the stack workload (7B-shaped predictor layers, the
+    residual stream between them) run back to back on the GPU at batch 1. Every
+    layer is checked against the oracle on the inputs the GPU layer received
+    (teacher forcing), with its threshold calibrated by the oracle at k = 0.9 on
+    8 calibration tokens propagated through the oracle's dense stack. Reported,
+    not gated: the end-to-end divergence of the residual stream between the GPU
+    stack and the oracle's own sparse stack (free running: a neuron whose score
+    lies within rounding of the threshold can be selected by one side only, and
+    with random layers such a difference grows from layer to layer), and between
+    the oracle's sparse and dense stacks (a random predictor's index set is not
+    the one the exact coefficients would pick). The GPU plan reduces y in a fixed
+    order, so the report repeats from run to run."""
+    from workloads.synth import T_CALIB, bf16_round
+
     w = WORKLOADS["stack32_llama7b_pred"]
-    B = 1
-    rng = stream(9100, w.d_model)
-    h = rng.standard_normal((B, w.d_model)).astype(np.float32)
-    y_prev = None
-    for l in range(3):
+    k, ncal = 0.9, 8
+
+    def norm_bits(h, y):
+        """The layer input: residual add, RMSNorm (fp64), rounded to bf16 via fp32."""
+        hs, xs = [], []
+        for b in range(h.shape[0]):
+            ho, r = oracle.residual_rmsnorm(h[b], None if y is None else y[b], eps=EPS)
+            hs.append(ho)
+            xs.append(r.astype(np.float32))
+        return np.stack(hs), bf16_round(np.stack(xs))
+
+    h_cal = stream(9200, T_CALIB, w.d_model).standard_normal((ncal, w.d_model))
+    h0 = stream(9100, w.d_model).standard_normal((1, w.d_model)).astype(np.float32)
+    y_cal = None
+    h, y_prev = h0, None                 # the GPU stack (fp32 residual stream)
+    h_os, y_os = h0.astype(np.float64), None  # the oracle's sparse stack, free running
+    h_od, y_od = h0.astype(np.float64), None  # the oracle's dense stack
+    plan = None
+    worst = 0.0
+    growth = {}
+
+    def rel_l2(a, b):
+        return float(np.linalg.norm(a - b) / np.linalg.norm(b))
+
+    for l in range(w.n_layers):
         L = w.layer(layer=l)
         P = w.predictor(layer=l)
-        layer = Layer(L, P)
-        X = np.stack([oracle.residual_rmsnorm(h[b], None if y_prev is None else y_prev[b],
-                                              eps=EPS)[1] for b in range(B)]).astype(np.float32)
-        from workloads.synth import bf16_round
-        thld = float(np.float32(oracle.calibrate("dual_pred", bf16_round(X), 0.9, A_t=P["A_t"],
+        h_cal, x_cal = norm_bits(h_cal, y_cal)
+        y_cal = oracle.dense(x_cal, L["W_gate"], L["W_up"], L["W_down"])
+        thld = float(np.float32(oracle.calibrate("dual_pred", x_cal, k, A_t=P["A_t"],
                                                  B_t=P["B_t"])[0]))
-        plan = plan_for(layer, max_batch=B)
+        layer = Layer(L, P)
+        if plan is None:  # fixed-order y: the reported divergence is reproducible
+            from paper_2505_17701_amd import binding as cd
+
+            plan = cd.Plan(w.d_model, w.d_ff, max_batch=1, d_rank=w.d_rank, keep_coef=True,
+                           deterministic=True)
         label = f"stack layer {l}"
         h_gpu, x_bits, out = run_residual(plan, "dual_pred", layer, h, y_prev, thld)
         check_norm(h, y_prev, h_gpu, x_bits, label)
         n, flips, rel = check_call("dual_pred", layer, x_bits, thld, out, label)
-        print(f"{label}: n={n} flips={flips} rel={rel:.2e}", flush=True)
+        worst = max(worst, rel)
+        print(f"{label}: thld={thld:.4f} n={n} flips={flips} rel={rel:.2e}", flush=True)
         h, y_prev = h_gpu, out[0].astype(np.float32)
-        del layer, plan
+        h_os, x_os = norm_bits(h_os, y_os)
+        _, y_os, _ = oracle.ffn_dual_pred(x_os, L["W_gate"], L["W_up"], L["W_down"], P["A_t"],
+                                          P["B_t"], thld)
+        h_od, x_od = norm_bits(h_od, y_od)
+        y_od = oracle.dense(x_od, L["W_gate"], L["W_up"], L["W_down"])
+        if l + 1 in (1, 2, 4, 8, 16, 32):
+            g_os = rel_l2(h.astype(np.float64) + y_prev, h_os + y_os)
+            growth[l + 1] = (g_os, rel_l2(h_os + y_os, h_od + y_od), int(np.sum(
+                np.isin(out[1], oracle.ffn_dual_pred(x_os, L["W_gate"], L["W_up"], L["W_down"],
+                                                      P["A_t"], P["B_t"], thld)[0],
+                        invert=True))))
+        del layer
         torch.cuda.empty_cache()
+    plan.close()
+    fin_gpu = h.astype(np.float64) + y_prev
+    fin_os, fin_od = h_os + y_os, h_od + y_od
+    assert np.all(np.isfinite(fin_gpu))
+    for d, (g_os, g_od, nd) in growth.items():
+        print(f"after {d} layers: GPU vs oracle sparse {g_os:.3e} (IDX of that layer: {nd} "
+              f"neurons the free-running oracle does not select); oracle sparse vs dense "
+              f"{g_od:.3e}", flush=True)
+    print(f"stack end to end (final h, relative l2): GPU vs oracle sparse stack "
+          f"{rel_l2(fin_gpu, fin_os):.3e}; oracle sparse vs oracle dense stack "
+          f"{rel_l2(fin_os, fin_od):.3e}; GPU vs oracle dense stack "
+          f"{rel_l2(fin_gpu, fin_od):.3e}; worst per-layer y error {worst:.2e}", flush=True)
