@@ -12,7 +12,9 @@ import ctypes as C
 import os
 
 PKG = os.path.dirname(os.path.abspath(__file__))
-LIB_PATH = os.path.join(PKG, "libcountdown.so")
+# CD_LIBRARY names another build of the library to load (the sanitizer test of
+# the host code loads an instrumented build this way)
+LIB_PATH = os.environ.get("CD_LIBRARY") or os.path.join(PKG, "libcountdown.so")
 
 CD_OK, CD_EINVAL, CD_EUNSUPPORTED, CD_EHIP, CD_ENOMEM = 0, -1, -2, -3, -4
 CD_VARIANT_MONO, CD_VARIANT_DUAL_IDEAL, CD_VARIANT_DUAL_PRED, CD_VARIANT_DENSE = 0, 1, 2, 3

@@ -280,3 +280,31 @@ def test_plan_create_refuses_unsupported_tile_before_hip(lib):
     with pytest.raises(cd.CountdownError) as e:
         cd.Plan(4160, 1024, max_batch=5)
     assert e.value.status == cd.CD_EUNSUPPORTED
+
+
+def _hip_devices():
+    import ctypes as C
+
+    try:
+        hip = C.CDLL("libamdhip64.so")
+    except OSError:
+        return 0
+    n = C.c_int(0)
+    return n.value if hip.hipGetDeviceCount(C.byref(n)) == 0 else 0
+
+
+def test_hip_failures_map_to_cd_ehip(lib):
+    """Where the HIP runtime has no device, the first HIP call after the host checks
+    fails, and plan creation, the entry point without allocation and the streaming
+    read aid each return CD_EHIP (the hipError_t mapping), writing no plan handle."""
+    import ctypes as C
+
+    if _hip_devices() > 0:
+        pytest.skip("a GPU is visible: these calls would reach it with placeholder pointers")
+    h = C.c_void_p()
+    assert lib.countdown_plan_create(4096, 11008, 1, 0, 0, C.byref(h)) == cd.CD_EHIP
+    assert h.value is None
+    vp = C.c_void_p
+    assert lib.countdown_ffn_mono_noalloc(vp(0x1000), 1, vp(0x2000), vp(0x3000), vp(0x4000), 256,
+                                          688, 1.0, vp(0x5000), None) == cd.CD_EHIP
+    assert lib.countdown_stream_read(vp(0x1000), 16, vp(0x2000), None) == cd.CD_EHIP
