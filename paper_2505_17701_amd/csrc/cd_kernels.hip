@@ -1302,20 +1302,19 @@ __global__ __launch_bounds__(kBlock) void k_reduce_parts(const float *__restrict
     const int i = blockIdx.x * kBlock + threadIdx.x;
     if (i >= n)
         return;
-    constexpr int U = 8;  // loads in flight; the additions stay in range order
+    // all of a column's partial sums in flight at once (64 ranges at 1-2 tokens);
+    // the additions stay in range order
+    constexpr int U = 64;
     float v = 0.0f;
-    int g = 0;
-    for (; g + U <= gr; g += U) {
+    for (int g0 = 0; g0 < gr; g0 += U) {
         float t[U];
 #pragma unroll
         for (int q = 0; q < U; ++q)
-            t[q] = part[(size_t)(g + q) * n + i];
+            t[q] = g0 + q < gr ? part[(size_t)(g0 + q) * n + i] : 0.0f;
 #pragma unroll
         for (int q = 0; q < U; ++q)
-            v += t[q];
+            v += t[q];  // + 0 past gr leaves v unchanged
     }
-    for (; g < gr; ++g)
-        v += part[(size_t)g * n + i];
     y[i] = v;
 }
 
