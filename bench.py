@@ -441,22 +441,22 @@ def kernel_desc(variant, B=1):
     """The kernel(s) of a line's coefficient phase, the dominant part of every call."""
     pred = "k_coef_pred_mfma" if B >= 5 else "k_coef_pred"
     tern = "k_coef_tern_mfma" if B >= 5 else "k_coef_tern"
+    sel = "k_topk_gather1 (select, flags and gather in one launch)" if B == 1 else \
+        "k_topk_select + k_gather_topk"
     return {"mono": "k_coef_mono (dense W_up GEMV, threshold, wave-local W_gate gather, s)",
             "dual_ideal": "k_coef_dual (dense W_gate + W_up GEMV, s, threshold)",
             "dual_pred": f"k_latent + {pred} (predictor latent, scores, threshold, block-local "
                          "W_gate / W_up gather, s)",
             "dense": "k_coef_dual (dense W_gate + W_up GEMV, s)",
-            "mono_topk": "k_coef_mono + k_topk_select + k_gather_topk (per-token threshold)",
+            "mono_topk": f"k_coef_mono + {sel} (per-token threshold)",
             "dual_ideal_topk": "k_coef_dual + k_topk_select (per-token threshold; the select "
                                "sets the flags, s is the coefficient)",
-            "dual_pred_topk": f"k_latent + {pred} + k_topk_select + k_gather_topk (per-token "
-                              "threshold)",
+            "dual_pred_topk": f"k_latent + {pred} + {sel} (per-token threshold)",
             "cats": "k_coef_mono<CATS> (dense W_gate GEMV, SiLU, threshold, W_up gather)",
-            "cats_topk": "k_coef_mono<CATS> + k_topk_select + k_gather_topk (per-token "
-                         "threshold)",
+            "cats_topk": f"k_coef_mono<CATS> + {sel} (per-token threshold)",
             "dual_tern": f"{tern} (ternary predictor scores, threshold, block-local W_gate / "
                          "W_up gather, s)",
-            "dual_tern_topk": f"{tern} + k_topk_select + k_gather_topk (per-token threshold)"
+            "dual_tern_topk": f"{tern} + {sel} (per-token threshold)"
             }[variant]
 
 

@@ -1790,6 +1790,20 @@ constexpr uint32_t kSelNoKey = 0xffffffffu;             // slot past the row: ab
 // LDS word of first-pass bin d
 __device__ __forceinline__ uint32_t sel_word(uint32_t d) { return d + 4u * (d >> 5); }
 
+// Order-preserving key of a coefficient: the bits of |c| (am = ~0, |c| keys) or
+// the signed float's bits mapped to an unsigned order (am = 0)
+__device__ __forceinline__ uint32_t sel_key(float c, uint32_t am)
+{
+    const uint32_t u = __float_as_uint(c);
+    const uint32_t sk = u ^ ((uint32_t)((int32_t)u >> 31) | 0x80000000u);
+    return ((u & 0x7fffffffu) & am) | (sk & ~am);
+}
+
+// A caller's hook into the select after the first pass, or nothing
+struct NoFirstPassHook {
+    __device__ __forceinline__ void operator()(uint32_t, uint32_t, int) const {}
+};
+
 // inclusive prefix sum over the 64 lanes (DPP row shifts, then row broadcasts)
 __device__ __forceinline__ uint32_t wave_incl_scan(uint32_t v)
 {
@@ -1851,15 +1865,17 @@ __device__ __forceinline__ void find_bin(const uint32_t *mine, const uint32_t (&
     out[2] = cnt;
 }
 
-// With act set (ideal D-CountDown, |s| keys), the workgroup also flags its
-// token's neurons with |c| > q: act starts at 0 (the coefficient kernel with
-// threshold +inf wrote it) and every token stores the same 1, so the union
-// needs no atomics and no gather kernel follows (s is the coefficient itself).
-template <int KPT>
-__global__ __launch_bounds__(kTopkThreads) void k_topk_select(const float *__restrict__ coef, int ld,
-                                                              int n, int use_abs, double k,
-                                                              double *__restrict__ q,
-                                                              int *__restrict__ act)
+// The quantile q of one row c[0, n) for the whole workgroup: every thread
+// returns the same q (both order statistics end up in every thread, which
+// interpolates them itself, so no broadcast is needed). key[] keeps this
+// thread's keys, slots threadIdx.x + j * kTopkThreads, for callers that
+// flag the row's neurons afterwards. hook(binA, binB, sh0) runs in every
+// thread once the first pass has found the bins of both ranks: a key whose
+// first-pass bin (key >> sh0) lies above binB is above q, one below binA is
+// below it.
+template <int KPT, class Hook>
+__device__ __forceinline__ double topk_row(const float *__restrict__ c, int n, int use_abs, double k,
+                                           uint32_t (&key)[KPT], const Hook &hook)
 {
     constexpr int kWaves = kTopkThreads / kWave;
     extern __shared__ __align__(16) uint32_t sm[];
@@ -1871,29 +1887,23 @@ __global__ __launch_bounds__(kTopkThreads) void k_topk_select(const float *__res
     __shared__ uint32_t sel[2][3];        // [rank][bin, rank within bin, keys in bin]
     __shared__ uint32_t val[2];
     const int lane = threadIdx.x % kWave;
-    const float *c = coef + (size_t)blockIdx.x * ld;
     const int jn = (n + kTopkThreads - 1) / kTopkThreads;  // key slots in use (uniform)
+    // every slot loads (slots past the row read the zero chunk): a load under a
+    // branch per slot can leave the compiler waiting for each load in turn
     float cv[KPT];
 #pragma unroll
     for (int j = 0; j < KPT; ++j) {
         const int i = threadIdx.x + j * kTopkThreads;
-        cv[j] = 0.0f;
-        if (j < jn)  // uniform
-            cv[j] = *or_zero(i < n, c + i);
+        cv[j] = *or_zero(i < n, c + i);
     }
     for (int i = threadIdx.x; i < kSelWords0 / 4; i += kTopkThreads)
         reinterpret_cast<uint4 *>(sm)[i] = make_uint4(0u, 0u, 0u, 0u);
     if (threadIdx.x < kSelList)
         list[threadIdx.x] = kSelNoKey;
-    uint32_t key[KPT];
     const uint32_t am = use_abs ? ~0u : 0u;  // order_key without a branch per slot
 #pragma unroll
-    for (int j = 0; j < KPT; ++j) {
-        const uint32_t u = __float_as_uint(cv[j]);
-        const uint32_t sk = u ^ ((uint32_t)((int32_t)u >> 31) | 0x80000000u);
-        key[j] = threadIdx.x + j * kTopkThreads < n ? ((u & 0x7fffffffu) & am) | (sk & ~am)
-                                                    : kSelNoKey;
-    }
+    for (int j = 0; j < KPT; ++j)
+        key[j] = threadIdx.x + j * kTopkThreads < n ? sel_key(cv[j], am) : kSelNoKey;
     const double h = k * (double)(n - 1);
     int lo = (int)floor(h);
     if (lo > n - 1)
@@ -1931,6 +1941,7 @@ __global__ __launch_bounds__(kTopkThreads) void k_topk_select(const float *__res
         __syncthreads();
     }
     const uint32_t binA = sel[0][0], binB = sel[1][0];
+    hook(binA, binB, sh0);
     uint32_t rA = sel[0][1], rB = sel[1][1];
     const uint32_t cA = sel[0][2];
     const bool apart = binA != binB;  // then rank lo is the last of its bin, lo + 1 the first of its
@@ -2031,16 +2042,29 @@ __global__ __launch_bounds__(kTopkThreads) void k_topk_select(const float *__res
         kA = pA;  // every bit is fixed
         kB = pB;
     }
-    __shared__ double qs;
-    if (threadIdx.x == 0) {
-        const double v0 = (double)key_value(kA, use_abs);
-        const double v1 = (double)key_value(two ? kB : kA, use_abs);
-        qs = v0 + (h - (double)lo) * (v1 - v0);
-        q[blockIdx.x] = qs;
-    }
+    const double v0 = (double)key_value(kA, use_abs);
+    const double v1 = (double)key_value(two ? kB : kA, use_abs);
+    return v0 + (h - (double)lo) * (v1 - v0);
+}
+
+// One workgroup per token. With act set (ideal D-CountDown, |s| keys), the
+// workgroup also flags its token's neurons with |c| > q: act starts at 0 (the
+// coefficient kernel with threshold +inf wrote it) and every token stores the
+// same 1, so the union needs no atomics and no gather kernel follows (s is the
+// coefficient itself).
+template <int KPT>
+__global__ __launch_bounds__(kTopkThreads) void k_topk_select(const float *__restrict__ coef, int ld,
+                                                              int n, int use_abs, double k,
+                                                              double *__restrict__ q,
+                                                              int *__restrict__ act)
+{
+    uint32_t key[KPT];
+    const double qv = topk_row<KPT>(coef + (size_t)blockIdx.x * ld, n, use_abs, k, key,
+                                    NoFirstPassHook{});
+    if (threadIdx.x == 0)
+        q[blockIdx.x] = qv;
     if (act) {  // uniform; |s| keys (use_abs): the key's bits are |c|
-        __syncthreads();
-        const double qv = qs;
+        const int jn = (n + kTopkThreads - 1) / kTopkThreads;
 #pragma unroll
         for (int j = 0; j < KPT; ++j) {
             const int i = threadIdx.x + j * kTopkThreads;
@@ -2192,6 +2216,100 @@ __global__ __launch_bounds__(kBlock) void k_gather_topk_w(const CoefArgs a, cons
                     a.s[(size_t)b * a.d_ff + row] = VARIANT == kCats ? p * cv : cv * silu(p);
             }
         }
+    }
+}
+
+// Per-token threshold, flags and gather of a single token in one launch (mono,
+// CATS and, TWO, the W_gate + W_up gather of the predictors). Every workgroup
+// (one per CU: the select's LDS fills it) finds the token's quantile itself,
+// the same way k_topk_select does, so no workgroup waits for another, and then
+// flags its own contiguous slice of at most 64 neurons. Every wave holds the
+// whole slice (lane l: neuron l) and takes the same ballots, so the active
+// neurons are dealt to the 16 waves without a barrier: in order, first those
+// known to be active early, then the rest; wave w gets positions w, w + 16,
+// ... A neuron is known to be active once the select's first pass has placed
+// the order statistics in their bins and its key lies in a higher bin: each
+// wave issues the loads of its early neuron's first row there, so their HBM
+// round trip overlaps the rest of the select (the predictors' W_up row follows
+// q: both rows in flight through the select would spill registers, and issuing
+// W_up once the keys are placed measured no faster). The token is loaded with
+// the keys and copied into LDS the select no longer uses after its first pass.
+// The dot products and reductions are those of k_gather_topk_w (the same
+// order, so s and act are the same bits). Workgroup 0 stores q.
+constexpr int kFusedTopkGrid = 256;        // one workgroup per CU of the MI355X
+constexpr int kFusedTopkSlice = kWave;     // neurons per workgroup at most
+constexpr int kFusedTokWord = 2 * kSelBins;  // token copy: past the later passes' bins
+
+// position n (from 0) among the set bits of m (n < popcount(m))
+__device__ __forceinline__ int nth_set_bit(uint64_t m, int n)
+{
+    for (int i = 0; i < n; ++i)
+        m &= m - 1;
+    return __builtin_ctzll(m);
+}
+
+template <int NK, bool TWO>
+__global__ __launch_bounds__(kTopkThreads) void k_topk_gather1(const CoefArgs a, int cats, double k,
+                                                               double *__restrict__ q)
+{
+    constexpr int KPT = 16;  // d_ff <= kFusedTopkGrid * kFusedTopkSlice
+    static_assert(kFusedTokWord + NK * kColsPerLoad / 2 <= kSelWords0, "token copy in LDS");
+    constexpr int kWaves = kTopkThreads / kWave;
+    extern __shared__ __align__(16) uint32_t sm[];
+    const int lane = threadIdx.x % kWave, wave = threadIdx.x / kWave;
+    const int per = (a.d_ff + (int)gridDim.x - 1) / (int)gridDim.x;  // <= kWave (host)
+    const int lo = blockIdx.x * per;
+    const int row = lo + lane;
+    const bool mine = lane < per && row < a.d_ff;
+    const float c = mine ? a.coef[row] : 0.0f;
+    const uint16_t *w1 = cats ? a.Wu : a.Wg;
+    constexpr int kTokChunks = NK * kColsPerLoad / 8;  // 16-byte chunks of the padded token
+    const bool xt = threadIdx.x < kTokChunks;
+    const u32x4 xv = xt ? load16(or_zero((int)threadIdx.x * 8 < a.d_model, a.x + threadIdx.x * 8))
+                        : zero16();
+
+    u32x4 wg[NK], wu[TWO ? NK : 1];
+    uint64_t early_m = 0;  // the slice's neurons known to be active after the first pass
+    int pre = -1;          // this wave's early neuron, its first row in flight (wave-uniform)
+    // c != 0: the signed keys of -0 and +0 differ while the values are equal
+    const auto early = [&](uint32_t, uint32_t binB, int sh0) {
+        if (xt)
+            *reinterpret_cast<u32x4 *>(sm + kFusedTokWord + 4 * threadIdx.x) = xv;
+        const uint32_t key = sel_key(c, TWO ? 0u : ~0u);
+        early_m = ballot(mine && c != 0.0f && ((key >> sh0) & (uint32_t)(kSelBins0 - 1)) > binB);
+        if (wave < __builtin_popcountll(early_m)) {
+            pre = lo + nth_set_bit(early_m, wave);
+            load_row<NK>(wg, w1 + (size_t)pre * a.d_model, a.d_model, lane);
+        }
+    };
+    uint32_t key[KPT];
+    const double qv = topk_row<KPT>(a.coef, a.d_ff, TWO ? 0 : 1, k, key, early);
+    if (blockIdx.x == 0 && threadIdx.x == 0)
+        q[0] = qv;
+    for (int i = blockIdx.x * kTopkThreads + threadIdx.x; i < a.d_model; i += gridDim.x * kTopkThreads)
+        a.y[i] = 0.0f;
+    const bool act = mine && (double)(TWO ? c : fabsf(c)) > qv;
+    if (wave == 0 && mine)
+        a.act[row] = act ? 1 : 0;
+    const uint64_t am = ballot(act);
+    const uint64_t first = am & early_m;  // (= early_m: an early neuron's value is above q)
+    const uint64_t rest = am & ~early_m;
+    const int nfirst = __builtin_popcountll(first), nall = __builtin_popcountll(am);
+    Tokens<1, NK, false> tok;
+    tok.lds = sm + kFusedTokWord;  // written before the select's later barriers
+    for (int p = wave; p < nall; p += kWaves) {
+        const int r = lo + (p < nfirst ? nth_set_bit(first, p) : nth_set_bit(rest, p - nfirst));
+        if (r != pre)
+            load_row<NK>(wg, w1 + (size_t)r * a.d_model, a.d_model, lane);
+        if constexpr (TWO)
+            load_row<NK>(wu, a.Wu + (size_t)r * a.d_model, a.d_model, lane);
+        pre = -1;
+        if constexpr (TWO)
+            pred_finish<1, NK, false>(a, tok, wg, wu, r, lane);
+        else if (cats)
+            mono_finish<1, NK, false, true>(a, tok, wg, r, lane);
+        else
+            mono_finish<1, NK, false, false>(a, tok, wg, r, lane);
     }
 }
 
@@ -2594,6 +2712,57 @@ static void launch_topk_select(const float *coef, int ld, int n, int T, int use_
     }
 }
 
+template <bool TWO>
+static hipError_t topk_gather1_two(int cats, const CoefArgs &a, double k, double *q, int grid,
+                                   hipStream_t s)
+{
+    const size_t lds = topk_select_lds_bytes();
+    switch (col_tile(a.d_model)) {
+    case 1:
+        allow_lds(k_topk_gather1<1, TWO>, lds);
+        k_topk_gather1<1, TWO><<<grid, kTopkThreads, lds, s>>>(a, cats, k, q);
+        break;
+    case 2:
+        allow_lds(k_topk_gather1<2, TWO>, lds);
+        k_topk_gather1<2, TWO><<<grid, kTopkThreads, lds, s>>>(a, cats, k, q);
+        break;
+    case 4:
+        allow_lds(k_topk_gather1<4, TWO>, lds);
+        k_topk_gather1<4, TWO><<<grid, kTopkThreads, lds, s>>>(a, cats, k, q);
+        break;
+    case 8:
+        allow_lds(k_topk_gather1<8, TWO>, lds);
+        k_topk_gather1<8, TWO><<<grid, kTopkThreads, lds, s>>>(a, cats, k, q);
+        break;
+    default:
+        return hipErrorInvalidValue;
+    }
+    return hipGetLastError();
+}
+
+// whether a call runs select, flags and gather in one launch: one token, d_model
+// <= 4096, d_ff within kFusedTopkGrid slices of kFusedTopkSlice neurons
+static bool topk_fused(int variant, const CoefArgs &a)
+{
+    return a.nb == 1 && variant != kDualIdeal && col_tile(a.d_model) <= 8 &&
+           a.d_ff <= kFusedTopkGrid * kFusedTopkSlice;
+}
+
+// slices of at least 16 neurons, at most kFusedTopkGrid of them
+static hipError_t launch_topk_gather1(int variant, const CoefArgs &a, double k, double *q,
+                                      hipStream_t s)
+{
+    if (!topk_fused(variant, a))
+        return hipErrorInvalidValue;
+    int grid = (a.d_ff + 15) / 16;
+    grid = grid < kFusedTopkGrid ? grid : kFusedTopkGrid;
+    if ((a.d_ff + grid - 1) / grid > kFusedTopkSlice)
+        return hipErrorInvalidValue;
+    const int cats = variant == kCats ? 1 : 0;
+    return variant == kDualPred ? topk_gather1_two<true>(cats, a, k, q, grid, s)
+                                : topk_gather1_two<false>(cats, a, k, q, grid, s);
+}
+
 hipError_t launch_topk(int variant, const CoefArgs &a, double k, double *q, hipStream_t s)
 {
     if (a.d_ff > kTopkThreads * kTopkPerThread)
@@ -2603,6 +2772,8 @@ hipError_t launch_topk(int variant, const CoefArgs &a, double k, double *q, hipS
     // ideal D: s is the dense coefficient, so the select sets the flags itself and
     // the down kernel reads s from a.coef (no gather kernel)
     const bool ideal = variant == kDualIdeal;
+    if (topk_fused(variant, a))
+        return launch_topk_gather1(variant, a, k, q, s);
     launch_topk_select(a.coef, a.d_ff, a.d_ff, a.nb, variant == kDualPred ? 0 : 1, k, q,
                        topk_select_lds_bytes(), s, ideal ? a.act : nullptr);
     hipError_t e = hipGetLastError();

@@ -69,15 +69,16 @@ def test_deterministic_y_is_bit_identical(layer, variant, B):
     atom.close()
 
 
+@pytest.mark.parametrize("B", [1, 3])
 @pytest.mark.parametrize("variant", ["mono", "dual_ideal", "dual_pred"])
-def test_deterministic_per_token_path(layer, variant):
+def test_deterministic_per_token_path(layer, variant, B):
     from paper_2505_17701_amd import binding as cd
 
     vid = {"mono": cd.CD_VARIANT_MONO, "dual_ideal": cd.CD_VARIANT_DUAL_IDEAL,
            "dual_pred": cd.CD_VARIANT_DUAL_PRED}[variant]
-    x = dev_bf16(make_tokens(2110, 3, DM))
+    x = dev_bf16(make_tokens(2110, B, DM))
     D = layer.d
-    det = cd.Plan(DM, DFF, max_batch=3, d_rank=RANK if variant == "dual_pred" else 0,
+    det = cd.Plan(DM, DFF, max_batch=B, d_rank=RANK if variant == "dual_pred" else 0,
                   deterministic=True)
     ys = []
     for _ in range(3):

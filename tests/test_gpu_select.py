@@ -140,7 +140,7 @@ def test_topk_long_rows(shape):
 @pytest.mark.parametrize("dup", [None, "pairs", "all", "cluster"])
 def test_per_token_call_exact_order_statistics(variant, dup):
     """The per-token FFN call's own select (|c| keys, or signed keys for the
-    predictor score): on five calls in a row of one plan, with batch sizes and
+    predictor score): on six calls in a row of one plan, with batch sizes and
     k that change from call to call, every token's threshold is exactly the
     interpolated order statistic of the coefficients the call wrote. "all"
     (every coefficient of a token equal) and "cluster" (most within a relative
@@ -172,7 +172,7 @@ def test_per_token_call_exact_order_statistics(variant, dup):
            "dual_ideal": cd.CD_VARIANT_DUAL_IDEAL, "dual_pred": cd.CD_VARIANT_DUAL_PRED}[variant]
     plan = cd.Plan(dm, dff, 8, dr if variant == "dual_pred" else 0, keep_coef=True)
     signed = variant == "dual_pred"
-    for call, (B, k) in enumerate([(5, 0.9), (3, 0.5), (8, 0.0), (1, 1.0), (2, 0.999)]):
+    for call, (B, k) in enumerate([(5, 0.9), (3, 0.5), (8, 0.0), (1, 1.0), (2, 0.999), (1, 0.7)]):
         X = make_tokens(1971 + call, B, dm, purpose=T_CALIB)
         q = torch.empty(B, dtype=torch.float64, device="cuda")
         cd.countdown_ffn_topk(plan, vid, dev_bf16(X), D["W_gate"], D["W_up"], D["W_down"], k,
