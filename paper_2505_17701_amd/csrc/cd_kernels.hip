@@ -1791,7 +1791,8 @@ constexpr uint32_t kSelNoKey = 0xffffffffu;             // slot past the row: ab
 __device__ __forceinline__ uint32_t sel_word(uint32_t d) { return d + 4u * (d >> 5); }
 
 // Order-preserving key of a coefficient: the bits of |c| (am = ~0, |c| keys) or
-// the signed float's bits mapped to an unsigned order (am = 0)
+// the signed float's bits mapped to an unsigned order (am = 0); the select
+// kernel's keys, written out there the same way
 __device__ __forceinline__ uint32_t sel_key(float c, uint32_t am)
 {
     const uint32_t u = __float_as_uint(c);
@@ -1870,10 +1871,14 @@ __device__ __forceinline__ void find_bin(const uint32_t *mine, const uint32_t (&
 // interpolates them itself, so no broadcast is needed). key[] keeps this
 // thread's keys, slots threadIdx.x + j * kTopkThreads, for callers that
 // flag the row's neurons afterwards. hook(binA, binB, sh0) runs in every
-// thread once the first pass has found the bins of both ranks: a key whose
-// first-pass bin (key >> sh0) lies above binB is above q, one below binA is
-// below it.
-template <int KPT, class Hook>
+// thread once the first pass has found the bins of ranks lo and lo + 1: a key
+// whose first-pass bin (key >> sh0 within the 15 bits) lies below binB is at
+// most the rank-lo value, so not above q. ALL_SLOTS: every key slot loads,
+// slots past the row reading the zero chunk; otherwise only the slots in use
+// load, each under a uniform branch, which saves the select kernel 0.14 us at
+// 11008 keys but, in a caller that keeps more registers live, lets the
+// compiler wait for each branch's load in turn.
+template <int KPT, bool ALL_SLOTS, class Hook>
 __device__ __forceinline__ double topk_row(const float *__restrict__ c, int n, int use_abs, double k,
                                            uint32_t (&key)[KPT], const Hook &hook)
 {
@@ -1888,22 +1893,32 @@ __device__ __forceinline__ double topk_row(const float *__restrict__ c, int n, i
     __shared__ uint32_t val[2];
     const int lane = threadIdx.x % kWave;
     const int jn = (n + kTopkThreads - 1) / kTopkThreads;  // key slots in use (uniform)
-    // every slot loads (slots past the row read the zero chunk): a load under a
-    // branch per slot can leave the compiler waiting for each load in turn
     float cv[KPT];
 #pragma unroll
     for (int j = 0; j < KPT; ++j) {
         const int i = threadIdx.x + j * kTopkThreads;
-        cv[j] = *or_zero(i < n, c + i);
+        if constexpr (ALL_SLOTS) {
+            cv[j] = *or_zero(i < n, c + i);
+        } else {
+            cv[j] = 0.0f;
+            if (j < jn)  // uniform
+                cv[j] = *or_zero(i < n, c + i);
+        }
     }
     for (int i = threadIdx.x; i < kSelWords0 / 4; i += kTopkThreads)
         reinterpret_cast<uint4 *>(sm)[i] = make_uint4(0u, 0u, 0u, 0u);
     if (threadIdx.x < kSelList)
         list[threadIdx.x] = kSelNoKey;
-    const uint32_t am = use_abs ? ~0u : 0u;  // order_key without a branch per slot
+    // sel_key written out: through the helper the compiler no longer folds the
+    // absolute value into its select (one more VALU per key, 0.1 us)
+    const uint32_t am = use_abs ? ~0u : 0u;
 #pragma unroll
-    for (int j = 0; j < KPT; ++j)
-        key[j] = threadIdx.x + j * kTopkThreads < n ? sel_key(cv[j], am) : kSelNoKey;
+    for (int j = 0; j < KPT; ++j) {
+        const uint32_t u = __float_as_uint(cv[j]);
+        const uint32_t sk = u ^ ((uint32_t)((int32_t)u >> 31) | 0x80000000u);
+        key[j] = threadIdx.x + j * kTopkThreads < n ? ((u & 0x7fffffffu) & am) | (sk & ~am)
+                                                    : kSelNoKey;
+    }
     const double h = k * (double)(n - 1);
     int lo = (int)floor(h);
     if (lo > n - 1)
@@ -2059,7 +2074,7 @@ __global__ __launch_bounds__(kTopkThreads) void k_topk_select(const float *__res
                                                               int *__restrict__ act)
 {
     uint32_t key[KPT];
-    const double qv = topk_row<KPT>(coef + (size_t)blockIdx.x * ld, n, use_abs, k, key,
+    const double qv = topk_row<KPT, false>(coef + (size_t)blockIdx.x * ld, n, use_abs, k, key,
                                     NoFirstPassHook{});
     if (threadIdx.x == 0)
         q[blockIdx.x] = qv;
@@ -2224,18 +2239,19 @@ __global__ __launch_bounds__(kBlock) void k_gather_topk_w(const CoefArgs a, cons
 // (one per CU: the select's LDS fills it) finds the token's quantile itself,
 // the same way k_topk_select does, so no workgroup waits for another, and then
 // flags its own contiguous slice of at most 64 neurons. Every wave holds the
-// whole slice (lane l: neuron l) and takes the same ballots, so the active
-// neurons are dealt to the 16 waves without a barrier: in order, first those
-// known to be active early, then the rest; wave w gets positions w, w + 16,
-// ... A neuron is known to be active once the select's first pass has placed
-// the order statistics in their bins and its key lies in a higher bin: each
-// wave issues the loads of its early neuron's first row there, so their HBM
-// round trip overlaps the rest of the select (the predictors' W_up row follows
-// q: both rows in flight through the select would spill registers, and issuing
-// W_up once the keys are placed measured no faster). The token is loaded with
-// the keys and copied into LDS the select no longer uses after its first pass.
-// The dot products and reductions are those of k_gather_topk_w (the same
-// order, so s and act are the same bits). Workgroup 0 stores q.
+// whole slice (lane l: neuron l) and takes the same ballots, so work is dealt
+// to the 16 waves without a barrier. Once the select's first pass has found
+// the bins of ranks lo and lo + 1, every active neuron has its key in the bin
+// of rank lo + 1 or above (keys in lower bins are at most the rank-lo value,
+// hence at most q), so the slice's candidates are known: the neurons of those
+// bins, in order, candidate p going to wave p % 16. Each wave issues the first
+// row of its first candidate there, so its HBM round trip overlaps the rest of
+// the select; after q it finishes the candidates that are active (the other
+// rows stay unused). The predictors' W_up row follows q: both rows in flight
+// through the select would spill registers. The token is loaded with the keys
+// and copied into LDS the select no longer uses after its first pass. The dot
+// products and reductions are those of k_gather_topk_w (the same order, so s
+// and act are the same bits). Workgroup 0 stores q.
 constexpr int kFusedTopkGrid = 256;        // one workgroup per CU of the MI355X
 constexpr int kFusedTopkSlice = kWave;     // neurons per workgroup at most
 constexpr int kFusedTokWord = 2 * kSelBins;  // token copy: past the later passes' bins
@@ -2269,21 +2285,18 @@ __global__ __launch_bounds__(kTopkThreads) void k_topk_gather1(const CoefArgs a,
                         : zero16();
 
     u32x4 wg[NK], wu[TWO ? NK : 1];
-    uint64_t early_m = 0;  // the slice's neurons known to be active after the first pass
-    int pre = -1;          // this wave's early neuron, its first row in flight (wave-uniform)
-    // c != 0: the signed keys of -0 and +0 differ while the values are equal
+    uint64_t cand = 0;  // the slice's candidates: keys in the bin of rank lo + 1 or above
     const auto early = [&](uint32_t, uint32_t binB, int sh0) {
         if (xt)
             *reinterpret_cast<u32x4 *>(sm + kFusedTokWord + 4 * threadIdx.x) = xv;
         const uint32_t key = sel_key(c, TWO ? 0u : ~0u);
-        early_m = ballot(mine && c != 0.0f && ((key >> sh0) & (uint32_t)(kSelBins0 - 1)) > binB);
-        if (wave < __builtin_popcountll(early_m)) {
-            pre = lo + nth_set_bit(early_m, wave);
-            load_row<NK>(wg, w1 + (size_t)pre * a.d_model, a.d_model, lane);
-        }
+        cand = ballot(mine && ((key >> sh0) & (uint32_t)(kSelBins0 - 1)) >= binB);
+        if (wave < __builtin_popcountll(cand))
+            load_row<NK>(wg, w1 + (size_t)(lo + nth_set_bit(cand, wave)) * a.d_model, a.d_model,
+                         lane);
     };
     uint32_t key[KPT];
-    const double qv = topk_row<KPT>(a.coef, a.d_ff, TWO ? 0 : 1, k, key, early);
+    const double qv = topk_row<KPT, true>(a.coef, a.d_ff, TWO ? 0 : 1, k, key, early);
     if (blockIdx.x == 0 && threadIdx.x == 0)
         q[0] = qv;
     for (int i = blockIdx.x * kTopkThreads + threadIdx.x; i < a.d_model; i += gridDim.x * kTopkThreads)
@@ -2291,19 +2304,19 @@ __global__ __launch_bounds__(kTopkThreads) void k_topk_gather1(const CoefArgs a,
     const bool act = mine && (double)(TWO ? c : fabsf(c)) > qv;
     if (wave == 0 && mine)
         a.act[row] = act ? 1 : 0;
-    const uint64_t am = ballot(act);
-    const uint64_t first = am & early_m;  // (= early_m: an early neuron's value is above q)
-    const uint64_t rest = am & ~early_m;
-    const int nfirst = __builtin_popcountll(first), nall = __builtin_popcountll(am);
+    const uint64_t am = ballot(act);  // within cand
+    const int ncand = __builtin_popcountll(cand);
     Tokens<1, NK, false> tok;
     tok.lds = sm + kFusedTokWord;  // written before the select's later barriers
-    for (int p = wave; p < nall; p += kWaves) {
-        const int r = lo + (p < nfirst ? nth_set_bit(first, p) : nth_set_bit(rest, p - nfirst));
-        if (r != pre)
+    for (int p = wave; p < ncand; p += kWaves) {
+        const int i = nth_set_bit(cand, p);
+        if (!((am >> i) & 1u))
+            continue;
+        const int r = lo + i;
+        if (p != wave)  // the first candidate's row is in flight already
             load_row<NK>(wg, w1 + (size_t)r * a.d_model, a.d_model, lane);
         if constexpr (TWO)
             load_row<NK>(wu, a.Wu + (size_t)r * a.d_model, a.d_model, lane);
-        pre = -1;
         if constexpr (TWO)
             pred_finish<1, NK, false>(a, tok, wg, wu, r, lane);
         else if (cats)
