@@ -27,7 +27,10 @@
 //   per-token threshold: the coefficient kernel writes the dense
 //     coefficients, one workgroup per token selects its quantile (one wide
 //     radix pass, then the few keys of the two bins ranked by counting), a
-//     gather kernel thresholds and gathers.
+//     gather kernel thresholds and gathers. A single token runs select,
+//     flags and gather in one launch: every workgroup selects on its own and
+//     gathers its slice, its rows loaded as soon as the select's first pass
+//     bounds the active set.
 // The residual stream of a layer stack (h += y, x = bf16(RMSNorm(h))) is a
 // small kernel of its own, or part of the latent kernel with the predictor.
 #include "cd_device.hpp"
