@@ -69,6 +69,27 @@ def test_deterministic_y_is_bit_identical(layer, variant, B):
     atom.close()
 
 
+@pytest.mark.parametrize("variant", ["mono", "cats"])
+def test_deterministic_wide_rows_single_token(variant):
+    """Rows of 8192 columns at batch 1 (16 loads per lane and row):
+    coefficients, s and y are the same bits on every call."""
+    from paper_2505_17701_amd import binding as cd
+
+    dm, dff = 8192, 1048
+    wide = Layer(make_layer(2130, dm, dff, 0.02))
+    x = make_tokens(2131, 1, dm)
+    u, g, _ = oracle.coefficients(x, wide.h["W_gate"], wide.h["W_up"])
+    c = np.abs(u if variant == "mono" else g / (1.0 + np.exp(-g)))
+    thld = float(np.float32(np.quantile(c, 0.8)))
+    det = cd.Plan(dm, dff, max_batch=1, keep_coef=True, deterministic=True)
+    outs = [run_gpu(det, variant, wide, x, thld) for _ in range(3)]
+    for o in outs[1:]:
+        for a, b in zip(o, outs[0]):
+            assert np.array_equal(a, b), "deterministic output differs between calls"
+    check_call(variant, wide, x, thld, outs[0], f"deterministic wide {variant}")
+    det.close()
+
+
 @pytest.mark.parametrize("B", [1, 3])
 @pytest.mark.parametrize("variant", ["mono", "dual_ideal", "dual_pred"])
 def test_deterministic_per_token_path(layer, variant, B):

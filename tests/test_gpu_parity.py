@@ -275,7 +275,8 @@ def test_single_active_row(tiny):
 
 @pytest.mark.parametrize("d_model,d_ff,B", [(264, 1000, 3), (1032, 520, 2), (8, 8, 1),
                                             (2056, 4104, 7), (512, 16, 4), (8192, 1048, 1),
-                                            (1544, 2056, 2), (4096, 776, 1), (4160, 1000, 4)])
+                                            (1544, 2056, 2), (4096, 776, 1), (4160, 1000, 4),
+                                            (4160, 1000, 1), (6152, 520, 1)])
 @pytest.mark.parametrize("variant", ["mono", "dual_ideal", "dual_pred", "cats"])
 def test_ragged_shapes(d_model, d_ff, B, variant):
     L = make_layer(700 + d_model, d_model, d_ff, 0.05)

@@ -189,6 +189,18 @@ def test_batch1_single_launch_matches_batch2_kernels(variant, shape):
     plan.close()
 
 
+@pytest.mark.parametrize("variant", ["mono", "cats"])
+def test_topk_wide_rows_single_token(variant):
+    """Rows of 8192 columns at batch 1 (16 loads per lane and row in the
+    coefficient kernel, d_ff above the one-launch limit's slices): the dense
+    coefficients, the select and the gather."""
+    layer = small(variant, 8192, 1048, 5)
+    x = make_tokens(1320, 1, 8192)
+    n, flips, rel = check_topk(variant, layer, x, 0.8, f"wide topk {variant}")
+    if flips == 0:
+        assert n == 1048 - 1 - math.floor(0.8 * 1047), n
+
+
 def test_topk_rejects():
     from paper_2505_17701_amd import binding as cd
 
