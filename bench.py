@@ -221,8 +221,9 @@ def pooled_thresholds(dm, dff, dr, L, X_cal, variants, ks):
 def stream_ceiling(ctx, nk):
     """Plain streaming reads (countdown_stream_read), timed like the kernels with one
     event pair around a graph-replayed loop: the W_up matrices of the rotated weight
-    copies (the bytes the M coefficient kernel streams densely, one launch each) and a
-    1 GiB buffer (the asymptotic read rate)."""
+    copies (the bytes the M coefficient kernel streams densely, one launch each), a
+    1 GiB buffer (the asymptotic read rate), and a 32-byte read, whose time per
+    launch is what one more dependent launch costs in a graph."""
     import torch
 
     from paper_2505_17701_amd import binding as cd
@@ -237,6 +238,9 @@ def stream_ceiling(ctx, nk):
     ms = time_steps_graph(lambda i: cd.countdown_stream_read(big, sink), 40, 5)
     out["1GiB"] = {"bytes": nb, "us": ms * 1e3, "GBs": nb / (ms * 1e-3) / 1e9}
     del big
+    tiny = torch.zeros(16, dtype=torch.bfloat16, device="cuda")
+    ms = time_steps_graph(lambda i: cd.countdown_stream_read(tiny, sink), 400, 20)
+    out["launch"] = {"bytes": 32, "us": ms * 1e3}
     torch.cuda.synchronize()
     torch.cuda.empty_cache()
     return out
@@ -474,7 +478,8 @@ def roofline(res, variant, key, ceiling=None):
         # measured read ceilings: a plain read of one rotated W_up per launch, and of 1 GiB
         obj.update({"stream_W_up_GBs": ceiling["W_up"]["GBs"],
                     "stream_1GiB_GBs": ceiling["1GiB"]["GBs"],
-                    "frac_of_stream_1GiB": ach / ceiling["1GiB"]["GBs"]})
+                    "frac_of_stream_1GiB": ach / ceiling["1GiB"]["GBs"],
+                    "dependent_launch_us": ceiling["launch"]["us"]})
     return obj
 
 
