@@ -454,7 +454,10 @@ def kernel_desc(variant, B=1):
             "dense": "k_coef_dual (dense W_gate + W_up GEMV, s)",
             "mono_topk": f"k_coef_mono + {sel} (per-token threshold)",
             "dual_ideal_topk": "k_coef_dual + k_topk_select (per-token threshold; the select "
-                               "sets the flags, s is the coefficient)",
+                               "sets the flags, s is the coefficient)"
+                               + ("; the phase timed alone: a whole one-token call runs "
+                                  "k_coef_dual, then k_topk_down1 (select, flags and down "
+                                  "projection in one launch)" if B == 1 else ""),
             "dual_pred_topk": f"k_latent + {pred} + {sel} (per-token threshold)",
             "cats": "k_coef_mono<CATS> (dense W_gate GEMV, SiLU, threshold, W_up gather)",
             "cats_topk": f"k_coef_mono<CATS> + {sel} (per-token threshold)",
@@ -997,9 +1000,13 @@ def main():
                    "realised_sparsity": main_res["realised_sparsity"],
                    "algorithmic_bytes_per_step": main_res["algorithmic_bytes"],
                    "parallelism": "single GPU"},
-        "kernels": {k: main_res.get(k) for k in ("coef_kernel_us", "coef_kernel_GBs",
-                                                  "down_kernel_us", "down_kernel_GBs")
-                    if main_res.get(k) is not None},
+        "kernels": {**{k: main_res.get(k) for k in ("coef_kernel_us", "coef_kernel_GBs",
+                                                     "down_kernel_us", "down_kernel_GBs")
+                       if main_res.get(k) is not None},
+                    **({"phases_note": "each phase timed alone (coefficient phase with its "
+                                       "select, then k_down); a whole one-token call fuses "
+                                       "the select into the down launch (k_topk_down1)"}
+                       if args.variant == "dual_ideal_topk" and args.batch == 1 else {})},
         "roofline_traffic_source": "profiles/ PMC summary of the same kernel source (FETCH_SIZE "
                                    "+ WRITE_SIZE scaled by a 256 MiB copy), null when absent "
                                    "or stale; not read in this run",

@@ -177,8 +177,10 @@ cd_status countdown_ffn_cats(cd_plan *plan, const uint16_t *x, int B, const uint
  * coefficients. k in [0, 1]; d_ff <= 32768 (CD_EUNSUPPORTED beyond). The
  * call runs the coefficient kernel over all neurons, a per-token selection
  * kernel, the gather of IDX and the down projection; for one token with
- * d_model <= 4096 and d_ff <= 16384 (not ideal D) the selection and the
- * gather are one launch. Results are the same either way.
+ * d_model <= 4096 and d_ff <= 16384 the selection and the gather are one
+ * launch (ideal D, which has nothing to gather: the selection, the flags and
+ * the down projection; not in a deterministic plan). Results are the same
+ * either way, y to fp32 rounding.
  */
 cd_status countdown_ffn_topk(cd_plan *plan, int variant, const uint16_t *x, int B,
                              const uint16_t *W_gate, const uint16_t *W_up, const uint16_t *W_down,

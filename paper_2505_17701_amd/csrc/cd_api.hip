@@ -362,7 +362,20 @@ cd_status run_ffn_topk(cd_plan *p, int variant, const uint16_t *x, int B, const 
         st = launched(cdk::launch_coef(kernel_variant(variant), ca, s));
         if (st != CD_OK)
             return st;
-        st = launched(cdk::launch_topk(kernel_variant(variant), ca, k, thld_out ? thld_out : p->q, s));
+        double *q = thld_out ? thld_out : p->q;
+        if (variant == CD_VARIANT_DUAL_IDEAL && (p->phases & CD_PHASE_DOWN)) {
+            // s is the coefficient itself: one token's select, flags and down
+            // projection can run as one launch
+            cdk::DownArgs da = down_args(p, B, Wd, y);
+            da.s = p->coef;
+            if (cdk::topk_down_fused(da)) {
+                st = launched(cdk::launch_topk_down1(da, p->coef, p->act, k, q, s));
+                if (st == CD_OK)
+                    keep_state(p, B, true);
+                return st;
+            }
+        }
+        st = launched(cdk::launch_topk(kernel_variant(variant), ca, k, q, s));
         if (st != CD_OK)
             return st;
         keep_state(p, B, variant == CD_VARIANT_DUAL_IDEAL);

@@ -79,6 +79,13 @@ hipError_t launch_export(const int *act, const float *s_rows, int nb, int d_ff, 
 // their tokens' thresholds (gathering W_gate, or W_gate and W_up). For ideal
 // D-CountDown the select sets act and s stays in a.coef. d_ff <= 32768.
 hipError_t launch_topk(int variant, const CoefArgs &a, double k, double *q, hipStream_t s);
+// Per-token ideal D-CountDown of one token: select, flags and down projection in
+// one launch (after the coefficient kernel wrote the dense s to coef and zeroed y),
+// when topk_down_fused(a) holds: one token, d_model <= 4096, d_ff <= 16384, no
+// per-range partials (deterministic plans keep the separate kernels).
+bool topk_down_fused(const DownArgs &a);
+hipError_t launch_topk_down1(const DownArgs &a, const float *coef, int *act, double k,
+                             double *q, hipStream_t s);
 constexpr int kTopkMaxDff = 32768;
 // Per-token linear-interpolation quantile of coef rows [T][ld] (n used entries).
 hipError_t launch_select(const float *coef, int ld, int n, int T, int use_abs, double k,

@@ -2353,6 +2353,109 @@ __global__ __launch_bounds__(kTopkThreads) void k_topk_gather1(const CoefArgs a,
     }
 }
 
+// Per-token ideal D-CountDown for a single token in one launch. s is the dense
+// coefficient already, so after the select only the flags and the down
+// projection remain, and for a neuron range both need nothing but q. Every
+// workgroup (one per CU) selects on its own, as k_topk_gather1 does, then
+// takes neuron range g and 512-column chunk c of y: it flags the range (the
+// workgroups of chunk 0 store the flags), compacts the active neurons into LDS
+// in ascending order, keeps kFusedDownRows W_down rows in flight per wave,
+// adds the 16 waves' partial sums per column in LDS and adds them to y with
+// one fp32 atomic per column (y was zeroed by the coefficient kernel).
+// Workgroup 0 stores q.
+constexpr int kFusedDownRows = 16;  // W_down rows in flight per wave
+
+__global__ __launch_bounds__(kTopkThreads) void k_topk_down1(const DownArgs a,
+                                                             const float *__restrict__ coef,
+                                                             int *__restrict__ act_out, double k,
+                                                             double *__restrict__ q)
+{
+    constexpr int kWaves = kTopkThreads / kWave;
+    constexpr int U = kFusedDownRows;
+    extern __shared__ __align__(16) uint32_t sm[];
+    __shared__ int wcnt[kWaves];
+    const int lane = threadIdx.x % kWave, wave = threadIdx.x / kWave;
+    uint32_t key[16];
+    const double qv = topk_row<16, true>(coef, a.d_ff, 1, k, key, NoFirstPassHook{});
+    if (blockIdx.x == 0 && threadIdx.x == 0)
+        q[0] = qv;
+    __syncthreads();  // the select's LDS is free from here on
+    int *lrow = reinterpret_cast<int *>(sm);                                 // [kTopkThreads]
+    float *lsv = reinterpret_cast<float *>(sm + kTopkThreads);               // [kTopkThreads]
+    float *red = reinterpret_cast<float *>(sm + 2 * kTopkThreads);           // [kWaves][512]
+    const int c = blockIdx.x % a.gc, g = blockIdx.x / a.gc;
+    const int r0 = g * a.rows_per_group;  // rows_per_group <= kTopkThreads (host)
+    const int r1 = min(a.d_ff, r0 + a.rows_per_group);
+    const int row = r0 + threadIdx.x;
+    float sv = 0.0f;
+    bool act = false;
+    if (row < r1) {  // threadIdx.x < rows_per_group included
+        sv = coef[row];
+        act = (double)fabsf(sv) > qv;
+        if (c == 0)
+            act_out[row] = act ? 1 : 0;
+    }
+    const uint64_t m = ballot(act);
+    if (lane == 0)
+        wcnt[wave] = __popcll(m);
+    __syncthreads();
+    int base = 0, nl = 0;
+    for (int v = 0; v < kWaves; ++v) {
+        base += v < wave ? wcnt[v] : 0;
+        nl += wcnt[v];
+    }
+    if (act) {
+        const int pos = base + lanes_below(m);
+        lrow[pos] = row;
+        lsv[pos] = sv;
+    }
+    __syncthreads();
+    if (nl == 0)  // uniform for the workgroup
+        return;
+
+    const int col = c * kColsPerLoad + lane * 8;
+    const bool colok = col < a.d_model;
+    float acc[8];
+#pragma unroll
+    for (int e = 0; e < 8; ++e)
+        acc[e] = 0.0f;
+    for (int q0 = wave; q0 < nl; q0 += kWaves * U) {
+        u32x4 w[U];
+#pragma unroll
+        for (int t = 0; t < U; ++t) {
+            const int r = q0 + t * kWaves;
+            w[t] = (r < nl && colok) ? load16_stream(a.Wd + (size_t)lrow[r] * a.d_model + col)
+                                     : zero16();
+        }
+#pragma unroll
+        for (int t = 0; t < U; ++t) {
+            const int r = q0 + t * kWaves;
+            if (r >= nl)
+                break;
+            const float wf[8] = {bf16_lo(w[t].x), bf16_hi(w[t].x), bf16_lo(w[t].y), bf16_hi(w[t].y),
+                                 bf16_lo(w[t].z), bf16_hi(w[t].z), bf16_lo(w[t].w), bf16_hi(w[t].w)};
+            const float s_r = lsv[r];
+#pragma unroll
+            for (int e = 0; e < 8; ++e)
+                acc[e] = fmaf(s_r, wf[e], acc[e]);
+        }
+    }
+#pragma unroll
+    for (int e = 0; e < 8; ++e)
+        red[wave * kColsPerLoad + lane * 8 + e] = acc[e];
+    __syncthreads();
+    if (threadIdx.x < kColsPerLoad) {
+        const int gcol = c * kColsPerLoad + threadIdx.x;
+        if (gcol < a.d_model) {
+            float v = 0.0f;
+#pragma unroll
+            for (int w = 0; w < kWaves; ++w)
+                v += red[w * kColsPerLoad + threadIdx.x];
+            unsafeAtomicAdd(a.y + gcol, v);
+        }
+    }
+}
+
 // ------------------------------------------------------------------ launchers
 
 // kernels staging more than 64 KB in LDS opt in to the larger gfx950 limit
@@ -2801,6 +2904,34 @@ static hipError_t launch_topk_gather1(int variant, const CoefArgs &a, double k, 
     const int cats = variant == kCats ? 1 : 0;
     return variant == kDualPred ? topk_gather1_two<true>(cats, a, k, q, grid, s)
                                 : topk_gather1_two<false>(cats, a, k, q, grid, s);
+}
+
+bool topk_down_fused(const DownArgs &a)
+{
+    return a.nb == 1 && !a.part && col_tile(a.d_model) <= 8 &&
+           a.d_ff <= kFusedTopkGrid * kFusedTopkSlice;
+}
+
+// 512-column chunks x neuron ranges, kFusedTopkGrid workgroups at most: at most
+// 8 chunks (d_model <= 4096), so at least 32 ranges of at most 512 neurons
+hipError_t launch_topk_down1(const DownArgs &args, const float *coef, int *act, double k,
+                             double *q, hipStream_t s)
+{
+    if (!topk_down_fused(args))
+        return hipErrorInvalidValue;
+    DownArgs a = args;
+    a.gc = (a.d_model + kColsPerLoad - 1) / kColsPerLoad;
+    a.gr = kFusedTopkGrid / a.gc;
+    a.rows_per_group = (a.d_ff + a.gr - 1) / a.gr;
+    if (a.rows_per_group > kTopkThreads)
+        return hipErrorInvalidValue;
+    const size_t lds = topk_select_lds_bytes();  // holds the lists and the partial sums too
+    static_assert((2 * kTopkThreads + (kTopkThreads / kWave) * kColsPerLoad) * 4 <=
+                      ((size_t)kSelWords0 + kSelList + kWave) * 4,
+                  "down lists and partial sums within the select's LDS");
+    allow_lds(k_topk_down1, lds);
+    k_topk_down1<<<a.gc * a.gr, kTopkThreads, lds, s>>>(a, coef, act, k, q);
+    return hipGetLastError();
 }
 
 hipError_t launch_topk(int variant, const CoefArgs &a, double k, double *q, hipStream_t s)

@@ -125,6 +125,11 @@ def test_topk_count_law_llama7b():
         print(f"7b topk k={k}: n={n} flips={flips} rel={rel:.2e}", flush=True)
     n, flips, rel = check_topk("dual_ideal", layer, w.tokens(2), 0.9, "7b dual topk B=2")
     print(f"7b dual topk B=2: n={n} flips={flips} rel={rel:.2e}", flush=True)
+    # one token: select, flags and down projection in one launch
+    n, flips, rel = check_topk("dual_ideal", layer, w.tokens(4)[3:4], 0.9, "7b dual topk B=1")
+    if flips == 0:
+        assert n == w.d_ff - 1 - math.floor(0.9 * (w.d_ff - 1)), n
+    print(f"7b dual topk B=1: n={n} flips={flips} rel={rel:.2e}", flush=True)
 
 
 def test_topk_predictor_batch():
@@ -135,20 +140,21 @@ def test_topk_predictor_batch():
         print(f"8b pred topk B={B}: n={n} flips={flips} rel={rel:.2e}", flush=True)
 
 
-@pytest.mark.parametrize("variant", ["mono", "cats", "dual_pred", "dual_tern"])
+@pytest.mark.parametrize("variant", ["mono", "cats", "dual_ideal", "dual_pred", "dual_tern"])
 @pytest.mark.parametrize("shape", [(4096, 11008, 0.9, None), (4096, 14336, 0.9, None),
                                    (512, 16384, 0.8, None), (256, 32768, 0.7, None),
                                    (1032, 1000, 0.75, None), (264, 16, 0.5, None),
                                    (1024, 11008, 0.7, "cluster"), (256, 4104, 0.5, "all")])
 def test_batch1_single_launch_matches_batch2_kernels(variant, shape):
-    """A single token (d_ff <= 16384, d_model <= 4096) runs its select, flags and
+    """A single token (d_model <= 4096, d_ff <= 16384) runs its select, flags and
     gather in one launch (every workgroup selects, then gathers its own slice of
     neurons, with the loads of neurons known to be active after the select's
-    first pass issued there); two tokens run a select kernel and a gather kernel.
-    A token alone and the same token twice give the same bits: coefficients,
-    threshold, index set and s. "cluster" (most coefficients within a relative
-    2^-8 of each other, with ties) and "all" (every coefficient equal) send the
-    select through its radix passes."""
+    first pass issued there), and for ideal D its select, flags and down
+    projection; two tokens run a select kernel and a gather kernel. A token
+    alone and the same token twice give the same bits (coefficients, threshold,
+    IDX and s) and the same y to fp32 rounding. "cluster" (most coefficients
+    within a relative 2^-8 of each other, with ties) and "all" (every
+    coefficient equal) send the select through its radix passes."""
     from paper_2505_17701_amd import binding as cd
     from workloads import make_ternary
 
@@ -159,7 +165,8 @@ def test_batch1_single_launch_matches_batch2_kernels(variant, shape):
     P = make_predictor(2200 + dm, dm, 64, dff, 0.05) if variant == "dual_pred" else None
     T = make_ternary(2200 + dm, dm, dff) if variant == "dual_tern" else None
     if dup:  # the matrix whose rows set the coefficient
-        W = {"mono": L["W_up"], "cats": L["W_gate"], "dual_pred": P["B_t"] if P else None}[variant]
+        W = {"mono": L["W_up"], "cats": L["W_gate"], "dual_ideal": L["W_up"],
+             "dual_pred": P["B_t"] if P else None}[variant]
         rows = np.arange(dff) % 16 != 0 if dup == "cluster" else np.arange(dff) >= 0
         W[rows] = W[0]
         if dup == "cluster":
@@ -174,18 +181,23 @@ def test_batch1_single_launch_matches_batch2_kernels(variant, shape):
         B = X.shape[0]
         q = torch.zeros(B, dtype=torch.float64, device="cuda")
         if variant == "dual_tern":
-            cd.countdown_ffn_tern_topk(plan, dev_bf16(X), D["W_gate"], D["W_up"], D["W_down"],
-                                       D["theta_p"], k, thld_out=q)
+            y = cd.countdown_ffn_tern_topk(plan, dev_bf16(X), D["W_gate"], D["W_up"], D["W_down"],
+                                           D["theta_p"], k, thld_out=q)
         else:
-            cd.countdown_ffn_topk(plan, VID[variant], dev_bf16(X), D["W_gate"], D["W_up"],
-                                  D["W_down"], k, A_t=D.get("A_t"), B_t=D.get("B_t"), thld_out=q)
+            y = cd.countdown_ffn_topk(plan, VID[variant], dev_bf16(X), D["W_gate"], D["W_up"],
+                                      D["W_down"], k, A_t=D.get("A_t"), B_t=D.get("B_t"),
+                                      thld_out=q)
         idx, s_c, coef = cd.countdown_export_active(plan)
-        got.append((q.cpu().numpy(), idx.cpu().numpy(), s_c.cpu().numpy(), coef.cpu().numpy()))
-    (q1, i1, s1, c1), (q2, i2, s2, c2) = got
+        got.append((q.cpu().numpy(), idx.cpu().numpy(), s_c.cpu().numpy(), coef.cpu().numpy(),
+                    y.cpu().numpy().astype(np.float64)))
+    (q1, i1, s1, c1, y1), (q2, i2, s2, c2, y2) = got
     assert np.array_equal(c1[0], c2[0]) and np.array_equal(c2[0], c2[1]), "coefficients"
     assert q1[0] == q2[0] == q2[1], (q1, q2)
     assert np.array_equal(i1, i2), (len(i1), len(i2))
     assert np.array_equal(s1[0], s2[0]) and np.array_equal(s2[0], s2[1]), "s"
+    scale = max(np.abs(y2).max(), 1e-30)
+    assert np.abs(y1[0] - y2[0]).max() <= 1e-5 * scale, "y"
+    assert np.abs(y2[0] - y2[1]).max() <= 1e-5 * scale, "y of the two tokens"
     plan.close()
 
 
