@@ -115,6 +115,36 @@ def test_topk_extremes(k):
         assert len(idx_g) >= layer.d_ff - 2
 
 
+@pytest.mark.parametrize("variant", ["mono", "dual_ideal", "dual_pred", "cats"])
+@pytest.mark.parametrize("shape", [(8, 8, 0.5), (8, 16384, 0.9), (4096, 8, 0.3), (520, 24, 0.6),
+                                   (1544, 9000, 0.1), (3080, 16384, 0.95)])
+def test_topk_single_token_edges(variant, shape):
+    """One token takes the one-launch kernels (select with gather, or for ideal
+    D select with down projection) at their smallest and largest shapes: 8
+    columns or neurons, 16384 neurons, a 520-column row (one 8-column chunk past
+    512), 90% active."""
+    dm, dff, k = shape
+    layer = small(variant, dm, dff, 7 * dm + dff)
+    x = make_tokens(1500 + dm + dff, 1, dm)
+    n, flips, rel = check_topk(variant, layer, x, k, f"one token {variant} {shape}")
+    if flips == 0:
+        assert n == dff - 1 - math.floor(k * (dff - 1)), (n, dff, k)
+
+
+@pytest.mark.parametrize("variant", ["mono", "dual_ideal", "cats"])
+@pytest.mark.parametrize("k", [0.0, 1.0])
+def test_topk_extremes_single_token(variant, k):
+    """k = 1 keeps nothing (y = 0); k = 0 keeps every neuron but the token's minimum."""
+    layer = small(variant, 512, 520, 5)
+    x = make_tokens(1401, 1, 512)
+    if k == 1.0:
+        y_g, idx_g, _, _ = run_topk(variant, layer, x, k)
+        assert len(idx_g) == 0 and not y_g.any()
+    else:
+        n, flips, rel = check_topk(variant, layer, x, k, f"one token {variant} k=0")
+        assert n == layer.d_ff - 1 or flips, n
+
+
 def test_topk_count_law_llama7b():
     w = WORKLOADS["llama7b_4096x11008"]
     layer = Layer(w.layer())
