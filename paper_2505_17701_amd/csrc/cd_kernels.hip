@@ -1367,35 +1367,46 @@ __global__ __launch_bounds__(kBlock) void k_down(const DownArgs a)
     const int r0 = g * cap;
     const int r1 = min(a.d_ff, r0 + cap);
 
+    // four consecutive neurons per thread: 16-byte flag and s loads, one pass
+    // per 1024 neurons (ranges are multiples of 4 neurons, so a quad is whole)
     int nl = 0;
-    for (int t0 = r0; t0 < r1; t0 += kBlock) {
-        const int row = t0 + threadIdx.x;
-        bool valid = false;
-        float sv[B];
+    for (int t0 = r0; t0 < r1; t0 += 4 * kBlock) {
+        const int row = t0 + 4 * threadIdx.x;
+        const bool ok = row < r1;
+        const int4 av = *or_zero(ok, reinterpret_cast<const int4 *>(a.act + row));
+        const int f[4] = {av.x != 0, av.y != 0, av.z != 0, av.w != 0};
+        float sv[B][4];
 #pragma unroll
-        for (int b = 0; b < B; ++b)
-            sv[b] = 0.0f;
-        if (row < r1) {
-            valid = a.act[row] != 0;
-#pragma unroll
-            for (int b = 0; b < B; ++b)
-                if (b < a.nb)
-                    sv[b] = a.s[(size_t)b * a.d_ff + row];
+        for (int b = 0; b < B; ++b) {
+            const float4 v =
+                *or_zero(ok && b < a.nb, reinterpret_cast<const float4 *>(a.s + (size_t)b * a.d_ff + row));
+            sv[b][0] = v.x;
+            sv[b][1] = v.y;
+            sv[b][2] = v.z;
+            sv[b][3] = v.w;
         }
-        const uint64_t m = ballot(valid);
+        int below = 0, tot = 0;
+#pragma unroll
+        for (int k = 0; k < 4; ++k) {
+            const uint64_t m = ballot(f[k] != 0);
+            below += lanes_below(m);
+            tot += __popcll(m);
+        }
         if (lane == 0)
-            wcnt[wave] = __popcll(m);
+            wcnt[wave] = tot;
         __syncthreads();
-        int base = nl;
+        int pos = nl + below;
         for (int v = 0; v < wave; ++v)
-            base += wcnt[v];
-        if (valid) {
-            const int pos = base + lanes_below(m);
-            lrow[pos] = row;
+            pos += wcnt[v];
 #pragma unroll
-            for (int b = 0; b < B; ++b)
-                lsv[b * cap + pos] = sv[b];
-        }
+        for (int k = 0; k < 4; ++k)
+            if (f[k]) {
+                lrow[pos] = row + k;
+#pragma unroll
+                for (int b = 0; b < B; ++b)
+                    lsv[b * cap + pos] = sv[b][k];
+                ++pos;
+            }
         nl += wcnt[0] + wcnt[1] + wcnt[2] + wcnt[3];
         __syncthreads();
     }
@@ -2526,10 +2537,10 @@ void down_grid(int d_model, int d_ff, int bt, int *gc, int *gr, int *rows_per_gr
         r = d_ff / 16;
     if (r < 1)
         r = 1;
-    const int max_rows = (int)((65536 - down_lds_bytes(0, bt)) / (4 * (1 + bt)));
+    const int max_rows = (int)((65536 - down_lds_bytes(0, bt)) / (4 * (1 + bt))) & ~3;
     if ((d_ff + r - 1) / r > max_rows)
         r = (d_ff + max_rows - 1) / max_rows;
-    *rows_per_group = (d_ff + r - 1) / r;
+    *rows_per_group = ((d_ff + r - 1) / r + 3) & ~3;  // whole quads of neurons (16-byte loads)
     *gr = (d_ff + *rows_per_group - 1) / *rows_per_group;
 }
 
