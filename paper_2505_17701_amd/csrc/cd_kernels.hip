@@ -693,61 +693,81 @@ struct MfmaTokens {
 // MFMA gather with the weight rows staged in LDS. Loads in the MFMA operand
 // layout (16 rows x 64 B per instruction) reach about 60% of the HBM rate of
 // row-contiguous loads on gathered rows (measured), so a wave loads each
-// batch of kWtSteps steps (128 columns) of its tile's 16 W_gate and W_up
-// rows four rows per instruction (256 B of a row per 16 lanes), writes them
-// to its own LDS tile (rows padded by 16 B) and reads the A operands back;
-// the token operand (L2-resident) is loaded with the batch. The next batch
-// is in flight while the current one is consumed.
-constexpr int kWtSteps = 4;
-constexpr int kWtCols = kWtSteps * 32;           // columns of a batch
-constexpr int kWtStride = kWtCols + 8;           // bf16 per tile row
-constexpr int kWtWave = 2 * kTile * kWtStride;   // bf16 per wave: W_gate and W_up tiles
-constexpr int kWtLoads = kTile / 4;              // loads per lane and matrix (4 rows each)
-
-struct WtBatch {
-    u32x4 w[2 * kWtLoads];  // [0, 4): W_gate rows 4q + (lane >> 4); [4, 8): W_up
-    u32x4 x[kWtSteps];
+// batch of STEPS steps (32 columns each) of its tile's 16 W_gate and W_up rows
+// with 4 STEPS lanes on each row's piece (256 B of a row per load at 4 steps,
+// 512 B at 8), writes them to its own LDS tile (rows padded by 16 B) and
+// reads the A operands back; the token operand (L2-resident) is loaded with
+// the batch.
+template <int STEPS>
+struct WtShape {
+    static constexpr int kCols = STEPS * 32;              // columns of a batch
+    static constexpr int kStride = kCols + 8;             // bf16 per tile row
+    static constexpr int kWaveElems = 2 * kTile * kStride;  // bf16 per wave: W_gate and W_up tiles
+    static constexpr int kLanesPerRow = kCols / 8;        // lanes on one row's piece
+    static constexpr int kRowsPerLoad = kWave / kLanesPerRow;
+    static constexpr int kLoads = kTile / kRowsPerLoad;   // loads per lane and matrix
 };
 
-__device__ __forceinline__ void wt_load(WtBatch &bt, const CoefArgs &a, const int (&row)[kWtLoads],
-                                        uint32_t have, const uint16_t *xrow, bool xreal, int s,
-                                        int s1, int lane)
+// batch widths: the low-rank kernel's 256 columns with one batch in flight
+// per wave measured 1-1.5% faster at 5-8 tokens than 128 columns with two in
+// flight (two 256-column batches take 254 VGPRs, one wave per SIMD); the
+// ternary kernel, and the low-rank one at rank 1024 (latent in LDS), keep
+// 128-column batches, two in flight (with 256 columns the ternary layer took
+// 80.7 against 64.4 us at 8 tokens)
+constexpr int kWtStepsWide = 8;
+constexpr int kWtStepsNarrow = 4;
+
+template <int STEPS>
+struct WtBatch {
+    using W = WtShape<STEPS>;
+    u32x4 w[2 * W::kLoads];  // W_gate rows kRowsPerLoad q + lane / kLanesPerRow, then W_up
+    u32x4 x[STEPS];
+};
+
+template <int STEPS>
+__device__ __forceinline__ void wt_load(WtBatch<STEPS> &bt, const CoefArgs &a,
+                                        const int (&row)[WtShape<STEPS>::kLoads], uint32_t have,
+                                        const uint16_t *xrow, bool xreal, int s, int s1, int lane)
 {
+    using W = WtShape<STEPS>;
     const int g = lane / kTile;
-    const int col = s * 32 + (lane & 15) * 8;
+    const int col = s * 32 + (lane % W::kLanesPerRow) * 8;
     const bool colok = col < s1 * 32 && col < a.d_model;
 #pragma unroll
-    for (int q = 0; q < kWtLoads; ++q) {
+    for (int q = 0; q < W::kLoads; ++q) {
         bt.w[q] = zero16();
-        bt.w[kWtLoads + q] = zero16();
+        bt.w[W::kLoads + q] = zero16();
         if (((have >> q) & 1u) && colok) {
             bt.w[q] = load16_stream(a.Wg + (size_t)row[q] * a.d_model + col);
-            bt.w[kWtLoads + q] = load16_stream(a.Wu + (size_t)row[q] * a.d_model + col);
+            bt.w[W::kLoads + q] = load16_stream(a.Wu + (size_t)row[q] * a.d_model + col);
         }
     }
 #pragma unroll
-    for (int q = 0; q < kWtSteps; ++q) {
+    for (int q = 0; q < STEPS; ++q) {
         const int xc = (s + q) * 32 + g * 8;
         bt.x[q] = load16(or_zero(xreal && xc < a.d_model, xrow + xc));
     }
 }
 
-__device__ __forceinline__ void wt_consume(uint16_t *wt, const WtBatch &bt, int s, int s1,
+template <int STEPS>
+__device__ __forceinline__ void wt_consume(uint16_t *wt, const WtBatch<STEPS> &bt, int s, int s1,
                                            int lane, f32x4_t &dg, f32x4_t &du)
 {
+    using W = WtShape<STEPS>;
     const int i = lane % kTile, g = lane / kTile;
-    const int c = (lane & 15) * 8, rr0 = lane >> 4;
+    const int c = (lane % W::kLanesPerRow) * 8, rr0 = lane / W::kLanesPerRow;
 #pragma unroll
-    for (int q = 0; q < kWtLoads; ++q) {
-        *reinterpret_cast<u32x4 *>(wt + (4 * q + rr0) * kWtStride + c) = bt.w[q];
-        *reinterpret_cast<u32x4 *>(wt + (kTile + 4 * q + rr0) * kWtStride + c) = bt.w[kWtLoads + q];
+    for (int q = 0; q < W::kLoads; ++q) {
+        const int rr = W::kRowsPerLoad * q + rr0;
+        *reinterpret_cast<u32x4 *>(wt + rr * W::kStride + c) = bt.w[q];
+        *reinterpret_cast<u32x4 *>(wt + (kTile + rr) * W::kStride + c) = bt.w[W::kLoads + q];
     }
 #pragma unroll
-    for (int q = 0; q < kWtSteps; ++q) {
+    for (int q = 0; q < STEPS; ++q) {
         if (s + q < s1) {  // uniform
-            const u32x4 ga = *reinterpret_cast<const u32x4 *>(wt + i * kWtStride + q * 32 + g * 8);
+            const u32x4 ga = *reinterpret_cast<const u32x4 *>(wt + i * W::kStride + q * 32 + g * 8);
             const u32x4 ua =
-                *reinterpret_cast<const u32x4 *>(wt + (kTile + i) * kWtStride + q * 32 + g * 8);
+                *reinterpret_cast<const u32x4 *>(wt + (kTile + i) * W::kStride + q * 32 + g * 8);
             dg = mfma16(ga, bt.x[q], dg);
             du = mfma16(ua, bt.x[q], du);
         }
@@ -757,16 +777,19 @@ __device__ __forceinline__ void wt_consume(uint16_t *wt, const WtBatch &bt, int 
 // The block's active neurons (bits of M, rows r0 + bit) in tiles of 16 on MFMA:
 // each tile's column steps are split among 4 / ntiles waves, which add their
 // 16 x 16 partial sums in `part` (LDS [4][2][256] fp32) and write s = u * SiLU(g).
-// wtiles: LDS [4 waves][kWtWave] bf16; lrow: LDS [32] rows of the active neurons.
-// INTERLEAVE: wave kw of a tile takes batches kw, kw + wpt, ... of kWtSteps
-// steps, so the tile's waves read adjacent pieces of each row together (after
-// the low-rank score: 57.5 -> 56.7 us per 8B layer at 8 tokens); otherwise each
-// takes one contiguous run of steps (the ternary kernel: interleaved, its layer
-// took 68.2 against 65.4 us).
-template <int B, int NK, bool INTERLEAVE>
+// wtiles: LDS [4 waves][WtShape<STEPS>::kWaveElems] bf16; lrow: LDS [32] rows
+// of the active neurons. INTERLEAVE: wave kw of a tile takes batches kw,
+// kw + wpt, ... of STEPS steps, so the tile's waves read adjacent pieces of
+// each row together (after the low-rank score: 57.5 -> 56.7 us per 8B layer at
+// 8 tokens); otherwise each takes one contiguous run of steps (the ternary
+// kernel: interleaved, its layer took 68.2 against 65.4 us). A wave keeps two
+// batches in flight at 4 steps, one at 8.
+template <int B, int NK, bool INTERLEAVE, int STEPS>
 __device__ __forceinline__ void gather_mfma_lds(const CoefArgs &a, uint16_t *wtiles, float *part,
                                                 int *lrow, uint32_t M, int r0, int wave, int lane)
 {
+    using W = WtShape<STEPS>;
+    constexpr int kWtSteps = STEPS, kWtLoads = W::kLoads;
     const int n = __builtin_popcount(M);
     if (threadIdx.x < kPredRows && ((M >> threadIdx.x) & 1u))
         lrow[__builtin_popcount(M & ((1u << threadIdx.x) - 1u))] = r0 + threadIdx.x;
@@ -787,14 +810,19 @@ __device__ __forceinline__ void gather_mfma_lds(const CoefArgs &a, uint16_t *wti
     uint32_t have = 0u;
 #pragma unroll
     for (int q = 0; q < kWtLoads; ++q) {
-        const int k = t0 + 4 * q + (lane >> 4);
+        const int k = t0 + W::kRowsPerLoad * q + lane / W::kLanesPerRow;
         row[q] = k < n ? lrow[k] : r0;
         have |= (k < n ? 1u : 0u) << q;
     }
-    uint16_t *wt = wtiles + (size_t)wave * kWtWave;
+    uint16_t *wt = wtiles + (size_t)wave * W::kWaveElems;
     f32x4_t dg = {0.0f, 0.0f, 0.0f, 0.0f}, du = {0.0f, 0.0f, 0.0f, 0.0f};
-    WtBatch b0, b1;  // the next batch is in flight while the current one is consumed
-    if constexpr (INTERLEAVE) {
+    WtBatch<STEPS> b0, b1;  // the next batch is in flight while the current one is consumed
+    if constexpr (INTERLEAVE && STEPS >= kWtStepsWide) {
+        for (int j = kw; j < nbat; j += wpt) {
+            wt_load(b0, a, row, have, xrow, xreal, j * kWtSteps, steps, lane);
+            wt_consume(wt, b0, j * kWtSteps, steps, lane, dg, du);
+        }
+    } else if constexpr (INTERLEAVE) {
         if (kw < nbat)
             wt_load(b0, a, row, have, xrow, xreal, kw * kWtSteps, steps, lane);
         for (int j = kw; j < nbat; j += 2 * wpt) {
@@ -849,7 +877,7 @@ __device__ __forceinline__ void gather_mfma_lds(const CoefArgs &a, uint16_t *wti
 template <int B, int NK, int LCPR>
 __global__ __launch_bounds__(kBlock) void k_coef_pred_mfma(const CoefArgs a)
 {
-    // LDS: the waves' weight tiles [4][kWtWave] bf16, then the latent [B][d_rank]
+    // LDS: the waves' weight tiles [4][kWaveElems] bf16, then the latent [B][d_rank]
     // fp32 (rank 1024 only), whose space later holds the partial sums [4][2][16 x 16]
     extern __shared__ __align__(16) uint32_t xs[];
     __shared__ uint32_t wflag[kWavesPerBlock];
@@ -870,7 +898,8 @@ __global__ __launch_bounds__(kBlock) void k_coef_pred_mfma(const CoefArgs a)
     __builtin_amdgcn_sched_barrier(0);
     zero_y(a.y, a.nb * a.d_model);
     uint16_t *wtiles = reinterpret_cast<uint16_t *>(xs);
-    uint32_t *latw = xs + kWavesPerBlock * kWtWave / 2;
+    constexpr int STEPS = LR::kRegs ? kWtStepsWide : kWtStepsNarrow;
+    uint32_t *latw = xs + kWavesPerBlock * WtShape<STEPS>::kWaveElems / 2;
     if constexpr (!LR::kRegs) {
         ls.write(reinterpret_cast<u32x4 *>(latw), a.lat, a.nb, a.d_rank);
         __syncthreads();
@@ -886,8 +915,8 @@ __global__ __launch_bounds__(kBlock) void k_coef_pred_mfma(const CoefArgs a)
     for (int v = 0; v < kWavesPerBlock; ++v)
         M |= wflag[v] << (v * kPredRowsPerWave);
     // the latent is no longer read once gather_mfma_lds's first barrier has passed
-    gather_mfma_lds<B, NK, true>(a, wtiles, reinterpret_cast<float *>(latw), lrow, M, r0, wave,
-                                 lane);
+    gather_mfma_lds<B, NK, true, STEPS>(a, wtiles, reinterpret_cast<float *>(latw), lrow, M, r0,
+                                        wave, lane);
 }
 
 // ------------------------------------------------ ternary predictor
@@ -1063,9 +1092,8 @@ __global__ __launch_bounds__(kBlock) void k_coef_tern(const CoefArgs a)
 template <int B, int NK>
 __host__ __device__ constexpr size_t tern_mfma_front_u32()
 {
-    return mfma_lds_tokens_u32<B, NK>() > (size_t)kWavesPerBlock * kWtWave / 2
-               ? mfma_lds_tokens_u32<B, NK>()
-               : (size_t)kWavesPerBlock * kWtWave / 2;
+    constexpr size_t kTiles = (size_t)kWavesPerBlock * WtShape<kWtStepsNarrow>::kWaveElems / 2;
+    return mfma_lds_tokens_u32<B, NK>() > kTiles ? mfma_lds_tokens_u32<B, NK>() : kTiles;
 }
 
 // Ternary-predictor coefficient kernel for batches of 5-8: the ternary score,
@@ -1109,7 +1137,7 @@ __global__ __launch_bounds__(kBlock) void k_coef_tern_mfma(const CoefArgs a)
         M |= wflag[v] << (v * kPredRowsPerWave);
     (void)zchunk;
     // (the barrier above ends the token reads: the tiles may overwrite them)
-    gather_mfma_lds<B, NK, false>(a, reinterpret_cast<uint16_t *>(xs),
+    gather_mfma_lds<B, NK, false, kWtStepsNarrow>(a, reinterpret_cast<uint16_t *>(xs),
                            reinterpret_cast<float *>(xs + tern_mfma_front_u32<B, NK>()), lrow, M,
                            r0, wave, lane);
 }
@@ -2553,7 +2581,8 @@ static void coef_pred_lcpr(const CoefArgs &a, hipStream_t s)
     // 16-row tile a third empty) the per-wave v_dot2 gather measured as fast
     if constexpr (B >= 8) {
         // weight tiles, then max(latent, 4 x 2 x 16 x 16 partial sums)
-        const size_t lds = (size_t)kWavesPerBlock * kWtWave * 2 +
+        constexpr int STEPS = LatentRegs<B, LCPR>::kRegs ? kWtStepsWide : kWtStepsNarrow;
+        const size_t lds = (size_t)kWavesPerBlock * WtShape<STEPS>::kWaveElems * 2 +
                            max(lat_lds, (size_t)kWavesPerBlock * 2 * 256 * 4);
         allow_lds(k_coef_pred_mfma<B, NK, LCPR>, lds);
         k_coef_pred_mfma<B, NK, LCPR><<<grid, kBlock, lds, s>>>(a);
