@@ -2553,14 +2553,16 @@ size_t down_lds_bytes(int rows_per_group, int bt)
     return (size_t)rows_per_group * 4 * (1 + bt) + (size_t)kWavesPerBlock * kColsPerLoad * 4;
 }
 
-// Down-kernel grid: 512-column chunks x 64 neuron ranges of at least 16
-// neurons (measured best at 4096 x 11008, 4096 x 14336 and 8192 x 28672 among
-// 16-128 ranges and 128-512-column chunks), more ranges when a range's lists
-// would not fit in 64 KB of LDS.
+// Down-kernel grid: 512-column chunks x 56 neuron ranges up to 8 chunks
+// (d_model 4096), 64 beyond, of at least 16 neurons each, more ranges when a
+// range's lists would not fit in 64 KB of LDS. Measured among 16-128 ranges
+// and 128-512-column chunks: at 4096 x 11008 and 4096 x 14336, 56 ranges
+// against 64 were 1% faster at 90% sparsity and as fast at 50% and at two
+// tokens (48 and fewer lost there); at 8192 x 28672, 64 (48 and 80 slower).
 void down_grid(int d_model, int d_ff, int bt, int *gc, int *gr, int *rows_per_group)
 {
     *gc = (d_model + kColsPerLoad - 1) / kColsPerLoad;
-    int r = 64;
+    int r = *gc <= 8 ? 56 : 64;
     if (r > d_ff / 16)
         r = d_ff / 16;
     if (r < 1)
