@@ -2637,7 +2637,9 @@ static hipError_t coef_bn(int variant, const CoefArgs &a, hipStream_t s)
     // The one-row kernel keeps the tokens in registers for one token only: at
     // two they cost it 114 VGPRs (4 waves per SIMD), and the LDS copy measured
     // 8-10% faster at 2 tokens (7B and 70B shapes); the two-row kernel gained
-    // nothing from it.
+    // nothing from it. At one token of d_model 8192 the registers win although
+    // they leave 3 waves per SIMD (LDS copy: 4): 87.1 against 88.6 us per 70B
+    // layer.
     constexpr bool XREG1 = B <= 1;
     const size_t lds = token_lds_bytes(B, NK);
     const size_t lds1 = XREG1 ? 0 : (size_t)B * NK * kColsPerLoad * 2;
