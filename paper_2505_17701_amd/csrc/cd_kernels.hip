@@ -816,7 +816,7 @@ __device__ __forceinline__ void gather_mfma_lds(const CoefArgs &a, uint16_t *wti
     }
     uint16_t *wt = wtiles + (size_t)wave * W::kWaveElems;
     f32x4_t dg = {0.0f, 0.0f, 0.0f, 0.0f}, du = {0.0f, 0.0f, 0.0f, 0.0f};
-    WtBatch<STEPS> b0, b1;  // the next batch is in flight while the current one is consumed
+    WtBatch<STEPS> b0, b1;  // 4 steps: the next batch is in flight while this one is consumed
     if constexpr (INTERLEAVE && STEPS >= kWtStepsWide) {
         for (int j = kw; j < nbat; j += wpt) {
             wt_load(b0, a, row, have, xrow, xreal, j * kWtSteps, steps, lane);
