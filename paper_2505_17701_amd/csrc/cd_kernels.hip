@@ -495,13 +495,14 @@ __device__ __forceinline__ void pred_finish(const CoefArgs &a, const Tokens<B, N
 
 // Next neuron of this wave's share of the block mask (every fourth active
 // neuron), or -1; advances the mask past it.
+template <int NW = kWavesPerBlock>
 __device__ __forceinline__ int pred_next(uint32_t &m)
 {
     if (!m)
         return -1;
     const int r = __builtin_ctz(m);
 #pragma unroll
-    for (int k = 0; k < kWavesPerBlock; ++k)
+    for (int k = 0; k < NW; ++k)
         m &= m - 1;
     return r;
 }
@@ -509,9 +510,10 @@ __device__ __forceinline__ int pred_next(uint32_t &m)
 // This wave's share of the block's active neurons: the waves' masks are
 // joined (one barrier) and every fourth active neuron, starting at number
 // `wave`, is kept.
+template <int NW = kWavesPerBlock>
 __device__ __forceinline__ uint32_t block_share(uint32_t *wflag, uint32_t wmask, int wave, int lane)
 {
-    if (lane == 0)
+    if (lane == 0 && wave < kWavesPerBlock)  // the scoring waves
         wflag[wave] = wmask;
     __syncthreads();
     uint32_t m = 0;
@@ -526,7 +528,7 @@ __device__ __forceinline__ uint32_t block_share(uint32_t *wflag, uint32_t wmask,
 // Gather of the wave's share m of the block's active neurons (block base r0):
 // W_gate and W_up rows, s = u * SiLU(g), the next neuron's rows in flight
 // while the current one is reduced.
-template <int B, int NK, bool XREG>
+template <int B, int NK, bool XREG, int NW = kWavesPerBlock>
 __device__ __forceinline__ void gather_rr(const CoefArgs &a, const Tokens<B, NK, XREG> &tok,
                                           uint32_t m, int r0, int lane)
 {
@@ -534,7 +536,7 @@ __device__ __forceinline__ void gather_rr(const CoefArgs &a, const Tokens<B, NK,
     // reduced, for 1-2 tokens; at 4 the second buffer cost occupancy (168 against
     // 100 VGPRs) and one buffer measured 1.5-4% faster (8B shape)
     constexpr bool kPrefetch = NK <= 8 && B <= 2;
-    int ra = pred_next(m);
+    int ra = pred_next<NW>(m);
     if (ra < 0)
         return;
     u32x4 ga[NK], ua[NK];
@@ -543,7 +545,7 @@ __device__ __forceinline__ void gather_rr(const CoefArgs &a, const Tokens<B, NK,
     if constexpr (kPrefetch) {
         u32x4 gb[NK], ub[NK];
         for (;;) {
-            const int rb = pred_next(m);
+            const int rb = pred_next<NW>(m);
             if (rb >= 0) {
                 load_row<NK>(gb, a.Wg + (size_t)(r0 + rb) * a.d_model, a.d_model, lane);
                 load_row<NK>(ub, a.Wu + (size_t)(r0 + rb) * a.d_model, a.d_model, lane);
@@ -551,7 +553,7 @@ __device__ __forceinline__ void gather_rr(const CoefArgs &a, const Tokens<B, NK,
             pred_finish<B, NK, XREG>(a, tok, ga, ua, r0 + ra, lane);
             if (rb < 0)
                 break;
-            ra = pred_next(m);
+            ra = pred_next<NW>(m);
             if (ra >= 0) {
                 load_row<NK>(ga, a.Wg + (size_t)(r0 + ra) * a.d_model, a.d_model, lane);
                 load_row<NK>(ua, a.Wu + (size_t)(r0 + ra) * a.d_model, a.d_model, lane);
@@ -563,7 +565,7 @@ __device__ __forceinline__ void gather_rr(const CoefArgs &a, const Tokens<B, NK,
     } else {
         for (;;) {
             pred_finish<B, NK, XREG>(a, tok, ga, ua, r0 + ra, lane);
-            ra = pred_next(m);
+            ra = pred_next<NW>(m);
             if (ra < 0)
                 break;
             load_row<NK>(ga, a.Wg + (size_t)(r0 + ra) * a.d_model, a.d_model, lane);
@@ -581,15 +583,18 @@ __device__ __forceinline__ void gather_rr(const CoefArgs &a, const Tokens<B, NK,
 // round-robin to the four waves, which gather their W_gate and W_up rows
 // (for 1-2 tokens the next row's loads in flight while the current one is
 // reduced) and write s = u * SiLU(g).
-template <int B, int NK, bool XREG, int LCPR>
-__global__ __launch_bounds__(kBlock) void k_coef_pred(const CoefArgs a)
+template <int B, int NK, bool XREG, int LCPR, int NWV = kWavesPerBlock>
+__global__ __launch_bounds__(NWV * kWave) void k_coef_pred(const CoefArgs a)
 {
     extern __shared__ __align__(16) uint32_t xs[];  // [tokens [B][NK * 256]], latent [B][d_rank]
     __shared__ uint32_t wflag[kWavesPerBlock];
     using S = PredShape<LCPR>;
     const int lane = threadIdx.x % kWave, wave = threadIdx.x / kWave;
+    // NWV 8: the first four waves score the block's rows; the others score
+    // nothing (their rows start past d_ff) and join the gather
+    const bool scorer = wave < kWavesPerBlock;  // wave-uniform
     const int r0 = blockIdx.x * kPredRows;
-    const int wr0 = r0 + wave * kPredRowsPerWave;
+    const int wr0 = scorer ? r0 + wave * kPredRowsPerWave : a.d_ff;
 
     // loads in the order they are needed: B_t and the latent for the scores,
     // then the tokens, which only the gather reads
@@ -600,21 +605,28 @@ __global__ __launch_bounds__(kBlock) void k_coef_pred(const CoefArgs a)
     lr.issue(a.lat, a.nb, a.d_rank, lane);
     LatentStage<LR::kRegs ? 1 : B> ls;  // the LDS copy, rank 1024 only
     if constexpr (!LR::kRegs)
-        ls.issue(a.lat, a.nb, a.d_rank);
+        if (scorer)
+            ls.issue(a.lat, a.nb, a.d_rank);
     Tokens<B, NK, XREG> tok;
-    tok.issue(a.x, a.nb, a.d_model, lane);
-    zero_y(a.y, a.nb * a.d_model);
+    if (XREG || scorer)  // the LDS copy: the first kBlock threads
+        tok.issue(a.x, a.nb, a.d_model, lane);
+    if (scorer)
+        zero_y(a.y, a.nb * a.d_model);
     uint32_t *latw = xs + (XREG ? 0 : B * NK * kColsPerLoad / 2);
     if constexpr (!LR::kRegs) {
-        ls.write(reinterpret_cast<u32x4 *>(latw), a.lat, a.nb, a.d_rank);
+        if (scorer)
+            ls.write(reinterpret_cast<u32x4 *>(latw), a.lat, a.nb, a.d_rank);
         __syncthreads();
     }
 
     const uint32_t wmask = pred_score<B, LCPR>(wb, lr, reinterpret_cast<const float *>(latw), a,
                                                wr0, lane);
-    tok.write(xs);  // (block_share's barrier publishes the LDS copy)
-    uint32_t m = block_share(wflag, wmask, wave, lane);
-    gather_rr<B, NK, XREG>(a, tok, m, r0, lane);
+    if (scorer)
+        tok.write(xs);  // (block_share's barrier publishes the LDS copy)
+    else
+        tok.lds = xs;
+    uint32_t m = block_share<NWV>(wflag, wmask, wave, lane);
+    gather_rr<B, NK, XREG, NWV>(a, tok, m, r0, lane);
 }
 
 // ------------------------------------------- MFMA gather for batches of 5-8
@@ -2575,6 +2587,12 @@ void down_grid(int d_model, int d_ff, int bt, int *gc, int *gr, int *rows_per_gr
     *gr = (d_ff + *rows_per_group - 1) / *rows_per_group;
 }
 
+// waves per block of the batch-4 predictor kernel: a block's ~11 active
+// neurons (34% of 32 at 4 tokens) dealt to 8 waves instead of 4 leave each
+// wave one or two row pairs to read instead of about three in a row (8B
+// layer: 38.2 -> 37.3 us at 4 tokens, 33.5 -> 32.5 at 3)
+constexpr int kPredWaves4 = 8;
+
 template <int B, int NK, bool XREG, int LCPR>
 static void coef_pred_lcpr(const CoefArgs &a, hipStream_t s)
 {
@@ -2592,8 +2610,9 @@ static void coef_pred_lcpr(const CoefArgs &a, hipStream_t s)
         k_coef_pred_mfma<B, NK, LCPR><<<grid, kBlock, lds, s>>>(a);
     } else {
         const size_t lds = (XREG ? 0 : (size_t)B * NK * kColsPerLoad * 2) + lat_lds;
-        allow_lds(k_coef_pred<B, NK, XREG, LCPR>, lds);
-        k_coef_pred<B, NK, XREG, LCPR><<<grid, kBlock, lds, s>>>(a);
+        constexpr int NWV = (B == 4 && !XREG) ? kPredWaves4 : kWavesPerBlock;
+        allow_lds(k_coef_pred<B, NK, XREG, LCPR, NWV>, lds);
+        k_coef_pred<B, NK, XREG, LCPR, NWV><<<grid, NWV * kWave, lds, s>>>(a);
     }
 }
 
