@@ -592,7 +592,7 @@ __global__ __launch_bounds__(NWV * kWave) void k_coef_pred(const CoefArgs a)
     const int lane = threadIdx.x % kWave, wave = threadIdx.x / kWave;
     // NWV 8: the first four waves score the block's rows; the others score
     // nothing (their rows start past d_ff) and join the gather
-    const bool scorer = wave < kWavesPerBlock;  // wave-uniform
+    const bool scorer = NWV == kWavesPerBlock || wave < kWavesPerBlock;  // wave-uniform
     const int r0 = blockIdx.x * kPredRows;
     const int wr0 = scorer ? r0 + wave * kPredRowsPerWave : a.d_ff;
 
@@ -619,8 +619,9 @@ __global__ __launch_bounds__(NWV * kWave) void k_coef_pred(const CoefArgs a)
         __syncthreads();
     }
 
-    const uint32_t wmask = pred_score<B, LCPR>(wb, lr, reinterpret_cast<const float *>(latw), a,
-                                               wr0, lane);
+    const uint32_t wmask =
+        scorer ? pred_score<B, LCPR>(wb, lr, reinterpret_cast<const float *>(latw), a, wr0, lane)
+               : 0u;
     if (scorer)
         tok.write(xs);  // (block_share's barrier publishes the LDS copy)
     else
@@ -1068,23 +1069,35 @@ __device__ __forceinline__ uint32_t tern_score(const TernRows<NK> &t, XF xget, c
 
 // Ternary-predictor coefficient kernel for batches of 1-4: k_coef_pred with
 // the ternary score in place of the latent . B_t one (no latent kernel).
-template <int B, int NK, bool XREG>
-__global__ __launch_bounds__(kBlock) void k_coef_tern(const CoefArgs a)
+template <int B, int NK, bool XREG, int NWV = kWavesPerBlock>
+__global__ __launch_bounds__(NWV * kWave) void k_coef_tern(const CoefArgs a)
 {
     extern __shared__ __align__(16) uint32_t xs[];  // tokens [B][NK * 256] (LDS path)
     __shared__ uint32_t wflag[kWavesPerBlock];
     const int lane = threadIdx.x % kWave, wave = threadIdx.x / kWave;
+    // NWV 8: as in k_coef_pred, the waves past the fourth only gather
+    const bool scorer = NWV == kWavesPerBlock || wave < kWavesPerBlock;  // wave-uniform
     const int r0 = blockIdx.x * kPredRows;
-    const int wr0 = r0 + wave * kPredRowsPerWave;
+    const int wr0 = scorer ? r0 + wave * kPredRowsPerWave : a.d_ff;
 
     TernRows<NK> tr;
     tr.issue(a, wr0, lane);
     Tokens<B, NK, XREG> tok;
-    tok.issue(a.x, a.nb, a.d_model, lane);
-    zero_y(a.y, a.nb * a.d_model);
-    tok.commit(xs);
-    uint32_t wmask;
-    if constexpr (XREG) {
+    if (XREG || scorer)  // the LDS copy: the first kBlock threads
+        tok.issue(a.x, a.nb, a.d_model, lane);
+    if (scorer)
+        zero_y(a.y, a.nb * a.d_model);
+    if constexpr (!XREG) {
+        if (scorer)
+            tok.write(xs);
+        else
+            tok.lds = xs;
+        __syncthreads();
+    }
+    uint32_t wmask = 0;
+    if (!scorer) {
+        // no rows to score
+    } else if constexpr (XREG) {
         wmask = tern_score<B, NK, false>(tr, [&](int b, int j) { return tok.r[b][j]; }, a, wr0,
                                          lane);
     } else {
@@ -1095,8 +1108,8 @@ __global__ __launch_bounds__(kBlock) void k_coef_tern(const CoefArgs a)
             },
             a, wr0, lane);
     }
-    const uint32_t m = block_share(wflag, wmask, wave, lane);
-    gather_rr<B, NK, XREG>(a, tok, m, r0, lane);
+    const uint32_t m = block_share<NWV>(wflag, wmask, wave, lane);
+    gather_rr<B, NK, XREG, NWV>(a, tok, m, r0, lane);
 }
 
 // LDS bytes of the ternary MFMA kernel: the token copy, which the gather's
@@ -2587,10 +2600,11 @@ void down_grid(int d_model, int d_ff, int bt, int *gc, int *gr, int *rows_per_gr
     *gr = (d_ff + *rows_per_group - 1) / *rows_per_group;
 }
 
-// waves per block of the batch-4 predictor kernel: a block's ~11 active
+// waves per block of the batch-4 predictor kernels: a block's ~11 active
 // neurons (34% of 32 at 4 tokens) dealt to 8 waves instead of 4 leave each
 // wave one or two row pairs to read instead of about three in a row (8B
-// layer: 38.2 -> 37.3 us at 4 tokens, 33.5 -> 32.5 at 3)
+// layer, low-rank: 38.2 -> 36.6 us at 4 tokens, 33.5 -> 32.5 at 3; ternary:
+// 40.6 -> 38.2 and 36.6 -> 34.9)
 constexpr int kPredWaves4 = 8;
 
 template <int B, int NK, bool XREG, int LCPR>
@@ -2644,8 +2658,9 @@ static hipError_t coef_tern_launch(const CoefArgs &a, hipStream_t s)
         k_coef_tern_mfma<B, NK><<<grid, kBlock, lds, s>>>(a);
     } else {
         const size_t lds = token_lds_bytes(B, NK);
-        allow_lds(k_coef_tern<B, NK, XREG>, lds);
-        k_coef_tern<B, NK, XREG><<<grid, kBlock, lds, s>>>(a);
+        constexpr int NWV = (B == 4 && !XREG) ? kPredWaves4 : kWavesPerBlock;
+        allow_lds(k_coef_tern<B, NK, XREG, NWV>, lds);
+        k_coef_tern<B, NK, XREG, NWV><<<grid, NWV * kWave, lds, s>>>(a);
     }
     return hipGetLastError();
 }
