@@ -1067,6 +1067,79 @@ __device__ __forceinline__ uint32_t tern_score(const TernRows<NK> &t, XF xget, c
     return wmask;
 }
 
+// The ternary score of a wave's kPredRowsPerWave rows on MFMA, for batches of
+// 5-8 and d_model 4096 (one 16-byte block of packed theta per lane and row):
+// s_hat = theta . x is a dense product with weights in {-1, 0, +1}. Lane
+// (n, g) = (lane % 16, lane / 16) reads block 4 t + g of row n (rows past the
+// wave's 8 read zeros) for t = 0 .. 15; unit j of that block, decoded by
+// tern_pair into 8 bf16 weights of +-0.5 or 0, is the A operand of one
+// v_mfma_f32_16x16x32_bf16 step whose B operand is token n's columns
+// 512 j + 8 (4 t + g) + [0, 8) from the LDS copy, so A and B agree on the
+// column order and the 128 steps cover every column once. D[row][token] is
+// half the score. Threshold, union and stores as in tern_score.
+template <int NK>
+struct TernMfmaRows {
+    static_assert(NK == 8, "one 16-byte block per lane and row");
+    static constexpr int kW = TernShape<NK>::kWords;  // 4
+    u32x4 blk[16];
+
+    __device__ __forceinline__ void issue(const CoefArgs &a, int wr0, int lane)
+    {
+        const int n = lane % kTile, g = lane / kTile;
+        const int row = wr0 + n;
+        const bool ok = n < kPredRowsPerWave && row < a.d_ff;
+        const uint32_t *rp = a.Tp + (size_t)(ok ? row : 0) * kWave * kW;
+#pragma unroll
+        for (int t = 0; t < 16; ++t)
+            blk[t] = __builtin_nontemporal_load(
+                reinterpret_cast<const u32x4 *>(or_zero(ok, rp + (4 * t + g) * kW)));
+    }
+};
+
+// xcol(col): this lane's token (lane % 16) at columns col .. col + 7, zeros
+// past the batch
+template <int NK, class XC>
+__device__ __forceinline__ uint32_t tern_score_mfma(const TernMfmaRows<NK> &tr, XC xcol,
+                                                    const CoefArgs &a, int wr0, int lane)
+{
+    const int n = lane % kTile, g = lane / kTile;
+    f32x4_t acc = {0.0f, 0.0f, 0.0f, 0.0f};
+#pragma unroll
+    for (int t = 0; t < 16; ++t) {
+        const u32x4 w = tr.blk[t];
+#pragma unroll
+        for (int j = 0; j < NK; ++j) {
+            const uint32_t W = w[j >> 1];
+            u32x4 wa;
+            wa.x = tern_pair(W, j, 0);
+            wa.y = tern_pair(W, j, 1);
+            wa.z = tern_pair(W, j, 2);
+            wa.w = tern_pair(W, j, 3);
+            acc = mfma16(wa, xcol(j * kColsPerLoad + 8 * (4 * t + g)), acc);
+        }
+    }
+    // lane l holds D[4 g + r][l % 16]: rows 4 g + r of the wave (g < 2), token l % 16
+    uint32_t wmask = 0;
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+        const int rw = 4 * g + r;
+        const int row = wr0 + rw;
+        const bool live = rw < kPredRowsPerWave && row < a.d_ff && n < a.nb;
+        const float v = 2.0f * acc[r];
+        if (a.coef && live)
+            a.coef[(size_t)n * a.d_ff + row] = v;
+        const uint64_t m = ballot(live && v > a.thld);
+        const bool act0 = (m & 0xffffull) != 0, act1 = ((m >> 16) & 0xffffull) != 0;
+        if (lane == 0 && wr0 + r < a.d_ff)
+            a.act[wr0 + r] = act0 ? 1 : 0;
+        if (lane == kTile && wr0 + 4 + r < a.d_ff)
+            a.act[wr0 + 4 + r] = act1 ? 1 : 0;
+        wmask |= (act0 && wr0 + r < a.d_ff ? 1u : 0u) << r;
+        wmask |= (act1 && wr0 + 4 + r < a.d_ff ? 1u : 0u) << (4 + r);
+    }
+    return wmask;
+}
+
 // Ternary-predictor coefficient kernel for batches of 1-4: k_coef_pred with
 // the ternary score in place of the latent . B_t one (no latent kernel).
 template <int B, int NK, bool XREG, int NWV = kWavesPerBlock>
@@ -1112,83 +1185,6 @@ __global__ __launch_bounds__(NWV * kWave) void k_coef_tern(const CoefArgs a)
     gather_rr<B, NK, XREG, NWV>(a, tok, m, r0, lane);
 }
 
-// The ternary score of a wave's kPredRowsPerWave rows on MFMA, for batches of
-// 5-8 and d_model 4096 (one 16-byte block of packed theta per lane and row):
-// s_hat = theta . x is a dense product with weights in {-1, 0, +1}. Lane
-// (n, g) = (lane % 16, lane / 16) reads block 4 t + g of row n (rows past the
-// wave's 8 read zeros) for t = 0 .. 15; unit j of that block, decoded by
-// tern_pair into 8 bf16 weights of +-0.5 or 0, is the A operand of one
-// v_mfma_f32_16x16x32_bf16 step whose B operand is token n's columns
-// 512 j + 8 (4 t + g) + [0, 8) from the LDS copy, so A and B agree on the
-// column order and the 128 steps cover every column once. D[row][token] is
-// half the score. Threshold, union and stores as in tern_score.
-template <int NK>
-struct TernMfmaRows {
-    static_assert(NK == 8, "one 16-byte block per lane and row");
-    static constexpr int kW = TernShape<NK>::kWords;  // 4
-    u32x4 blk[16];
-
-    __device__ __forceinline__ void issue(const CoefArgs &a, int wr0, int lane)
-    {
-        const int n = lane % kTile, g = lane / kTile;
-        const int row = wr0 + n;
-        const bool ok = n < kPredRowsPerWave && row < a.d_ff;
-        const uint32_t *rp = a.Tp + (size_t)(ok ? row : 0) * kWave * kW;
-#pragma unroll
-        for (int t = 0; t < 16; ++t)
-            blk[t] = __builtin_nontemporal_load(
-                reinterpret_cast<const u32x4 *>(or_zero(ok, rp + (4 * t + g) * kW)));
-    }
-};
-
-template <int B, int NK>
-__device__ __forceinline__ uint32_t tern_score_mfma(const TernMfmaRows<NK> &tr, const uint32_t *xs,
-                                                    const uint32_t *zchunk, const CoefArgs &a,
-                                                    int wr0, int lane)
-{
-    using TL = MfmaTokLayout<NK>;
-    const int n = lane % kTile, g = lane / kTile;
-    const uint32_t *xt = n < a.nb ? xs + Tokens<B, NK, false>::opaque_zero() + (size_t)n * TL::kStride
-                                  : nullptr;
-    f32x4_t acc = {0.0f, 0.0f, 0.0f, 0.0f};
-#pragma unroll
-    for (int t = 0; t < 16; ++t) {
-        const u32x4 w = tr.blk[t];
-#pragma unroll
-        for (int j = 0; j < NK; ++j) {
-            const uint32_t W = w[j >> 1];
-            u32x4 wa;
-            wa.x = tern_pair(W, j, 0);
-            wa.y = tern_pair(W, j, 1);
-            wa.z = tern_pair(W, j, 2);
-            wa.w = tern_pair(W, j, 3);
-            const int col = j * kColsPerLoad + 8 * (4 * t + g);
-            const u32x4 xb = *reinterpret_cast<const u32x4 *>(xt ? xt + col / 2 : zchunk);
-            acc = mfma16(wa, xb, acc);
-        }
-    }
-    // lane l holds D[4 g + r][l % 16]: rows 4 g + r of the wave (g < 2), token l % 16
-    uint32_t wmask = 0;
-#pragma unroll
-    for (int r = 0; r < 4; ++r) {
-        const int rw = 4 * g + r;
-        const int row = wr0 + rw;
-        const bool live = rw < kPredRowsPerWave && row < a.d_ff && n < a.nb;
-        const float v = 2.0f * acc[r];
-        if (a.coef && live)
-            a.coef[(size_t)n * a.d_ff + row] = v;
-        const uint64_t m = ballot(live && v > a.thld);
-        const bool act0 = (m & 0xffffull) != 0, act1 = ((m >> 16) & 0xffffull) != 0;
-        if (lane == 0 && wr0 + r < a.d_ff)
-            a.act[wr0 + r] = act0 ? 1 : 0;
-        if (lane == kTile && wr0 + 4 + r < a.d_ff)
-            a.act[wr0 + 4 + r] = act1 ? 1 : 0;
-        wmask |= (act0 && wr0 + r < a.d_ff ? 1u : 0u) << r;
-        wmask |= (act1 && wr0 + 4 + r < a.d_ff ? 1u : 0u) << (4 + r);
-    }
-    return wmask;
-}
-
 // LDS bytes of the ternary MFMA kernel: the token copy, which the gather's
 // weight tiles reuse once the scores are in, then the partial sums
 template <int B, int NK>
@@ -1213,8 +1209,9 @@ __global__ __launch_bounds__(kBlock) void k_coef_tern_mfma(const CoefArgs a)
     const int r0 = blockIdx.x * kPredRows;
     const int wr0 = r0 + wave * kPredRowsPerWave;
 
-    // the score on MFMA at d_model 4096 (8B layer at 8 tokens: 64.4 -> 59.8 us,
-    // at 5: 54.3 -> 49.0); v_dot2 for the other widths
+    // the score on MFMA at d_model 4096 (8B layer at 8 tokens: 64.4 -> 58.0 us,
+    // at 5: 54.3 -> 49.0); v_dot2 for the other widths. (At 3-4 tokens, in
+    // k_coef_tern, it measured no faster: 38.5 against 38.2 us at 4.)
     constexpr bool kMfmaScore = NK == 8;
     using TR = std::conditional_t<kMfmaScore, TernMfmaRows<8>, TernRows<NK>>;
     TR tr;
@@ -1228,7 +1225,15 @@ __global__ __launch_bounds__(kBlock) void k_coef_tern_mfma(const CoefArgs a)
 
     uint32_t wmask;
     if constexpr (kMfmaScore) {
-        wmask = tern_score_mfma<B, NK>(tr, xs, zchunk, a, wr0, lane);
+        const int n = lane % kTile;
+        const uint32_t *xt =
+            n < a.nb ? xs + Tokens<B, NK, false>::opaque_zero() + (size_t)n * TL::kStride : zchunk;
+        // past the batch the zero chunk for every column: a mask on the offset,
+        // not a pointer select per step (the select cost 1.7 us at 8 tokens)
+        const int cm = n < a.nb ? ~0 : 0;
+        wmask = tern_score_mfma<NK>(
+            tr, [&](int col) { return *reinterpret_cast<const u32x4 *>(xt + ((col / 2) & cm)); }, a,
+            wr0, lane);
     } else {
         wmask = tern_score<B, NK, true>(
             tr,
