@@ -755,10 +755,19 @@ __device__ __forceinline__ void wt_load(WtBatch<STEPS> &bt, const CoefArgs &a,
             bt.w[W::kLoads + q] = load16_stream(a.Wu + (size_t)row[q] * a.d_model + col);
         }
     }
+    // a batch inside the row needs no column checks; lanes past the batch read
+    // token 0 there (xrow), which only feeds output columns that are never
+    // stored (MFMA output column j depends on B column j alone)
+    if ((s + STEPS) * 32 <= a.d_model) {  // uniform
 #pragma unroll
-    for (int q = 0; q < STEPS; ++q) {
-        const int xc = (s + q) * 32 + g * 8;
-        bt.x[q] = load16(or_zero(xreal && xc < a.d_model, xrow + xc));
+        for (int q = 0; q < STEPS; ++q)
+            bt.x[q] = load16(xrow + (s + q) * 32 + g * 8);
+    } else {
+#pragma unroll
+        for (int q = 0; q < STEPS; ++q) {
+            const int xc = (s + q) * 32 + g * 8;
+            bt.x[q] = load16(or_zero(xreal && xc < a.d_model, xrow + xc));
+        }
     }
 }
 
