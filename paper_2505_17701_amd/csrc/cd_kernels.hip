@@ -2704,7 +2704,8 @@ void down_grid(int d_model, int d_ff, int bt, int *gc, int *gr, int *rows_per_gr
 // neurons (34% of 32 at 4 tokens) dealt to 8 waves instead of 4 leave each
 // wave one or two row pairs to read instead of about three in a row (8B
 // layer, low-rank: 38.2 -> 36.6 us at 4 tokens, 33.5 -> 32.5 at 3; ternary:
-// 40.6 -> 38.2 and 36.6 -> 34.9)
+// 40.6 -> 38.2 and 36.6 -> 34.9). Up to d_model 4096: at 8192 the 8-wave
+// kernels take 192 VGPRs, one block per CU.
 constexpr int kPredWaves4 = 8;
 
 template <int B, int NK, bool XREG, int LCPR>
@@ -2724,7 +2725,7 @@ static void coef_pred_lcpr(const CoefArgs &a, hipStream_t s)
         k_coef_pred_mfma<B, NK, LCPR><<<grid, kBlock, lds, s>>>(a);
     } else {
         const size_t lds = (XREG ? 0 : (size_t)B * NK * kColsPerLoad * 2) + lat_lds;
-        constexpr int NWV = (B == 4 && !XREG) ? kPredWaves4 : kWavesPerBlock;
+        constexpr int NWV = (B == 4 && !XREG && NK <= 8) ? kPredWaves4 : kWavesPerBlock;
         allow_lds(k_coef_pred<B, NK, XREG, LCPR, NWV>, lds);
         k_coef_pred<B, NK, XREG, LCPR, NWV><<<grid, NWV * kWave, lds, s>>>(a);
     }
@@ -2758,7 +2759,7 @@ static hipError_t coef_tern_launch(const CoefArgs &a, hipStream_t s)
         k_coef_tern_mfma<B, NK><<<grid, kBlock, lds, s>>>(a);
     } else {
         const size_t lds = token_lds_bytes(B, NK);
-        constexpr int NWV = (B == 4 && !XREG) ? kPredWaves4 : kWavesPerBlock;
+        constexpr int NWV = (B == 4 && !XREG && NK <= 8) ? kPredWaves4 : kWavesPerBlock;
         allow_lds(k_coef_tern<B, NK, XREG, NWV>, lds);
         k_coef_tern<B, NK, XREG, NWV><<<grid, NWV * kWave, lds, s>>>(a);
     }
