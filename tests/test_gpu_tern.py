@@ -37,7 +37,11 @@ def thld_at(layer, x, q):
 
 @pytest.mark.parametrize("shape", [(8, 16, 1), (256, 688, 1), (520, 776, 2), (1032, 1000, 3),
                                    (4096, 1376, 4), (1024, 520, 5), (2048, 776, 8),
-                                   (8192, 264, 4)])
+                                   (8192, 264, 4),
+                                   # 5-8 tokens at 3585-4096 columns: the score on MFMA,
+                                   # ragged last chunk and ragged neuron count
+                                   (3592, 1000, 5), (3848, 264, 7), (4088, 1032, 8),
+                                   (4096, 776, 6)])
 def test_tern_parity(shape):
     from paper_2505_17701_amd import binding as cd
 
@@ -49,7 +53,8 @@ def test_tern_parity(shape):
         th = thld_at(layer, x, q)
         n, flips, rel = check_call("dual_tern", layer, x, th, run_gpu(plan, "dual_tern", layer, x, th),
                                    f"tern {shape} q={q}")
-        assert 0 < n < dff
+        # at q 0.5 the union over 5-8 tokens (1 - 0.5^B of the neurons) may be all of them
+        assert 0 < n <= dff and (q < 0.9 or n < dff), (n, dff)
     plan.close()
 
 
@@ -67,13 +72,16 @@ def test_tern_all_and_none():
     plan.close()
 
 
-def test_tern_calibration_matches_oracle():
+@pytest.mark.parametrize("dm", [1024, 4096])
+def test_tern_calibration_matches_oracle(dm):
+    """Calibration runs the coefficient kernel on batches of 8 (at d_model 4096
+    the MFMA score) and the exact select on the dense scores."""
     from paper_2505_17701_amd import binding as cd
 
-    layer = tern_layer(1024, 1376, 2)
-    X = make_tokens(1950, 40, 1024, purpose=T_CALIB)
+    layer = tern_layer(dm, 1376, 2)
+    X = make_tokens(1950, 40, dm, purpose=T_CALIB)
     for k in (0.5, 0.9):
-        plan = cd.Plan(1024, 1376, max_batch=8)
+        plan = cd.Plan(dm, 1376, max_batch=8)
         th, q = cd.countdown_calibrate_tern(plan, dev_bf16(X), layer.d["theta_p"], k)
         plan.close()
         tau, q_o = oracle.calibrate("dual_tern", X, k, theta_t=layer.h["theta_t"])
@@ -84,7 +92,7 @@ def test_tern_calibration_matches_oracle():
 
 
 @pytest.mark.parametrize("shape", [(256, 688, 1, 0.9), (1032, 1000, 3, 0.75), (2048, 776, 8, 0.9),
-                                   (4096, 1376, 2, 0.5)])
+                                   (4096, 1376, 2, 0.5), (4096, 1000, 6, 0.7), (3592, 520, 8, 0.9)])
 def test_tern_topk(shape):
     dm, dff, B, k = shape
     layer = tern_layer(dm, dff, 3 + dm)
