@@ -2775,7 +2775,8 @@ static hipError_t coef_bn(int variant, const CoefArgs &a, hipStream_t s)
     // 8-10% faster at 2 tokens (7B and 70B shapes); the two-row kernel gained
     // nothing from it. At one token of d_model 8192 the registers win although
     // they leave 3 waves per SIMD (LDS copy: 4): 87.1 against 88.6 us per 70B
-    // layer.
+    // layer; at 4096 the two tie (22.1 us per 7B layer, 5 against 8 waves per
+    // SIMD).
     constexpr bool XREG1 = B <= 1;
     const size_t lds = token_lds_bytes(B, NK);
     const size_t lds1 = XREG1 ? 0 : (size_t)B * NK * kColsPerLoad * 2;
