@@ -308,3 +308,32 @@ def test_hip_failures_map_to_cd_ehip(lib):
     assert lib.countdown_ffn_mono_noalloc(vp(0x1000), 1, vp(0x2000), vp(0x3000), vp(0x4000), 256,
                                           688, 1.0, vp(0x5000), None) == cd.CD_EHIP
     assert lib.countdown_stream_read(vp(0x1000), 16, vp(0x2000), None) == cd.CD_EHIP
+
+
+def test_bench_traffic_gated_by_kernel_source(tmp_path, monkeypatch):
+    """bench.py reports a committed FETCH_SIZE + WRITE_SIZE figure only while the
+    kernel source it was taken on is unchanged: the digest ignores comments and
+    whitespace, a code change invalidates the figure (traffic null)."""
+    import bench
+
+    a = tmp_path / "a.hip"
+    b = tmp_path / "b.hip"
+    a.write_text("int f(int x) { return x + 1; } // one\n/* block */\n")
+    b.write_text("int f(int x)  {\n  return x + 1;  }  // two\n")
+    monkeypatch.setattr(bench, "KERNEL_SRCS", [str(a)])
+    d_a = bench.kernel_source_digest()
+    monkeypatch.setattr(bench, "KERNEL_SRCS", [str(b)])
+    assert bench.kernel_source_digest() == d_a  # comments and spacing only
+    b.write_text("int f(int x) { return x + 2; }\n")
+    assert bench.kernel_source_digest() != d_a
+
+    monkeypatch.setattr(bench, "KERNEL_SRCS", [str(a)])
+    (tmp_path / "profiles").mkdir()
+    summary = tmp_path / "profiles" / "line_traffic.md"
+    monkeypatch.setattr(bench, "ROOT", str(tmp_path))
+    monkeypatch.setattr(bench, "TRAFFIC_SUMMARIES", {("w", "v", 0.9, 1): "line_traffic.md"})
+    summary.write_text(f"# x\n\n- kernel_source_digest: `{d_a}`\n- hbm_bytes_per_launch: `1234.0`\n")
+    assert bench.measured_traffic(("w", "v", 0.9, 1)) == 1234.0
+    assert bench.measured_traffic(("w", "v", 0.7, 1)) is None  # no summary for the line
+    summary.write_text("# x\n\n- kernel_source_digest: `stale`\n- hbm_bytes_per_launch: `1234.0`\n")
+    assert bench.measured_traffic(("w", "v", 0.9, 1)) is None
