@@ -103,8 +103,8 @@ def test_tern_topk(shape):
 
 
 def test_tern_llama3_8b_full_size():
-    """The 8B-shaped layer (4096 x 14336) with a seeded ternary predictor at batch 1
-    and 8, thresholds calibrated on the GPU at k = 0.9, against the oracle."""
+    """The 8B-shaped layer (4096 x 14336) with a seeded ternary predictor at batch 1,
+    4 and 8, thresholds calibrated on the GPU at k = 0.9, against the oracle."""
     from paper_2505_17701_amd import binding as cd
 
     w = WORKLOADS["llama3_8b_4096x14336_pred"]
@@ -114,7 +114,7 @@ def test_tern_llama3_8b_full_size():
                                         layer.d["theta_p"], 0.9)
     cal.close()
     th = float(th.item())
-    for B in (1, 8):
+    for B in (1, 4, 8):
         plan = cd.Plan(w.d_model, w.d_ff, max_batch=B, keep_coef=True)
         x = w.tokens(B)
         n, flips, rel = check_call("dual_tern", layer, x, th, run_gpu(plan, "dual_tern", layer, x, th),
