@@ -39,6 +39,8 @@ TRAFFIC_SUMMARIES = {
     ("llama7b_4096x11008", "mono", 0.9, 1): "k_coef_mono_llama7b_4096x11008_k0.9_traffic.md",
     ("llama3_8b_4096x14336_pred", "dual_pred", 0.9, 1):
         "k_coef_pred_llama3_8b_4096x14336_k0.9_b1_traffic.md",
+    ("llama3_8b_4096x14336_pred", "dual_pred", 0.9, 4):
+        "k_coef_pred_llama3_8b_4096x14336_k0.9_b4_traffic.md",
     ("llama3_8b_4096x14336_pred", "dual_pred", 0.9, 8):
         "k_coef_pred_mfma_llama3_8b_4096x14336_k0.9_b8_traffic.md",
 }
