@@ -445,8 +445,10 @@ def optimal_dense_us(ctx, k, steps):
 
 def kernel_desc(variant, B=1):
     """The kernel(s) of a line's coefficient phase, the dominant part of every call."""
-    pred = "k_coef_pred_mfma" if B >= 5 else "k_coef_pred"
-    tern = "k_coef_tern_mfma" if B >= 5 else "k_coef_tern"
+    pred = ("k_coef_pred_mfma" if B >= 5 else
+            "k_coef_pred (8 waves per block)" if B >= 3 else "k_coef_pred")
+    tern = ("k_coef_tern_mfma (score on MFMA at d_model 4096)" if B >= 5 else
+            "k_coef_tern (8 waves per block)" if B >= 3 else "k_coef_tern")
     sel = "k_topk_gather1 (select, flags and gather in one launch)" if B == 1 else \
         "k_topk_select + k_gather_topk"
     return {"mono": "k_coef_mono (dense W_up GEMV, threshold, wave-local W_gate gather, s)",
@@ -600,7 +602,8 @@ def eight_b_block(args):
     log(f"[bench] {w.name} dual_pred per-token B=1: {json.dumps(r8['per-token k=0.9 B=1'])}")
     for B in w.batches:  # the ternary predictor (Sec. 6) in the low-rank one's place
         r = ctx.measure("dual_tern", 0.9, B, n, 50)
-        r8[f"ternary B={B}"] = brief(r)
+        r8[f"ternary B={B}"] = {**brief(r), "roofline": roofline(r, "dual_tern",
+                                                                 (w.name, "dual_tern", 0.9, B))}
         log(f"[bench] {w.name} dual_tern B={B}: {json.dumps(r8[f'ternary B={B}'])}")
     r = ctx.measure("dense", None, 1, n, 50)
     r8["dense B=1"] = brief(r)
