@@ -43,6 +43,10 @@ TRAFFIC_SUMMARIES = {
         "k_coef_pred_llama3_8b_4096x14336_k0.9_b4_traffic.md",
     ("llama3_8b_4096x14336_pred", "dual_pred", 0.9, 8):
         "k_coef_pred_mfma_llama3_8b_4096x14336_k0.9_b8_traffic.md",
+    ("llama3_8b_4096x14336_pred", "dual_tern", 0.9, 1):
+        "k_coef_tern_llama3_8b_4096x14336_k0.9_b1_traffic.md",
+    ("llama3_8b_4096x14336_pred", "dual_tern", 0.9, 8):
+        "k_coef_tern_mfma_llama3_8b_4096x14336_k0.9_b8_traffic.md",
 }
 
 
