@@ -1203,8 +1203,9 @@ __host__ __device__ constexpr size_t tern_mfma_front_u32()
     return mfma_lds_tokens_u32<B, NK>() > kTiles ? mfma_lds_tokens_u32<B, NK>() : kTiles;
 }
 
-// Ternary-predictor coefficient kernel for batches of 5-8: the ternary score,
-// then the MFMA gather with LDS-staged weight rows.
+// Ternary-predictor coefficient kernel for batches of 5-8: the ternary score
+// (on MFMA at d_model 4096, tern_score_mfma; v_dot2 otherwise), then the MFMA
+// gather with LDS-staged weight rows.
 template <int B, int NK>
 __global__ __launch_bounds__(kBlock) void k_coef_tern_mfma(const CoefArgs a)
 {
