@@ -2325,17 +2325,20 @@ __device__ __forceinline__ void mono_finish(const CoefArgs &a, const Tokens<B, N
 // (|u|, |s| or signed s_hat > q_b, union over the batch) and set act; the
 // active neurons are dealt round-robin to the four waves, which gather W_gate
 // (mono) or W_gate and W_up (pred) and write s; ideal D-CountDown copies s.
-template <int B, int NK, bool XREG, int VARIANT>
-__global__ __launch_bounds__(kBlock) void k_gather_topk(const CoefArgs a, const double *__restrict__ q)
+template <int B, int NK, bool XREG, int VARIANT, int NWV = kWavesPerBlock>
+__global__ __launch_bounds__(NWV * kWave) void k_gather_topk(const CoefArgs a, const double *__restrict__ q)
 {
     extern __shared__ __align__(16) uint32_t xs[];
     __shared__ uint32_t mask;
     constexpr bool kGather = VARIANT != kDualIdeal;
     const int lane = threadIdx.x % kWave, wave = threadIdx.x / kWave;
+    // NWV 8: the first kBlock threads stage the tokens and zero y; all gather
+    const bool first = NWV == kWavesPerBlock || threadIdx.x < kBlock;  // wave-uniform
     const int r0 = blockIdx.x * kPredRows;
     Tokens<B, NK, XREG> tok;
     if constexpr (kGather)
-        tok.issue(a.x, a.nb, a.d_model, lane);
+        if (XREG || first)
+            tok.issue(a.x, a.nb, a.d_model, lane);
     bool act = false;
     const int row = r0 + threadIdx.x;
     if (threadIdx.x < kPredRows && row < a.d_ff) {
@@ -2356,14 +2359,18 @@ __global__ __launch_bounds__(kBlock) void k_gather_topk(const CoefArgs a, const 
     const uint64_t m = ballot(act);
     if (threadIdx.x == 0)
         mask = (uint32_t)m;  // the first kPredRows threads are lanes 0..31 of wave 0
-    zero_y(a.y, a.nb * a.d_model);
+    if (first)
+        zero_y(a.y, a.nb * a.d_model);
     if constexpr (kGather) {
-        tok.write(xs);
+        if (first)
+            tok.write(xs);
+        else
+            tok.lds = xs;
         __syncthreads();
         uint32_t mm = mask;
         for (int v = 0; v < wave; ++v)
             mm &= mm - 1;
-        for (int r = pred_next(mm); r >= 0; r = pred_next(mm)) {
+        for (int r = pred_next<NWV>(mm); r >= 0; r = pred_next<NWV>(mm)) {
             u32x4 wg[NK];
             const uint16_t *w2 = VARIANT == kCats ? a.Wu : a.Wg;
             load_row<NK>(wg, w2 + (size_t)(r0 + r) * a.d_model, a.d_model, lane);
@@ -2997,23 +3004,28 @@ static hipError_t gather_topk_bn(int variant, const CoefArgs &a, const double *q
         default: return hipErrorInvalidValue;
         }
     } else {
+        // 8 waves per block up to d_model 4096, as in the predictor kernels: each
+        // wave gathers one or two of a block's active neurons instead of about
+        // three in a row (per-token M at 4 tokens 52.4 -> 48.7 us per 7B layer,
+        // low-rank predictor at 8 tokens 74.5 -> 69.9 us per 8B layer)
+        constexpr int GW = NK <= 8 ? 8 : kWavesPerBlock;
         const size_t lds = token_lds_bytes(B, NK);
         const int grid = (a.d_ff + kPredRows - 1) / kPredRows;
         switch (variant) {
         case kMono:
-            allow_lds(k_gather_topk<B, NK, XREG, kMono>, lds);
-            k_gather_topk<B, NK, XREG, kMono><<<grid, kBlock, lds, s>>>(a, q);
+            allow_lds(k_gather_topk<B, NK, XREG, kMono, GW>, lds);
+            k_gather_topk<B, NK, XREG, kMono, GW><<<grid, GW * kWave, lds, s>>>(a, q);
             break;
         case kCats:
-            allow_lds(k_gather_topk<B, NK, XREG, kCats>, lds);
-            k_gather_topk<B, NK, XREG, kCats><<<grid, kBlock, lds, s>>>(a, q);
+            allow_lds(k_gather_topk<B, NK, XREG, kCats, GW>, lds);
+            k_gather_topk<B, NK, XREG, kCats, GW><<<grid, GW * kWave, lds, s>>>(a, q);
             break;
         case kDualIdeal:
             k_gather_topk<B, NK, XREG, kDualIdeal><<<grid, kBlock, 0, s>>>(a, q);
             break;
         case kDualPred:
-            allow_lds(k_gather_topk<B, NK, XREG, kDualPred>, lds);
-            k_gather_topk<B, NK, XREG, kDualPred><<<grid, kBlock, lds, s>>>(a, q);
+            allow_lds(k_gather_topk<B, NK, XREG, kDualPred, GW>, lds);
+            k_gather_topk<B, NK, XREG, kDualPred, GW><<<grid, GW * kWave, lds, s>>>(a, q);
             break;
         default:
             return hipErrorInvalidValue;
